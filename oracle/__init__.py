@@ -1,0 +1,21 @@
+"""CPU oracle for PIPO's decoder forward pass -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The GPU library never uses it.
+
+PIPO offloads weights and KV cache without changing the arithmetic: for fp16
+or INT4 weights with fp16 activations (Section 4.1, "Workload") its result is
+the plain decoder forward pass with greedy decoding.  The paper evaluates OPT
+models (Section 4.1, "Model") and does not restate their architecture, so
+this oracle writes out the OPT decoder in its plain definition (the readings
+taken where the paper is silent are listed in ``opt.py``).
+"""
+from .opt import (  # noqa: F401
+    OracleDecoder,
+    causal_attention,
+    dequant_int4_g64,
+    layer_norm,
+    param_count,
+    layer_param_count,
+    streamed_bytes_per_step,
+)

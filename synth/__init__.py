@@ -1,0 +1,261 @@
+"""Seeded synthetic inputs for OPT-shaped decoder workloads.
+
+This package draws and encodes inputs only: random fp16 weights, their
+group-wise int4 codes, and prompt token ids.  It holds none of the decoder's
+arithmetic.  The CPU oracle (``oracle/``) and the GPU library both consume
+what it produces; neither of them is imported here.
+
+Every tensor has its own counter-based stream (Philox4x64-10, see
+``csrc/synth.c``), keyed by ``(seed, tensor_key(layer, name))``, so a tensor,
+or a row range of it, can be regenerated independently of all others.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+import subprocess
+from typing import Dict, Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "csrc", "synth.c")
+_LIB_PATH = os.path.join(_HERE, "libsynth.so")
+_lib = None
+
+WEIGHT_STD = 0.02
+DEFAULT_SEED = 20250404
+
+
+def build(force: bool = True) -> str:
+    """Compile ``libsynth.so`` next to this file with gcc (OpenMP, F16C)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O3", "-fPIC", "-shared", "-fopenmp", "-mf16c", "-mavx2", "-mfma", "-fno-math-errno", "-std=c11",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=False)
+        L = ctypes.CDLL(_LIB_PATH)
+        u64, i64, i32 = ctypes.c_uint64, ctypes.c_int64, ctypes.c_int
+        vp = ctypes.c_void_p
+        L.synth_philox4x64_10.argtypes = [vp, vp, vp]
+        L.synth_f32_to_f16.argtypes = [ctypes.c_float]
+        L.synth_f32_to_f16.restype = ctypes.c_uint16
+        L.synth_normal_f16.argtypes = [u64, u64, u64, u64, ctypes.c_double, vp, i32]
+        L.synth_fill_f16.argtypes = [ctypes.c_uint16, u64, vp]
+        L.synth_quant_int4_g64.argtypes = [vp, i64, i64, vp, vp, i32]
+        L.synth_normal_int4_g64.argtypes = [u64, u64, i64, i64, ctypes.c_double, vp, vp, i32]
+        _lib = L
+    return _lib
+
+
+def n_threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    env = os.environ.get("OMP_NUM_THREADS")
+    if env and env.isdigit():
+        n = min(n, int(env)) if int(env) > 0 else n
+    return max(1, n)
+
+
+def _ptr(a: np.ndarray) -> int:
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data
+
+
+def philox4x64_10(ctr, key) -> np.ndarray:
+    c = np.ascontiguousarray(ctr, dtype=np.uint64)
+    k = np.ascontiguousarray(key, dtype=np.uint64)
+    out = np.zeros(4, dtype=np.uint64)
+    lib().synth_philox4x64_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+# ----------------------------------------------------------------------------
+# tensor naming
+_TENSOR_CODES = {
+    "tok_emb": 1, "pos_emb": 2, "lnf_g": 3, "lnf_b": 4,
+    "ln1_g": 10, "ln1_b": 11, "wqkv": 12, "bqkv": 13, "wo": 14, "bo": 15,
+    "ln2_g": 16, "ln2_b": 17, "w1": 18, "b1": 19, "w2": 20, "b2": 21,
+}
+MATRICES = ("wqkv", "wo", "w1", "w2")
+SMALL = ("ln1_g", "ln1_b", "bqkv", "bo", "ln2_g", "ln2_b", "b1", "b2")
+
+
+def tensor_key(layer: int, name: str) -> int:
+    """Stream id of a tensor: layer -1 for the embeddings and the final LN."""
+    return ((layer + 1) << 16) | _TENSOR_CODES[name]
+
+
+def normal_f16(seed: int, key: int, n: int, std: float = WEIGHT_STD, first: int = 0,
+               out: Optional[np.ndarray] = None) -> np.ndarray:
+    """fp16 values std*z[first:first+n] of stream (seed, key)."""
+    if out is None:
+        out = np.empty(n, dtype=np.float16)
+    flat = out.reshape(-1)
+    assert flat.size == n and flat.dtype.itemsize == 2
+    lib().synth_normal_f16(seed, key, first, n, std, _ptr(flat), n_threads())
+    return out
+
+
+def f32_to_f16_bits(x: float) -> int:
+    return int(lib().synth_f32_to_f16(float(x)))
+
+
+def quant_int4_g64(w16: np.ndarray):
+    """Encode fp16 W[N][K] as (q[N][K/2] uint8, sm[N][K/64][2] fp16)."""
+    w16 = np.ascontiguousarray(w16, dtype=np.float16)
+    N, K = w16.shape
+    assert K % 64 == 0
+    q = np.empty((N, K // 2), dtype=np.uint8)
+    sm = np.empty((N, K // 64, 2), dtype=np.float16)
+    lib().synth_quant_int4_g64(_ptr(w16), N, K, _ptr(q), _ptr(sm), n_threads())
+    return q, sm
+
+
+def normal_int4_g64(seed: int, key: int, N: int, K: int, std: float = WEIGHT_STD,
+                    q: Optional[np.ndarray] = None, sm: Optional[np.ndarray] = None):
+    """int4 codes of normal_f16(seed, key, N*K) viewed as [N][K], without the fp16 copy."""
+    assert K % 64 == 0
+    if q is None:
+        q = np.empty((N, K // 2), dtype=np.uint8)
+    if sm is None:
+        sm = np.empty((N, K // 64, 2), dtype=np.float16)
+    assert q.size == N * K // 2 and sm.size == N * K // 32
+    lib().synth_normal_int4_g64(seed, key, N, K, std, _ptr(q.reshape(-1)),
+                                _ptr(sm.reshape(-1)), n_threads())
+    return q, sm
+
+
+# ----------------------------------------------------------------------------
+# model shapes and workloads
+@dataclasses.dataclass(frozen=True)
+class OPTShape:
+    n_layers: int
+    d_model: int
+    n_heads: int
+    d_ffn: int
+    vocab: int = 50272
+    max_pos: int = 2048
+    pos_offset: int = 2
+    ln_eps: float = 1e-5
+
+    @property
+    def head_dim(self) -> int:
+        return self.d_model // self.n_heads
+
+    def with_layers(self, n: int) -> "OPTShape":
+        return dataclasses.replace(self, n_layers=n)
+
+
+OPT_125M = OPTShape(12, 768, 12, 3072)
+OPT_6_7B = OPTShape(32, 4096, 32, 16384)
+OPT_13B = OPTShape(40, 5120, 40, 20480)
+OPT_30B = OPTShape(48, 7168, 56, 28672)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    shape: OPTShape
+    batch: int
+    prompt: int
+    gen: int
+    wfmt: str            # "fp16" or "int4"
+    kv_on_host: bool
+
+
+WORKLOADS = (
+    Workload("opt-125m b4 p32 g8 fp16", OPT_125M, 4, 32, 8, "fp16", False),
+    Workload("opt-6.7b b16 p512 g32 fp16", OPT_6_7B, 16, 512, 32, "fp16", False),
+    Workload("opt-13b b32 p512 g32 int4-g64", OPT_13B, 32, 512, 32, "int4", False),
+    Workload("opt-30b b64 p512 g32 fp16", OPT_30B, 64, 512, 32, "fp16", False),
+    Workload("opt-30b b128 p512 g32 int4-g64 kv-host", OPT_30B, 128, 512, 32, "int4", True),
+)
+
+
+def prompt_tokens(batch: int, prompt: int, vocab: int, seed: int = 1,
+                  stream: int = 0) -> np.ndarray:
+    """Uniform token ids in [0, vocab), int32 [batch][prompt]."""
+    rng = np.random.Generator(np.random.Philox(key=np.array([seed, 0x70726F6D + stream],
+                                                            dtype=np.uint64)))
+    return rng.integers(0, vocab, size=(batch, prompt), dtype=np.int64).astype(np.int32)
+
+
+class SyntheticOPT:
+    """Random-init OPT-shaped weights, drawn per tensor on demand.
+
+    fp16 tensors are returned as float16 arrays.  With ``wfmt == "int4"`` the
+    four per-layer matrices come as ``{name: (q, sm)}`` int4 codes of the same
+    fp16 draw; embeddings, LayerNorm parameters and biases stay fp16.
+    LayerNorm gamma is 1 and beta 0; biases are N(0, std) unless
+    ``zero_bias``.
+    """
+
+    def __init__(self, shape: OPTShape, seed: int = DEFAULT_SEED, wfmt: str = "fp16",
+                 zero_bias: bool = False, std: float = WEIGHT_STD):
+        assert wfmt in ("fp16", "int4")
+        self.shape, self.seed, self.wfmt = shape, seed, wfmt
+        self.zero_bias, self.std = zero_bias, std
+
+    # shapes of every tensor of one layer
+    def layer_shapes(self) -> Dict[str, tuple]:
+        d, F = self.shape.d_model, self.shape.d_ffn
+        return {"ln1_g": (d,), "ln1_b": (d,), "wqkv": (3 * d, d), "bqkv": (3 * d,),
+                "wo": (d, d), "bo": (d,), "ln2_g": (d,), "ln2_b": (d,),
+                "w1": (F, d), "b1": (F,), "w2": (d, F), "b2": (d,)}
+
+    def fill(self, layer: int, name: str, out: np.ndarray) -> np.ndarray:
+        """Write fp16 tensor (layer, name) into ``out``."""
+        if name.endswith("_g"):
+            out[...] = np.float16(1.0)
+        elif name.endswith("_b") and name.startswith("ln"):
+            out[...] = np.float16(0.0)
+        elif name.startswith("b") and self.zero_bias:
+            out[...] = np.float16(0.0)
+        else:
+            normal_f16(self.seed, tensor_key(layer, name), out.size, self.std, out=out)
+        return out
+
+    def fill_int4(self, layer: int, name: str, q: np.ndarray, sm: np.ndarray):
+        N, K = self.layer_shapes()[name]
+        return normal_int4_g64(self.seed, tensor_key(layer, name), N, K, self.std, q, sm)
+
+    def tensor(self, layer: int, name: str) -> np.ndarray:
+        shp = (self.layer_shapes()[name] if layer >= 0 else
+               {"tok_emb": (self.shape.vocab, self.shape.d_model),
+                "pos_emb": (self.shape.max_pos + self.shape.pos_offset, self.shape.d_model),
+                "lnf_g": (self.shape.d_model,), "lnf_b": (self.shape.d_model,)}[name])
+        return self.fill(layer, name, np.empty(shp, dtype=np.float16))
+
+    def tok_emb(self) -> np.ndarray:
+        return self.tensor(-1, "tok_emb")
+
+    def pos_emb(self) -> np.ndarray:
+        return self.tensor(-1, "pos_emb")
+
+    def lnf(self):
+        return self.tensor(-1, "lnf_g"), self.tensor(-1, "lnf_b")
+
+    def layer(self, j: int) -> Dict[str, object]:
+        out: Dict[str, object] = {}
+        for name, shp in self.layer_shapes().items():
+            if name in MATRICES and self.wfmt == "int4":
+                N, K = shp
+                q = np.empty((N, K // 2), dtype=np.uint8)
+                sm = np.empty((N, K // 64, 2), dtype=np.float16)
+                out[name] = self.fill_int4(j, name, q, sm)
+            else:
+                out[name] = self.tensor(j, name)
+        return out
