@@ -1,0 +1,225 @@
+/*
+ * pipo.h -- C ABI of an MI355X (gfx950) pipelined-offloading decoder.
+ *
+ * The library runs the forward pass of an OPT-style decoder (pre-LN blocks:
+ * LayerNorm, QKV projection, causal softmax attention over a KV cache,
+ * output projection, LayerNorm, ReLU MLP; tied output head; greedy
+ * decoding) on one GPU while the weights of each layer -- and, optionally,
+ * its KV cache -- live in pinned host memory and are streamed into HBM a
+ * few layers ahead of the computation.  This is the pipelined offloading of
+ * PIPO (Liu, Li, Li; arXiv 2504.03664):
+ *   - weights are loaded layer by layer and released after use
+ *     (Section 3.1.1), in fine-grained chunks of merged per-layer tensors
+ *     (Section 3.3, blockwise transfer and data merging);
+ *   - four task types -- computation, weight loading, KV-cache loading and
+ *     KV-cache saving -- overlap, each load finishing before its layer
+ *     computes and each save finishing before the same layer loads its
+ *     cache at the next token (Section 3.1.2; Section 3.2.2, Algorithm 1);
+ *   - loading runs ahead of computation so that two or more layers are
+ *     resident (Section 3.2.3, performance-optimized pipeline);
+ *   - INT4 weights are consumed directly by the GEMM (Section 3.4).
+ * The lifecycle follows the paper's workflow (Algorithm 2): pipo_create
+ * initialises the model data, the transfer machinery and the schedule;
+ * pipo_prefill and pipo_decode_step run the generation loop.
+ *
+ * Conventions for every entry point:
+ *   - fp16 values are passed as their IEEE binary16 bit patterns (uint16_t);
+ *   - matrices are row-major [out][in] ("N rows of K inputs");
+ *   - host pointers are plain CPU pointers; "device" pointers are HBM
+ *     addresses on the current HIP device;
+ *   - every call returns a pipo_status (no exceptions cross the ABI); on
+ *     failure pipo_last_error() describes it;
+ *   - a context is used by one host thread at a time.
+ */
+#ifndef PIPO_H
+#define PIPO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PIPO_OK = 0,
+  PIPO_ERR_ARG = -1,          /* invalid argument or shape */
+  PIPO_ERR_OOM_DEVICE = -2,   /* HBM allocation failed or exceeds hbm_budget_bytes */
+  PIPO_ERR_OOM_HOST = -3,     /* pinned host allocation failed */
+  PIPO_ERR_HIP = -4,          /* a HIP runtime call failed */
+  PIPO_ERR_STATE = -5,        /* call not valid in the context's state */
+  PIPO_ERR_UNSUPPORTED = -6   /* shape or policy outside what the kernels support */
+} pipo_status;
+
+/* Weight storage format of the four per-layer matrices. */
+enum { PIPO_W_FP16 = 0, PIPO_W_INT4_G64 = 1 };
+
+/* pipo_policy.debug_flags */
+enum {
+  PIPO_DBG_POISON_SLOTS = 1,  /* fill a weight/KV slot with NaN before every refill */
+  PIPO_DBG_COPY_DELAY = 2,    /* host-side sleep of copy_delay_us before every chunk copy */
+  PIPO_DBG_TIMESTAMPS = 4     /* record device timestamps of copies and kernels (stats) */
+};
+
+/* Decoder shape.  Constraints: d_model = n_heads * head_dim with head_dim
+ * 64 or 128; d_model and d_ffn multiples of 128; vocab >= 1. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, d_ffn, vocab;
+  int32_t max_pos;      /* positions the learned table covers (rows = max_pos + pos_offset) */
+  int32_t pos_offset;   /* row of position 0 in the position table (2 for OPT) */
+  float ln_eps;         /* LayerNorm epsilon (1e-5) */
+} pipo_shape;
+
+/* One group-wise INT4 matrix W[N][K]: W[n][k] = code * scale + min, one
+ * (scale, min) pair per 64 consecutive k of a row (Section 3.4 keeps the
+ * weights in 4 bits; the grouping is the workload's definition). */
+typedef struct {
+  const uint8_t* q;           /* [N][K/2]; code(2i) in the low nibble of byte i */
+  const uint16_t* scale_min;  /* [N][K/64][2] fp16: {scale, min} */
+} pipo_q4;
+
+/* Host tensors of one layer (caller-owned; read, never written). */
+typedef struct {
+  const uint16_t *ln1_g, *ln1_b;   /* [d] */
+  const uint16_t *bqkv;            /* [3d]: q, k, v biases */
+  const uint16_t *bo;              /* [d] */
+  const uint16_t *ln2_g, *ln2_b;   /* [d] */
+  const uint16_t *b1;              /* [d_ffn] */
+  const uint16_t *b2;              /* [d] */
+  const uint16_t *wqkv;            /* [3d][d] rows: q, k, v       (PIPO_W_FP16) */
+  const uint16_t *wo;              /* [d][d]                      (PIPO_W_FP16) */
+  const uint16_t *w1;              /* [d_ffn][d]                  (PIPO_W_FP16) */
+  const uint16_t *w2;              /* [d][d_ffn]                  (PIPO_W_FP16) */
+  pipo_q4 qqkv, qo, q1, q2;        /* same matrices               (PIPO_W_INT4_G64) */
+} pipo_layer_host;
+
+typedef struct {
+  const uint16_t* tok_emb;   /* [vocab][d]; also the output head (tied) */
+  const uint16_t* pos_emb;   /* [max_pos + pos_offset][d] */
+  const uint16_t *lnf_g, *lnf_b;   /* final LayerNorm [d] */
+  const pipo_layer_host* layers;   /* [n_layers] */
+} pipo_host_weights;
+
+/* Offload policy (the paper's (S_off, S_pipe) pair, Algorithm 2, made
+ * explicit).  Zero-initialise and set what you need; 0 picks the default. */
+typedef struct {
+  int32_t wfmt;              /* PIPO_W_FP16 or PIPO_W_INT4_G64 */
+  int32_t weights_on_host;   /* 1: stream every layer each pass; 0: all layers resident in HBM */
+  int32_t embed_on_host;     /* 1: stream the output head each pass, gather embeddings on the
+                                host; 0: token table resident in HBM */
+  int32_t kv_on_host;        /* 1: KV cache in library-owned pinned host memory, each layer's
+                                prefix loaded before its attention and the new rows saved
+                                after it; 0: KV cache resident in HBM */
+  int32_t n_weight_slots;    /* HBM slots the layers rotate through (default 3, min 2) */
+  int32_t n_h2d_streams;     /* host-to-device copy streams (default 1, max 2) */
+  int64_t chunk_bytes;       /* bytes per copy chunk (default 64 MiB; rounded to 4 KiB) */
+  int32_t max_batch;         /* sequences per pass (>= 1) */
+  int32_t max_seq;           /* prompt + generated positions per sequence (<= max_pos) */
+  int64_t hbm_budget_bytes;  /* 0: unlimited; else pipo_create fails with OOM_DEVICE above it */
+  int32_t debug_flags;       /* PIPO_DBG_* */
+  int32_t copy_delay_us;     /* delay for PIPO_DBG_COPY_DELAY */
+} pipo_policy;
+
+/* Per-kernel timing (filled when PIPO_DBG_TIMESTAMPS is set): each launch
+ * is bracketed by events on the stream that runs it. */
+typedef struct {
+  char name[32];
+  int64_t launches;
+  double total_ms;           /* summed launch durations */
+  double alg_bytes;          /* algorithmic bytes summed over launches */
+  double alg_flops;          /* algorithmic flops summed over launches */
+} pipo_kernel_stat;
+
+#define PIPO_MAX_KERNEL_STATS 16
+
+typedef struct {
+  int64_t h2d_bytes;         /* host-to-device bytes issued since the last reset */
+  int64_t h2d_weight_bytes;  /*   of which weights (incl. output head) */
+  int64_t h2d_kv_bytes;      /*   of which KV-cache prefixes */
+  int64_t d2h_bytes;         /* device-to-host bytes (KV saves, tokens, logits) */
+  int64_t n_copies;          /* copy commands issued */
+  int64_t n_kernels;         /* kernel launches issued */
+  int64_t decode_steps;      /* pipo_decode_step calls since the last reset */
+  double decode_wall_ms;     /* host wall time inside those calls */
+  double prefill_wall_ms;    /* host wall time of the last pipo_prefill */
+  /* device timeline of the decode steps since the last reset (PIPO_DBG_TIMESTAMPS) */
+  double window_ms;          /* first decode-step start to last decode-step end */
+  double copy_busy_ms;       /* union of host-to-device copy intervals inside the window */
+  double kernel_busy_ms;     /* union of compute-stream kernel intervals inside the window */
+  double busy_ms;            /* union of both */
+  int64_t hbm_bytes;         /* HBM the context holds */
+  int64_t pinned_host_bytes; /* pinned host memory the context holds */
+  int32_t n_kernel_stats;
+  pipo_kernel_stat kernels[PIPO_MAX_KERNEL_STATS];
+} pipo_stats;
+
+typedef struct pipo_ctx pipo_ctx;
+
+/*
+ * Create a context on the current HIP device.
+ *   shape, weights, policy: read during the call.  The matrices in `weights`
+ *     must stay valid and unchanged until pipo_destroy when weights_on_host
+ *     (or embed_on_host) is set: matrices in pinned memory from
+ *     pipo_host_alloc are streamed in place; other host memory is first
+ *     copied into library-owned pinned memory.
+ *   out: receives the context (NULL on failure).
+ * Errors: ARG (bad shape/policy/NULL tensor), UNSUPPORTED (shape outside the
+ * kernels' range), OOM_DEVICE, OOM_HOST, HIP.
+ */
+pipo_status pipo_create(const pipo_shape* shape, const pipo_host_weights* weights,
+                        const pipo_policy* policy, pipo_ctx** out);
+
+/*
+ * Start b new sequences: run the whole prompt tokens[b][P] (row-major host
+ * int32, ids in [0, vocab)), fill the KV cache for positions 0..P-1, and
+ * return the greedy next token of each sequence in next_out[b] (host).  If
+ * logits_out is not NULL it receives the fp32 logits [b][vocab] of the last
+ * prompt position.  Returns once next_out is written.
+ * Errors: ARG (b < 1 or > max_batch, P < 1 or > max_seq, id out of range),
+ * HIP.
+ */
+pipo_status pipo_prefill(pipo_ctx* ctx, const int32_t* tokens, int32_t b, int32_t P,
+                         float* logits_out, int32_t* next_out);
+
+/*
+ * Append one token per sequence (tokens[b], host int32; usually the previous
+ * next_out, any id for teacher forcing) at the next position and return the
+ * greedy next tokens (next_out[b]) and optionally the fp32 logits [b][vocab].
+ * b must equal the prefill's b.
+ * Errors: STATE (no prefill yet, or the sequences already hold max_seq
+ * positions), ARG, HIP.
+ */
+pipo_status pipo_decode_step(pipo_ctx* ctx, const int32_t* tokens, float* logits_out,
+                             int32_t* next_out);
+
+/* Copy the context's counters into *out (see pipo_stats). */
+pipo_status pipo_get_stats(pipo_ctx* ctx, pipo_stats* out);
+
+/* Zero the counters and timelines of pipo_stats (allocation figures stay). */
+pipo_status pipo_reset_stats(pipo_ctx* ctx);
+
+/* Release everything the context holds.  NULL is allowed. */
+void pipo_destroy(pipo_ctx* ctx);
+
+/*
+ * Host-to-device link probe: copy `bytes` from pinned host memory to HBM
+ * `iters` times, split evenly over n_streams (1 or 2) copy streams, and
+ * return the best rate in *gbps (1e9 bytes per second).  Allocates and
+ * frees its own buffers.  Errors: ARG, OOM_HOST, OOM_DEVICE, HIP.
+ */
+pipo_status pipo_measure_h2d_peak(int64_t bytes, int32_t iters, int32_t n_streams,
+                                  double* gbps);
+
+/* Pinned (page-locked) host memory, 4 KiB aligned; NULL on failure.
+ * Matrices placed here are streamed by the copy engines without staging. */
+void* pipo_host_alloc(size_t bytes);
+void pipo_host_free(void* p);
+
+/* Text of the last error on the calling thread ("" if none). */
+const char* pipo_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PIPO_H */

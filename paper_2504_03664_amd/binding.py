@@ -1,0 +1,322 @@
+"""ctypes binding of libpipo.so: the C ABI of include/pipo.h, pipo_ops.h and
+pipo_sched.h under the same names.  Argument marshalling only; every step
+of the decoder runs in the library's HIP kernels.
+
+Loading fails loudly (ImportError at first use) when the library has not
+been built: there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libpipo.so")
+SCHED_LIB_PATH = os.path.join(_PKG, "libpipo_sched.so")
+
+i32, i64, f32, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double
+vp, sz = ctypes.c_void_p, ctypes.c_size_t
+
+PIPO_OK = 0
+STATUS_NAMES = {0: "PIPO_OK", -1: "PIPO_ERR_ARG", -2: "PIPO_ERR_OOM_DEVICE",
+                -3: "PIPO_ERR_OOM_HOST", -4: "PIPO_ERR_HIP", -5: "PIPO_ERR_STATE",
+                -6: "PIPO_ERR_UNSUPPORTED"}
+PIPO_W_FP16, PIPO_W_INT4_G64 = 0, 1
+PIPO_DBG_POISON_SLOTS, PIPO_DBG_COPY_DELAY, PIPO_DBG_TIMESTAMPS = 1, 2, 4
+PIPO_EPI_F16, PIPO_EPI_RELU_F16, PIPO_EPI_ADD_F32, PIPO_EPI_F32 = 0, 1, 2, 3
+PIPO_MAX_KERNEL_STATS = 16
+
+
+class PipoShape(ctypes.Structure):
+    _fields_ = [("n_layers", i32), ("d_model", i32), ("n_heads", i32), ("d_ffn", i32),
+                ("vocab", i32), ("max_pos", i32), ("pos_offset", i32), ("ln_eps", f32)]
+
+
+class PipoQ4(ctypes.Structure):
+    _fields_ = [("q", vp), ("scale_min", vp)]
+
+
+class PipoLayerHost(ctypes.Structure):
+    _fields_ = [("ln1_g", vp), ("ln1_b", vp), ("bqkv", vp), ("bo", vp), ("ln2_g", vp),
+                ("ln2_b", vp), ("b1", vp), ("b2", vp), ("wqkv", vp), ("wo", vp), ("w1", vp),
+                ("w2", vp), ("qqkv", PipoQ4), ("qo", PipoQ4), ("q1", PipoQ4), ("q2", PipoQ4)]
+
+
+class PipoHostWeights(ctypes.Structure):
+    _fields_ = [("tok_emb", vp), ("pos_emb", vp), ("lnf_g", vp), ("lnf_b", vp),
+                ("layers", ctypes.POINTER(PipoLayerHost))]
+
+
+class PipoPolicy(ctypes.Structure):
+    _fields_ = [("wfmt", i32), ("weights_on_host", i32), ("embed_on_host", i32),
+                ("kv_on_host", i32), ("n_weight_slots", i32), ("n_h2d_streams", i32),
+                ("chunk_bytes", i64), ("max_batch", i32), ("max_seq", i32),
+                ("hbm_budget_bytes", i64), ("debug_flags", i32), ("copy_delay_us", i32)]
+
+
+class PipoKernelStat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", i64), ("total_ms", f64),
+                ("alg_bytes", f64), ("alg_flops", f64)]
+
+
+class PipoStats(ctypes.Structure):
+    _fields_ = [("h2d_bytes", i64), ("h2d_weight_bytes", i64), ("h2d_kv_bytes", i64),
+                ("d2h_bytes", i64), ("n_copies", i64), ("n_kernels", i64),
+                ("decode_steps", i64), ("decode_wall_ms", f64), ("prefill_wall_ms", f64),
+                ("window_ms", f64), ("copy_busy_ms", f64), ("kernel_busy_ms", f64),
+                ("busy_ms", f64), ("hbm_bytes", i64), ("pinned_host_bytes", i64),
+                ("n_kernel_stats", i32),
+                ("kernels", PipoKernelStat * PIPO_MAX_KERNEL_STATS)]
+
+
+class PipoSchedConfig(ctypes.Structure):
+    _fields_ = [("n_layers", i32), ("n_slots", i32), ("n_h2d", i32), ("layers_streamed", i32),
+                ("head_streamed", i32), ("kv_on_host", i32), ("poison", i32), ("delay", i32),
+                ("chunk_bytes", i64), ("layer_seg_bytes", i64 * 10), ("head_bytes", i64)]
+
+
+class PipoError(RuntimeError):
+    def __init__(self, status: int, where: str, msg: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)}: {msg}")
+
+
+# ---------------------------------------------------------------------------
+_lib = None
+_sched_lib = None
+
+_SIGNATURES = {
+    "pipo_create": ([ctypes.POINTER(PipoShape), ctypes.POINTER(PipoHostWeights),
+                     ctypes.POINTER(PipoPolicy), ctypes.POINTER(vp)], i32),
+    "pipo_prefill": ([vp, vp, i32, i32, vp, vp], i32),
+    "pipo_decode_step": ([vp, vp, vp, vp], i32),
+    "pipo_get_stats": ([vp, ctypes.POINTER(PipoStats)], i32),
+    "pipo_reset_stats": ([vp], i32),
+    "pipo_destroy": ([vp], None),
+    "pipo_measure_h2d_peak": ([i64, i32, i32, ctypes.POINTER(f64)], i32),
+    "pipo_host_alloc": ([sz], vp),
+    "pipo_host_free": ([vp], None),
+    "pipo_last_error": ([], ctypes.c_char_p),
+    "pipo_dev_alloc": ([sz, ctypes.POINTER(vp)], i32),
+    "pipo_dev_free": ([vp], i32),
+    "pipo_copy_h2d": ([vp, vp, sz], i32),
+    "pipo_copy_d2h": ([vp, vp, sz], i32),
+    "pipo_dev_synchronize": ([], i32),
+    "pipo_op_gemm_f16": ([vp, vp, vp, vp, i64, i64, i64, i32, vp], i32),
+    "pipo_op_gemm_w4": ([vp, vp, vp, vp, vp, i64, i64, i64, i32, vp], i32),
+    "pipo_op_layernorm": ([vp, vp, vp, vp, i64, i64, i64, i64, f32, vp], i32),
+    "pipo_op_attn_decode": ([vp, vp, vp, vp, i32, i32, i32, i32, vp], i32),
+    "pipo_op_attn_prefill": ([vp, vp, vp, vp, i32, i32, i32, i32, vp], i32),
+    "pipo_op_argmax": ([vp, vp, i64, i64, vp], i32),
+    "pipo_sched_trace": ([ctypes.POINTER(PipoSchedConfig), i32, vp, vp, vp, i64, vp, i64], i64),
+}
+
+
+def _declare(lib, names):
+    for name in names:
+        args, res = _SIGNATURES[name]
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+def lib():
+    """The GPU library; raises ImportError if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_2504_03664_amd.build`")
+        _lib = _declare(ctypes.CDLL(LIB_PATH), _SIGNATURES.keys())
+    return _lib
+
+
+def sched_lib():
+    """The CPU-only schedule library (no HIP runtime needed)."""
+    global _sched_lib
+    if _sched_lib is None:
+        if not os.path.exists(SCHED_LIB_PATH):
+            raise ImportError(f"{SCHED_LIB_PATH} is missing: run the build")
+        _sched_lib = _declare(ctypes.CDLL(SCHED_LIB_PATH), ["pipo_sched_trace"])
+    return _sched_lib
+
+
+def _check(status: int, where: str):
+    if status != PIPO_OK:
+        raise PipoError(status, where, lib().pipo_last_error().decode())
+
+
+def _ptr(a: Optional[np.ndarray]) -> Optional[int]:
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data
+
+
+# ---------------------------------------------------------------------------
+# main ABI
+def pipo_create(shape: PipoShape, weights: PipoHostWeights, policy: PipoPolicy) -> int:
+    ctx = vp()
+    _check(lib().pipo_create(ctypes.byref(shape), ctypes.byref(weights), ctypes.byref(policy),
+                             ctypes.byref(ctx)), "pipo_create")
+    return ctx.value
+
+
+def pipo_prefill(ctx: int, tokens: np.ndarray, logits: Optional[np.ndarray] = None
+                 ) -> np.ndarray:
+    """tokens int32 [b][P]; logits: optional float32 [b][vocab] to receive the
+    last position's logits.  Returns the greedy next tokens [b]."""
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+    b, P = tokens.shape
+    nxt = np.empty(b, dtype=np.int32)
+    if logits is not None:
+        assert logits.dtype == np.float32 and logits.shape[0] == b and logits.flags["C_CONTIGUOUS"]
+    _check(lib().pipo_prefill(ctx, _ptr(tokens), b, P, _ptr(logits), _ptr(nxt)), "pipo_prefill")
+    return nxt
+
+
+def pipo_decode_step(ctx: int, tokens: np.ndarray, logits: Optional[np.ndarray] = None
+                     ) -> np.ndarray:
+    """tokens int32 [b]; returns the greedy next tokens [b]."""
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+    b = tokens.shape[0]
+    nxt = np.empty(b, dtype=np.int32)
+    if logits is not None:
+        assert logits.dtype == np.float32 and logits.shape[0] == b and logits.flags["C_CONTIGUOUS"]
+    _check(lib().pipo_decode_step(ctx, _ptr(tokens), _ptr(logits), _ptr(nxt)), "pipo_decode_step")
+    return nxt
+
+
+def pipo_get_stats(ctx: int) -> dict:
+    st = PipoStats()
+    _check(lib().pipo_get_stats(ctx, ctypes.byref(st)), "pipo_get_stats")
+    out = {name: getattr(st, name) for name, _ in PipoStats._fields_
+           if name not in ("kernels", "n_kernel_stats")}
+    out["kernels"] = {
+        st.kernels[i].name.decode(): dict(launches=st.kernels[i].launches,
+                                          total_ms=st.kernels[i].total_ms,
+                                          alg_bytes=st.kernels[i].alg_bytes,
+                                          alg_flops=st.kernels[i].alg_flops)
+        for i in range(st.n_kernel_stats)}
+    return out
+
+
+def pipo_reset_stats(ctx: int) -> None:
+    _check(lib().pipo_reset_stats(ctx), "pipo_reset_stats")
+
+
+def pipo_destroy(ctx: int) -> None:
+    lib().pipo_destroy(ctx)
+
+
+def pipo_measure_h2d_peak(nbytes: int, iters: int = 10, n_streams: int = 1) -> float:
+    g = f64()
+    _check(lib().pipo_measure_h2d_peak(nbytes, iters, n_streams, ctypes.byref(g)),
+           "pipo_measure_h2d_peak")
+    return g.value
+
+
+def pipo_host_alloc(nbytes: int) -> int:
+    p = lib().pipo_host_alloc(nbytes)
+    if not p:
+        raise MemoryError(f"pipo_host_alloc({nbytes}) failed")
+    return p
+
+
+def pipo_host_free(p: int) -> None:
+    lib().pipo_host_free(p)
+
+
+def pipo_last_error() -> str:
+    return lib().pipo_last_error().decode()
+
+
+# ---------------------------------------------------------------------------
+# op-level ABI (device pointers as ints)
+class DeviceBuffer:
+    """HBM buffer owned by the caller through pipo_dev_alloc / pipo_dev_free."""
+
+    def __init__(self, nbytes: int):
+        p = vp()
+        _check(lib().pipo_dev_alloc(max(int(nbytes), 1), ctypes.byref(p)), "pipo_dev_alloc")
+        self.ptr, self.nbytes = p.value, int(nbytes)
+
+    @classmethod
+    def from_array(cls, a: np.ndarray) -> "DeviceBuffer":
+        a = np.ascontiguousarray(a)
+        buf = cls(a.nbytes)
+        _check(lib().pipo_copy_h2d(buf.ptr, _ptr(a), a.nbytes), "pipo_copy_h2d")
+        return buf
+
+    def to_array(self, dtype, shape) -> np.ndarray:
+        out = np.empty(shape, dtype=dtype)
+        assert out.nbytes <= self.nbytes
+        _check(lib().pipo_copy_d2h(_ptr(out), self.ptr, out.nbytes), "pipo_copy_d2h")
+        return out
+
+    def free(self):
+        if self.ptr:
+            lib().pipo_dev_free(self.ptr)
+            self.ptr = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def pipo_dev_synchronize() -> None:
+    _check(lib().pipo_dev_synchronize(), "pipo_dev_synchronize")
+
+
+def pipo_op_gemm_f16(X, W, bias, out, M, N, K, epi, stream=None):
+    _check(lib().pipo_op_gemm_f16(X, W, bias, out, M, N, K, epi, stream), "pipo_op_gemm_f16")
+
+
+def pipo_op_gemm_w4(X, Wq, Wsm, bias, out, M, N, K, epi, stream=None):
+    _check(lib().pipo_op_gemm_w4(X, Wq, Wsm, bias, out, M, N, K, epi, stream), "pipo_op_gemm_w4")
+
+
+def pipo_op_layernorm(x, g, b, y, rows, d, src_stride, src_offset, eps, stream=None):
+    _check(lib().pipo_op_layernorm(x, g, b, y, rows, d, src_stride, src_offset, eps, stream),
+           "pipo_op_layernorm")
+
+
+def pipo_op_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, stream=None):
+    _check(lib().pipo_op_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, stream),
+           "pipo_op_attn_decode")
+
+
+def pipo_op_attn_prefill(q, kc, vc, o, b, P, n_heads, head_dim, stream=None):
+    _check(lib().pipo_op_attn_prefill(q, kc, vc, o, b, P, n_heads, head_dim, stream),
+           "pipo_op_attn_prefill")
+
+
+def pipo_op_argmax(logits, nxt, rows, V, stream=None):
+    _check(lib().pipo_op_argmax(logits, nxt, rows, V, stream), "pipo_op_argmax")
+
+
+# ---------------------------------------------------------------------------
+def pipo_sched_trace(cfg: PipoSchedConfig, passes, kv_row_bytes: int = 0,
+                     use_gpu_lib: bool = False) -> str:
+    """passes: list of (prefill: bool, pos0, T).  Uses the CPU-only library
+    unless use_gpu_lib."""
+    L = lib() if use_gpu_lib else sched_lib()
+    n = len(passes)
+    pf = np.array([int(p[0]) for p in passes], dtype=np.int32)
+    p0 = np.array([p[1] for p in passes], dtype=np.int64)
+    T = np.array([p[2] for p in passes], dtype=np.int64)
+    size = 1 << 20
+    while True:
+        buf = ctypes.create_string_buffer(size)
+        r = L.pipo_sched_trace(ctypes.byref(cfg), n, _ptr(pf), _ptr(p0), _ptr(T), kv_row_bytes,
+                               ctypes.addressof(buf), size)
+        if r >= 0:
+            return buf.value.decode()
+        if size > (1 << 30):
+            raise ValueError("pipo_sched_trace: invalid configuration")
+        size *= 4

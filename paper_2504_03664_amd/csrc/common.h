@@ -1,0 +1,82 @@
+// Shared host/device definitions of the pipelined-offloading decoder library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+
+#include "pipo.h"
+#include "pipo_ops.h"
+
+namespace pipo {
+
+// thread-local error text behind pipo_last_error()
+void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
+void clear_error();
+
+#define PIPO_HIP_TRY(call)                                                                  \
+  do {                                                                                      \
+    hipError_t e_ = (call);                                                                 \
+    if (e_ != hipSuccess) {                                                                 \
+      ::pipo::set_error("%s: %s (%s:%d)", #call, hipGetErrorString(e_), __FILE__, __LINE__); \
+      return PIPO_ERR_HIP;                                                                  \
+    }                                                                                       \
+  } while (0)
+
+#define PIPO_TRY(expr)             \
+  do {                             \
+    pipo_status s_ = (expr);       \
+    if (s_ != PIPO_OK) return s_;  \
+  } while (0)
+
+// GEMM epilogues (the first four are the public PIPO_EPI_* values)
+enum : int {
+  EPI_F16 = PIPO_EPI_F16,
+  EPI_RELU_F16 = PIPO_EPI_RELU_F16,
+  EPI_ADD_F32 = PIPO_EPI_ADD_F32,
+  EPI_F32 = PIPO_EPI_F32,
+  EPI_QKV = 4,  // q (scaled) to q_out, k and v rows into a position-major KV cache
+};
+
+struct GemmArgs {
+  const uint16_t* X = nullptr;    // [M][K] fp16
+  const uint16_t* W = nullptr;    // [N][K] fp16
+  const uint8_t* Wq = nullptr;    // [N][K/2] int4 codes
+  const uint16_t* Wsm = nullptr;  // [N][K/64][2] fp16 (scale, min)
+  const uint16_t* bias = nullptr; // [N] fp16 or null
+  int64_t M = 0, N = 0, K = 0;
+  uint16_t* out16 = nullptr;      // [M][ldo]
+  float* out32 = nullptr;         // [M][ldo]
+  int64_t ldo = 0;
+  // EPI_QKV: row m is sequence m / rows_per_seq at position pos0 + m % rows_per_seq
+  uint16_t* q_out = nullptr;      // [M][d]
+  uint16_t* k_out = nullptr;      // cache rows (p * batch + seq), [.][d]
+  uint16_t* v_out = nullptr;
+  int64_t d = 0;
+  float q_scale = 1.f;
+  int64_t rows_per_seq = 1, pos0 = 0, batch = 1;
+};
+
+// kernel launchers (gemm.hip, attention.hip, elementwise.hip)
+pipo_status launch_gemm(const GemmArgs& a, bool w4, int epi, hipStream_t st);
+pipo_status launch_layernorm(const float* x, const uint16_t* g, const uint16_t* b, uint16_t* y,
+                             int64_t rows, int64_t d, int64_t src_stride, int64_t src_offset,
+                             float eps, hipStream_t st);
+pipo_status launch_embed(const uint16_t* tok_rows, const int32_t* ids, const uint16_t* tok_table,
+                         const uint16_t* pos_table, float* x, int64_t rows, int64_t d,
+                         int64_t rows_per_seq, int64_t pos0, int64_t pos_offset, hipStream_t st);
+pipo_status launch_attn_decode(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                               uint16_t* o, int b, int n_heads, int head_dim, int t,
+                               hipStream_t st);
+pipo_status launch_attn_prefill(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                                uint16_t* o, int b, int P, int n_heads, int head_dim,
+                                hipStream_t st);
+pipo_status launch_argmax(const float* logits, int32_t* next, int64_t rows, int64_t V,
+                          hipStream_t st);
+pipo_status launch_fill_u16(uint16_t* p, uint16_t value, int64_t n, hipStream_t st);
+
+// largest key count the decode-attention kernel holds in LDS
+constexpr int kAttnDecodeMaxT = 8192;
+
+}  // namespace pipo

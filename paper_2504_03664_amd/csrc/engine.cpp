@@ -1,0 +1,1057 @@
+// Context, executor and C ABI of the pipelined-offloading decoder
+// (include/pipo.h).  The Scheduler emits each pass as a list of stream
+// operations; this file owns the memory the operations refer to and runs
+// them on HIP streams: hipMemcpyAsync on the copy streams (SDMA engines),
+// hipStreamWaitEvent / hipEventRecord for ordering, and the HIP kernels.
+//
+// Memory layout
+//   HBM  - weight slots: n_slots x slot_bytes; a layer unit holds its
+//          segments (packed small tensors, then each matrix, INT4 codes
+//          followed by their scale/min) at 4 KiB-aligned offsets;
+//        - resident layers (weights_on_host = 0): n_layers units back to back;
+//        - position table, final LayerNorm, token table (if resident);
+//        - activations for max_batch * max_seq rows: x fp32, LN output,
+//          q and attention output fp16, MLP hidden fp16, logits fp32;
+//        - KV cache [n_layers][K|V][max_seq][b][d] fp16 (resident) or
+//          n_slots KV buffers [K|V][max_seq][b][d] (KV in host memory).
+//   host - pinned: packed small tensors per layer, copies of matrices the
+//          caller did not place in pinned memory, embedding staging, token
+//          readback, KV cache [n_layers][K|V][max_seq][b][d] (KV on host).
+#include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <cmath>
+#include <cstdarg>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "common.h"
+#include "schedule.h"
+
+namespace pipo {
+
+// ---------------------------------------------------------------------------
+// errors
+static thread_local std::string g_err;
+
+void set_error(const char* fmt, ...) {
+  char buf[1024];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+}
+void clear_error() { g_err.clear(); }
+
+// ---------------------------------------------------------------------------
+// pinned host allocations made through pipo_host_alloc (base -> bytes), so a
+// caller pointer can be recognised as streamable in place
+static std::mutex g_pin_mu;
+static std::map<uintptr_t, size_t> g_pinned;
+
+static bool is_registered_pinned(const void* p, size_t bytes) {
+  std::lock_guard<std::mutex> lk(g_pin_mu);
+  const uintptr_t a = (uintptr_t)p;
+  auto it = g_pinned.upper_bound(a);
+  if (it == g_pinned.begin()) return false;
+  --it;
+  return a >= it->first && a + bytes <= it->first + it->second;
+}
+
+static void* host_alloc_pinned(size_t bytes) {
+  void* p = nullptr;
+  if (hipHostMalloc(&p, bytes, hipHostMallocDefault) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lk(g_pin_mu);
+  g_pinned[(uintptr_t)p] = bytes;
+  return p;
+}
+
+static void host_free_pinned(void* p) {
+  if (!p) return;
+  {
+    std::lock_guard<std::mutex> lk(g_pin_mu);
+    g_pinned.erase((uintptr_t)p);
+  }
+  (void)hipHostFree(p);
+}
+
+// host memcpy on several threads (large weight copies at create)
+static void par_memcpy(void* dst, const void* src, size_t n) {
+  const size_t kMin = 64u << 20;
+  unsigned nt = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+  if (n < kMin || nt == 1) {
+    std::memcpy(dst, src, n);
+    return;
+  }
+  std::vector<std::thread> th;
+  const size_t per = (n + nt - 1) / nt;
+  for (unsigned i = 0; i < nt; ++i) {
+    const size_t a = i * per, b = std::min(n, a + per);
+    if (a >= b) break;
+    th.emplace_back([=] { std::memcpy((char*)dst + a, (const char*)src + a, b - a); });
+  }
+  for (auto& t : th) t.join();
+}
+
+static inline int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+// ---------------------------------------------------------------------------
+static const char* kKernelNames[kNumKernels] = {"embed", "ln1",  "qkv",  "attn", "oproj", "ln2",
+                                                "fc1",   "fc2",  "lnf",  "head", "argmax"};
+
+struct TimedRec {
+  int cls;        // kernel class (kernel id * 2 + prefill), -1 for copies
+  int kind;       // 0 kernel, 1 h2d copy, 2 d2h copy, 3 window begin, 4 window end
+  hipEvent_t a, b;
+  double bytes, flops;
+};
+
+}  // namespace pipo
+
+using namespace pipo;
+
+struct pipo_ctx {
+  pipo_shape sh{};
+  pipo_policy pol{};
+  int64_t d = 0, F = 0, V = 0, L = 0, H = 0, dh = 0;
+  bool w4 = false;
+  int device = 0;
+  hipStream_t st[kNumStreams] = {};
+  std::vector<hipEvent_t> ev;
+  Scheduler* sched = nullptr;
+  SchedConfig scfg;
+  int64_t seg_off[kNumSegs] = {};
+  int64_t seg_bytes[kNumSegs] = {};
+  int64_t layer_bytes = 0, head_bytes = 0, slot_bytes = 0, misc_bytes = 0;
+
+  // host side
+  std::vector<std::vector<const void*>> layer_src;  // [L][seg] host pointer
+  const void* head_src = nullptr;
+  const uint16_t* tok_host = nullptr;               // for the host-side gather
+  std::vector<void*> pinned;                        // library-owned pinned buffers
+  int64_t pinned_bytes = 0;
+  uint16_t* emb_stage = nullptr;                    // [max_batch * max_seq][d]
+  int32_t* ids_stage = nullptr;                     // [max_batch * max_seq]
+  int32_t* next_stage = nullptr;                    // [max_batch]
+  uint16_t* kv_host = nullptr;
+
+  // device side
+  std::vector<void*> dev;
+  int64_t hbm_bytes = 0;
+  char* slots = nullptr;
+  char* resident = nullptr;
+  uint16_t* tok_dev = nullptr;
+  uint16_t* pos_dev = nullptr;
+  uint16_t* lnf_g = nullptr;
+  uint16_t* lnf_b = nullptr;
+  float* x = nullptr;
+  uint16_t* a = nullptr;
+  uint16_t* q = nullptr;
+  uint16_t* o = nullptr;
+  uint16_t* h = nullptr;
+  float* logits = nullptr;
+  int32_t* next_dev = nullptr;
+  int32_t* ids_dev = nullptr;
+  uint16_t* emb_dev = nullptr;
+  char* kv = nullptr;          // resident cache or KV slots
+  int64_t kv_part_bytes = 0;   // max_seq * max_batch * d * 2
+
+  // sequence state
+  int b = 0;
+  int64_t pos = 0;   // positions held per sequence
+  bool have_seq = false;
+
+  // pass being executed
+  PassInfo pass;
+  std::vector<Op> ops;
+
+  // statistics
+  pipo_stats stats{};
+  bool timestamps = false;
+  std::vector<hipEvent_t> tpool;
+  size_t tpool_used = 0;
+  std::vector<TimedRec> trec;
+  double kstat_ms[kNumKernels * 2] = {};
+  double kstat_bytes[kNumKernels * 2] = {};
+  double kstat_flops[kNumKernels * 2] = {};
+  int64_t kstat_n[kNumKernels * 2] = {};
+};
+
+namespace pipo {
+
+// ---------------------------------------------------------------------------
+static pipo_status dev_alloc(pipo_ctx* c, void** p, int64_t bytes) {
+  *p = nullptr;
+  if (bytes <= 0) return PIPO_OK;
+  if (c->pol.hbm_budget_bytes > 0 && c->hbm_bytes + bytes > c->pol.hbm_budget_bytes) {
+    set_error("HBM budget exceeded: %lld + %lld > %lld bytes", (long long)c->hbm_bytes,
+              (long long)bytes, (long long)c->pol.hbm_budget_bytes);
+    return PIPO_ERR_OOM_DEVICE;
+  }
+  if (hipMalloc(p, (size_t)bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    set_error("hipMalloc of %lld bytes failed", (long long)bytes);
+    return PIPO_ERR_OOM_DEVICE;
+  }
+  c->dev.push_back(*p);
+  c->hbm_bytes += bytes;
+  return PIPO_OK;
+}
+
+static pipo_status pin_alloc(pipo_ctx* c, void** p, int64_t bytes) {
+  *p = host_alloc_pinned((size_t)bytes);
+  if (!*p) {
+    set_error("pinned host allocation of %lld bytes failed", (long long)bytes);
+    return PIPO_ERR_OOM_HOST;
+  }
+  c->pinned.push_back(*p);
+  c->pinned_bytes += bytes;
+  return PIPO_OK;
+}
+
+static hipEvent_t tevent(pipo_ctx* c) {
+  if (c->tpool_used == c->tpool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    c->tpool.push_back(e);
+  }
+  return c->tpool[c->tpool_used++];
+}
+
+// ---------------------------------------------------------------------------
+// validation
+static pipo_status check_shape(const pipo_shape* s) {
+  if (!s) {
+    set_error("shape is NULL");
+    return PIPO_ERR_ARG;
+  }
+  if (s->n_layers < 1 || s->d_model < 1 || s->n_heads < 1 || s->d_ffn < 1 || s->vocab < 1 ||
+      s->max_pos < 1 || s->pos_offset < 0 || !(s->ln_eps >= 0.f)) {
+    set_error("invalid shape");
+    return PIPO_ERR_ARG;
+  }
+  if (s->d_model % s->n_heads != 0) {
+    set_error("d_model %d is not a multiple of n_heads %d", s->d_model, s->n_heads);
+    return PIPO_ERR_ARG;
+  }
+  const int dh = s->d_model / s->n_heads;
+  if (dh != 64 && dh != 128) {
+    set_error("head_dim %d not supported (64 or 128)", dh);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  if (s->d_model % 128 != 0 || s->d_ffn % 128 != 0 || s->d_model > 8192) {
+    set_error("d_model %d / d_ffn %d must be multiples of 128 (d_model <= 8192)", s->d_model,
+              s->d_ffn);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  return PIPO_OK;
+}
+
+// ---------------------------------------------------------------------------
+// kernels of one op
+static const uint16_t* misc_ptr(const char* base, const pipo_ctx* c) {
+  return reinterpret_cast<const uint16_t*>(base + c->seg_off[kSegMisc]);
+}
+
+static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
+  hipStream_t s = c->st[kCompute];
+  const PassInfo& p = c->pass;
+  const int64_t rows = (int64_t)c->b * p.T;
+  const int64_t d = c->d, F = c->F;
+  const int j = op.layer;
+  // weights of the unit
+  const char* base = nullptr;
+  if (op.kernel != kEmbed && op.kernel != kArgmax) {
+    if (op.unit >= 0) {
+      base = c->slots + (int64_t)op.slot * c->slot_bytes;
+    } else if (j >= 0) {
+      base = c->resident + (int64_t)j * c->layer_bytes;
+    } else {
+      base = reinterpret_cast<const char*>(c->tok_dev);
+    }
+  }
+  const uint16_t* misc = base ? misc_ptr(base, c) : nullptr;
+  // KV cache of layer j
+  uint16_t *kc = nullptr, *vc = nullptr;
+  if (j >= 0) {
+    char* kvb = c->pol.kv_on_host ? c->kv + (int64_t)op.slot * 2 * c->kv_part_bytes
+                                  : c->kv + (int64_t)j * 2 * c->kv_part_bytes;
+    kc = reinterpret_cast<uint16_t*>(kvb);
+    vc = reinterpret_cast<uint16_t*>(kvb + c->kv_part_bytes);
+  }
+  const auto gemm = [&](int seg, const uint16_t* X, const uint16_t* bias, int64_t M, int64_t N,
+                        int64_t K, int epi, GemmArgs& ga) {
+    ga.X = X;
+    ga.bias = bias;
+    ga.M = M;
+    ga.N = N;
+    ga.K = K;
+    if (c->w4) {
+      ga.Wq = reinterpret_cast<const uint8_t*>(base + c->seg_off[seg]);
+      ga.Wsm = reinterpret_cast<const uint16_t*>(base + c->seg_off[seg + 1]);
+    } else {
+      ga.W = reinterpret_cast<const uint16_t*>(base + c->seg_off[seg]);
+    }
+    return launch_gemm(ga, c->w4, epi, s);
+  };
+  switch (op.kernel) {
+    case kEmbed: {
+      if (c->pol.embed_on_host) {
+        PIPO_HIP_TRY(hipMemcpyAsync(c->emb_dev, c->emb_stage, (size_t)(rows * d * 2),
+                                    hipMemcpyHostToDevice, s));
+        c->stats.n_copies++;
+        return launch_embed(c->emb_dev, nullptr, nullptr, c->pos_dev, c->x, rows, d, p.T, p.pos0,
+                            c->sh.pos_offset, s);
+      }
+      PIPO_HIP_TRY(hipMemcpyAsync(c->ids_dev, c->ids_stage, (size_t)(rows * 4),
+                                  hipMemcpyHostToDevice, s));
+      c->stats.n_copies++;
+      return launch_embed(nullptr, c->ids_dev, c->tok_dev, c->pos_dev, c->x, rows, d, p.T, p.pos0,
+                          c->sh.pos_offset, s);
+    }
+    case kLn1:
+      return launch_layernorm(c->x, misc, misc + d, c->a, rows, d, 1, 0, c->sh.ln_eps, s);
+    case kQkv: {
+      GemmArgs ga;
+      ga.q_out = c->q;
+      ga.k_out = kc;
+      ga.v_out = vc;
+      ga.d = d;
+      ga.q_scale = 1.0f / std::sqrt((float)c->dh);
+      ga.rows_per_seq = p.T;
+      ga.pos0 = p.pos0;
+      ga.batch = c->b;
+      return gemm(kSegWqkv, c->a, misc + 2 * d, rows, 3 * d, d, EPI_QKV, ga);
+    }
+    case kAttn:
+      if (p.prefill)
+        return launch_attn_prefill(c->q, kc, vc, c->o, c->b, (int)p.T, (int)c->H, (int)c->dh, s);
+      return launch_attn_decode(c->q, kc, vc, c->o, c->b, (int)c->H, (int)c->dh, (int)p.pos0, s);
+    case kOproj: {
+      GemmArgs ga;
+      ga.out32 = c->x;
+      ga.ldo = d;
+      return gemm(kSegWo, c->o, misc + 5 * d, rows, d, d, EPI_ADD_F32, ga);
+    }
+    case kLn2:
+      return launch_layernorm(c->x, misc + 6 * d, misc + 7 * d, c->a, rows, d, 1, 0, c->sh.ln_eps,
+                              s);
+    case kFc1: {
+      GemmArgs ga;
+      ga.out16 = c->h;
+      ga.ldo = F;
+      return gemm(kSegW1, c->a, misc + 8 * d, rows, F, d, EPI_RELU_F16, ga);
+    }
+    case kFc2: {
+      GemmArgs ga;
+      ga.out32 = c->x;
+      ga.ldo = d;
+      return gemm(kSegW2, c->h, misc + 8 * d + F, rows, d, F, EPI_ADD_F32, ga);
+    }
+    case kLnf:
+      return launch_layernorm(c->x, c->lnf_g, c->lnf_b, c->a, c->b, d, p.T, p.T - 1, c->sh.ln_eps,
+                              s);
+    case kHead: {
+      GemmArgs ga;
+      ga.X = c->a;
+      ga.W = reinterpret_cast<const uint16_t*>(base);  // slot offset 0, or the resident table
+      ga.M = c->b;
+      ga.N = c->V;
+      ga.K = d;
+      ga.out32 = c->logits;
+      ga.ldo = c->V;
+      return launch_gemm(ga, false, EPI_F32, s);
+    }
+    case kArgmax:
+      return launch_argmax(c->logits, c->next_dev, c->b, c->V, s);
+    default:
+      set_error("unknown kernel %d", op.kernel);
+      return PIPO_ERR_ARG;
+  }
+}
+
+// algorithmic bytes and flops of a kernel op (for the per-kernel roofline)
+static void kernel_cost(const pipo_ctx* c, const Op& op, double* bytes, double* flops) {
+  const PassInfo& p = c->pass;
+  const double rows = (double)c->b * p.T, d = (double)c->d, F = (double)c->F, V = (double)c->V;
+  const auto wbytes = [&](double N, double K) { return c->w4 ? N * K / 2 + N * K / 16 : N * K * 2; };
+  const auto g = [&](double M, double N, double K, double out_bytes, double wb) {
+    *bytes = wb + M * K * 2 + M * N * out_bytes + N * 2;
+    *flops = 2 * M * N * K;
+  };
+  *bytes = 0;
+  *flops = 0;
+  switch (op.kernel) {
+    case kQkv: g(rows, 3 * d, d, 2, wbytes(3 * d, d)); break;
+    case kOproj: g(rows, d, d, 8, wbytes(d, d)); break;
+    case kFc1: g(rows, F, d, 2, wbytes(F, d)); break;
+    case kFc2: g(rows, d, F, 8, wbytes(d, F)); break;
+    case kHead: g(c->b, V, d, 4, V * d * 2); break;
+    case kLn1:
+    case kLn2: *bytes = rows * d * 6 + d * 4; *flops = rows * d * 8; break;
+    case kLnf: *bytes = c->b * d * 6 + d * 4; *flops = c->b * d * 8; break;
+    case kAttn:
+      if (p.prefill) {
+        *bytes = 4 * rows * d * 2;
+        *flops = 4.0 * c->b * p.T * (p.T + 1) / 2 * d;
+      } else {
+        *bytes = 2.0 * c->b * (p.pos0 + 1) * d * 2 + 2 * rows * d * 2;
+        *flops = 4.0 * c->b * (p.pos0 + 1) * d;
+      }
+      break;
+    case kEmbed: *bytes = rows * d * 8; break;
+    case kArgmax: *bytes = c->b * V * 4; break;
+    default: break;
+  }
+}
+
+static void delay_cb(void* arg) {
+  const int64_t us = (int64_t)(intptr_t)arg;
+  std::this_thread::sleep_for(std::chrono::microseconds(us));
+}
+
+static pipo_status exec_op(pipo_ctx* c, const Op& op) {
+  hipStream_t s = c->st[op.stream];
+  switch (op.kind) {
+    case OpKind::Wait:
+      PIPO_HIP_TRY(hipStreamWaitEvent(s, c->ev[op.event], 0));
+      return PIPO_OK;
+    case OpKind::Record:
+      PIPO_HIP_TRY(hipEventRecord(c->ev[op.event], s));
+      return PIPO_OK;
+    case OpKind::Delay:
+      PIPO_HIP_TRY(hipLaunchHostFunc(s, delay_cb, (void*)(intptr_t)c->pol.copy_delay_us));
+      return PIPO_OK;
+    case OpKind::Poison: {
+      if (op.kv)
+        return launch_fill_u16(reinterpret_cast<uint16_t*>(c->kv + (int64_t)op.slot * 2 * c->kv_part_bytes),
+                               0x7E00, c->kv_part_bytes, s);
+      return launch_fill_u16(reinterpret_cast<uint16_t*>(c->slots + (int64_t)op.slot * c->slot_bytes),
+                             0x7E00, c->slot_bytes / 2, s);
+    }
+    case OpKind::CopyH2D:
+    case OpKind::CopyD2H: {
+      void* dst;
+      const void* src;
+      const bool h2d = op.kind == OpKind::CopyH2D;
+      if (op.kv) {
+        // host cache [layer][K|V][max_seq][b][d] for the current batch b
+        const int64_t host_off = ((int64_t)op.layer * 2 + op.seg) * c->pol.max_seq * c->b * c->d * 2;
+        char* hptr = reinterpret_cast<char*>(c->kv_host) + host_off + op.off;
+        char* dptr = c->kv + (int64_t)op.slot * 2 * c->kv_part_bytes + op.seg * c->kv_part_bytes + op.off;
+        dst = h2d ? (void*)dptr : (void*)hptr;
+        src = h2d ? (const void*)hptr : (const void*)dptr;
+      } else {
+        const char* hbase = reinterpret_cast<const char*>(
+            op.layer >= 0 ? c->layer_src[op.layer][op.seg] : c->head_src);
+        src = hbase + op.off;
+        dst = c->slots + (int64_t)op.slot * c->slot_bytes +
+              (op.layer >= 0 ? c->seg_off[op.seg] : 0) + op.off;
+      }
+      hipEvent_t e0 = nullptr, e1 = nullptr;
+      if (c->timestamps) {
+        e0 = tevent(c);
+        e1 = tevent(c);
+        PIPO_HIP_TRY(hipEventRecord(e0, s));
+      }
+      PIPO_HIP_TRY(hipMemcpyAsync(dst, src, (size_t)op.bytes,
+                                  h2d ? hipMemcpyHostToDevice : hipMemcpyDeviceToHost, s));
+      if (c->timestamps) {
+        PIPO_HIP_TRY(hipEventRecord(e1, s));
+        c->trec.push_back(TimedRec{-1, h2d ? 1 : 2, e0, e1, (double)op.bytes, 0});
+      }
+      c->stats.n_copies++;
+      if (h2d) {
+        c->stats.h2d_bytes += op.bytes;
+        (op.kv ? c->stats.h2d_kv_bytes : c->stats.h2d_weight_bytes) += op.bytes;
+      } else {
+        c->stats.d2h_bytes += op.bytes;
+      }
+      return PIPO_OK;
+    }
+    case OpKind::Kernel: {
+      hipEvent_t e0 = nullptr, e1 = nullptr;
+      if (c->timestamps) {
+        e0 = tevent(c);
+        e1 = tevent(c);
+        PIPO_HIP_TRY(hipEventRecord(e0, s));
+      }
+      PIPO_TRY(run_kernel(c, op));
+      c->stats.n_kernels++;
+      if (c->timestamps) {
+        PIPO_HIP_TRY(hipEventRecord(e1, s));
+        double by, fl;
+        kernel_cost(c, op, &by, &fl);
+        c->trec.push_back(TimedRec{op.kernel * 2 + (c->pass.prefill ? 1 : 0), 0, e0, e1, by, fl});
+      }
+      return PIPO_OK;
+    }
+    case OpKind::Readback: {
+      PIPO_HIP_TRY(hipMemcpyAsync(c->next_stage, c->next_dev, (size_t)c->b * 4,
+                                  hipMemcpyDeviceToHost, s));
+      c->stats.d2h_bytes += (int64_t)c->b * 4;
+      c->stats.n_copies++;
+      return PIPO_OK;
+    }
+  }
+  set_error("unknown op kind");
+  return PIPO_ERR_ARG;
+}
+
+static pipo_status run_pass(pipo_ctx* c, float* logits_out, int32_t* next_out, bool decode) {
+  c->ops.clear();
+  c->sched->pass(c->pass, c->ops);
+  hipEvent_t w0 = nullptr, w1 = nullptr;
+  if (c->timestamps && decode) {
+    w0 = tevent(c);
+    PIPO_HIP_TRY(hipEventRecord(w0, c->st[kCompute]));
+  }
+  for (const Op& op : c->ops) PIPO_TRY(exec_op(c, op));
+  if (c->timestamps && decode) {
+    w1 = tevent(c);
+    PIPO_HIP_TRY(hipEventRecord(w1, c->st[kCompute]));
+    c->trec.push_back(TimedRec{-1, 3, w0, w1, 0, 0});
+  }
+  PIPO_HIP_TRY(hipStreamSynchronize(c->st[kCompute]));
+  std::memcpy(next_out, c->next_stage, (size_t)c->b * 4);
+  if (logits_out) {
+    PIPO_HIP_TRY(hipMemcpy(logits_out, c->logits, (size_t)c->b * c->V * 4, hipMemcpyDeviceToHost));
+    c->stats.d2h_bytes += (int64_t)c->b * c->V * 4;
+  }
+  return PIPO_OK;
+}
+
+// ---------------------------------------------------------------------------
+static void destroy_ctx(pipo_ctx* c) {
+  if (!c) return;
+  (void)hipSetDevice(c->device);
+  for (int i = 0; i < kNumStreams; ++i)
+    if (c->st[i]) (void)hipStreamSynchronize(c->st[i]);
+  for (auto e : c->ev) (void)hipEventDestroy(e);
+  for (auto e : c->tpool) (void)hipEventDestroy(e);
+  for (int i = 0; i < kNumStreams; ++i)
+    if (c->st[i]) (void)hipStreamDestroy(c->st[i]);
+  for (void* p : c->dev) (void)hipFree(p);
+  for (void* p : c->pinned) host_free_pinned(p);
+  delete c->sched;
+  delete c;
+}
+
+static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* w,
+                              const pipo_policy* policy, pipo_ctx* c) {
+  PIPO_TRY(check_shape(shape));
+  if (!w || !policy || !w->tok_emb || !w->pos_emb || !w->lnf_g || !w->lnf_b || !w->layers) {
+    set_error("weights or policy incomplete");
+    return PIPO_ERR_ARG;
+  }
+  c->sh = *shape;
+  c->pol = *policy;
+  pipo_policy& pol = c->pol;
+  if (pol.wfmt != PIPO_W_FP16 && pol.wfmt != PIPO_W_INT4_G64) {
+    set_error("unknown weight format %d", pol.wfmt);
+    return PIPO_ERR_ARG;
+  }
+  if (pol.n_weight_slots == 0) pol.n_weight_slots = 3;
+  if (pol.n_h2d_streams == 0) pol.n_h2d_streams = 1;
+  if (pol.chunk_bytes == 0) pol.chunk_bytes = 64ll << 20;
+  pol.chunk_bytes = align_up(pol.chunk_bytes, 4096);
+  if (pol.n_weight_slots < 2 || pol.n_weight_slots > 16 || pol.n_h2d_streams < 1 ||
+      pol.n_h2d_streams > 2 || pol.max_batch < 1 || pol.max_seq < 1 || pol.chunk_bytes < 0 ||
+      pol.copy_delay_us < 0) {
+    set_error("invalid policy");
+    return PIPO_ERR_ARG;
+  }
+  if (pol.max_seq > shape->max_pos || pol.max_seq > kAttnDecodeMaxT) {
+    set_error("max_seq %d exceeds max_pos %d or the decode kernel's %d keys", pol.max_seq,
+              shape->max_pos, kAttnDecodeMaxT);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  if (pol.kv_on_host && !pol.weights_on_host) {
+    set_error("kv_on_host requires weights_on_host");
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  c->w4 = pol.wfmt == PIPO_W_INT4_G64;
+  c->d = shape->d_model;
+  c->F = shape->d_ffn;
+  c->V = shape->vocab;
+  c->L = shape->n_layers;
+  c->H = shape->n_heads;
+  c->dh = c->d / c->H;
+  c->timestamps = (pol.debug_flags & PIPO_DBG_TIMESTAMPS) != 0;
+  PIPO_HIP_TRY(hipGetDevice(&c->device));
+  const int64_t d = c->d, F = c->F, V = c->V, L = c->L;
+
+  // unit layout
+  c->misc_bytes = (9 * d + F) * 2;
+  const auto mat = [&](int seg, int64_t N, int64_t K) {
+    if (c->w4) {
+      c->seg_bytes[seg] = N * K / 2;
+      c->seg_bytes[seg + 1] = N * (K / 64) * 4;
+    } else {
+      c->seg_bytes[seg] = N * K * 2;
+    }
+  };
+  c->seg_bytes[kSegMisc] = c->misc_bytes;
+  mat(kSegWqkv, 3 * d, d);
+  mat(kSegWo, d, d);
+  mat(kSegW1, F, d);
+  mat(kSegW2, d, F);
+  int64_t off = 0;
+  for (int sg = 0; sg < kNumSegs; ++sg) {
+    if (sg == kSegHead) continue;
+    c->seg_off[sg] = off;
+    off = align_up(off + c->seg_bytes[sg], 4096);
+  }
+  c->layer_bytes = off;
+  c->head_bytes = V * d * 2;
+  c->slot_bytes = 0;
+  if (pol.weights_on_host) c->slot_bytes = c->layer_bytes;
+  if (pol.embed_on_host) c->slot_bytes = std::max(c->slot_bytes, align_up(c->head_bytes, 4096));
+
+  // host sources: small tensors packed per layer; matrices in place when
+  // they sit in pipo_host_alloc memory, else copied into a merged pinned
+  // region per layer (data merging, Section 3.3)
+  const bool need_host = pol.weights_on_host != 0;
+  c->layer_src.assign((size_t)L, std::vector<const void*>(kNumSegs, nullptr));
+  void* misc_all = nullptr;
+  PIPO_TRY(pin_alloc(c, &misc_all, L * c->misc_bytes));
+  for (int64_t j = 0; j < L; ++j) {
+    const pipo_layer_host& lw = w->layers[j];
+    const uint16_t* small[8] = {lw.ln1_g, lw.ln1_b, lw.bqkv, lw.bo, lw.ln2_g, lw.ln2_b, lw.b1, lw.b2};
+    const int64_t cnt[8] = {d, d, 3 * d, d, d, d, F, d};
+    char* dst = (char*)misc_all + j * c->misc_bytes;
+    for (int i = 0; i < 8; ++i) {
+      if (!small[i]) {
+        set_error("layer %lld: small tensor %d is NULL", (long long)j, i);
+        return PIPO_ERR_ARG;
+      }
+      std::memcpy(dst, small[i], (size_t)cnt[i] * 2);
+      dst += cnt[i] * 2;
+    }
+    c->layer_src[j][kSegMisc] = (char*)misc_all + j * c->misc_bytes;
+    const void* mats[8];
+    if (c->w4) {
+      const pipo_q4* q4[4] = {&lw.qqkv, &lw.qo, &lw.q1, &lw.q2};
+      for (int i = 0; i < 4; ++i) {
+        mats[2 * i] = q4[i]->q;
+        mats[2 * i + 1] = q4[i]->scale_min;
+      }
+    } else {
+      const uint16_t* m16[4] = {lw.wqkv, lw.wo, lw.w1, lw.w2};
+      for (int i = 0; i < 4; ++i) {
+        mats[2 * i] = m16[i];
+        mats[2 * i + 1] = nullptr;
+      }
+    }
+    int64_t copy_bytes = 0;
+    for (int i = 0; i < 8; ++i) {
+      const int sg = kSegWqkv + i;
+      if (c->seg_bytes[sg] == 0) continue;
+      if (!mats[i]) {
+        set_error("layer %lld: matrix segment %d is NULL", (long long)j, sg);
+        return PIPO_ERR_ARG;
+      }
+      c->layer_src[j][sg] = mats[i];
+      if (need_host && !is_registered_pinned(mats[i], (size_t)c->seg_bytes[sg]))
+        copy_bytes = align_up(copy_bytes + c->seg_bytes[sg], 4096);
+    }
+    if (copy_bytes > 0) {
+      void* merged = nullptr;
+      PIPO_TRY(pin_alloc(c, &merged, copy_bytes));
+      int64_t o2 = 0;
+      for (int i = 0; i < 8; ++i) {
+        const int sg = kSegWqkv + i;
+        if (c->seg_bytes[sg] == 0 || is_registered_pinned(mats[i], (size_t)c->seg_bytes[sg]))
+          continue;
+        par_memcpy((char*)merged + o2, mats[i], (size_t)c->seg_bytes[sg]);
+        c->layer_src[j][sg] = (char*)merged + o2;
+        o2 = align_up(o2 + c->seg_bytes[sg], 4096);
+      }
+    }
+  }
+  c->tok_host = w->tok_emb;
+  c->head_src = w->tok_emb;
+  if (pol.embed_on_host && !is_registered_pinned(w->tok_emb, (size_t)c->head_bytes)) {
+    void* t = nullptr;
+    PIPO_TRY(pin_alloc(c, &t, c->head_bytes));
+    par_memcpy(t, w->tok_emb, (size_t)c->head_bytes);
+    c->head_src = t;
+  }
+
+  // streams (default priority) and ordering events
+  for (int i = 0; i < kNumStreams; ++i) PIPO_HIP_TRY(hipStreamCreateWithFlags(&c->st[i], hipStreamNonBlocking));
+  c->scfg.n_layers = (int)L;
+  c->scfg.n_slots = pol.n_weight_slots;
+  c->scfg.n_h2d = pol.n_h2d_streams;
+  c->scfg.layers_streamed = pol.weights_on_host != 0;
+  c->scfg.head_streamed = pol.embed_on_host != 0;
+  c->scfg.kv_on_host = pol.kv_on_host != 0;
+  c->scfg.chunk_bytes = pol.chunk_bytes;
+  for (int sg = 0; sg < kNumSegs; ++sg) c->scfg.layer_seg_bytes[sg] = c->seg_bytes[sg];
+  c->scfg.layer_seg_bytes[kSegHead] = 0;
+  c->scfg.head_bytes = c->head_bytes;
+  c->scfg.poison = (pol.debug_flags & PIPO_DBG_POISON_SLOTS) != 0;
+  c->scfg.delay = (pol.debug_flags & PIPO_DBG_COPY_DELAY) != 0;
+  c->sched = new Scheduler(c->scfg);
+  c->ev.resize((size_t)c->sched->events().count(), nullptr);
+  for (auto& e : c->ev) PIPO_HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+
+  // HBM
+  const int64_t rows = (int64_t)pol.max_batch * pol.max_seq;
+  void* p = nullptr;
+  if (c->slot_bytes > 0) {
+    PIPO_TRY(dev_alloc(c, &p, c->slot_bytes * pol.n_weight_slots));
+    c->slots = (char*)p;
+  }
+  if (!pol.weights_on_host) {
+    PIPO_TRY(dev_alloc(c, &p, c->layer_bytes * L));
+    c->resident = (char*)p;
+    for (int64_t j = 0; j < L; ++j)
+      for (int sg = 0; sg < kNumSegs; ++sg)
+        if (c->seg_bytes[sg] > 0 && sg != kSegHead)
+          PIPO_HIP_TRY(hipMemcpy(c->resident + j * c->layer_bytes + c->seg_off[sg],
+                                 c->layer_src[j][sg], (size_t)c->seg_bytes[sg],
+                                 hipMemcpyHostToDevice));
+  }
+  if (!pol.embed_on_host) {
+    PIPO_TRY(dev_alloc(c, &p, c->head_bytes));
+    c->tok_dev = (uint16_t*)p;
+    PIPO_HIP_TRY(hipMemcpy(c->tok_dev, w->tok_emb, (size_t)c->head_bytes, hipMemcpyHostToDevice));
+  }
+  const int64_t pos_bytes = ((int64_t)shape->max_pos + shape->pos_offset) * d * 2;
+  PIPO_TRY(dev_alloc(c, &p, pos_bytes));
+  c->pos_dev = (uint16_t*)p;
+  PIPO_HIP_TRY(hipMemcpy(c->pos_dev, w->pos_emb, (size_t)pos_bytes, hipMemcpyHostToDevice));
+  PIPO_TRY(dev_alloc(c, &p, d * 4));
+  c->lnf_g = (uint16_t*)p;
+  c->lnf_b = c->lnf_g + d;
+  PIPO_HIP_TRY(hipMemcpy(c->lnf_g, w->lnf_g, (size_t)d * 2, hipMemcpyHostToDevice));
+  PIPO_HIP_TRY(hipMemcpy(c->lnf_b, w->lnf_b, (size_t)d * 2, hipMemcpyHostToDevice));
+  PIPO_TRY(dev_alloc(c, &p, rows * d * 4));
+  c->x = (float*)p;
+  PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+  c->a = (uint16_t*)p;
+  PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+  c->q = (uint16_t*)p;
+  PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+  c->o = (uint16_t*)p;
+  PIPO_TRY(dev_alloc(c, &p, rows * F * 2));
+  c->h = (uint16_t*)p;
+  PIPO_TRY(dev_alloc(c, &p, (int64_t)pol.max_batch * V * 4));
+  c->logits = (float*)p;
+  PIPO_TRY(dev_alloc(c, &p, (int64_t)pol.max_batch * 4));
+  c->next_dev = (int32_t*)p;
+  PIPO_TRY(dev_alloc(c, &p, rows * 4));
+  c->ids_dev = (int32_t*)p;
+  if (pol.embed_on_host) {
+    PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+    c->emb_dev = (uint16_t*)p;
+  }
+  c->kv_part_bytes = rows * d * 2;
+  const int64_t kv_units = pol.kv_on_host ? pol.n_weight_slots : L;
+  PIPO_TRY(dev_alloc(c, &p, kv_units * 2 * c->kv_part_bytes));
+  c->kv = (char*)p;
+
+  // pinned staging
+  if (pol.embed_on_host) {
+    PIPO_TRY(pin_alloc(c, &p, rows * d * 2));
+    c->emb_stage = (uint16_t*)p;
+  }
+  PIPO_TRY(pin_alloc(c, &p, rows * 4));
+  c->ids_stage = (int32_t*)p;
+  PIPO_TRY(pin_alloc(c, &p, (int64_t)pol.max_batch * 4));
+  c->next_stage = (int32_t*)p;
+  if (pol.kv_on_host) {
+    PIPO_TRY(pin_alloc(c, &p, L * 2 * c->kv_part_bytes));
+    c->kv_host = (uint16_t*)p;
+  }
+  c->stats.hbm_bytes = c->hbm_bytes;
+  c->stats.pinned_host_bytes = c->pinned_bytes;
+  return PIPO_OK;
+}
+
+static pipo_status stage_tokens(pipo_ctx* c, const int32_t* tokens, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) {
+    if (tokens[i] < 0 || tokens[i] >= c->sh.vocab) {
+      set_error("token id %d at %lld outside [0, %d)", tokens[i], (long long)i, c->sh.vocab);
+      return PIPO_ERR_ARG;
+    }
+  }
+  if (c->pol.embed_on_host) {
+    const int64_t d = c->d;
+    for (int64_t i = 0; i < n; ++i)
+      std::memcpy(c->emb_stage + i * d, c->tok_host + (int64_t)tokens[i] * d, (size_t)d * 2);
+  } else {
+    std::memcpy(c->ids_stage, tokens, (size_t)n * 4);
+  }
+  return PIPO_OK;
+}
+
+// union of [a, b) intervals clipped to [lo, hi)
+static double interval_union(std::vector<std::pair<double, double>>& iv, double lo, double hi) {
+  std::sort(iv.begin(), iv.end());
+  double total = 0, cur_a = 0, cur_b = -1e300;
+  bool open = false;
+  for (auto& [a0, b0] : iv) {
+    const double a = std::max(a0, lo), b = std::min(b0, hi);
+    if (b <= a) continue;
+    if (!open || a > cur_b) {
+      if (open) total += cur_b - cur_a;
+      cur_a = a;
+      cur_b = b;
+      open = true;
+    } else {
+      cur_b = std::max(cur_b, b);
+    }
+  }
+  if (open) total += cur_b - cur_a;
+  return total;
+}
+
+static pipo_status resolve_timeline(pipo_ctx* c) {
+  if (!c->timestamps || c->trec.empty()) return PIPO_OK;
+  for (int i = 0; i < kNumStreams; ++i) PIPO_HIP_TRY(hipStreamSynchronize(c->st[i]));
+  hipEvent_t ref = c->trec.front().a;
+  const auto t = [&](hipEvent_t e, double* ms) -> pipo_status {
+    float v = 0;
+    PIPO_HIP_TRY(hipEventElapsedTime(&v, ref, e));
+    *ms = v;
+    return PIPO_OK;
+  };
+  double lo = 1e300, hi = -1e300;
+  std::vector<std::pair<double, double>> copies, kernels, all;
+  for (const TimedRec& r : c->trec) {
+    double a, b;
+    PIPO_TRY(t(r.a, &a));
+    PIPO_TRY(t(r.b, &b));
+    if (r.kind == 3) {
+      lo = std::min(lo, a);
+      hi = std::max(hi, b);
+    } else if (r.kind == 0) {
+      kernels.push_back({a, b});
+      all.push_back({a, b});
+      c->kstat_n[r.cls]++;
+      c->kstat_ms[r.cls] += b - a;
+      c->kstat_bytes[r.cls] += r.bytes;
+      c->kstat_flops[r.cls] += r.flops;
+    } else {
+      if (r.kind == 1) copies.push_back({a, b});
+      all.push_back({a, b});
+    }
+  }
+  if (hi > lo) {
+    c->stats.window_ms += hi - lo;
+    c->stats.copy_busy_ms += interval_union(copies, lo, hi);
+    c->stats.kernel_busy_ms += interval_union(kernels, lo, hi);
+    c->stats.busy_ms += interval_union(all, lo, hi);
+  }
+  c->trec.clear();
+  c->tpool_used = 0;
+  return PIPO_OK;
+}
+
+}  // namespace pipo
+
+// ---------------------------------------------------------------------------
+// C ABI
+extern "C" {
+
+const char* pipo_last_error(void) { return pipo::g_err.c_str(); }
+
+void* pipo_host_alloc(size_t bytes) { return pipo::host_alloc_pinned(bytes); }
+void pipo_host_free(void* p) { pipo::host_free_pinned(p); }
+
+pipo_status pipo_create(const pipo_shape* shape, const pipo_host_weights* weights,
+                        const pipo_policy* policy, pipo_ctx** out) {
+  clear_error();
+  if (!out) {
+    set_error("out is NULL");
+    return PIPO_ERR_ARG;
+  }
+  *out = nullptr;
+  pipo_ctx* c = new pipo_ctx();
+  const pipo_status s = create_ctx(shape, weights, policy, c);
+  if (s != PIPO_OK) {
+    destroy_ctx(c);
+    return s;
+  }
+  *out = c;
+  return PIPO_OK;
+}
+
+void pipo_destroy(pipo_ctx* c) { destroy_ctx(c); }
+
+pipo_status pipo_prefill(pipo_ctx* c, const int32_t* tokens, int32_t b, int32_t P,
+                         float* logits_out, int32_t* next_out) {
+  clear_error();
+  if (!c || !tokens || !next_out) {
+    set_error("NULL argument");
+    return PIPO_ERR_ARG;
+  }
+  if (b < 1 || b > c->pol.max_batch || P < 1 || P > c->pol.max_seq) {
+    set_error("prefill b=%d P=%d outside max_batch=%d max_seq=%d", b, P, c->pol.max_batch,
+              c->pol.max_seq);
+    return PIPO_ERR_ARG;
+  }
+  PIPO_HIP_TRY(hipSetDevice(c->device));
+  const auto t0 = std::chrono::steady_clock::now();
+  c->have_seq = false;
+  c->b = b;
+  // tokens[b][P] -> row i * P + p, the order the kernels use
+  PIPO_TRY(stage_tokens(c, tokens, (int64_t)b * P));
+  c->pass = PassInfo{true, 0, P, (int64_t)b * c->d * 2};
+  PIPO_TRY(run_pass(c, logits_out, next_out, false));
+  c->pos = P;
+  c->have_seq = true;
+  c->stats.prefill_wall_ms =
+      std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+  return PIPO_OK;
+}
+
+pipo_status pipo_decode_step(pipo_ctx* c, const int32_t* tokens, float* logits_out,
+                             int32_t* next_out) {
+  clear_error();
+  if (!c || !tokens || !next_out) {
+    set_error("NULL argument");
+    return PIPO_ERR_ARG;
+  }
+  if (!c->have_seq) {
+    set_error("decode before prefill");
+    return PIPO_ERR_STATE;
+  }
+  if (c->pos >= c->pol.max_seq) {
+    set_error("sequences already hold max_seq=%d positions", c->pol.max_seq);
+    return PIPO_ERR_STATE;
+  }
+  PIPO_HIP_TRY(hipSetDevice(c->device));
+  const auto t0 = std::chrono::steady_clock::now();
+  PIPO_TRY(stage_tokens(c, tokens, c->b));
+  c->pass = PassInfo{false, c->pos, 1, (int64_t)c->b * c->d * 2};
+  PIPO_TRY(run_pass(c, logits_out, next_out, true));
+  c->pos += 1;
+  c->stats.decode_steps++;
+  c->stats.decode_wall_ms +=
+      std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+  return PIPO_OK;
+}
+
+pipo_status pipo_get_stats(pipo_ctx* c, pipo_stats* out) {
+  clear_error();
+  if (!c || !out) {
+    set_error("NULL argument");
+    return PIPO_ERR_ARG;
+  }
+  PIPO_HIP_TRY(hipSetDevice(c->device));
+  PIPO_TRY(resolve_timeline(c));
+  *out = c->stats;
+  int n = 0;
+  for (int k = 0; k < kNumKernels * 2 && n < PIPO_MAX_KERNEL_STATS; ++k) {
+    if (c->kstat_n[k] == 0) continue;
+    pipo_kernel_stat& ks = out->kernels[n++];
+    std::snprintf(ks.name, sizeof ks.name, "%s_%s", kKernelNames[k / 2],
+                  (k & 1) ? "prefill" : "decode");
+    ks.launches = c->kstat_n[k];
+    ks.total_ms = c->kstat_ms[k];
+    ks.alg_bytes = c->kstat_bytes[k];
+    ks.alg_flops = c->kstat_flops[k];
+  }
+  out->n_kernel_stats = n;
+  return PIPO_OK;
+}
+
+pipo_status pipo_reset_stats(pipo_ctx* c) {
+  clear_error();
+  if (!c) {
+    set_error("NULL argument");
+    return PIPO_ERR_ARG;
+  }
+  PIPO_HIP_TRY(hipSetDevice(c->device));
+  for (int i = 0; i < kNumStreams; ++i) PIPO_HIP_TRY(hipStreamSynchronize(c->st[i]));
+  c->trec.clear();
+  c->tpool_used = 0;
+  const int64_t hbm = c->stats.hbm_bytes, pin = c->stats.pinned_host_bytes;
+  c->stats = pipo_stats{};
+  c->stats.hbm_bytes = hbm;
+  c->stats.pinned_host_bytes = pin;
+  for (int k = 0; k < kNumKernels * 2; ++k) {
+    c->kstat_n[k] = 0;
+    c->kstat_ms[k] = c->kstat_bytes[k] = c->kstat_flops[k] = 0;
+  }
+  return PIPO_OK;
+}
+
+pipo_status pipo_measure_h2d_peak(int64_t bytes, int32_t iters, int32_t n_streams, double* gbps) {
+  clear_error();
+  if (bytes <= 0 || iters < 1 || n_streams < 1 || n_streams > 2 || !gbps) {
+    set_error("invalid arguments");
+    return PIPO_ERR_ARG;
+  }
+  void* h = pipo::host_alloc_pinned((size_t)bytes);
+  if (!h) {
+    set_error("pinned allocation of %lld bytes failed", (long long)bytes);
+    return PIPO_ERR_OOM_HOST;
+  }
+  std::memset(h, 1, (size_t)bytes);
+  void* dptr = nullptr;
+  if (hipMalloc(&dptr, (size_t)bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    pipo::host_free_pinned(h);
+    set_error("hipMalloc of %lld bytes failed", (long long)bytes);
+    return PIPO_ERR_OOM_DEVICE;
+  }
+  hipStream_t st[2] = {};
+  hipEvent_t e0, e1, ej;
+  pipo_status status = PIPO_OK;
+  double best = 0;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess ||
+      hipEventCreateWithFlags(&ej, hipEventDisableTiming) != hipSuccess) {
+    set_error("hipEventCreate failed");
+    status = PIPO_ERR_HIP;
+  }
+  for (int i = 0; i < n_streams && status == PIPO_OK; ++i)
+    if (hipStreamCreateWithFlags(&st[i], hipStreamNonBlocking) != hipSuccess) status = PIPO_ERR_HIP;
+  const int64_t half = pipo::align_up(bytes / n_streams, 4096);
+  for (int it = 0; it <= iters && status == PIPO_OK; ++it) {  // first round warms up
+    bool ok = hipEventRecord(e0, st[0]) == hipSuccess;
+    if (n_streams == 2) ok = ok && hipStreamWaitEvent(st[1], e0, 0) == hipSuccess;
+    for (int i = 0; i < n_streams && ok; ++i) {
+      const int64_t a = i * half, n = std::min(bytes, a + half) - a;
+      if (n > 0)
+        ok = hipMemcpyAsync((char*)dptr + a, (char*)h + a, (size_t)n, hipMemcpyHostToDevice,
+                            st[i]) == hipSuccess;
+    }
+    if (n_streams == 2) {
+      ok = ok && hipEventRecord(ej, st[1]) == hipSuccess &&
+           hipStreamWaitEvent(st[0], ej, 0) == hipSuccess;
+    }
+    ok = ok && hipEventRecord(e1, st[0]) == hipSuccess && hipEventSynchronize(e1) == hipSuccess;
+    float ms = 0;
+    ok = ok && hipEventElapsedTime(&ms, e0, e1) == hipSuccess;
+    if (!ok) {
+      set_error("h2d probe: HIP call failed");
+      status = PIPO_ERR_HIP;
+      break;
+    }
+    if (it > 0 && ms > 0) best = std::max(best, (double)bytes / (ms * 1e-3) / 1e9);
+  }
+  for (int i = 0; i < 2; ++i)
+    if (st[i]) (void)hipStreamDestroy(st[i]);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  (void)hipEventDestroy(ej);
+  (void)hipFree(dptr);
+  pipo::host_free_pinned(h);
+  *gbps = best;
+  return status;
+}
+
+}  // extern "C"

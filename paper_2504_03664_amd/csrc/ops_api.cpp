@@ -1,0 +1,137 @@
+// C ABI of the individual operations (include/pipo_ops.h).
+#include "common.h"
+
+using namespace pipo;
+
+extern "C" {
+
+pipo_status pipo_dev_alloc(size_t bytes, void** out) {
+  clear_error();
+  if (!out) {
+    set_error("out is NULL");
+    return PIPO_ERR_ARG;
+  }
+  *out = nullptr;
+  if (bytes == 0) return PIPO_OK;
+  if (hipMalloc(out, bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    *out = nullptr;
+    set_error("hipMalloc of %zu bytes failed", bytes);
+    return PIPO_ERR_OOM_DEVICE;
+  }
+  return PIPO_OK;
+}
+
+pipo_status pipo_dev_free(void* p) {
+  clear_error();
+  if (p) PIPO_HIP_TRY(hipFree(p));
+  return PIPO_OK;
+}
+
+pipo_status pipo_copy_h2d(void* dst, const void* src, size_t bytes) {
+  clear_error();
+  if (bytes) PIPO_HIP_TRY(hipMemcpy(dst, src, bytes, hipMemcpyHostToDevice));
+  return PIPO_OK;
+}
+
+pipo_status pipo_copy_d2h(void* dst, const void* src, size_t bytes) {
+  clear_error();
+  if (bytes) PIPO_HIP_TRY(hipMemcpy(dst, src, bytes, hipMemcpyDeviceToHost));
+  return PIPO_OK;
+}
+
+pipo_status pipo_dev_synchronize(void) {
+  clear_error();
+  PIPO_HIP_TRY(hipDeviceSynchronize());
+  return PIPO_OK;
+}
+
+static pipo_status gemm_common(GemmArgs& a, bool w4, void* out, int32_t epi, void* stream) {
+  if (epi < 0 || epi > PIPO_EPI_F32 || !out) {
+    set_error("gemm: bad epilogue %d or NULL output", epi);
+    return PIPO_ERR_ARG;
+  }
+  a.ldo = a.N;
+  if (epi == PIPO_EPI_F16 || epi == PIPO_EPI_RELU_F16)
+    a.out16 = static_cast<uint16_t*>(out);
+  else
+    a.out32 = static_cast<float*>(out);
+  return launch_gemm(a, w4, epi, static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_gemm_f16(const uint16_t* X, const uint16_t* W, const uint16_t* bias,
+                             void* out, int64_t M, int64_t N, int64_t K, int32_t epi,
+                             void* stream) {
+  clear_error();
+  GemmArgs a;
+  a.X = X;
+  a.W = W;
+  a.bias = bias;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  return gemm_common(a, false, out, epi, stream);
+}
+
+pipo_status pipo_op_gemm_w4(const uint16_t* X, const uint8_t* Wq, const uint16_t* Wsm,
+                            const uint16_t* bias, void* out, int64_t M, int64_t N, int64_t K,
+                            int32_t epi, void* stream) {
+  clear_error();
+  GemmArgs a;
+  a.X = X;
+  a.Wq = Wq;
+  a.Wsm = Wsm;
+  a.bias = bias;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  return gemm_common(a, true, out, epi, stream);
+}
+
+pipo_status pipo_op_layernorm(const float* x, const uint16_t* gamma, const uint16_t* beta,
+                              uint16_t* y, int64_t rows, int64_t d, int64_t src_stride,
+                              int64_t src_offset, float eps, void* stream) {
+  clear_error();
+  if (!x || !gamma || !beta || !y || src_stride < 1 || src_offset < 0 || src_offset >= src_stride) {
+    set_error("layernorm: bad arguments");
+    return PIPO_ERR_ARG;
+  }
+  return launch_layernorm(x, gamma, beta, y, rows, d, src_stride, src_offset, eps,
+                          static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_attn_decode(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                                uint16_t* o, int32_t b, int32_t n_heads, int32_t head_dim,
+                                int32_t t, void* stream) {
+  clear_error();
+  if (!q || !kc || !vc || !o) {
+    set_error("attn_decode: NULL pointer");
+    return PIPO_ERR_ARG;
+  }
+  return launch_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t,
+                            static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_attn_prefill(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                                 uint16_t* o, int32_t b, int32_t P, int32_t n_heads,
+                                 int32_t head_dim, void* stream) {
+  clear_error();
+  if (!q || !kc || !vc || !o) {
+    set_error("attn_prefill: NULL pointer");
+    return PIPO_ERR_ARG;
+  }
+  return launch_attn_prefill(q, kc, vc, o, b, P, n_heads, head_dim,
+                             static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_argmax(const float* logits, int32_t* next, int64_t rows, int64_t V,
+                           void* stream) {
+  clear_error();
+  if (!logits || !next) {
+    set_error("argmax: NULL pointer");
+    return PIPO_ERR_ARG;
+  }
+  return launch_argmax(logits, next, rows, V, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,207 @@
+"""Host-side setup around the C ABI: weights laid out in pinned host memory
+for streaming, and a small Decoder wrapper over pipo_create / pipo_prefill /
+pipo_decode_step.  Nothing here computes any part of the decoder.
+
+Host layout (data merging, Section 3.3 of the paper): each layer's four
+matrices -- fp16, or INT4 codes each followed by its (scale, min) pairs --
+share one pinned region at 4 KiB-aligned offsets, so the copy engine streams
+them without staging; the token table (also the output head) has a pinned
+region of its own.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+from . import binding as B
+
+MATRIX_SHAPES = ("wqkv", "wo", "w1", "w2")
+SMALL = ("ln1_g", "ln1_b", "bqkv", "bo", "ln2_g", "ln2_b", "b1", "b2")
+
+
+def _align(v: int, a: int = 4096) -> int:
+    return (v + a - 1) // a * a
+
+
+def _pinned_view(ptr: int, nbytes: int) -> np.ndarray:
+    return np.frombuffer((ctypes.c_uint8 * nbytes).from_address(ptr), dtype=np.uint8)
+
+
+class HostWeights:
+    """Decoder weights in host memory, filled by a provider with
+    ``fill(layer, name, out)`` (fp16 tensors, layer -1 for embeddings and
+    the final LayerNorm) and ``fill_int4(layer, name, q, sm)``.
+
+    ``pinned_matrices`` puts the layer matrices in pipo_host_alloc memory
+    (streamed in place); ``pinned_head`` does the same for the token table.
+    """
+
+    def __init__(self, shape, wfmt: str, provider, pinned_matrices: bool = True,
+                 pinned_head: bool = True):
+        assert wfmt in ("fp16", "int4")
+        self.shape, self.wfmt = shape, wfmt
+        d, F, V, L = shape.d_model, shape.d_ffn, shape.vocab, shape.n_layers
+        self._pinned: List[int] = []
+        self._keep: List[object] = []
+        dims = {"wqkv": (3 * d, d), "wo": (d, d), "w1": (F, d), "w2": (d, F)}
+        self.layers: List[Dict[str, object]] = []
+        c_layers = (B.PipoLayerHost * L)()
+        for j in range(L):
+            mats: Dict[str, object] = {}
+            if pinned_matrices:
+                sizes = []
+                for nm in MATRIX_SHAPES:
+                    N, K = dims[nm]
+                    if wfmt == "fp16":
+                        sizes += [N * K * 2]
+                    else:
+                        sizes += [N * K // 2, N * (K // 64) * 4]
+                total = sum(_align(s) for s in sizes)
+                ptr = B.pipo_host_alloc(total)
+                self._pinned.append(ptr)
+                region = _pinned_view(ptr, total)
+                off = 0
+                views = []
+                for s in sizes:
+                    views.append(region[off:off + s])
+                    off += _align(s)
+                for i, nm in enumerate(MATRIX_SHAPES):
+                    N, K = dims[nm]
+                    if wfmt == "fp16":
+                        mats[nm] = views[i].view(np.float16).reshape(N, K)
+                    else:
+                        mats[nm] = (views[2 * i].reshape(N, K // 2),
+                                    views[2 * i + 1].view(np.float16).reshape(N, K // 64, 2))
+            else:
+                for nm in MATRIX_SHAPES:
+                    N, K = dims[nm]
+                    mats[nm] = (np.empty((N, K), np.float16) if wfmt == "fp16" else
+                                (np.empty((N, K // 2), np.uint8),
+                                 np.empty((N, K // 64, 2), np.float16)))
+            for nm in MATRIX_SHAPES:
+                if wfmt == "fp16":
+                    provider.fill(j, nm, mats[nm])
+                else:
+                    provider.fill_int4(j, nm, mats[nm][0], mats[nm][1])
+            small = {"ln1_g": d, "ln1_b": d, "bqkv": 3 * d, "bo": d, "ln2_g": d, "ln2_b": d,
+                     "b1": F, "b2": d}
+            for nm, n in small.items():
+                mats[nm] = provider.fill(j, nm, np.empty(n, np.float16))
+            self.layers.append(mats)
+            cl = c_layers[j]
+            for nm in SMALL:
+                setattr(cl, nm, mats[nm].ctypes.data)
+            for nm, qn in zip(MATRIX_SHAPES, ("qqkv", "qo", "q1", "q2")):
+                if wfmt == "fp16":
+                    setattr(cl, nm, mats[nm].ctypes.data)
+                else:
+                    q4 = getattr(cl, qn)
+                    q4.q = mats[nm][0].ctypes.data
+                    q4.scale_min = mats[nm][1].ctypes.data
+        self.c_layers = c_layers
+        if pinned_head:
+            ptr = B.pipo_host_alloc(V * d * 2)
+            self._pinned.append(ptr)
+            self.tok_emb = _pinned_view(ptr, V * d * 2).view(np.float16).reshape(V, d)
+        else:
+            self.tok_emb = np.empty((V, d), np.float16)
+        provider.fill(-1, "tok_emb", self.tok_emb)
+        self.pos_emb = provider.fill(-1, "pos_emb",
+                                     np.empty((shape.max_pos + shape.pos_offset, d), np.float16))
+        self.lnf_g = provider.fill(-1, "lnf_g", np.empty(d, np.float16))
+        self.lnf_b = provider.fill(-1, "lnf_b", np.empty(d, np.float16))
+        self.c_weights = B.PipoHostWeights(self.tok_emb.ctypes.data, self.pos_emb.ctypes.data,
+                                           self.lnf_g.ctypes.data, self.lnf_b.ctypes.data,
+                                           ctypes.cast(c_layers, ctypes.POINTER(B.PipoLayerHost)))
+
+    def free(self):
+        """Release the pinned regions (after every context using them is destroyed)."""
+        self.layers = []
+        self.tok_emb = None
+        for p in self._pinned:
+            B.pipo_host_free(p)
+        self._pinned = []
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def c_shape(shape) -> B.PipoShape:
+    return B.PipoShape(shape.n_layers, shape.d_model, shape.n_heads, shape.d_ffn, shape.vocab,
+                       shape.max_pos, shape.pos_offset, shape.ln_eps)
+
+
+def c_policy(wfmt: str = "fp16", weights_on_host: bool = True, embed_on_host: bool = True,
+             kv_on_host: bool = False, n_weight_slots: int = 3, n_h2d_streams: int = 1,
+             chunk_bytes: int = 64 << 20, max_batch: int = 1, max_seq: int = 1,
+             hbm_budget_bytes: int = 0, debug_flags: int = 0,
+             copy_delay_us: int = 0) -> B.PipoPolicy:
+    return B.PipoPolicy(B.PIPO_W_FP16 if wfmt == "fp16" else B.PIPO_W_INT4_G64,
+                        int(weights_on_host), int(embed_on_host), int(kv_on_host),
+                        n_weight_slots, n_h2d_streams, chunk_bytes, max_batch, max_seq,
+                        hbm_budget_bytes, debug_flags, copy_delay_us)
+
+
+class Decoder:
+    """One pipo context over HostWeights."""
+
+    def __init__(self, weights: HostWeights, **policy):
+        policy.setdefault("wfmt", weights.wfmt)
+        self.weights = weights
+        self.vocab = weights.shape.vocab
+        self.policy = c_policy(**policy)
+        self.ctx = B.pipo_create(c_shape(weights.shape), weights.c_weights, self.policy)
+
+    def prefill(self, tokens: np.ndarray, want_logits: bool = False
+                ) -> Tuple[np.ndarray, Optional[np.ndarray]]:
+        logits = (np.empty((tokens.shape[0], self.vocab), np.float32) if want_logits else None)
+        return B.pipo_prefill(self.ctx, tokens, logits), logits
+
+    def decode(self, tokens: np.ndarray, want_logits: bool = False
+               ) -> Tuple[np.ndarray, Optional[np.ndarray]]:
+        logits = (np.empty((tokens.shape[0], self.vocab), np.float32) if want_logits else None)
+        return B.pipo_decode_step(self.ctx, tokens, logits), logits
+
+    def generate(self, prompt: np.ndarray, gen: int, want_logits: bool = False,
+                 forced: Optional[np.ndarray] = None):
+        """Greedy generation of `gen` tokens per sequence.  With `forced`
+        ([b][gen-1]) those tokens are fed instead of the model's own
+        (teacher forcing).  Returns (tokens [b][gen], logits list or None)."""
+        out, logs = [], []
+        nxt, lg = self.prefill(prompt, want_logits)
+        out.append(nxt)
+        logs.append(lg)
+        for i in range(gen - 1):
+            feed = nxt if forced is None else forced[:, i]
+            nxt, lg = self.decode(feed, want_logits)
+            out.append(nxt)
+            logs.append(lg)
+        return np.stack(out, axis=1), (logs if want_logits else None)
+
+    def stats(self) -> dict:
+        return B.pipo_get_stats(self.ctx)
+
+    def reset_stats(self) -> None:
+        B.pipo_reset_stats(self.ctx)
+
+    def close(self) -> None:
+        if self.ctx:
+            B.pipo_destroy(self.ctx)
+            self.ctx = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

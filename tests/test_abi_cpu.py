@@ -1,0 +1,97 @@
+"""The C ABI without a GPU: every declared symbol is exported, and invalid
+shapes and policies are rejected before any device work."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2504_03664_amd import binding as B
+from paper_2504_03664_amd.model import c_policy, c_shape
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("pipo.h", "pipo_ops.h", "pipo_sched.h")]
+
+
+def declared_functions():
+    names = []
+    for h in HEADERS:
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names += re.findall(r"\b(pipo_[a-z0-9_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+def exported(path):
+    out = subprocess.run(["nm", "-D", "--defined-only", path], capture_output=True, text=True,
+                         check=True).stdout
+    return {line.split()[-1] for line in out.splitlines() if line.strip()}
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 20
+    syms = exported(B.LIB_PATH)
+    missing = [n for n in names if n not in syms]
+    assert not missing, missing
+    L = B.lib()
+    for n in names:
+        assert getattr(L, n) is not None
+
+
+def test_schedule_library_exports_trace():
+    assert "pipo_sched_trace" in exported(B.SCHED_LIB_PATH)
+
+
+class _Shape:
+    def __init__(self, **kw):
+        base = dict(n_layers=2, d_model=256, n_heads=2, d_ffn=512, vocab=100, max_pos=64,
+                    pos_offset=2, ln_eps=1e-5)
+        base.update(kw)
+        self.__dict__.update(base)
+
+
+def _create(shape, **pol):
+    dummy = np.zeros(8, np.uint16)
+    layers = (B.PipoLayerHost * max(shape.n_layers, 1))()
+    w = B.PipoHostWeights(dummy.ctypes.data, dummy.ctypes.data, dummy.ctypes.data,
+                          dummy.ctypes.data, ctypes.cast(layers, ctypes.POINTER(B.PipoLayerHost)))
+    pol.setdefault("max_batch", 1)
+    pol.setdefault("max_seq", 8)
+    return B.pipo_create(c_shape(shape), w, c_policy(**pol))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_layers=0), "PIPO_ERR_ARG"),
+    (dict(n_heads=3), "PIPO_ERR_ARG"),                 # d_model not a multiple of n_heads
+    (dict(n_heads=8), "PIPO_ERR_UNSUPPORTED"),         # head_dim 32
+    (dict(d_model=320, n_heads=5), "PIPO_ERR_UNSUPPORTED"),  # d not a multiple of 128
+    (dict(d_ffn=500), "PIPO_ERR_UNSUPPORTED"),
+    (dict(vocab=0), "PIPO_ERR_ARG"),
+])
+def test_bad_shapes_rejected(kw, status):
+    with pytest.raises(B.PipoError) as e:
+        _create(_Shape(**kw))
+    assert B.STATUS_NAMES[e.value.status] == status
+    assert B.pipo_last_error() != ""
+
+
+@pytest.mark.parametrize("pol,status", [
+    (dict(max_batch=0), "PIPO_ERR_ARG"),
+    (dict(max_seq=65), "PIPO_ERR_UNSUPPORTED"),        # beyond max_pos
+    (dict(n_weight_slots=1), "PIPO_ERR_ARG"),
+    (dict(n_h2d_streams=3), "PIPO_ERR_ARG"),
+    (dict(kv_on_host=True, weights_on_host=False), "PIPO_ERR_UNSUPPORTED"),
+])
+def test_bad_policies_rejected(pol, status):
+    with pytest.raises(B.PipoError) as e:
+        _create(_Shape(), **pol)
+    assert B.STATUS_NAMES[e.value.status] == status
+
+
+def test_null_weights_rejected():
+    with pytest.raises(B.PipoError) as e:
+        B.pipo_create(c_shape(_Shape()), B.PipoHostWeights(), c_policy(max_batch=1, max_seq=4))
+    assert e.value.status == -1
