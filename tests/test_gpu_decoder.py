@@ -1,0 +1,198 @@
+"""End-to-end decoder on the GPU against the oracle, and the pipelined run
+against the same kernels with every weight resident in HBM."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import OracleDecoder
+from paper_2504_03664_amd import binding as B
+from paper_2504_03664_amd.model import Decoder, HostWeights
+
+pytestmark = pytest.mark.gpu
+
+REL_TOL = 2e-2          # normwise per logits row: max|g - o| / max|o|
+ARGMAX_MIN = 0.99
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def normwise(g, o):
+    return np.abs(g - o).max(axis=-1) / np.abs(o).max(axis=-1)
+
+
+def teacher_forced_check(model, wfmt, prompt, gen_tokens, gpu_logits, dtype=np.float32):
+    """Oracle logits at every generated position, fed the GPU's tokens."""
+    full = np.concatenate([prompt, gen_tokens[:, :-1]], axis=1)
+    ref = OracleDecoder(model, dtype).forward(full)
+    P = prompt.shape[1]
+    errs, agree, total, ties = [], 0, 0, 0
+    for s, lg in enumerate(gpu_logits):
+        o = ref[:, P - 1 + s]
+        e = normwise(lg.astype(np.float64), o.astype(np.float64))
+        errs.append(e.max())
+        ga, oa = lg.argmax(-1), o.argmax(-1)
+        agree += int((ga == oa).sum())
+        total += len(ga)
+        for r in np.nonzero(ga != oa)[0]:
+            gap = o[r, oa[r]] - o[r, ga[r]]
+            assert gap <= REL_TOL * np.abs(o[r]).max(), "argmax differs without a near tie"
+            ties += 1
+        assert (ga == gen_tokens[:, s]).all()
+    return max(errs), agree / total, ties
+
+
+@pytest.fixture(scope="module")
+def opt125m():
+    wl = synth.WORKLOADS[0]
+    model = synth.SyntheticOPT(wl.shape, seed=synth.DEFAULT_SEED)
+    hw = HostWeights(wl.shape, "fp16", model)
+    yield wl, model, hw
+    hw.free()
+
+
+def test_opt125m_streamed_parity(opt125m):
+    """OPT-125m shape, batch 4, prompt 32, 8 greedy tokens, every layer and
+    the output head streamed per matrix from pinned host memory."""
+    wl, model, hw = opt125m
+    log(f"parity {wl.name}")
+    prompt = synth.prompt_tokens(wl.batch, wl.prompt, wl.shape.vocab, seed=1, stream=0)
+    with Decoder(hw, max_batch=wl.batch, max_seq=wl.prompt + wl.gen, chunk_bytes=1 << 20) as dec:
+        toks, logits = dec.generate(prompt, wl.gen, want_logits=True)
+    err, agree, ties = teacher_forced_check(model, "fp16", prompt, toks, logits)
+    log(f"  max normwise err {err:.2e}, argmax agreement {agree:.4f} ({ties} near ties)")
+    assert err <= REL_TOL
+    assert agree >= ARGMAX_MIN or ties <= 1
+
+
+def test_opt125m_longer_generation_parity(opt125m):
+    wl, model, hw = opt125m
+    log("parity opt-125m b4 p48 g40")
+    prompt = synth.prompt_tokens(4, 48, wl.shape.vocab, seed=2)
+    with Decoder(hw, max_batch=4, max_seq=88) as dec:
+        toks, logits = dec.generate(prompt, 40, want_logits=True)
+    err, agree, ties = teacher_forced_check(model, "fp16", prompt, toks, logits)
+    log(f"  max normwise err {err:.2e}, argmax agreement {agree:.4f}")
+    assert err <= REL_TOL and agree >= ARGMAX_MIN
+
+
+def _run(hw, prompt, gen, **pol):
+    with Decoder(hw, max_batch=prompt.shape[0], max_seq=prompt.shape[1] + gen, **pol) as dec:
+        toks, logits = dec.generate(prompt, gen, want_logits=True)
+    return toks, np.stack(logits)
+
+
+def test_streamed_bit_identical_to_resident(opt125m):
+    wl, model, hw = opt125m
+    prompt = synth.prompt_tokens(4, 32, wl.shape.vocab, seed=3)
+    log("resident reference")
+    t0, l0 = _run(hw, prompt, 6, weights_on_host=False, embed_on_host=False)
+    variants = [
+        dict(),
+        dict(n_weight_slots=2, chunk_bytes=4096 * 37),
+        dict(n_h2d_streams=2, chunk_bytes=1 << 20, n_weight_slots=4),
+        dict(debug_flags=B.PIPO_DBG_POISON_SLOTS | B.PIPO_DBG_COPY_DELAY, copy_delay_us=200,
+             n_h2d_streams=2, chunk_bytes=1 << 21),
+        dict(embed_on_host=False),
+        dict(weights_on_host=False, embed_on_host=True),
+    ]
+    for v in variants:
+        log(f"streamed variant {v}")
+        t1, l1 = _run(hw, prompt, 6, **v)
+        assert np.array_equal(t1, t0)
+        assert np.array_equal(l1.view(np.uint32), l0.view(np.uint32))
+
+
+def test_new_prefill_resets_sequences(opt125m):
+    wl, model, hw = opt125m
+    pa = synth.prompt_tokens(2, 20, wl.shape.vocab, seed=4)
+    pb = synth.prompt_tokens(3, 9, wl.shape.vocab, seed=5)
+    log("prefill after decode")
+    with Decoder(hw, max_batch=3, max_seq=40) as dec:
+        dec.generate(pa, 5)
+        tb, lb = dec.generate(pb, 4, want_logits=True)
+    with Decoder(hw, max_batch=3, max_seq=40) as dec:
+        tf, lf = dec.generate(pb, 4, want_logits=True)
+    assert np.array_equal(tb, tf)
+    assert np.array_equal(np.stack(lb).view(np.uint32), np.stack(lf).view(np.uint32))
+
+
+def test_edge_shapes_and_states(opt125m):
+    wl, model, hw = opt125m
+    log("edge shapes and states")
+    with Decoder(hw, max_batch=2, max_seq=3) as dec:
+        with pytest.raises(B.PipoError) as e:
+            dec.decode(np.array([1, 2], np.int32))
+        assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_STATE"
+        with pytest.raises(B.PipoError) as e:
+            dec.prefill(np.zeros((3, 2), np.int32))            # batch above max_batch
+        assert e.value.status == -1
+        with pytest.raises(B.PipoError) as e:
+            dec.prefill(np.array([[0, wl.shape.vocab]], np.int32))   # id out of range
+        assert e.value.status == -1
+        # one sequence, one prompt token
+        prompt = np.array([[7]], np.int32)
+        n0, l0 = dec.prefill(prompt, want_logits=True)
+        n1, l1 = dec.decode(n0, want_logits=True)
+        n2, l2 = dec.decode(n1, want_logits=True)
+        with pytest.raises(B.PipoError) as e:
+            dec.decode(n2)                                     # max_seq reached
+        assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_STATE"
+    full = np.array([[7, n0[0], n1[0]]])
+    ref = OracleDecoder(model).forward(full)[0]
+    for s, lg in enumerate((l0, l1, l2)):
+        assert normwise(lg[0].astype(np.float64), ref[s].astype(np.float64)) <= REL_TOL
+
+
+def test_hbm_budget_is_enforced(opt125m):
+    wl, model, hw = opt125m
+    with pytest.raises(B.PipoError) as e:
+        Decoder(hw, max_batch=4, max_seq=40, hbm_budget_bytes=10 << 20)
+    assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_OOM_DEVICE"
+
+
+# ---------------------------------------------------------------------------
+SMALL = synth.OPTShape(4, 512, 4, 2048, vocab=1000, max_pos=128)
+
+
+@pytest.mark.parametrize("wfmt", ["fp16", "int4"])
+def test_small_model_parity_and_kv_on_host(wfmt):
+    """A 4-layer model (head_dim 128) with prompt 70 (two prefill tiles and a
+    ragged tail); fp16 and INT4 weights; KV cache resident or in host memory."""
+    log(f"small model {wfmt}")
+    model = synth.SyntheticOPT(SMALL, seed=11, wfmt=wfmt)
+    hw = HostWeights(SMALL, wfmt, model)
+    try:
+        prompt = synth.prompt_tokens(3, 70, SMALL.vocab, seed=6)
+        t0, l0 = _run(hw, prompt, 6)
+        err, agree, ties = teacher_forced_check(model, wfmt, prompt, t0, list(l0))
+        log(f"  err {err:.2e} agree {agree:.3f}")
+        assert err <= REL_TOL
+        tr, lr = _run(hw, prompt, 6, weights_on_host=False, embed_on_host=False)
+        assert np.array_equal(lr.view(np.uint32), l0.view(np.uint32))
+        for v in (dict(kv_on_host=True),
+                  dict(kv_on_host=True, n_h2d_streams=2, chunk_bytes=8192,
+                       debug_flags=B.PIPO_DBG_POISON_SLOTS)):
+            log(f"  kv on host {v}")
+            tk, lk = _run(hw, prompt, 6, **v)
+            assert np.array_equal(tk, t0)
+            assert np.array_equal(lk.view(np.uint32), l0.view(np.uint32))
+    finally:
+        hw.free()
+
+
+def test_head_dim_64_kv_on_host():
+    shape = synth.OPTShape(3, 256, 4, 1024, vocab=512, max_pos=64)
+    log("head_dim 64, kv on host")
+    model = synth.SyntheticOPT(shape, seed=12)
+    hw = HostWeights(shape, "fp16", model, pinned_matrices=False, pinned_head=False)
+    try:
+        prompt = synth.prompt_tokens(5, 17, shape.vocab, seed=7)
+        t0, l0 = _run(hw, prompt, 9, kv_on_host=True, n_weight_slots=2)
+        err, agree, ties = teacher_forced_check(model, "fp16", prompt, t0, list(l0))
+        assert err <= REL_TOL
+        tr, lr = _run(hw, prompt, 9, weights_on_host=False, embed_on_host=False)
+        assert np.array_equal(lr.view(np.uint32), l0.view(np.uint32))
+    finally:
+        hw.free()

@@ -1,0 +1,195 @@
+"""Each GPU operation through the C ABI (pipo_ops.h) against the oracle or an
+exact integer reference."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import causal_attention, dequant_int4_g64, layer_norm
+from paper_2504_03664_amd import binding as B
+from paper_2504_03664_amd.binding import DeviceBuffer as DB
+
+pytestmark = pytest.mark.gpu
+
+GEMM_SHAPES = [(1, 50, 128), (4, 100, 256), (16, 64, 128), (33, 130, 384), (64, 96, 128),
+               (65, 200, 256), (128, 128, 128), (300, 257, 512)]
+EPIS = [B.PIPO_EPI_F16, B.PIPO_EPI_RELU_F16, B.PIPO_EPI_ADD_F32, B.PIPO_EPI_F32]
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def run_gemm(X, W, bias, epi, out_init=None, w4=None):
+    M, K = X.shape
+    N = W.shape[0] if w4 is None else w4[0].shape[0]
+    dX = DB.from_array(X.astype(np.float16))
+    dB = DB.from_array(bias.astype(np.float16)) if bias is not None else None
+    f32 = epi in (B.PIPO_EPI_ADD_F32, B.PIPO_EPI_F32)
+    if out_init is not None:
+        dO = DB.from_array(out_init.astype(np.float32))
+    else:
+        dO = DB(M * N * (4 if f32 else 2))
+    if w4 is None:
+        dW = DB.from_array(W.astype(np.float16))
+        B.pipo_op_gemm_f16(dX.ptr, dW.ptr, dB.ptr if dB else None, dO.ptr, M, N, K, epi)
+    else:
+        dq, dsm = DB.from_array(w4[0]), DB.from_array(w4[1])
+        B.pipo_op_gemm_w4(dX.ptr, dq.ptr, dsm.ptr, dB.ptr if dB else None, dO.ptr, M, N, K, epi)
+    B.pipo_dev_synchronize()
+    return dO.to_array(np.float32 if f32 else np.float16, (M, N))
+
+
+def expected(acc, bias, epi, out_init):
+    v = acc + (bias if bias is not None else 0)
+    if epi == B.PIPO_EPI_RELU_F16:
+        v = np.maximum(v, 0)
+    if epi == B.PIPO_EPI_ADD_F32:
+        v = out_init + v
+    return v
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+@pytest.mark.parametrize("epi", EPIS)
+def test_gemm_f16_exact_on_integers(M, N, K, epi):
+    log(f"gemm_f16 exact M={M} N={N} K={K} epi={epi}")
+    rng = np.random.default_rng(M * 7 + N + K + epi)
+    X = rng.integers(-2, 3, (M, K)).astype(np.float64)
+    W = rng.integers(-2, 3, (N, K)).astype(np.float64)
+    bias = rng.integers(-8, 9, N).astype(np.float64)
+    init = rng.integers(-100, 100, (M, N)).astype(np.float64) if epi == B.PIPO_EPI_ADD_F32 else None
+    got = run_gemm(X, W, bias, epi, init)
+    want = expected(X @ W.T, bias, epi, init)
+    assert np.array_equal(got.astype(np.float64), want)
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+def test_gemm_w4_exact_on_integers(M, N, K):
+    log(f"gemm_w4 exact M={M} N={N} K={K}")
+    rng = np.random.default_rng(M + 3 * N + K)
+    codes = rng.integers(0, 16, (N, K))
+    q = (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
+    sm = np.empty((N, K // 64, 2), np.float16)
+    sm[..., 0] = rng.choice([0.25, 0.5, 1.0], (N, K // 64))
+    sm[..., 1] = rng.choice([-2.0, -1.0, 0.0], (N, K // 64))
+    X = rng.integers(-1, 2, (M, K)).astype(np.float64)
+    Wd = dequant_int4_g64(q, sm, np.float64)
+    for epi in (B.PIPO_EPI_F32, B.PIPO_EPI_RELU_F16):
+        got = run_gemm(X, None, None, epi, w4=(q, sm))
+        assert np.array_equal(got.astype(np.float64), expected(X @ Wd.T, None, epi, None))
+
+
+@pytest.mark.parametrize("M", [3, 64, 200])
+def test_gemm_random_vs_oracle_definition(M):
+    log(f"gemm random M={M}")
+    rng = np.random.default_rng(M)
+    K, N = 1024, 384
+    X = (rng.standard_normal((M, K)) * 0.5).astype(np.float16)
+    W = (rng.standard_normal((N, K)) * 0.02).astype(np.float16)
+    bias = (rng.standard_normal(N) * 0.02).astype(np.float16)
+    got = run_gemm(X, W, bias, B.PIPO_EPI_F32)
+    want = X.astype(np.float64) @ W.astype(np.float64).T + bias.astype(np.float64)
+    assert np.abs(got - want).max() <= 1e-4 * np.abs(want).max() + 1e-5
+    q, sm = synth.quant_int4_g64(W)
+    got4 = run_gemm(X, None, bias, B.PIPO_EPI_F32, w4=(q, sm))
+    want4 = X.astype(np.float64) @ dequant_int4_g64(q, sm, np.float64).T + bias.astype(np.float64)
+    # the kernel rounds each expanded weight to fp16 (relative 2^-11)
+    assert np.abs(got4 - want4).max() <= 2e-3 * np.abs(want4).max()
+
+
+@pytest.mark.parametrize("M", [4, 100])
+@pytest.mark.parametrize("w4", [False, True])
+def test_gemm_row_chunks_bit_identical(M, w4):
+    """A launch over a row range of W equals those rows of the whole launch."""
+    log(f"gemm chunk invariance M={M} w4={w4}")
+    rng = np.random.default_rng(5)
+    K, N = 512, 640
+    X = (rng.standard_normal((M, K))).astype(np.float16)
+    W = (rng.standard_normal((N, K)) * 0.05).astype(np.float16)
+    full = run_gemm(X, W, None, B.PIPO_EPI_F32, w4=synth.quant_int4_g64(W) if w4 else None)
+    for n0, n1 in ((0, 32), (32, 160), (160, 640), (7 * 32, 9 * 32)):
+        part = W[n0:n1]
+        got = run_gemm(X, part, None, B.PIPO_EPI_F32,
+                       w4=synth.quant_int4_g64(part) if w4 else None)
+        assert np.array_equal(got.view(np.uint32), full[:, n0:n1].view(np.uint32))
+
+
+@pytest.mark.parametrize("rows,d,stride,offset", [(1, 768, 1, 0), (5, 4096, 1, 0),
+                                                  (3, 7168, 4, 3), (33, 128, 2, 0)])
+def test_layernorm_vs_oracle(rows, d, stride, offset):
+    log(f"layernorm rows={rows} d={d}")
+    rng = np.random.default_rng(d + rows)
+    x = (rng.standard_normal((rows * stride, d)) * 3 + 1).astype(np.float32)
+    g = (1 + 0.1 * rng.standard_normal(d)).astype(np.float16)
+    b = (0.1 * rng.standard_normal(d)).astype(np.float16)
+    dx, dg, db = DB.from_array(x), DB.from_array(g), DB.from_array(b)
+    dy = DB(rows * d * 2)
+    B.pipo_op_layernorm(dx.ptr, dg.ptr, db.ptr, dy.ptr, rows, d, stride, offset, 1e-5)
+    B.pipo_dev_synchronize()
+    got = dy.to_array(np.float16, (rows, d)).astype(np.float64)
+    src = x.astype(np.float64)[offset::stride][:rows]
+    want = layer_norm(src, g.astype(np.float64), b.astype(np.float64), 1e-5)
+    assert np.abs(got - want).max() <= 4e-3 * np.abs(want).max()
+
+
+def _attn_inputs(rng, b, T, H, D):
+    d = H * D
+    q = (rng.standard_normal((b, d)) * 0.3).astype(np.float16)
+    kc = rng.standard_normal((T, b, d)).astype(np.float16)
+    vc = rng.standard_normal((T, b, d)).astype(np.float16)
+    return q, kc, vc
+
+
+@pytest.mark.parametrize("b,T,H,D", [(1, 1, 2, 64), (3, 7, 4, 128), (2, 64, 2, 64),
+                                     (2, 65, 3, 128), (1, 544, 2, 128), (4, 300, 1, 64)])
+def test_attn_decode_vs_oracle(b, T, H, D):
+    log(f"attn_decode b={b} T={T} H={H} D={D}")
+    rng = np.random.default_rng(T * 10 + b)
+    q, kc, vc = _attn_inputs(rng, b, T, H, D)
+    dq, dk, dv = DB.from_array(q), DB.from_array(kc), DB.from_array(vc)
+    do = DB(b * H * D * 2)
+    B.pipo_op_attn_decode(dq.ptr, dk.ptr, dv.ptr, do.ptr, b, H, D, T - 1)
+    B.pipo_dev_synchronize()
+    got = do.to_array(np.float16, (b, H * D)).astype(np.float64)
+    for i in range(b):
+        want = causal_attention(q[i:i + 1].astype(np.float64), kc[:, i].astype(np.float64),
+                                vc[:, i].astype(np.float64), H)[0]
+        assert np.abs(got[i] - want).max() <= 5e-3 * max(1.0, np.abs(want).max())
+
+
+@pytest.mark.parametrize("b,P,H,D", [(1, 1, 2, 64), (2, 5, 2, 128), (1, 64, 3, 64),
+                                     (2, 100, 2, 128), (1, 130, 1, 64), (3, 33, 4, 128)])
+def test_attn_prefill_vs_oracle(b, P, H, D):
+    log(f"attn_prefill b={b} P={P} H={H} D={D}")
+    rng = np.random.default_rng(P * 3 + b)
+    d = H * D
+    q = (rng.standard_normal((b, P, d)) * 0.3).astype(np.float16)
+    kc = rng.standard_normal((P, b, d)).astype(np.float16)
+    vc = rng.standard_normal((P, b, d)).astype(np.float16)
+    dq, dk, dv = DB.from_array(q), DB.from_array(kc), DB.from_array(vc)
+    do = DB(b * P * d * 2)
+    B.pipo_op_attn_prefill(dq.ptr, dk.ptr, dv.ptr, do.ptr, b, P, H, D)
+    B.pipo_dev_synchronize()
+    got = do.to_array(np.float16, (b, P, d)).astype(np.float64)
+    for i in range(b):
+        want = causal_attention(q[i].astype(np.float64), kc[:, i].astype(np.float64),
+                                vc[:, i].astype(np.float64), H)
+        # P is rounded to fp16 before P.V (relative 2^-11 per weight)
+        assert np.abs(got[i] - want).max() <= 8e-3 * max(1.0, np.abs(want).max())
+
+
+def test_argmax_ties_and_ragged():
+    log("argmax")
+    rng = np.random.default_rng(0)
+    V = 50272
+    L = rng.standard_normal((6, V)).astype(np.float32)
+    L[1, 17] = L[1, 40000] = L[1].max() + 1          # tie: lowest index wins
+    L[2, :] = -np.inf
+    L[2, 5:] = 0.0                                    # first finite maximum
+    L[3, V - 1] = 100.0                               # ragged tail
+    L[4, :] = 7.0                                     # all equal -> 0
+    dl, dn = DB.from_array(L), DB(6 * 4)
+    B.pipo_op_argmax(dl.ptr, dn.ptr, 6, V)
+    B.pipo_dev_synchronize()
+    got = dn.to_array(np.int32, (6,))
+    assert got.tolist() == np.argmax(L, axis=1).tolist()
+    assert got[1] == 17 and got[2] == 5 and got[3] == V - 1 and got[4] == 0
