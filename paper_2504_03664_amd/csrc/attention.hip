@@ -158,8 +158,10 @@ __global__ __launch_bounds__(256) void attn_prefill_k(const uint16_t* __restrict
       const h8 kv = kp < P ? load_h8(kc + off) : zero_h8();
       const h8 vv = kp < P ? load_h8(vc + off) : zero_h8();
       *reinterpret_cast<h8*>(&Ks[key * KROW + col]) = kv;
+      const u32x4 vw = __builtin_bit_cast(u32x4, vv);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) Vt[(col + i) * VROW + key] = __builtin_bit_cast(uint16_t, vv[i]);
+      for (int i = 0; i < 8; ++i)
+        Vt[(col + i) * VROW + key] = (uint16_t)(vw[i >> 1] >> (16 * (i & 1)));
     }
     __syncthreads();
 

@@ -45,6 +45,8 @@ def expected(acc, bias, epi, out_init):
         v = np.maximum(v, 0)
     if epi == B.PIPO_EPI_ADD_F32:
         v = out_init + v
+    if epi in (B.PIPO_EPI_F16, B.PIPO_EPI_RELU_F16):
+        v = v.astype(np.float16).astype(np.float64)   # the exact fp32 sum, rounded once
     return v
 
 
