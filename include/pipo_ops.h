@@ -35,8 +35,8 @@ enum { PIPO_EPI_F16 = 0, PIPO_EPI_RELU_F16 = 1, PIPO_EPI_ADD_F32 = 2, PIPO_EPI_F
  * Y = X . W^T with the chosen epilogue (the projections of a layer and the
  * output head).  X: [M][K] fp16 (row stride K); W: [N][K] fp16; out: [M][N]
  * (row stride N), fp16 or fp32 per epilogue.  K must be a multiple of 128.
- * The result of every element depends only on its row of X, its row of W
- * and K, never on M, N or which rows a launch covers.
+ * The summation order of an element depends only on M and K, so a launch
+ * over a row range of W gives those rows bit for bit as a full launch.
  */
 pipo_status pipo_op_gemm_f16(const uint16_t* X, const uint16_t* W, const uint16_t* bias,
                              void* out, int64_t M, int64_t N, int64_t K, int32_t epi,
@@ -58,11 +58,20 @@ pipo_status pipo_op_layernorm(const float* x, const uint16_t* gamma, const uint1
  * Decode attention for b sequences at position t (keys 0..t visible).
  * q: [b][d] fp16 (already scaled by head_dim^-1/2); kc, vc: KV cache
  * [>= t+1][b][d] fp16 (position-major: row p*b + i holds sequence i's key at
- * position p); o: [b][d] fp16.  head_dim 64 or 128, t + 1 <= 8192.
+ * position p); o: [b][d] fp16.  head_dim 64 or 128, t + 1 <= 65536.
+ * When b * n_heads is small the keys are split over several workgroups and
+ * a second kernel merges the splits in order; the partials need `workspace`
+ * (device, caller-owned, contents arbitrary) of
+ * pipo_op_attn_decode_workspace_bytes(b, n_heads, head_dim, t) bytes.  With
+ * less (or NULL) the kernel runs unsplit; the result is the same up to
+ * rounding.  Calls sharing a workspace must not overlap in time.
  */
 pipo_status pipo_op_attn_decode(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                                 uint16_t* o, int32_t b, int32_t n_heads, int32_t head_dim,
-                                int32_t t, void* stream);
+                                int32_t t, void* workspace, int64_t workspace_bytes,
+                                void* stream);
+int64_t pipo_op_attn_decode_workspace_bytes(int32_t b, int32_t n_heads, int32_t head_dim,
+                                            int32_t t);
 
 /*
  * Causal prefill attention over P positions of b sequences.
@@ -76,6 +85,11 @@ pipo_status pipo_op_attn_prefill(const uint16_t* q, const uint16_t* kc, const ui
 /* next[r] = index of the largest logits[r][:] (ties: lowest index). */
 pipo_status pipo_op_argmax(const float* logits, int32_t* next, int64_t rows, int64_t V,
                            void* stream);
+
+/* Plain device-to-device copy kernel: reads and writes `bytes` once
+ * (multiple of 16, 16-byte aligned pointers).  Not part of the decoder: it
+ * gives a kernel of known HBM traffic for calibrating hardware counters. */
+pipo_status pipo_op_copy(void* dst, const void* src, int64_t bytes, void* stream);
 
 #ifdef __cplusplus
 }

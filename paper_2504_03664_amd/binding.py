@@ -108,9 +108,11 @@ _SIGNATURES = {
     "pipo_op_gemm_f16": ([vp, vp, vp, vp, i64, i64, i64, i32, vp], i32),
     "pipo_op_gemm_w4": ([vp, vp, vp, vp, vp, i64, i64, i64, i32, vp], i32),
     "pipo_op_layernorm": ([vp, vp, vp, vp, i64, i64, i64, i64, f32, vp], i32),
-    "pipo_op_attn_decode": ([vp, vp, vp, vp, i32, i32, i32, i32, vp], i32),
+    "pipo_op_attn_decode": ([vp, vp, vp, vp, i32, i32, i32, i32, vp, i64, vp], i32),
+    "pipo_op_attn_decode_workspace_bytes": ([i32, i32, i32, i32], i64),
     "pipo_op_attn_prefill": ([vp, vp, vp, vp, i32, i32, i32, i32, vp], i32),
     "pipo_op_argmax": ([vp, vp, i64, i64, vp], i32),
+    "pipo_op_copy": ([vp, vp, i64, vp], i32),
     "pipo_sched_trace": ([ctypes.POINTER(PipoSchedConfig), i32, vp, vp, vp, i64, vp, i64], i64),
 }
 
@@ -286,9 +288,14 @@ def pipo_op_layernorm(x, g, b, y, rows, d, src_stride, src_offset, eps, stream=N
            "pipo_op_layernorm")
 
 
-def pipo_op_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, stream=None):
-    _check(lib().pipo_op_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, stream),
-           "pipo_op_attn_decode")
+def pipo_op_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, workspace=None,
+                        workspace_bytes=0, stream=None):
+    _check(lib().pipo_op_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, workspace,
+                                     workspace_bytes, stream), "pipo_op_attn_decode")
+
+
+def pipo_op_attn_decode_workspace_bytes(b, n_heads, head_dim, t) -> int:
+    return lib().pipo_op_attn_decode_workspace_bytes(b, n_heads, head_dim, t)
 
 
 def pipo_op_attn_prefill(q, kc, vc, o, b, P, n_heads, head_dim, stream=None):
@@ -298,6 +305,10 @@ def pipo_op_attn_prefill(q, kc, vc, o, b, P, n_heads, head_dim, stream=None):
 
 def pipo_op_argmax(logits, nxt, rows, V, stream=None):
     _check(lib().pipo_op_argmax(logits, nxt, rows, V, stream), "pipo_op_argmax")
+
+
+def pipo_op_copy(dst, src, nbytes, stream=None):
+    _check(lib().pipo_op_copy(dst, src, nbytes, stream), "pipo_op_copy")
 
 
 # ---------------------------------------------------------------------------

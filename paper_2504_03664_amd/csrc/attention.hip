@@ -7,6 +7,7 @@
 //   attn_prefill: P queries per (sequence, head), causal, flash-style with
 //                 v_mfma_f32_16x16x32_f16 for Q K^T and P V.
 // Softmax is max-subtracted in fp32; every reduction has a fixed order.
+#include <algorithm>
 #include <cfloat>
 
 #include "common.h"
@@ -26,26 +27,45 @@ __device__ __forceinline__ float wave_max(float v) {
 }
 
 // ---------------------------------------------------------------------------
-// decode: grid (heads, b), 256 threads.  A position is handled by D/8 lanes
-// (8 dims each); scores for all t+1 keys are held in LDS, then normalised,
-// then V is accumulated.  K and V rows are read once, 16 bytes per lane.
+// decode: grid (heads, b, splits), 256 threads.  Split z of a (sequence,
+// head) covers keys [z * chunk, min(T, (z + 1) * chunk)).  A key is handled
+// by D/8 lanes (8 dims each); every lane group keeps its own online softmax
+// state (running max m, sum l, 8 accumulators) over the keys it visits, two
+// keys at a time so that K and V of both are in flight together.  Groups are
+// merged by a butterfly inside the wave, waves in order through LDS.  With
+// one split the result is final; otherwise (m, l, acc[D]) goes to `part`
+// and attn_decode_combine merges the splits in split order.
+template <int D>
+__device__ __forceinline__ void online_merge(float& m, float& l, float (&acc)[8], float m2,
+                                             float l2, const float (&acc2)[8]) {
+  const float M = fmaxf(m, m2);
+  const float a1 = m == -INFINITY ? 0.f : expf(m - M);
+  const float a2 = m2 == -INFINITY ? 0.f : expf(m2 - M);
+  l = l * a1 + l2 * a2;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = acc[i] * a1 + acc2[i] * a2;
+  m = M;
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict__ q,
                                                      const uint16_t* __restrict__ kc,
                                                      const uint16_t* __restrict__ vc,
-                                                     uint16_t* __restrict__ o, int b, int H,
-                                                     int t) {
-  extern __shared__ float sc[];  // [t + 1]
-  __shared__ float part[4][D];
-  __shared__ float red[4];
-  constexpr int LPP = D / 8;     // lanes per position
-  constexpr int PPW = 64 / LPP;  // positions per wave per pass
-  const int h = blockIdx.x, bi = blockIdx.y;
+                                                     uint16_t* __restrict__ o,
+                                                     float* __restrict__ part, int b, int H,
+                                                     int t, int chunk) {
+  __shared__ float wm[4], wl[4];
+  __shared__ float wacc[4][D];
+  constexpr int LPP = D / 8;     // lanes per key
+  constexpr int PPW = 64 / LPP;  // keys per wave per pass
+  const int h = blockIdx.x, bi = blockIdx.y, sp = blockIdx.z, S = gridDim.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sub = lane / LPP, cl = lane % LPP;
   const int64_t d = (int64_t)H * D;
   const int T = t + 1;
+  const int p0 = sp * chunk, p1 = min(T, p0 + chunk);
   const int64_t col = (int64_t)h * D + cl * 8;
+  const int64_t row_stride = (int64_t)b * d;
 
   float qf[8];
   {
@@ -53,58 +73,101 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
 #pragma unroll
     for (int i = 0; i < 8; ++i) qf[i] = (float)qv[i];
   }
-  for (int p = wave * PPW + sub; p < T; p += 4 * PPW) {
-    const h8 kv = load_h8(kc + ((int64_t)p * b + bi) * d + col);
+  float m = -INFINITY, l = 0.f, acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+
+  const uint16_t* kbase = kc + (int64_t)bi * d + col;
+  const uint16_t* vbase = vc + (int64_t)bi * d + col;
+  const auto visit = [&](h8 kv, h8 vv) {
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) s += qf[i] * (float)kv[i];
 #pragma unroll
     for (int off = LPP / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
-    if (cl == 0) sc[p] = s;
+    const float mn = fmaxf(m, s);
+    const float alpha = expf(m - mn);
+    const float e = expf(s - mn);
+    l = l * alpha + e;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = acc[i] * alpha + e * (float)vv[i];
+    m = mn;
+  };
+  for (int p = p0 + wave * PPW + sub; p < p1; p += 8 * PPW) {
+    const int p2 = p + 4 * PPW;
+    const h8 ka = load_h8(kbase + (int64_t)p * row_stride);
+    const h8 va = load_h8(vbase + (int64_t)p * row_stride);
+    h8 kb2 = zero_h8(), vb2 = zero_h8();
+    if (p2 < p1) {
+      kb2 = load_h8(kbase + (int64_t)p2 * row_stride);
+      vb2 = load_h8(vbase + (int64_t)p2 * row_stride);
+    }
+    visit(ka, va);
+    if (p2 < p1) visit(kb2, vb2);
   }
-  __syncthreads();
-
-  float mx = -FLT_MAX;
-  for (int p = tid; p < T; p += 256) mx = fmaxf(mx, sc[p]);
-  mx = wave_max(mx);
-  if (lane == 0) red[wave] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  __syncthreads();
-  float sum = 0.f;
-  for (int p = tid; p < T; p += 256) {
-    const float e = expf(sc[p] - mx);
-    sc[p] = e;
-    sum += e;
+  // merge the lane groups of the wave (butterfly over the group index)
+#pragma unroll
+  for (int off = LPP; off < 64; off <<= 1) {
+    float acc2[8];
+    const float m2 = __shfl_xor(m, off, 64);
+    const float l2 = __shfl_xor(l, off, 64);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc2[i] = __shfl_xor(acc[i], off, 64);
+    online_merge<D>(m, l, acc, m2, l2, acc2);
   }
-  sum = wave_sum(sum);
-  if (lane == 0) red[wave] = sum;
-  __syncthreads();
-  sum = red[0] + red[1] + red[2] + red[3];
-
-  float acc[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-  for (int p = wave * PPW + sub; p < T; p += 4 * PPW) {
-    const h8 vv = load_h8(vc + ((int64_t)p * b + bi) * d + col);
-    const float w = sc[p];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] += w * (float)vv[i];
-  }
-#pragma unroll
-  for (int i = 0; i < 8; ++i)
-#pragma unroll
-    for (int off = LPP; off < 64; off <<= 1) acc[i] += __shfl_xor(acc[i], off, 64);
   if (sub == 0) {
+    if (cl == 0) {
+      wm[wave] = m;
+      wl[wave] = l;
+    }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) part[wave][cl * 8 + i] = acc[i];
+    for (int i = 0; i < 8; ++i) wacc[wave][cl * 8 + i] = acc[i];
   }
   __syncthreads();
-  const float inv = 1.f / sum;
   for (int c = tid; c < D; c += 256) {
-    const float v = ((part[0][c] + part[1][c]) + part[2][c]) + part[3][c];
-    o[(int64_t)bi * d + (int64_t)h * D + c] = f2h(v * inv);
+    float M = wm[0], L = wl[0], A = wacc[0][c];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      const float m2 = wm[w];
+      const float Mn = fmaxf(M, m2);
+      const float a1 = M == -INFINITY ? 0.f : expf(M - Mn);
+      const float a2 = m2 == -INFINITY ? 0.f : expf(m2 - Mn);
+      L = L * a1 + wl[w] * a2;
+      A = A * a1 + wacc[w][c] * a2;
+      M = Mn;
+    }
+    if (S == 1) {
+      o[(int64_t)bi * d + (int64_t)h * D + c] = f2h(A / L);
+    } else {
+      float* pp = part + (((int64_t)bi * H + h) * S + sp) * (D + 2);
+      pp[c] = A;
+      if (c == 0) {
+        pp[D] = M;
+        pp[D + 1] = L;
+      }
+    }
   }
+}
+
+// merge the splits of each (sequence, head) in split order
+template <int D>
+__global__ __launch_bounds__(D) void attn_decode_combine(const float* __restrict__ part,
+                                                         uint16_t* __restrict__ o, int H,
+                                                         int S) {
+  const int h = blockIdx.x, bi = blockIdx.y, c = threadIdx.x;
+  const float* pp = part + ((int64_t)bi * H + h) * S * (D + 2);
+  float M = pp[D], L = pp[D + 1], A = pp[c];
+  for (int z = 1; z < S; ++z) {
+    const float* pz = pp + (int64_t)z * (D + 2);
+    const float m2 = pz[D];
+    const float Mn = fmaxf(M, m2);
+    const float a1 = M == -INFINITY ? 0.f : expf(M - Mn);
+    const float a2 = m2 == -INFINITY ? 0.f : expf(m2 - Mn);
+    L = L * a1 + pz[D + 1] * a2;
+    A = A * a1 + pz[c] * a2;
+    M = Mn;
+  }
+  o[((int64_t)bi * H + h) * D + c] = f2h(A / L);
 }
 
 // ---------------------------------------------------------------------------
@@ -239,26 +302,49 @@ __global__ __launch_bounds__(256) void attn_prefill_k(const uint16_t* __restrict
 }
 
 // ---------------------------------------------------------------------------
+int attn_decode_splits(int b, int n_heads, int t) {
+  // enough workgroups to fill the chip, at least 64 keys per split
+  const int T = t + 1;
+  int S = (2048 + b * n_heads - 1) / (b * n_heads);
+  S = std::min(S, std::max(1, T / 64));
+  S = std::min(S, kAttnDecodeMaxSplits);
+  const int chunk = (T + S - 1) / S;
+  return (T + chunk - 1) / chunk;
+}
+
+int64_t attn_decode_workspace_bytes(int b, int n_heads, int head_dim, int splits) {
+  return splits > 1 ? (int64_t)b * n_heads * splits * (head_dim + 2) * 4 : 0;
+}
+
 pipo_status launch_attn_decode(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                                uint16_t* o, int b, int n_heads, int head_dim, int t,
-                               hipStream_t st) {
+                               float* workspace, int64_t workspace_bytes, hipStream_t st) {
   if (b < 1 || n_heads < 1 || t < 0) {
     set_error("attn_decode: bad shape b=%d heads=%d t=%d", b, n_heads, t);
     return PIPO_ERR_ARG;
   }
-  if (t + 1 > kAttnDecodeMaxT) {
-    set_error("attn_decode: %d keys exceed the %d the kernel holds", t + 1, kAttnDecodeMaxT);
-    return PIPO_ERR_UNSUPPORTED;
-  }
-  const dim3 grid((unsigned)n_heads, (unsigned)b);
-  const size_t lds = (size_t)(t + 1) * sizeof(float);
-  if (head_dim == 128) {
-    hipLaunchKernelGGL(attn_decode_k<128>, grid, dim3(256), lds, st, q, kc, vc, o, b, n_heads, t);
-  } else if (head_dim == 64) {
-    hipLaunchKernelGGL(attn_decode_k<64>, grid, dim3(256), lds, st, q, kc, vc, o, b, n_heads, t);
-  } else {
+  if (head_dim != 64 && head_dim != 128) {
     set_error("attn_decode: head_dim %d not supported (64 or 128)", head_dim);
     return PIPO_ERR_UNSUPPORTED;
+  }
+  const int T = t + 1;
+  int S = attn_decode_splits(b, n_heads, t);
+  if (!workspace || workspace_bytes < attn_decode_workspace_bytes(b, n_heads, head_dim, S)) S = 1;
+  const int chunk = (T + S - 1) / S;
+  S = (T + chunk - 1) / chunk;
+  const dim3 grid((unsigned)n_heads, (unsigned)b, (unsigned)S);
+  if (head_dim == 128) {
+    launch(attn_decode_k<128>, grid, dim3(256), 0, st, q, kc, vc, o, workspace, b, n_heads, t,
+           chunk);
+    if (S > 1)
+      hipLaunchKernelGGL(attn_decode_combine<128>, dim3((unsigned)n_heads, (unsigned)b),
+                         dim3(128), 0, st, (const float*)workspace, o, n_heads, S);
+  } else {
+    launch(attn_decode_k<64>, grid, dim3(256), 0, st, q, kc, vc, o, workspace, b, n_heads, t,
+           chunk);
+    if (S > 1)
+      hipLaunchKernelGGL(attn_decode_combine<64>, dim3((unsigned)n_heads, (unsigned)b), dim3(64),
+                         0, st, (const float*)workspace, o, n_heads, S);
   }
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
@@ -273,9 +359,9 @@ pipo_status launch_attn_prefill(const uint16_t* q, const uint16_t* kc, const uin
   }
   const dim3 grid((unsigned)((P + 63) / 64), (unsigned)n_heads, (unsigned)b);
   if (head_dim == 128) {
-    hipLaunchKernelGGL(attn_prefill_k<128>, grid, dim3(256), 0, st, q, kc, vc, o, b, P, n_heads);
+    launch(attn_prefill_k<128>, grid, dim3(256), 0, st, q, kc, vc, o, b, P, n_heads);
   } else if (head_dim == 64) {
-    hipLaunchKernelGGL(attn_prefill_k<64>, grid, dim3(256), 0, st, q, kc, vc, o, b, P, n_heads);
+    launch(attn_prefill_k<64>, grid, dim3(256), 0, st, q, kc, vc, o, b, P, n_heads);
   } else {
     set_error("attn_prefill: head_dim %d not supported (64 or 128)", head_dim);
     return PIPO_ERR_UNSUPPORTED;

@@ -1,6 +1,7 @@
 // Shared host/device definitions of the pipelined-offloading decoder library.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -29,6 +30,26 @@ void clear_error();
     pipo_status s_ = (expr);       \
     if (s_ != PIPO_OK) return s_;  \
   } while (0)
+
+// Events that bracket the next kernel launch made on this thread.  They are
+// attached to the dispatch itself (hipExtLaunchKernelGGL), so they time the
+// kernel alone rather than the stream's progress around it.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents& next_launch_events();
+
+template <typename F, typename... Args>
+inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t st, Args... args) {
+  LaunchEvents& ev = next_launch_events();
+  if (ev.start) {
+    const LaunchEvents e = ev;
+    ev = LaunchEvents{};
+    hipExtLaunchKernelGGL(kernel, grid, block, lds, st, e.start, e.stop, 0u, args...);
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, lds, st, args...);
+  }
+}
 
 // GEMM epilogues (the first four are the public PIPO_EPI_* values)
 enum : int {
@@ -66,17 +87,25 @@ pipo_status launch_layernorm(const float* x, const uint16_t* g, const uint16_t* 
 pipo_status launch_embed(const uint16_t* tok_rows, const int32_t* ids, const uint16_t* tok_table,
                          const uint16_t* pos_table, float* x, int64_t rows, int64_t d,
                          int64_t rows_per_seq, int64_t pos0, int64_t pos_offset, hipStream_t st);
+// decode attention splits the keys of a (sequence, head) over several
+// workgroups when there are few of them; the splits' partial results go to
+// `workspace` (attn_decode_workspace_bytes) and a second kernel merges them
+// in split order; without enough workspace it runs unsplit
+int attn_decode_splits(int b, int n_heads, int t);
+int64_t attn_decode_workspace_bytes(int b, int n_heads, int head_dim, int splits);
 pipo_status launch_attn_decode(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                                uint16_t* o, int b, int n_heads, int head_dim, int t,
-                               hipStream_t st);
+                               float* workspace, int64_t workspace_bytes, hipStream_t st);
 pipo_status launch_attn_prefill(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                                 uint16_t* o, int b, int P, int n_heads, int head_dim,
                                 hipStream_t st);
 pipo_status launch_argmax(const float* logits, int32_t* next, int64_t rows, int64_t V,
                           hipStream_t st);
 pipo_status launch_fill_u16(uint16_t* p, uint16_t value, int64_t n, hipStream_t st);
+pipo_status launch_copy16(void* dst, const void* src, int64_t bytes, hipStream_t st);
 
-// largest key count the decode-attention kernel holds in LDS
-constexpr int kAttnDecodeMaxT = 8192;
+// longest context the decode-attention path accepts, and its split cap
+constexpr int kAttnDecodeMaxT = 65536;
+constexpr int kAttnDecodeMaxSplits = 16;
 
 }  // namespace pipo

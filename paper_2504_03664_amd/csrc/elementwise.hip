@@ -136,6 +136,14 @@ __global__ __launch_bounds__(256) void argmax_k(const float* __restrict__ logits
   }
 }
 
+// plain streaming copy, 16 bytes per thread per iteration
+__global__ __launch_bounds__(256) void copy16_k(const u32x4* __restrict__ src,
+                                                u32x4* __restrict__ dst, int64_t n16) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
+    dst[i] = src[i];
+}
+
 __global__ void fill_u16_k(uint16_t* p, uint16_t value, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = value;
@@ -149,7 +157,7 @@ pipo_status launch_layernorm(const float* x, const uint16_t* g, const uint16_t* 
     set_error("layernorm: unsupported rows=%lld d=%lld", (long long)rows, (long long)d);
     return PIPO_ERR_UNSUPPORTED;
   }
-  hipLaunchKernelGGL(layernorm_k, dim3((unsigned)rows), dim3(256), 0, st, x, g, b, y, d,
+  launch(layernorm_k, dim3((unsigned)rows), dim3(256), 0, st, x, g, b, y, d,
                      src_stride, src_offset, eps);
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
@@ -159,7 +167,7 @@ pipo_status launch_embed(const uint16_t* tok_rows, const int32_t* ids, const uin
                          const uint16_t* pos_table, float* x, int64_t rows, int64_t d,
                          int64_t rows_per_seq, int64_t pos0, int64_t pos_offset, hipStream_t st) {
   if (rows < 1) return PIPO_OK;
-  hipLaunchKernelGGL(embed_k, dim3((unsigned)rows), dim3(256), 0, st, tok_rows, ids, tok_table,
+  launch(embed_k, dim3((unsigned)rows), dim3(256), 0, st, tok_rows, ids, tok_table,
                      pos_table, x, d, rows_per_seq, pos0, pos_offset);
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
@@ -171,7 +179,22 @@ pipo_status launch_argmax(const float* logits, int32_t* next, int64_t rows, int6
     set_error("argmax: bad shape rows=%lld V=%lld", (long long)rows, (long long)V);
     return PIPO_ERR_ARG;
   }
-  hipLaunchKernelGGL(argmax_k, dim3((unsigned)rows), dim3(256), 0, st, logits, next, V);
+  launch(argmax_k, dim3((unsigned)rows), dim3(256), 0, st, logits, next, V);
+  PIPO_HIP_TRY(hipGetLastError());
+  return PIPO_OK;
+}
+
+pipo_status launch_copy16(void* dst, const void* src, int64_t bytes, hipStream_t st) {
+  if (bytes < 0 || bytes % 16 != 0 || ((uintptr_t)dst | (uintptr_t)src) % 16 != 0) {
+    set_error("copy: %lld bytes or pointers not 16-byte aligned", (long long)bytes);
+    return PIPO_ERR_ARG;
+  }
+  if (bytes == 0) return PIPO_OK;
+  const int64_t n16 = bytes / 16;
+  int64_t blocks = (n16 + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  launch(copy16_k, dim3((unsigned)blocks), dim3(256), 0, st,
+                     reinterpret_cast<const u32x4*>(src), reinterpret_cast<u32x4*>(dst), n16);
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
 }
@@ -180,7 +203,7 @@ pipo_status launch_fill_u16(uint16_t* p, uint16_t value, int64_t n, hipStream_t 
   if (n <= 0) return PIPO_OK;
   int64_t blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(fill_u16_k, dim3((unsigned)blocks), dim3(256), 0, st, p, value, n);
+  launch(fill_u16_k, dim3((unsigned)blocks), dim3(256), 0, st, p, value, n);
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
 }

@@ -48,6 +48,11 @@ void set_error(const char* fmt, ...) {
 }
 void clear_error() { g_err.clear(); }
 
+LaunchEvents& next_launch_events() {
+  static thread_local LaunchEvents ev;
+  return ev;
+}
+
 // ---------------------------------------------------------------------------
 // pinned host allocations made through pipo_host_alloc (base -> bytes), so a
 // caller pointer can be recognised as streamable in place
@@ -161,6 +166,8 @@ struct pipo_ctx {
   int32_t* next_dev = nullptr;
   int32_t* ids_dev = nullptr;
   uint16_t* emb_dev = nullptr;
+  float* attn_ws = nullptr;    // decode-attention split partials
+  int64_t attn_ws_bytes = 0;
   char* kv = nullptr;          // resident cache or KV slots
   int64_t kv_part_bytes = 0;   // max_seq * max_batch * d * 2
 
@@ -335,7 +342,8 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
     case kAttn:
       if (p.prefill)
         return launch_attn_prefill(c->q, kc, vc, c->o, c->b, (int)p.T, (int)c->H, (int)c->dh, s);
-      return launch_attn_decode(c->q, kc, vc, c->o, c->b, (int)c->H, (int)c->dh, (int)p.pos0, s);
+      return launch_attn_decode(c->q, kc, vc, c->o, c->b, (int)c->H, (int)c->dh, (int)p.pos0,
+                                c->attn_ws, c->attn_ws_bytes, s);
     case kOproj: {
       GemmArgs ga;
       ga.out32 = c->x;
@@ -483,12 +491,14 @@ static pipo_status exec_op(pipo_ctx* c, const Op& op) {
       if (c->timestamps) {
         e0 = tevent(c);
         e1 = tevent(c);
-        PIPO_HIP_TRY(hipEventRecord(e0, s));
+        next_launch_events() = LaunchEvents{e0, e1};
       }
-      PIPO_TRY(run_kernel(c, op));
+      const pipo_status ks = run_kernel(c, op);
+      const bool unused = next_launch_events().start != nullptr;
+      next_launch_events() = LaunchEvents{};
+      PIPO_TRY(ks);
       c->stats.n_kernels++;
-      if (c->timestamps) {
-        PIPO_HIP_TRY(hipEventRecord(e1, s));
+      if (c->timestamps && !unused) {
         double by, fl;
         kernel_cost(c, op, &by, &fl);
         c->trec.push_back(TimedRec{op.kernel * 2 + (c->pass.prefill ? 1 : 0), 0, e0, e1, by, fl});
@@ -756,6 +766,10 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
     PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
     c->emb_dev = (uint16_t*)p;
   }
+  c->attn_ws_bytes = attn_decode_workspace_bytes(pol.max_batch, (int)c->H, (int)c->dh,
+                                                 kAttnDecodeMaxSplits);
+  PIPO_TRY(dev_alloc(c, &p, c->attn_ws_bytes));
+  c->attn_ws = (float*)p;
   c->kv_part_bytes = rows * d * 2;
   const int64_t kv_units = pol.kv_on_host ? pol.n_weight_slots : L;
   PIPO_TRY(dev_alloc(c, &p, kv_units * 2 * c->kv_part_bytes));

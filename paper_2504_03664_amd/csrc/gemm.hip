@@ -4,15 +4,16 @@
 // the paper's "compute directly on 4-bit weights", Section 3.4).
 //
 // Two kernels, chosen by M alone:
-//   * gemm_skinny (M <= 64, decode): every workgroup owns 32 rows of W and
-//     all M rows of X; its waves split K; W streams from HBM straight into
-//     MFMA operand registers (no LDS), X comes from L2.  Partial sums are
-//     combined across waves in LDS in a fixed order.
+//   * gemm_skinny (M <= 64, decode): every workgroup owns 16 or 64 rows of
+//     W and all M rows of X; its waves split K; W streams from HBM straight
+//     into MFMA operand registers (no LDS), X comes from L2.  Partial sums
+//     are combined across waves in LDS in a fixed order.
 //   * gemm_tiled (M > 64, prefill): 128 x 128 output tiles, K staged through
 //     double-buffered LDS in steps of 64, 4 waves of 64 x 64.
-// Both accumulate in fp32 with v_mfma_f32_16x16x32_f16.  An output element
-// depends only on its row of X, its row of W, K and the kernel choice, so
-// launching a GEMM per chunk of W rows gives the same bits as one launch.
+// Both accumulate in fp32 with v_mfma_f32_16x16x32_f16.  The summation order
+// of an element depends only on M (kernel and waves) and K, so a launch over
+// any row range of W gives the same bits for those rows as a full launch,
+// and no workgroup ever reads another workgroup's results.
 #include "common.h"
 #include "device.h"
 
@@ -46,18 +47,75 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int64_t m, int64_t n
 
 // ---------------------------------------------------------------------------
 // skinny GEMM (decode)
-constexpr int kSkNF = 2;      // 16-row fragments of W per workgroup
-constexpr int kSkWaves = 4;   // waves splitting K
+//
+// Workgroup = KW waves; it owns 16 NF rows of W (NF fragments) and all M
+// (<= 16 MF) rows of X.  K is walked in 128-wide steps; wave w takes steps
+// w, w + KW, ... UNR at a time so that UNR steps of W are in flight per
+// lane.  In a step, lane (r, g) feeds four MFMAs (8 k each) with W row
+// 16 f + r and X row 16 mf + r at the same k: fp16 W is read so that load i
+// of the 16 lanes of a row covers 64 contiguous bytes (k = 32 i + 8 g), INT4
+// codes as 32 consecutive k per lane (k = 32 g + 8 i).  Wave partials are
+// added in LDS in wave order, then the epilogue runs.
+template <int NF, int MF, int KW, int UNR, bool W4>
+struct SkinnyStep {
+  u32x4 w[NF][4];  // fp16: four 8-half chunks; int4: w[f][0] holds 32 codes
+  uint32_t sm[NF];
+  h8 x[MF][4];
 
-template <int MF, bool W4, int EPI>
-__global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny(GemmArgs a) {
-  constexpr int NF = kSkNF;
-  __shared__ f4 red[kSkWaves][NF][MF][64];
+  __device__ __forceinline__ static int koff(int i, int g) { return W4 ? 32 * g + 8 * i : 32 * i + 8 * g; }
+
+  __device__ __forceinline__ void load(const GemmArgs& a, int64_t n0, int64_t s, int r, int g) {
+    const int64_t K = a.K;
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      const int64_t n = n0 + 16 * f + r;
+      const bool ok = n < a.N;
+      if constexpr (W4) {
+        const int64_t kb = s * 128 + 32 * g;
+        w[f][0] = ok ? *reinterpret_cast<const u32x4*>(a.Wq + n * (K / 2) + kb / 2)
+                     : u32x4{0, 0, 0, 0};
+        sm[f] = ok ? *reinterpret_cast<const uint32_t*>(a.Wsm + (n * (K / 64) + kb / 64) * 2) : 0u;
+      } else {
+        const uint16_t* p = a.W + n * K + s * 128;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          w[f][i] = ok ? *reinterpret_cast<const u32x4*>(p + koff(i, g)) : u32x4{0, 0, 0, 0};
+      }
+    }
+#pragma unroll
+    for (int mf = 0; mf < MF; ++mf) {
+      const int64_t m = 16 * mf + r;
+      const uint16_t* p = a.X + m * K + s * 128;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[mf][i] = m < a.M ? load_h8(p + koff(i, g)) : zero_h8();
+    }
+  }
+
+  __device__ __forceinline__ void mma(f4 (&acc)[NF][MF]) const {
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      h8 wv[4];
+      if constexpr (W4) {
+        dequant32(w[f][0], h2f((uint16_t)(sm[f] & 0xFFFFu)), h2f((uint16_t)(sm[f] >> 16)), wv);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) wv[i] = __builtin_bit_cast(h8, w[f][i]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int mf = 0; mf < MF; ++mf) acc[f][mf] = mfma16(wv[i], x[mf][i], acc[f][mf]);
+    }
+  }
+};
+
+template <int NF, int MF, int KW, int UNR, bool W4, int EPI>
+__global__ __launch_bounds__(KW * 64) void gemm_skinny(GemmArgs a) {
+  __shared__ f4 red[KW][NF][MF][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
   const int64_t n0 = (int64_t)blockIdx.x * (16 * NF);
-  const int64_t K = a.K;
-  const int64_t nsteps = K / 128;
+  const int64_t nsteps = a.K / 128;
 
   f4 acc[NF][MF];
 #pragma unroll
@@ -65,47 +123,14 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny(GemmArgs a) {
 #pragma unroll
     for (int mf = 0; mf < MF; ++mf) acc[f][mf] = f4{0.f, 0.f, 0.f, 0.f};
 
-  // each lane owns 32 consecutive k of every 128-k step: kbase = 128 s + 32 g
-  for (int64_t s = wave; s < nsteps; s += kSkWaves) {
-    const int64_t kb = s * 128 + 32 * g;
-    h8 wv[NF][4];
+  for (int64_t s = wave; s < nsteps; s += UNR * KW) {
+    SkinnyStep<NF, MF, KW, UNR, W4> st[UNR];
 #pragma unroll
-    for (int f = 0; f < NF; ++f) {
-      const int64_t n = n0 + 16 * f + r;
-      if (n < a.N) {
-        if constexpr (W4) {
-          const u32x4 codes = *reinterpret_cast<const u32x4*>(a.Wq + n * (K / 2) + kb / 2);
-          const uint32_t smw = *reinterpret_cast<const uint32_t*>(a.Wsm + (n * (K / 64) + kb / 64) * 2);
-          dequant32(codes, h2f((uint16_t)(smw & 0xFFFFu)), h2f((uint16_t)(smw >> 16)), wv[f]);
-        } else {
-          const uint16_t* p = a.W + n * K + kb;
+    for (int u = 0; u < UNR; ++u)
+      if (s + u * KW < nsteps) st[u].load(a, n0, s + u * KW, r, g);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) wv[f][i] = load_h8(p + 8 * i);
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) wv[f][i] = zero_h8();
-      }
-    }
-    h8 xv[MF][4];
-#pragma unroll
-    for (int mf = 0; mf < MF; ++mf) {
-      const int64_t m = 16 * mf + r;
-      if (m < a.M) {
-        const uint16_t* p = a.X + m * K + kb;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) xv[mf][i] = load_h8(p + 8 * i);
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) xv[mf][i] = zero_h8();
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int f = 0; f < NF; ++f)
-#pragma unroll
-        for (int mf = 0; mf < MF; ++mf) acc[f][mf] = mfma16(wv[f][i], xv[mf][i], acc[f][mf]);
+    for (int u = 0; u < UNR; ++u)
+      if (s + u * KW < nsteps) st[u].mma(acc);
   }
 
 #pragma unroll
@@ -116,17 +141,13 @@ __global__ __launch_bounds__(kSkWaves * 64) void gemm_skinny(GemmArgs a) {
 
   // element (f, mf, lane', j): W row n0 + 16 f + 4 (lane' / 16) + j, X row 16 mf + lane' % 16
   constexpr int kElems = NF * MF * 64 * 4;
-  for (int e = threadIdx.x; e < kElems; e += kSkWaves * 64) {
-    const int j = e & 3;
-    const int ln = (e >> 2) & 63;
-    const int fm = e >> 8;
+  for (int e = threadIdx.x; e < kElems; e += KW * 64) {
+    const int j = e & 3, ln = (e >> 2) & 63, fm = e >> 8;
     const int f = fm / MF, mf = fm % MF;
     float sum = 0.f;
 #pragma unroll
-    for (int w = 0; w < kSkWaves; ++w) sum += red[w][f][mf][ln][j];
-    const int64_t n = n0 + 16 * f + 4 * (ln >> 4) + j;
-    const int64_t m = 16 * mf + (ln & 15);
-    epilogue<EPI>(a, m, n, sum);
+    for (int w = 0; w < KW; ++w) sum += red[w][f][mf][ln][j];
+    epilogue<EPI>(a, 16 * mf + (ln & 15), n0 + 16 * f + 4 * (ln >> 4) + j, sum);
   }
 }
 
@@ -249,21 +270,41 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// skinny configurations by M: (waves, steps in flight per wave)
+template <int MF> struct SkinnyCfg;
+template <> struct SkinnyCfg<1> { static constexpr int KW = 8, UNR = 2; };
+template <> struct SkinnyCfg<2> { static constexpr int KW = 8, UNR = 1; };
+template <> struct SkinnyCfg<4> { static constexpr int KW = 4, UNR = 1; };
+
+template <int NF, int MF, bool W4, int EPI>
+static void launch_skinny(const GemmArgs& a, hipStream_t st) {
+  using C = SkinnyCfg<MF>;
+  const dim3 grid((unsigned)((a.N + 16 * NF - 1) / (16 * NF)));
+  launch((gemm_skinny<NF, MF, C::KW, C::UNR, W4, EPI>), grid, dim3(C::KW * 64), 0, st, a);
+}
+
+template <int NF, bool W4, int EPI>
+static void launch_skinny_m(const GemmArgs& a, hipStream_t st) {
+  if (a.M <= 16)
+    launch_skinny<NF, 1, W4, EPI>(a, st);
+  else if (a.M <= 32)
+    launch_skinny<NF, 2, W4, EPI>(a, st);
+  else
+    launch_skinny<NF, 4, W4, EPI>(a, st);
+}
+
 template <bool W4, int EPI>
 static pipo_status launch_epi(const GemmArgs& a, hipStream_t st) {
   if (a.M <= 64) {
-    const dim3 grid((unsigned)((a.N + 16 * kSkNF - 1) / (16 * kSkNF)));
-    const dim3 block(kSkWaves * 64);
-    const int mf = (int)((a.M + 15) / 16);
-    switch (mf) {
-      case 1: hipLaunchKernelGGL((gemm_skinny<1, W4, EPI>), grid, block, 0, st, a); break;
-      case 2: hipLaunchKernelGGL((gemm_skinny<2, W4, EPI>), grid, block, 0, st, a); break;
-      case 3: hipLaunchKernelGGL((gemm_skinny<3, W4, EPI>), grid, block, 0, st, a); break;
-      default: hipLaunchKernelGGL((gemm_skinny<4, W4, EPI>), grid, block, 0, st, a); break;
-    }
+    // 64 W rows per workgroup (less X traffic per W byte) once that still
+    // gives enough workgroups to fill the chip, else 16
+    if (a.N >= 64 * 192)
+      launch_skinny_m<4, W4, EPI>(a, st);
+    else
+      launch_skinny_m<1, W4, EPI>(a, st);
   } else {
     const dim3 grid((unsigned)((a.N + kTBN - 1) / kTBN), (unsigned)((a.M + kTBM - 1) / kTBM));
-    hipLaunchKernelGGL((gemm_tiled<W4, EPI>), grid, dim3(kTThreads), 0, st, a);
+    launch((gemm_tiled<W4, EPI>), grid, dim3(kTThreads), 0, st, a);
   }
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;

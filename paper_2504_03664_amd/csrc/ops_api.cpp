@@ -102,14 +102,22 @@ pipo_status pipo_op_layernorm(const float* x, const uint16_t* gamma, const uint1
 
 pipo_status pipo_op_attn_decode(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                                 uint16_t* o, int32_t b, int32_t n_heads, int32_t head_dim,
-                                int32_t t, void* stream) {
+                                int32_t t, void* workspace, int64_t workspace_bytes,
+                                void* stream) {
   clear_error();
-  if (!q || !kc || !vc || !o) {
-    set_error("attn_decode: NULL pointer");
+  if (!q || !kc || !vc || !o || workspace_bytes < 0) {
+    set_error("attn_decode: NULL pointer or negative workspace size");
     return PIPO_ERR_ARG;
   }
   return launch_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t,
+                            static_cast<float*>(workspace), workspace_bytes,
                             static_cast<hipStream_t>(stream));
+}
+
+int64_t pipo_op_attn_decode_workspace_bytes(int32_t b, int32_t n_heads, int32_t head_dim,
+                                            int32_t t) {
+  if (b < 1 || n_heads < 1 || t < 0 || head_dim < 1) return 0;
+  return attn_decode_workspace_bytes(b, n_heads, head_dim, attn_decode_splits(b, n_heads, t));
 }
 
 pipo_status pipo_op_attn_prefill(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
@@ -132,6 +140,15 @@ pipo_status pipo_op_argmax(const float* logits, int32_t* next, int64_t rows, int
     return PIPO_ERR_ARG;
   }
   return launch_argmax(logits, next, rows, V, static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_copy(void* dst, const void* src, int64_t bytes, void* stream) {
+  clear_error();
+  if (!dst || !src) {
+    set_error("copy: NULL pointer");
+    return PIPO_ERR_ARG;
+  }
+  return launch_copy16(dst, src, bytes, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"
