@@ -16,7 +16,7 @@
 //          n_slots KV buffers [K|V][max_seq][b][d] (KV in host memory).
 //   host - pinned: packed small tensors per layer, copies of matrices the
 //          caller did not place in pinned memory, embedding staging, token
-//          readback, KV cache [n_layers][K|V][max_seq][b][d] (KV on host).
+//          readback, KV cache per layer [K|V][max_seq][b][d] (KV on host).
 #include <algorithm>
 #include <atomic>
 #include <chrono>
@@ -146,7 +146,7 @@ struct pipo_ctx {
   uint16_t* emb_stage = nullptr;                    // [max_batch * max_seq][d]
   int32_t* ids_stage = nullptr;                     // [max_batch * max_seq]
   int32_t* next_stage = nullptr;                    // [max_batch]
-  uint16_t* kv_host = nullptr;
+  std::vector<char*> kv_host;                       // per layer: [K|V][max_seq][b][d]
 
   // device side
   std::vector<void*> dev;
@@ -452,9 +452,9 @@ static pipo_status exec_op(pipo_ctx* c, const Op& op) {
       const void* src;
       const bool h2d = op.kind == OpKind::CopyH2D;
       if (op.kv) {
-        // host cache [layer][K|V][max_seq][b][d] for the current batch b
-        const int64_t host_off = ((int64_t)op.layer * 2 + op.seg) * c->pol.max_seq * c->b * c->d * 2;
-        char* hptr = reinterpret_cast<char*>(c->kv_host) + host_off + op.off;
+        // host cache of the layer: [K|V][max_seq][b][d] for the current batch b
+        const int64_t host_off = (int64_t)op.seg * c->pol.max_seq * c->b * c->d * 2;
+        char* hptr = c->kv_host[op.layer] + host_off + op.off;
         char* dptr = c->kv + (int64_t)op.slot * 2 * c->kv_part_bytes + op.seg * c->kv_part_bytes + op.off;
         dst = h2d ? (void*)dptr : (void*)hptr;
         src = h2d ? (const void*)hptr : (const void*)dptr;
@@ -785,8 +785,13 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   PIPO_TRY(pin_alloc(c, &p, (int64_t)pol.max_batch * 4));
   c->next_stage = (int32_t*)p;
   if (pol.kv_on_host) {
-    PIPO_TRY(pin_alloc(c, &p, L * 2 * c->kv_part_bytes));
-    c->kv_host = (uint16_t*)p;
+    // one pinned region per layer (the copies are per layer, and very large
+    // single pinned allocations can fail where many smaller ones succeed)
+    c->kv_host.assign((size_t)L, nullptr);
+    for (int64_t j = 0; j < L; ++j) {
+      PIPO_TRY(pin_alloc(c, &p, 2 * c->kv_part_bytes));
+      c->kv_host[j] = (char*)p;
+    }
   }
   c->stats.hbm_bytes = c->hbm_bytes;
   c->stats.pinned_host_bytes = c->pinned_bytes;
