@@ -210,13 +210,15 @@ def main():
         "config": {"workload": wl.name, "layers": shape.n_layers, "d_model": shape.d_model,
                    "batch": wl.batch, "prompt": wl.prompt,
                    "generated": 1 + W + K, "weights": f"{wl.wfmt}, pinned host, streamed",
-                   "kv_cache": "pinned host, streamed" if wl.kv_on_host else "HBM",
+                   "kv_cache": "host (pinned, or pageable through pinned staging), streamed"
+                               if wl.kv_on_host else "HBM",
                    "chunk_bytes": args.chunk_mb << 20, "slots": args.slots,
                    "h2d_streams": args.h2d_streams},
         "h2d_link": {"peak_gbps": round(peak, 2), "peak_1stream_gbps": round(peak1, 2),
                      "sustained_gbps": round(sustained, 2),
                      "frac_of_peak": round(sustained / peak, 4),
                      "bytes_per_step": int(bytes_step),
+                     "staged_bytes_per_step": int(st["staged_bytes"] / K),
                      "roofline_tokens_per_s": round(roof, 3),
                      "frac_of_roofline": round(value / roof, 4)},
         "ttft_ms": round(ttft_ms, 1),

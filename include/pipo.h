@@ -58,7 +58,8 @@ enum { PIPO_W_FP16 = 0, PIPO_W_INT4_G64 = 1 };
 enum {
   PIPO_DBG_POISON_SLOTS = 1,  /* fill a weight/KV slot with NaN before every refill */
   PIPO_DBG_COPY_DELAY = 2,    /* host-side sleep of copy_delay_us before every chunk copy */
-  PIPO_DBG_TIMESTAMPS = 4     /* record device timestamps of copies and kernels (stats) */
+  PIPO_DBG_TIMESTAMPS = 4,    /* record device timestamps of copies and kernels (stats) */
+  PIPO_DBG_KV_PAGEABLE = 8    /* keep the host KV cache in pageable memory (staged copies) */
 };
 
 /* Decoder shape.  Constraints: d_model = n_heads * head_dim with head_dim
@@ -107,9 +108,10 @@ typedef struct {
   int32_t weights_on_host;   /* 1: stream every layer each pass; 0: all layers resident in HBM */
   int32_t embed_on_host;     /* 1: stream the output head each pass, gather embeddings on the
                                 host; 0: token table resident in HBM */
-  int32_t kv_on_host;        /* 1: KV cache in library-owned pinned host memory, each layer's
-                                prefix loaded before its attention and the new rows saved
-                                after it; 0: KV cache resident in HBM */
+  int32_t kv_on_host;        /* 1: KV cache in library-owned host memory (pinned where
+                                possible, see pinned_budget_bytes), each layer's prefix loaded
+                                before its attention and the new rows saved after it (a call
+                                returns with its rows saved); 0: KV cache resident in HBM */
   int32_t n_weight_slots;    /* HBM slots the layers rotate through (default 3, min 2) */
   int32_t n_h2d_streams;     /* host-to-device copy streams (default 1, max 2) */
   int64_t chunk_bytes;       /* bytes per copy chunk (default 64 MiB; rounded to 4 KiB) */
@@ -118,6 +120,12 @@ typedef struct {
   int64_t hbm_budget_bytes;  /* 0: unlimited; else pipo_create fails with OOM_DEVICE above it */
   int32_t debug_flags;       /* PIPO_DBG_* */
   int32_t copy_delay_us;     /* delay for PIPO_DBG_COPY_DELAY */
+  int64_t pinned_budget_bytes; /* 0: pin host KV layers while the system grants pinned memory;
+                                  else at most this many bytes of pinned host KV.  KV layers
+                                  that are not pinned live in pageable memory and move through
+                                  pinned staging buffers, copied by host worker threads (the
+                                  paper's multi-thread transfer, Section 3.3) */
+  int32_t copy_threads;      /* host threads for staged copies (default 8) */
 } pipo_policy;
 
 /* Per-kernel timing (filled when PIPO_DBG_TIMESTAMPS is set): each launch
@@ -147,6 +155,7 @@ typedef struct {
   double copy_busy_ms;       /* union of host-to-device copy intervals inside the window */
   double kernel_busy_ms;     /* union of compute-stream kernel intervals inside the window */
   double busy_ms;            /* union of both */
+  int64_t staged_bytes;      /* bytes that went through the pinned staging buffers */
   int64_t hbm_bytes;         /* HBM the context holds */
   int64_t pinned_host_bytes; /* pinned host memory the context holds */
   int32_t n_kernel_stats;

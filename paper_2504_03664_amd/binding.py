@@ -26,6 +26,7 @@ STATUS_NAMES = {0: "PIPO_OK", -1: "PIPO_ERR_ARG", -2: "PIPO_ERR_OOM_DEVICE",
                 -6: "PIPO_ERR_UNSUPPORTED"}
 PIPO_W_FP16, PIPO_W_INT4_G64 = 0, 1
 PIPO_DBG_POISON_SLOTS, PIPO_DBG_COPY_DELAY, PIPO_DBG_TIMESTAMPS = 1, 2, 4
+PIPO_DBG_KV_PAGEABLE = 8
 PIPO_EPI_F16, PIPO_EPI_RELU_F16, PIPO_EPI_ADD_F32, PIPO_EPI_F32 = 0, 1, 2, 3
 PIPO_MAX_KERNEL_STATS = 16
 
@@ -54,7 +55,8 @@ class PipoPolicy(ctypes.Structure):
     _fields_ = [("wfmt", i32), ("weights_on_host", i32), ("embed_on_host", i32),
                 ("kv_on_host", i32), ("n_weight_slots", i32), ("n_h2d_streams", i32),
                 ("chunk_bytes", i64), ("max_batch", i32), ("max_seq", i32),
-                ("hbm_budget_bytes", i64), ("debug_flags", i32), ("copy_delay_us", i32)]
+                ("hbm_budget_bytes", i64), ("debug_flags", i32), ("copy_delay_us", i32),
+                ("pinned_budget_bytes", i64), ("copy_threads", i32)]
 
 
 class PipoKernelStat(ctypes.Structure):
@@ -67,7 +69,8 @@ class PipoStats(ctypes.Structure):
                 ("d2h_bytes", i64), ("n_copies", i64), ("n_kernels", i64),
                 ("decode_steps", i64), ("decode_wall_ms", f64), ("prefill_wall_ms", f64),
                 ("window_ms", f64), ("copy_busy_ms", f64), ("kernel_busy_ms", f64),
-                ("busy_ms", f64), ("hbm_bytes", i64), ("pinned_host_bytes", i64),
+                ("busy_ms", f64), ("staged_bytes", i64), ("hbm_bytes", i64),
+                ("pinned_host_bytes", i64),
                 ("n_kernel_stats", i32),
                 ("kernels", PipoKernelStat * PIPO_MAX_KERNEL_STATS)]
 

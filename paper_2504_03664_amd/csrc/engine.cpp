@@ -21,8 +21,11 @@
 #include <atomic>
 #include <chrono>
 #include <cmath>
+#include <condition_variable>
 #include <cstdarg>
+#include <cstdlib>
 #include <cstring>
+#include <functional>
 #include <map>
 #include <mutex>
 #include <string>
@@ -108,6 +111,88 @@ static void par_memcpy(void* dst, const void* src, size_t n) {
 
 static inline int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
+// Host worker threads for copies between pageable and pinned memory (the
+// paper's multi-thread parallel transfer, Section 3.3): a copy is cut into
+// one contiguous piece per thread; the caller runs piece 0 and waits.
+class CopyPool {
+ public:
+  explicit CopyPool(int n) : n_(std::max(1, n)) {
+    for (int i = 1; i < n_; ++i) th_.emplace_back([this, i] { worker(i); });
+  }
+  ~CopyPool() {
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      stop_ = true;
+    }
+    cv_.notify_all();
+    for (auto& t : th_) t.join();
+  }
+  void copy(void* dst, const void* src, size_t n) {
+    run([=](int i) {
+      const size_t per = (n + n_ - 1) / n_, a = std::min(n, i * per), b = std::min(n, a + per);
+      if (b > a) std::memcpy((char*)dst + a, (const char*)src + a, b - a);
+    });
+  }
+  void fill(void* dst, int v, size_t n) {
+    run([=](int i) {
+      const size_t per = (n + n_ - 1) / n_, a = std::min(n, i * per), b = std::min(n, a + per);
+      if (b > a) std::memset((char*)dst + a, v, b - a);
+    });
+  }
+
+ private:
+  void run(const std::function<void(int)>& fn) {
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      job_ = fn;
+      pending_ = n_ - 1;
+      ++gen_;
+    }
+    cv_.notify_all();
+    fn(0);
+    std::unique_lock<std::mutex> lk(mu_);
+    done_.wait(lk, [this] { return pending_ == 0; });
+  }
+  void worker(int i) {
+    int64_t seen = 0;
+    for (;;) {
+      std::function<void(int)> fn;
+      {
+        std::unique_lock<std::mutex> lk(mu_);
+        cv_.wait(lk, [&] { return stop_ || gen_ != seen; });
+        if (stop_) return;
+        seen = gen_;
+        fn = job_;
+      }
+      fn(i);
+      {
+        std::lock_guard<std::mutex> lk(mu_);
+        if (--pending_ == 0) done_.notify_one();
+      }
+    }
+  }
+  int n_;
+  std::vector<std::thread> th_;
+  std::mutex mu_;
+  std::condition_variable cv_, done_;
+  std::function<void(int)> job_;
+  int64_t gen_ = 0;
+  int pending_ = 0;
+  bool stop_ = false;
+};
+
+// A ring of pinned staging buffers, each with the event of the last copy
+// that used it; a D2H buffer also remembers where its data must go.
+struct StagingRing {
+  std::vector<char*> buf;
+  std::vector<hipEvent_t> ev;
+  std::vector<bool> busy;
+  std::vector<char*> dst;       // D2H: pageable destination still to be filled
+  std::vector<int64_t> bytes;
+  int64_t buf_bytes = 0;
+  int next = 0;
+};
+
 // ---------------------------------------------------------------------------
 static const char* kKernelNames[kNumKernels] = {"embed", "ln1",  "qkv",  "attn", "oproj", "ln2",
                                                 "fc1",   "fc2",  "lnf",  "head", "argmax"};
@@ -147,6 +232,10 @@ struct pipo_ctx {
   int32_t* ids_stage = nullptr;                     // [max_batch * max_seq]
   int32_t* next_stage = nullptr;                    // [max_batch]
   std::vector<char*> kv_host;                       // per layer: [K|V][max_seq][b][d]
+  std::vector<bool> kv_pinned;                      // per layer: pinned (else pageable, staged)
+  std::vector<char*> kv_pageable;                   // pageable regions to free
+  StagingRing stage_h2d, stage_d2h;
+  CopyPool* pool = nullptr;
 
   // device side
   std::vector<void*> dev;
@@ -422,6 +511,69 @@ static void kernel_cost(const pipo_ctx* c, const Op& op, double* bytes, double* 
   }
 }
 
+// ---------------------------------------------------------------------------
+// staged copies for host KV layers in pageable memory.  They run inline in
+// the executor, so every event record and wait keeps program order: a H2D
+// chunk is copied by the worker threads into a free pinned buffer and DMA'd
+// from there; a D2H chunk is DMA'd into a buffer and copied out to pageable
+// memory when that buffer is needed again or at the end of the pass.
+static pipo_status finish_d2h(pipo_ctx* c, int b) {
+  StagingRing& r = c->stage_d2h;
+  if (!r.busy[b]) return PIPO_OK;
+  PIPO_HIP_TRY(hipEventSynchronize(r.ev[b]));
+  c->pool->copy(r.dst[b], r.buf[b], (size_t)r.bytes[b]);
+  r.busy[b] = false;
+  return PIPO_OK;
+}
+
+static pipo_status drain_d2h(pipo_ctx* c) {
+  for (size_t i = 0; i < c->stage_d2h.buf.size(); ++i) {
+    const int b = (int)((c->stage_d2h.next + i) % c->stage_d2h.buf.size());  // oldest first
+    PIPO_TRY(finish_d2h(c, b));
+  }
+  return PIPO_OK;
+}
+
+// `first` (optional) is recorded right before the first DMA, so that a
+// timeline interval covers the DMA and not the host-side copy before it
+static pipo_status staged_h2d(pipo_ctx* c, void* dst, const void* src, int64_t bytes,
+                              hipStream_t s, hipEvent_t first) {
+  StagingRing& r = c->stage_h2d;
+  for (int64_t off = 0; off < bytes; off += r.buf_bytes) {
+    const int64_t n = std::min(r.buf_bytes, bytes - off);
+    const int b = r.next;
+    r.next = (r.next + 1) % (int)r.buf.size();
+    if (r.busy[b]) PIPO_HIP_TRY(hipEventSynchronize(r.ev[b]));
+    c->pool->copy(r.buf[b], (const char*)src + off, (size_t)n);
+    if (off == 0 && first) PIPO_HIP_TRY(hipEventRecord(first, s));
+    PIPO_HIP_TRY(hipMemcpyAsync((char*)dst + off, r.buf[b], (size_t)n, hipMemcpyHostToDevice, s));
+    PIPO_HIP_TRY(hipEventRecord(r.ev[b], s));
+    r.busy[b] = true;
+    c->stats.staged_bytes += n;
+  }
+  return PIPO_OK;
+}
+
+static pipo_status staged_d2h(pipo_ctx* c, void* dst, const void* src, int64_t bytes,
+                              hipStream_t s, hipEvent_t first) {
+  StagingRing& r = c->stage_d2h;
+  for (int64_t off = 0; off < bytes; off += r.buf_bytes) {
+    const int64_t n = std::min(r.buf_bytes, bytes - off);
+    const int b = r.next;
+    r.next = (r.next + 1) % (int)r.buf.size();
+    PIPO_TRY(finish_d2h(c, b));
+    if (off == 0 && first) PIPO_HIP_TRY(hipEventRecord(first, s));
+    PIPO_HIP_TRY(hipMemcpyAsync(r.buf[b], (const char*)src + off, (size_t)n, hipMemcpyDeviceToHost,
+                                s));
+    PIPO_HIP_TRY(hipEventRecord(r.ev[b], s));
+    r.busy[b] = true;
+    r.dst[b] = (char*)dst + off;
+    r.bytes[b] = n;
+    c->stats.staged_bytes += n;
+  }
+  return PIPO_OK;
+}
+
 static void delay_cb(void* arg) {
   const int64_t us = (int64_t)(intptr_t)arg;
   std::this_thread::sleep_for(std::chrono::microseconds(us));
@@ -469,10 +621,15 @@ static pipo_status exec_op(pipo_ctx* c, const Op& op) {
       if (c->timestamps) {
         e0 = tevent(c);
         e1 = tevent(c);
-        PIPO_HIP_TRY(hipEventRecord(e0, s));
       }
-      PIPO_HIP_TRY(hipMemcpyAsync(dst, src, (size_t)op.bytes,
-                                  h2d ? hipMemcpyHostToDevice : hipMemcpyDeviceToHost, s));
+      if (op.kv && !c->kv_pinned[op.layer]) {
+        PIPO_TRY(h2d ? staged_h2d(c, dst, src, op.bytes, s, e0)
+                     : staged_d2h(c, dst, src, op.bytes, s, e0));
+      } else {
+        if (e0) PIPO_HIP_TRY(hipEventRecord(e0, s));
+        PIPO_HIP_TRY(hipMemcpyAsync(dst, src, (size_t)op.bytes,
+                                    h2d ? hipMemcpyHostToDevice : hipMemcpyDeviceToHost, s));
+      }
       if (c->timestamps) {
         PIPO_HIP_TRY(hipEventRecord(e1, s));
         c->trec.push_back(TimedRec{-1, h2d ? 1 : 2, e0, e1, (double)op.bytes, 0});
@@ -532,6 +689,7 @@ static pipo_status run_pass(pipo_ctx* c, float* logits_out, int32_t* next_out, b
     c->trec.push_back(TimedRec{-1, 3, w0, w1, 0, 0});
   }
   PIPO_HIP_TRY(hipStreamSynchronize(c->st[kCompute]));
+  if (c->pool) PIPO_TRY(drain_d2h(c));   // the pass's KV saves reach pageable memory
   std::memcpy(next_out, c->next_stage, (size_t)c->b * 4);
   if (logits_out) {
     PIPO_HIP_TRY(hipMemcpy(logits_out, c->logits, (size_t)c->b * c->V * 4, hipMemcpyDeviceToHost));
@@ -546,6 +704,10 @@ static void destroy_ctx(pipo_ctx* c) {
   (void)hipSetDevice(c->device);
   for (int i = 0; i < kNumStreams; ++i)
     if (c->st[i]) (void)hipStreamSynchronize(c->st[i]);
+  for (StagingRing* r : {&c->stage_h2d, &c->stage_d2h})
+    for (auto e : r->ev) (void)hipEventDestroy(e);
+  delete c->pool;
+  for (char* p : c->kv_pageable) std::free(p);
   for (auto e : c->ev) (void)hipEventDestroy(e);
   for (auto e : c->tpool) (void)hipEventDestroy(e);
   for (int i = 0; i < kNumStreams; ++i)
@@ -785,13 +947,56 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   PIPO_TRY(pin_alloc(c, &p, (int64_t)pol.max_batch * 4));
   c->next_stage = (int32_t*)p;
   if (pol.kv_on_host) {
-    // one pinned region per layer (the copies are per layer, and very large
-    // single pinned allocations can fail where many smaller ones succeed)
-    c->kv_host.assign((size_t)L, nullptr);
-    for (int64_t j = 0; j < L; ++j) {
-      PIPO_TRY(pin_alloc(c, &p, 2 * c->kv_part_bytes));
-      c->kv_host[j] = (char*)p;
+    // One region per layer.  Layers are pinned while the budget and the
+    // system allow (the copy engines stream those directly); the rest live
+    // in pageable memory and go through pinned staging rings, which are
+    // allocated first, with 1 GiB of pinned memory held back meanwhile so
+    // that the KV layers do not take the last of what the system grants.
+    const int64_t per_layer = align_up(2 * c->kv_part_bytes, 4096);
+    const bool force_pageable = (pol.debug_flags & PIPO_DBG_KV_PAGEABLE) != 0;
+    c->pool = new CopyPool(pol.copy_threads > 0 ? pol.copy_threads : 8);
+    const int64_t buf_bytes = pol.chunk_bytes;
+    for (auto [ring, n] : {std::pair<StagingRing*, int>{&c->stage_h2d, 16},
+                           std::pair<StagingRing*, int>{&c->stage_d2h, 8}}) {
+      ring->buf_bytes = buf_bytes;
+      ring->buf.assign((size_t)n, nullptr);
+      ring->ev.assign((size_t)n, nullptr);
+      ring->busy.assign((size_t)n, false);
+      ring->dst.assign((size_t)n, nullptr);
+      ring->bytes.assign((size_t)n, 0);
+      for (int i = 0; i < n; ++i) {
+        PIPO_TRY(pin_alloc(c, &p, buf_bytes));
+        ring->buf[(size_t)i] = (char*)p;
+        PIPO_HIP_TRY(hipEventCreateWithFlags(&ring->ev[(size_t)i], hipEventDisableTiming));
+      }
     }
+    void* reserve = force_pageable ? nullptr : host_alloc_pinned((size_t)1 << 30);
+    c->kv_host.assign((size_t)L, nullptr);
+    c->kv_pinned.assign((size_t)L, false);
+    int64_t pinned_kv = 0;
+    for (int64_t j = 0; j < L; ++j) {
+      void* h = nullptr;
+      if (!force_pageable && reserve &&
+          (pol.pinned_budget_bytes == 0 || pinned_kv + per_layer <= pol.pinned_budget_bytes))
+        h = host_alloc_pinned((size_t)per_layer);
+      if (h) {
+        c->pinned.push_back(h);
+        c->pinned_bytes += per_layer;
+        pinned_kv += per_layer;
+        c->kv_pinned[j] = true;
+      } else {
+        h = std::aligned_alloc(4096, (size_t)per_layer);
+        if (!h) {
+          host_free_pinned(reserve);
+          set_error("host allocation of %lld bytes for the KV cache failed", (long long)per_layer);
+          return PIPO_ERR_OOM_HOST;
+        }
+        c->kv_pageable.push_back((char*)h);
+        c->pool->fill(h, 0, (size_t)per_layer);  // fault the pages in now
+      }
+      c->kv_host[j] = (char*)h;
+    }
+    host_free_pinned(reserve);
   }
   c->stats.hbm_bytes = c->hbm_bytes;
   c->stats.pinned_host_bytes = c->pinned_bytes;

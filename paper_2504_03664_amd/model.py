@@ -140,11 +140,13 @@ def c_policy(wfmt: str = "fp16", weights_on_host: bool = True, embed_on_host: bo
              kv_on_host: bool = False, n_weight_slots: int = 3, n_h2d_streams: int = 1,
              chunk_bytes: int = 64 << 20, max_batch: int = 1, max_seq: int = 1,
              hbm_budget_bytes: int = 0, debug_flags: int = 0,
-             copy_delay_us: int = 0) -> B.PipoPolicy:
+             copy_delay_us: int = 0, pinned_budget_bytes: int = 0,
+             copy_threads: int = 0) -> B.PipoPolicy:
     return B.PipoPolicy(B.PIPO_W_FP16 if wfmt == "fp16" else B.PIPO_W_INT4_G64,
                         int(weights_on_host), int(embed_on_host), int(kv_on_host),
                         n_weight_slots, n_h2d_streams, chunk_bytes, max_batch, max_seq,
-                        hbm_budget_bytes, debug_flags, copy_delay_us)
+                        hbm_budget_bytes, debug_flags, copy_delay_us, pinned_budget_bytes,
+                        copy_threads)
 
 
 class Decoder:

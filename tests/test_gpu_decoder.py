@@ -173,7 +173,13 @@ def test_small_model_parity_and_kv_on_host(wfmt):
         assert np.array_equal(lr.view(np.uint32), l0.view(np.uint32))
         for v in (dict(kv_on_host=True),
                   dict(kv_on_host=True, n_h2d_streams=2, chunk_bytes=8192,
-                       debug_flags=B.PIPO_DBG_POISON_SLOTS)):
+                       debug_flags=B.PIPO_DBG_POISON_SLOTS),
+                  # KV layers in pageable memory, copied through the staging rings
+                  dict(kv_on_host=True, debug_flags=B.PIPO_DBG_KV_PAGEABLE, chunk_bytes=1 << 16),
+                  dict(kv_on_host=True, debug_flags=B.PIPO_DBG_KV_PAGEABLE | B.PIPO_DBG_COPY_DELAY,
+                       copy_delay_us=100, n_h2d_streams=2, chunk_bytes=3 * 4096, copy_threads=3),
+                  # the first two layers pinned, the rest pageable
+                  dict(kv_on_host=True, pinned_budget_bytes=2 * (2 * 3 * 76 * 512 * 2) + 100)):
             log(f"  kv on host {v}")
             tk, lk = _run(hw, prompt, 6, **v)
             assert np.array_equal(tk, t0)
