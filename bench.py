@@ -41,7 +41,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", type=int, default=1, help="index into synth.WORKLOADS")
+    ap.add_argument("--workload", type=int, default=3,
+                    help="index into synth.WORKLOADS (default: the OPT-30B fp16 decode)")
     ap.add_argument("--chunk-mb", type=int, default=64)
     ap.add_argument("--slots", type=int, default=3)
     ap.add_argument("--h2d-streams", type=int, default=1)
@@ -52,19 +53,46 @@ def parse():
     return ap.parse_args()
 
 
-def skinny_symbol(M, N, epi, w4):
-    """Kernel symbol the library launches for a decode GEMM (gemm.hip's rule:
-    64 W rows per workgroup when N >= 12288, else 16; waves by M)."""
-    nf = 4 if N >= 64 * 192 else 1
-    mf = 1 if M <= 16 else (2 if M <= 32 else 4)
-    kw, unr = {1: (8, 2), 2: (8, 1), 4: (4, 1)}[mf]
-    return f"gemm_skinny<{nf}, {mf}, {kw}, {unr}, {'true' if w4 else 'false'}, {epi}>(GemmArgs)"
+# the decode GEMM kernel plan of gemm.hip, restated to name the kernels in
+# rocprofv3 output: (NF, KW, PD, KC) of the streaming kernel by (INT4, MF)
+_STREAM_SEL = {(False, 2): (1, 8, 2, 128), (False, 4): (1, 8, 2, 128), (False, 8): (1, 8, 2, 128),
+               (True, 2): (1, 8, 4, 256), (True, 4): (2, 8, 4, 256), (True, 8): (2, 8, 4, 128)}
 
 
-def measured_traffic(workload_name, symbol):
-    """HBM bytes per dispatch of `symbol` from the committed rocprofv3 PMC
-    summary of this workload, or None if there is none or the kernel
-    sources changed since it was taken."""
+def gemm_family(M):
+    return "gemm_skinny" if M <= 16 else ("gemm_stream" if M <= 128 else "gemm_tiled")
+
+
+def gemm_symbols(M, N, K, epi, w4):
+    """Kernel symbols one GEMM launches: skinny (M <= 16; 64 W rows per
+    workgroup when N >= 12288), streaming (16 < M <= 128; K split into the
+    largest power of two <= 8 keeping the grid within 256 workgroups, plus
+    its combine kernel), or tiled."""
+    b = "true" if w4 else "false"
+    if M <= 16:
+        nf = 4 if N >= 64 * 192 else 1
+        return [f"gemm_skinny<{nf}, 1, 8, 2, {b}, {epi}>(GemmArgs)"]
+    if M > 128:
+        return [f"gemm_tiled<{b}, {epi}>(GemmArgs)"]
+    mf = 2 if M <= 32 else (4 if M <= 64 else 8)
+    nf, kw, pd, kc = _STREAM_SEL[(w4, mf)]
+    if K % kc:
+        pd, kc = (pd if kc == 128 else 2 * pd), 128
+    blocks = -(-N // (16 * nf * kw))
+    S = 1
+    while S < 8 and blocks * 2 * S <= 256 and K % (2 * S * kc) == 0:
+        S *= 2
+    syms = [f"gemm_stream<{nf}, {mf}, {kw}, {pd}, {b}, {kc}, {epi}>(GemmArgs, float*, long)"]
+    if S > 1:
+        syms.append(f"gemm_combine<{epi}>(GemmArgs, float const*, int)")
+    return syms
+
+
+def measured_traffic(workload_name, symbols):
+    """HBM bytes per dispatch of the kernels `symbols` (summed) from the
+    committed rocprofv3 PMC summary of this workload, or None if there is
+    none, a kernel is missing from it, or the kernel sources changed since
+    it was taken."""
     import hashlib
     tag = workload_name.split()[0] + "_" + workload_name.split()[1]
     path = os.path.join(ROOT, "profiles", f"hbm_traffic_{tag}.json")
@@ -76,10 +104,13 @@ def measured_traffic(workload_name, symbol):
     for src in KERNEL_SOURCES:
         with open(os.path.join(ROOT, "paper_2504_03664_amd", "csrc", src), "rb") as f:
             h.update(f.read())
-    if rec.get("kernel_source_sha256") != h.hexdigest() or symbol not in rec["per_dispatch"]:
+    if rec.get("kernel_source_sha256") != h.hexdigest():
         return None, None
-    d = rec["per_dispatch"][symbol]
-    return d["fetch_bytes"] + d["write_bytes"], os.path.relpath(path, ROOT).replace(".json", ".md")
+    if any(sym not in rec["per_dispatch"] for sym in symbols):
+        return None, None
+    total = sum(rec["per_dispatch"][sym]["fetch_bytes"] + rec["per_dispatch"][sym]["write_bytes"]
+                for sym in symbols)
+    return total, os.path.relpath(path, ROOT).replace(".json", ".md")
 
 
 def cpu_baseline(wl, seed, sample_layers=2, steps=3):
@@ -231,12 +262,12 @@ def main():
                            "source": "HIP events around every copy and kernel"}
         # dominant decode kernel, grouped by kernel symbol: the GEMM epilogue is
         # a template parameter, so the out-projection and FC2 share one symbol
-        gemm = "gemm_skinny" if wl.batch <= 64 else "gemm_tiled"
+        gemm = gemm_family(wl.batch)
         families = {f"{gemm}<add_f32> (oproj+fc2)": ("oproj_decode", "fc2_decode"),
                     f"{gemm}<relu_f16> (fc1)": ("fc1_decode",),
                     f"{gemm}<qkv> (qkv)": ("qkv_decode",),
                     f"{gemm}<f32> (head)": ("head_decode",),
-                    "attn_decode_k (attention)": ("attn_decode",)}
+                    "attn_decode_k+combine (attention)": ("attn_decode",)}
         fam = {}
         for fname, members in families.items():
             ks = [st["kernels"][m] for m in members if m in st["kernels"]]
@@ -248,15 +279,16 @@ def main():
         ach = ks["alg_bytes"] / (ks["total_ms"] * 1e-3) / 1e9
         epi = {"oproj": 2, "fc1": 1, "qkv": 4, "head": 3}
         fam_key = name.split("(")[1].split("+")[0].rstrip(")")
-        symbol = None
-        if fam_key in epi and wl.batch <= 64:
-            n_of = {"oproj": shape.d_model, "fc1": shape.d_ffn, "qkv": 3 * shape.d_model,
-                    "head": shape.vocab}
-            symbol = skinny_symbol(wl.batch, n_of[fam_key], epi[fam_key],
+        symbols = None
+        if fam_key in epi:
+            d, F = shape.d_model, shape.d_ffn
+            nk = {"oproj": (d, d), "fc1": (F, d), "qkv": (3 * d, d), "head": (shape.vocab, d)}
+            symbols = gemm_symbols(wl.batch, *nk[fam_key], epi[fam_key],
                                    wl.wfmt == "int4" and fam_key != "head")
         elif fam_key == "attention":
-            symbol = f"attn_decode_k<{shape.d_model // shape.n_heads}>"
-        traffic, tsrc = measured_traffic(wl.name, symbol) if symbol else (None, None)
+            symbols = [f"attn_decode_k<{shape.d_model // shape.n_heads}>"]
+        symbol = " + ".join(symbols) if symbols else None
+        traffic, tsrc = measured_traffic(wl.name, symbols) if symbols else (None, None)
         out["roofline"] = {"kernel": name, "symbol": symbol, "bound": "hbm",
                            "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                            "frac": round(ach / HBM_PEAK_GBPS, 4),

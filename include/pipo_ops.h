@@ -35,18 +35,30 @@ enum { PIPO_EPI_F16 = 0, PIPO_EPI_RELU_F16 = 1, PIPO_EPI_ADD_F32 = 2, PIPO_EPI_F
  * Y = X . W^T with the chosen epilogue (the projections of a layer and the
  * output head).  X: [M][K] fp16 (row stride K); W: [N][K] fp16; out: [M][N]
  * (row stride N), fp16 or fp32 per epilogue.  K must be a multiple of 128.
- * The summation order of an element depends only on M and K, so a launch
- * over a row range of W gives those rows bit for bit as a full launch.
+ * For 16 < M <= 128 the K range may be split over workgroups whose fp32
+ * partial sums go to `workspace` (device, caller-owned, contents
+ * arbitrary) of pipo_op_gemm_workspace_bytes(M, N, K, wfmt) bytes; a second
+ * kernel adds them in a fixed order and applies the epilogue.  With less
+ * (or NULL) workspace the GEMM runs unsplit; the result is the same up to
+ * rounding.  Calls sharing a workspace must not overlap in time.  For a
+ * given (M, N, K, workspace sufficient or not) the summation order is
+ * fixed, so repeated calls give the same bits.
  */
 pipo_status pipo_op_gemm_f16(const uint16_t* X, const uint16_t* W, const uint16_t* bias,
                              void* out, int64_t M, int64_t N, int64_t K, int32_t epi,
-                             void* stream);
+                             void* workspace, int64_t workspace_bytes, void* stream);
 
 /* Same with group-wise INT4 W (pipo_q4 layout, device pointers): the codes
- * are expanded to fp16 inside the GEMM (Section 3.4), never in HBM. */
+ * are expanded to fp16 inside the GEMM (Section 3.4), never in HBM; every
+ * code becomes code * scale + min rounded once to fp16. */
 pipo_status pipo_op_gemm_w4(const uint16_t* X, const uint8_t* Wq, const uint16_t* Wsm,
                             const uint16_t* bias, void* out, int64_t M, int64_t N, int64_t K,
-                            int32_t epi, void* stream);
+                            int32_t epi, void* workspace, int64_t workspace_bytes,
+                            void* stream);
+
+/* Workspace bytes the GEMM of this shape uses to split K (0: never splits).
+ * wfmt: PIPO_W_FP16 or PIPO_W_INT4_G64. */
+int64_t pipo_op_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int32_t wfmt);
 
 /* y[r][:] = LN(x[r*src_stride + src_offset][:]) * gamma + beta, r < rows;
  * x fp32 [.][d], y fp16 [rows][d], statistics in fp32. */

@@ -108,8 +108,9 @@ _SIGNATURES = {
     "pipo_copy_h2d": ([vp, vp, sz], i32),
     "pipo_copy_d2h": ([vp, vp, sz], i32),
     "pipo_dev_synchronize": ([], i32),
-    "pipo_op_gemm_f16": ([vp, vp, vp, vp, i64, i64, i64, i32, vp], i32),
-    "pipo_op_gemm_w4": ([vp, vp, vp, vp, vp, i64, i64, i64, i32, vp], i32),
+    "pipo_op_gemm_f16": ([vp, vp, vp, vp, i64, i64, i64, i32, vp, i64, vp], i32),
+    "pipo_op_gemm_w4": ([vp, vp, vp, vp, vp, i64, i64, i64, i32, vp, i64, vp], i32),
+    "pipo_op_gemm_workspace_bytes": ([i64, i64, i64, i32], i64),
     "pipo_op_layernorm": ([vp, vp, vp, vp, i64, i64, i64, i64, f32, vp], i32),
     "pipo_op_attn_decode": ([vp, vp, vp, vp, i32, i32, i32, i32, vp, i64, vp], i32),
     "pipo_op_attn_decode_workspace_bytes": ([i32, i32, i32, i32], i64),
@@ -278,12 +279,21 @@ def pipo_dev_synchronize() -> None:
     _check(lib().pipo_dev_synchronize(), "pipo_dev_synchronize")
 
 
-def pipo_op_gemm_f16(X, W, bias, out, M, N, K, epi, stream=None):
-    _check(lib().pipo_op_gemm_f16(X, W, bias, out, M, N, K, epi, stream), "pipo_op_gemm_f16")
+def pipo_op_gemm_f16(X, W, bias, out, M, N, K, epi, workspace=None, workspace_bytes=0,
+                     stream=None):
+    _check(lib().pipo_op_gemm_f16(X, W, bias, out, M, N, K, epi, workspace, workspace_bytes,
+                                  stream), "pipo_op_gemm_f16")
 
 
-def pipo_op_gemm_w4(X, Wq, Wsm, bias, out, M, N, K, epi, stream=None):
-    _check(lib().pipo_op_gemm_w4(X, Wq, Wsm, bias, out, M, N, K, epi, stream), "pipo_op_gemm_w4")
+def pipo_op_gemm_w4(X, Wq, Wsm, bias, out, M, N, K, epi, workspace=None, workspace_bytes=0,
+                    stream=None):
+    _check(lib().pipo_op_gemm_w4(X, Wq, Wsm, bias, out, M, N, K, epi, workspace,
+                                 workspace_bytes, stream), "pipo_op_gemm_w4")
+
+
+def pipo_op_gemm_workspace_bytes(M, N, K, wfmt) -> int:
+    """wfmt: PIPO_W_FP16 or PIPO_W_INT4_G64."""
+    return lib().pipo_op_gemm_workspace_bytes(M, N, K, wfmt)
 
 
 def pipo_op_layernorm(x, g, b, y, rows, d, src_stride, src_offset, eps, stream=None):

@@ -31,9 +31,13 @@ void clear_error();
     if (s_ != PIPO_OK) return s_;  \
   } while (0)
 
-// Events that bracket the next kernel launch made on this thread.  They are
-// attached to the dispatch itself (hipExtLaunchKernelGGL), so they time the
-// kernel alone rather than the stream's progress around it.
+// Events that bracket the kernel launches of one operation made on this
+// thread.  They are attached to the dispatches themselves
+// (hipExtLaunchKernelGGL), so they time the kernels rather than the
+// stream's progress around them: `start` marks the start of the first
+// dispatch, and `stop` is re-recorded at the end of every dispatch until the
+// caller clears it, so an operation of several kernels (a split GEMM and its
+// combine) is timed from its first kernel's start to its last one's end.
 struct LaunchEvents {
   hipEvent_t start = nullptr, stop = nullptr;
 };
@@ -42,9 +46,9 @@ LaunchEvents& next_launch_events();
 template <typename F, typename... Args>
 inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t st, Args... args) {
   LaunchEvents& ev = next_launch_events();
-  if (ev.start) {
+  if (ev.start || ev.stop) {
     const LaunchEvents e = ev;
-    ev = LaunchEvents{};
+    ev.start = nullptr;
     hipExtLaunchKernelGGL(kernel, grid, block, lds, st, e.start, e.stop, 0u, args...);
   } else {
     hipLaunchKernelGGL(kernel, grid, block, lds, st, args...);
@@ -80,7 +84,14 @@ struct GemmArgs {
 };
 
 // kernel launchers (gemm.hip, attention.hip, elementwise.hip)
-pipo_status launch_gemm(const GemmArgs& a, bool w4, int epi, hipStream_t st);
+// 16 < M <= 128 may split K over workgroups; their partial sums need
+// `workspace` (gemm_workspace_bytes; contents arbitrary, not shared by
+// overlapping launches).  With less the GEMM runs unsplit, equal up to
+// rounding.  gemm_workspace_bytes_upto covers every M up to M_max.
+pipo_status launch_gemm(const GemmArgs& a, bool w4, int epi, float* workspace,
+                        int64_t workspace_bytes, hipStream_t st);
+int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, bool w4);
+int64_t gemm_workspace_bytes_upto(int64_t M_max, int64_t N, int64_t K, bool w4);
 pipo_status launch_layernorm(const float* x, const uint16_t* g, const uint16_t* b, uint16_t* y,
                              int64_t rows, int64_t d, int64_t src_stride, int64_t src_offset,
                              float eps, hipStream_t st);

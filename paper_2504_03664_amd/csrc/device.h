@@ -35,18 +35,60 @@ __device__ __forceinline__ f4 mfma16(h8 a, h8 b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 
-// expand 32 int4 codes (16 bytes, code 2i in the low nibble of byte i) to
-// fp16 (code * s + m, computed in fp32) as four groups of eight
-__device__ __forceinline__ void dequant32(u32x4 codes, float s, float m, h8 out[4]) {
+// INT4 expansion.  A code c (0..15) placed in the low mantissa bits under
+// the exponent of 1024.0 (fp16 0x6400, where the spacing is exactly 1) reads
+// as 1024 + c; subtracting 1024 is exact, and one fused multiply-add gives
+// c * s + m rounded once to fp16.  Two codes are expanded per packed fp16
+// operation.  Codes come four bytes (eight codes, code 2i in the low nibble
+// of byte i) to a 32-bit word.
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+
+// (scale, min) pair word -> (s, s) and (m, m)
+__device__ __forceinline__ void scale_min_pairs(uint32_t sm, h2& s2, h2& m2) {
+  s2 = __builtin_bit_cast(h2, (sm & 0xFFFFu) | (sm << 16));
+  m2 = __builtin_bit_cast(h2, (sm >> 16) | (sm & 0xFFFF0000u));
+}
+
+__device__ __forceinline__ h2 dequant_pair(uint32_t t, h2 s2, h2 m2) {
+  const h2 c = __builtin_bit_cast(h2, t | 0x64006400u) - h2{(_Float16)1024.f, (_Float16)1024.f};
+  return __builtin_elementwise_fma(c, s2, m2);
+}
+
+// eight codes in the order (0, 4, 1, 5, 2, 6, 3, 7): two operations per pair
+__device__ __forceinline__ h8 dequant8_interleaved(uint32_t v, h2 s2, h2 m2) {
+  h8 out;
 #pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    uint32_t v = codes[w];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      float c = (float)((v >> (4 * i)) & 0xFu);
-      out[w][i] = (_Float16)__builtin_fmaf(c, s, m);
-    }
+  for (int j = 0; j < 4; ++j) {
+    const h2 w = dequant_pair((v >> (4 * j)) & 0x000F000Fu, s2, m2);
+    out[2 * j] = w[0];
+    out[2 * j + 1] = w[1];
   }
+  return out;
+}
+
+// eight codes in natural order
+__device__ __forceinline__ h8 dequant8(uint32_t v, h2 s2, h2 m2) {
+  h8 out;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t b = v >> (8 * j);
+    const h2 w = dequant_pair((b & 0xFu) | ((b << 12) & 0xF0000u), s2, m2);
+    out[2 * j] = w[0];
+    out[2 * j + 1] = w[1];
+  }
+  return out;
+}
+
+// eight fp16 values permuted to the order of dequant8_interleaved, so that
+// an MFMA sees matching k on both operands
+__device__ __forceinline__ h8 interleave_h8(h8 x) {
+  const u32x4 d = __builtin_bit_cast(u32x4, x);
+  u32x4 o;
+  o[0] = (d[0] & 0xFFFFu) | (d[2] << 16);
+  o[1] = (d[0] >> 16) | (d[2] & 0xFFFF0000u);
+  o[2] = (d[1] & 0xFFFFu) | (d[3] << 16);
+  o[3] = (d[1] >> 16) | (d[3] & 0xFFFF0000u);
+  return __builtin_bit_cast(h8, o);
 }
 
 template <typename T>

@@ -257,6 +257,8 @@ struct pipo_ctx {
   uint16_t* emb_dev = nullptr;
   float* attn_ws = nullptr;    // decode-attention split partials
   int64_t attn_ws_bytes = 0;
+  float* gemm_ws = nullptr;    // GEMM K-split partials
+  int64_t gemm_ws_bytes = 0;
   char* kv = nullptr;          // resident cache or KV slots
   int64_t kv_part_bytes = 0;   // max_seq * max_batch * d * 2
 
@@ -397,7 +399,7 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
     } else {
       ga.W = reinterpret_cast<const uint16_t*>(base + c->seg_off[seg]);
     }
-    return launch_gemm(ga, c->w4, epi, s);
+    return launch_gemm(ga, c->w4, epi, c->gemm_ws, c->gemm_ws_bytes, s);
   };
   switch (op.kernel) {
     case kEmbed: {
@@ -466,7 +468,7 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
       ga.K = d;
       ga.out32 = c->logits;
       ga.ldo = c->V;
-      return launch_gemm(ga, false, EPI_F32, s);
+      return launch_gemm(ga, false, EPI_F32, c->gemm_ws, c->gemm_ws_bytes, s);
     }
     case kArgmax:
       return launch_argmax(c->logits, c->next_dev, c->b, c->V, s);
@@ -932,6 +934,20 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
                                                  kAttnDecodeMaxSplits);
   PIPO_TRY(dev_alloc(c, &p, c->attn_ws_bytes));
   c->attn_ws = (float*)p;
+  {
+    // GEMM rows: b (decode) or b * P (prefill), at most max_batch * max_seq
+    const int64_t m_max = rows;
+    const int64_t shapes[5][3] = {{3 * d, d, c->w4}, {d, d, c->w4}, {F, d, c->w4},
+                                  {d, F, c->w4}, {V, d, 0}};
+    for (const auto& sh : shapes) {
+      const int64_t b = gemm_workspace_bytes_upto(m_max, sh[0], sh[1], sh[2] != 0);
+      c->gemm_ws_bytes = b > c->gemm_ws_bytes ? b : c->gemm_ws_bytes;
+    }
+    if (c->gemm_ws_bytes > 0) {
+      PIPO_TRY(dev_alloc(c, &p, c->gemm_ws_bytes));
+      c->gemm_ws = (float*)p;
+    }
+  }
   c->kv_part_bytes = rows * d * 2;
   const int64_t kv_units = pol.kv_on_host ? pol.n_weight_slots : L;
   PIPO_TRY(dev_alloc(c, &p, kv_units * 2 * c->kv_part_bytes));

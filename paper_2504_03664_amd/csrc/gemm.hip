@@ -3,17 +3,24 @@
 // with W in fp16 or group-wise INT4 (codes expanded to fp16 in registers,
 // the paper's "compute directly on 4-bit weights", Section 3.4).
 //
-// Two kernels, chosen by M alone:
-//   * gemm_skinny (M <= 64, decode): every workgroup owns 16 or 64 rows of
+// Three kernels, chosen by M:
+//   * gemm_skinny (M <= 16, decode): every workgroup owns 16 or 64 rows of
 //     W and all M rows of X; its waves split K; W streams from HBM straight
 //     into MFMA operand registers (no LDS), X comes from L2.  Partial sums
 //     are combined across waves in LDS in a fixed order.
-//   * gemm_tiled (M > 64, prefill): 128 x 128 output tiles, K staged through
-//     double-buffered LDS in steps of 64, 4 waves of 64 x 64.
-// Both accumulate in fp32 with v_mfma_f32_16x16x32_f16.  The summation order
-// of an element depends only on M (kernel and waves) and K, so a launch over
-// any row range of W gives the same bits for those rows as a full launch,
-// and no workgroup ever reads another workgroup's results.
+//   * gemm_stream (16 < M <= 128, decode): waves split the rows of W, the
+//     chunk of X that all of them need is staged once per workgroup in LDS,
+//     and each wave keeps several chunks of its W rows in flight in
+//     registers.  K may be split over workgroups; their fp32 partial sums
+//     go to a workspace that gemm_combine adds up in a fixed order.
+//   * gemm_tiled (M > 128, prefill): 128 x 128 output tiles, K staged
+//     through double-buffered LDS in steps of 64, 4 waves of 64 x 64; tiles
+//     ordered per XCD so that each XCD's L2 serves a compact block.
+// All accumulate in fp32 with v_mfma_f32_16x16x32_f16, and INT4 codes
+// become the same fp16 values (code * scale + min, rounded once) in every
+// kernel.  The kernel, its configuration and the K split depend only on
+// (M, N, K), so a given shape always sums in the same order; no workgroup
+// reads another workgroup's results within a launch.
 #include "common.h"
 #include "device.h"
 
@@ -92,19 +99,23 @@ struct SkinnyStep {
   }
 
   __device__ __forceinline__ void mma(f4 (&acc)[NF][MF]) const {
+    // INT4: codes are expanded in the order (0, 4, 1, 5, ...) of each group
+    // of eight k; X is permuted to match
+    h8 xv[MF][4];
+#pragma unroll
+    for (int mf = 0; mf < MF; ++mf)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xv[mf][i] = W4 ? interleave_h8(x[mf][i]) : x[mf][i];
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
-      h8 wv[4];
-      if constexpr (W4) {
-        dequant32(w[f][0], h2f((uint16_t)(sm[f] & 0xFFFFu)), h2f((uint16_t)(sm[f] >> 16)), wv);
-      } else {
+      h2 s2, m2;
+      if constexpr (W4) scale_min_pairs(sm[f], s2, m2);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) wv[i] = __builtin_bit_cast(h8, w[f][i]);
+      for (int i = 0; i < 4; ++i) {
+        const h8 wv = W4 ? dequant8_interleaved(w[f][0][i], s2, m2) : __builtin_bit_cast(h8, w[f][i]);
+#pragma unroll
+        for (int mf = 0; mf < MF; ++mf) acc[f][mf] = mfma16(wv, xv[mf][i], acc[f][mf]);
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int mf = 0; mf < MF; ++mf) acc[f][mf] = mfma16(wv[i], x[mf][i], acc[f][mf]);
     }
   }
 };
@@ -152,9 +163,179 @@ __global__ __launch_bounds__(KW * 64) void gemm_skinny(GemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// streaming GEMM (decode at 16 < M <= 128)
+//
+// Workgroup = KW waves; wave w owns W rows n0 + 16 NF w .. + 16 NF and the
+// workgroup covers k in [z kper, (z + 1) kper), z = blockIdx.y.  K is walked
+// in chunks of KC: the X chunk (16 MF rows x KC) is loaded once per
+// workgroup into one of two LDS buffers, one barrier per chunk; each wave
+// holds PD chunks of its W rows in registers, refilling a chunk's registers
+// as soon as its MFMAs are issued.  Every load is unconditional (row and
+// chunk indexes are clamped: rows past M or N are computed and never
+// stored, a clamped chunk is loaded again and not used), which keeps the
+// compiler's wait counts exact so that the prefetch really stays in flight.
+// In a chunk, lane (r, g) feeds MFMA i with W row 16 f + r at
+// k = 32 i + 8 g (fp16) or k = 32 g + 8 i (INT4: 32 consecutive codes per
+// lane, expanded in interleaved order, X permuted to match).
+template <int NF, int MF, int KW, int PD, bool W4, int KC>
+struct StreamCfg {
+  static constexpr int kXRows = 16 * MF;
+  static constexpr int kXLd = KC + 8;  // halves per LDS row (padding against bank conflicts)
+  static constexpr int kThreads = KW * 64;
+  static constexpr int kXH8 = kXRows * KC / 8;                       // 8-half pieces per X chunk
+  static constexpr int kXPerThread = (kXH8 + kThreads - 1) / kThreads;
+  static constexpr int kWRegs = W4 ? KC / 128 : KC / 32;             // u32x4 per W row per chunk
+  static constexpr int kRowsPerWG = 16 * NF * KW;
+};
+
+__device__ __forceinline__ int64_t clamp_hi(int64_t v, int64_t hi) { return v < hi ? v : hi; }
+
+template <int NF, int MF, int KW, int PD, bool W4, int KC, int EPI>
+__global__ __launch_bounds__(KW * 64) void gemm_stream(GemmArgs a, float* part, int64_t kper) {
+  using C = StreamCfg<NF, MF, KW, PD, W4, KC>;
+  __shared__ __attribute__((aligned(16))) uint16_t Xs[2][C::kXRows * C::kXLd];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15, g = lane >> 4;
+  const int64_t nw0 = ((int64_t)blockIdx.x * KW + wave) * (16 * NF);
+  const int64_t kbeg = (int64_t)blockIdx.y * kper;
+  const int64_t nch = kper / KC;
+  const int64_t K = a.K;
+  int64_t wrow[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) wrow[f] = clamp_hi(nw0 + 16 * f + r, a.N - 1);
+
+  struct WChunk {
+    u32x4 w[NF][C::kWRegs];
+    uint32_t sm[NF][W4 ? KC / 128 : 1];
+  };
+  const auto load_w = [&](WChunk& F, int64_t c) {
+    const int64_t k0 = kbeg + clamp_hi(c, nch - 1) * KC;
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      if constexpr (W4) {
+#pragma unroll
+        for (int t = 0; t < KC / 128; ++t) {
+          const int64_t kb = k0 + 128 * t + 32 * g;
+          F.w[f][t] = *reinterpret_cast<const u32x4*>(a.Wq + wrow[f] * (K / 2) + kb / 2);
+          F.sm[f][t] = *reinterpret_cast<const uint32_t*>(a.Wsm + (wrow[f] * (K / 64) + kb / 64) * 2);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < C::kWRegs; ++i)
+          F.w[f][i] = *reinterpret_cast<const u32x4*>(a.W + wrow[f] * K + k0 + 32 * i + 8 * g);
+      }
+    }
+  };
+  h8 xr[C::kXPerThread];
+  const auto load_x = [&](int64_t c) {
+    const int64_t k0 = kbeg + clamp_hi(c, nch - 1) * KC;
+#pragma unroll
+    for (int j = 0; j < C::kXPerThread; ++j) {
+      const int e = tid + j * C::kThreads < C::kXH8 ? tid + j * C::kThreads : C::kXH8 - 1;
+      const int row = e / (KC / 8), col = (e % (KC / 8)) * 8;
+      xr[j] = load_h8(a.X + clamp_hi(row, a.M - 1) * K + k0 + col);
+    }
+  };
+  const auto store_x = [&](int b) {
+#pragma unroll
+    for (int j = 0; j < C::kXPerThread; ++j) {
+      const int e = tid + j * C::kThreads;
+      if (e < C::kXH8) {
+        const int row = e / (KC / 8), col = (e % (KC / 8)) * 8;
+        *reinterpret_cast<h8*>(&Xs[b][row * C::kXLd + col]) = xr[j];
+      }
+    }
+  };
+  f4 acc[NF][MF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int mf = 0; mf < MF; ++mf) acc[f][mf] = f4{0.f, 0.f, 0.f, 0.f};
+  const auto compute = [&](const WChunk& F, int b) {
+#pragma unroll
+    for (int t = 0; t < KC / 128; ++t) {
+      h2 s2[NF], m2[NF];
+      if constexpr (W4) {
+#pragma unroll
+        for (int f = 0; f < NF; ++f) scale_min_pairs(F.sm[f][t], s2[f], m2[f]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int kl = 128 * t + (W4 ? 32 * g + 8 * i : 32 * i + 8 * g);
+        h8 xv[MF];
+#pragma unroll
+        for (int mf = 0; mf < MF; ++mf) {
+          xv[mf] = *reinterpret_cast<const h8*>(&Xs[b][(16 * mf + r) * C::kXLd + kl]);
+          if constexpr (W4) xv[mf] = interleave_h8(xv[mf]);
+        }
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+          const h8 wv = W4 ? dequant8_interleaved(F.w[f][t][i], s2[f], m2[f])
+                           : __builtin_bit_cast(h8, F.w[f][4 * t + i]);
+#pragma unroll
+          for (int mf = 0; mf < MF; ++mf) acc[f][mf] = mfma16(wv, xv[mf], acc[f][mf]);
+        }
+      }
+    }
+  };
+
+  WChunk F[PD];
+#pragma unroll
+  for (int p = 0; p < PD; ++p) {
+    load_w(F[p], p);
+    __builtin_amdgcn_sched_barrier(0);  // keep the chunks' loads in chunk order
+  }
+  load_x(0);
+  store_x(0);
+  __syncthreads();
+  for (int64_t c0 = 0; c0 < nch; c0 += PD) {
+#pragma unroll
+    for (int p = 0; p < PD; ++p) {
+      const int64_t c = c0 + p;
+      load_x(c + 1);
+      if (c < nch) compute(F[p], (int)(c & 1));
+      load_w(F[p], c + PD);
+      __builtin_amdgcn_sched_barrier(0);
+      // buffer (c + 1) & 1 was last read in chunk c - 1, before the barrier
+      store_x((int)((c + 1) & 1));
+      __syncthreads();
+    }
+  }
+
+  // acc[f][mf] element j: W row nw0 + 16 f + 4 g + j, X row 16 mf + r
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int mf = 0; mf < MF; ++mf)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t m = 16 * mf + r, n = nw0 + 16 * f + 4 * g + j;
+        if (gridDim.y == 1) {
+          epilogue<EPI>(a, m, n, acc[f][mf][j]);
+        } else if (m < a.M && n < a.N) {
+          part[((int64_t)blockIdx.y * a.M + m) * a.N + n] = acc[f][mf][j];
+        }
+      }
+}
+
+// out = sum over z = 0 .. S-1 (in that order) of part[z], then the epilogue
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_combine(GemmArgs a, const float* part, int S) {
+  const int64_t MN = a.M * a.N;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= MN) return;
+  float sum = 0.f;
+  for (int z = 0; z < S; ++z) sum += part[z * MN + e];
+  epilogue<EPI>(a, e / a.N, e % a.N, sum);
+}
+
+// ---------------------------------------------------------------------------
 // tiled GEMM (prefill)
 constexpr int kTBM = 128, kTBN = 128, kTBK = 64, kTPad = 8;
 constexpr int kTThreads = 256;  // 2 x 2 waves of 64 x 64
+constexpr int kXcds = 8;        // accelerator complex dies of an MI355X, each with its own L2
+constexpr int kTGroupM = 8;
 
 template <bool W4, int EPI>
 __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
@@ -166,8 +347,21 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
   const int lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, g = lane >> 4;
   const int wm = wave >> 1, wn = wave & 1;
-  const int64_t m0 = (int64_t)blockIdx.y * kTBM;
-  const int64_t n0 = (int64_t)blockIdx.x * kTBN;
+  // Tile order.  Workgroups are dealt to the 8 XCDs round-robin, and each
+  // XCD has its own L2: give XCD x a contiguous range of tiles, and walk
+  // that range in groups of kTGroupM row tiles (row tile fastest), so that
+  // the workgroups an XCD runs at once share A rows and B columns in L2.
+  const int64_t tiles_m = (a.M + kTBM - 1) / kTBM, tiles_n = (a.N + kTBN - 1) / kTBN;
+  const int64_t total = tiles_m * tiles_n;
+  const int64_t per_xcd = (total + kXcds - 1) / kXcds;
+  const int64_t tile = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (tile >= total) return;
+  const int64_t group = tile / (kTGroupM * tiles_n);
+  const int64_t first_m = group * kTGroupM;
+  const int64_t gm = tiles_m - first_m < kTGroupM ? tiles_m - first_m : kTGroupM;
+  const int64_t in_group = tile - group * kTGroupM * tiles_n;
+  const int64_t m0 = (first_m + in_group % gm) * kTBM;
+  const int64_t n0 = (in_group / gm) * kTBN;
   const int64_t K = a.K;
   const int64_t KT = K / kTBK;
 
@@ -189,7 +383,10 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
         const u32x4 codes =
             *reinterpret_cast<const u32x4*>(a.Wq + n * (K / 2) + kt * (kTBK / 2) + half * 16);
         const uint32_t smw = *reinterpret_cast<const uint32_t*>(a.Wsm + (n * (K / 64) + kt) * 2);
-        dequant32(codes, h2f((uint16_t)(smw & 0xFFFFu)), h2f((uint16_t)(smw >> 16)), rb);
+        h2 s2, m2;
+        scale_min_pairs(smw, s2, m2);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rb[i] = dequant8(codes[i], s2, m2);
       } else {
 #pragma unroll
         for (int i = 0; i < 4; ++i) rb[i] = zero_h8();
@@ -273,56 +470,156 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
 // skinny configurations by M: (waves, steps in flight per wave)
 template <int MF> struct SkinnyCfg;
 template <> struct SkinnyCfg<1> { static constexpr int KW = 8, UNR = 2; };
-template <> struct SkinnyCfg<2> { static constexpr int KW = 8, UNR = 1; };
-template <> struct SkinnyCfg<4> { static constexpr int KW = 4, UNR = 1; };
-
-template <int NF, int MF, bool W4, int EPI>
-static void launch_skinny(const GemmArgs& a, hipStream_t st) {
-  using C = SkinnyCfg<MF>;
-  const dim3 grid((unsigned)((a.N + 16 * NF - 1) / (16 * NF)));
-  launch((gemm_skinny<NF, MF, C::KW, C::UNR, W4, EPI>), grid, dim3(C::KW * 64), 0, st, a);
-}
 
 template <int NF, bool W4, int EPI>
-static void launch_skinny_m(const GemmArgs& a, hipStream_t st) {
-  if (a.M <= 16)
-    launch_skinny<NF, 1, W4, EPI>(a, st);
-  else if (a.M <= 32)
-    launch_skinny<NF, 2, W4, EPI>(a, st);
-  else
-    launch_skinny<NF, 4, W4, EPI>(a, st);
+static void launch_skinny(const GemmArgs& a, hipStream_t st) {
+  using C = SkinnyCfg<1>;
+  const dim3 grid((unsigned)((a.N + 16 * NF - 1) / (16 * NF)));
+  launch((gemm_skinny<NF, 1, C::KW, C::UNR, W4, EPI>), grid, dim3(C::KW * 64), 0, st, a);
+}
+
+// streaming configurations by (W format, 16-row blocks of X): rows per
+// wave (16 NF), waves, chunks in flight, chunk length; and a fallback with
+// 128-k chunks for K that the chunk length does not divide
+template <bool W4, int MF> struct StreamSel;
+template <> struct StreamSel<false, 2> { static constexpr int NF = 1, KW = 8, PD = 2, KC = 128; };
+template <> struct StreamSel<false, 4> { static constexpr int NF = 1, KW = 8, PD = 2, KC = 128; };
+template <> struct StreamSel<false, 8> { static constexpr int NF = 1, KW = 8, PD = 2, KC = 128; };
+template <> struct StreamSel<true, 2> { static constexpr int NF = 1, KW = 8, PD = 4, KC = 256; };
+template <> struct StreamSel<true, 4> { static constexpr int NF = 2, KW = 8, PD = 4, KC = 256; };
+template <> struct StreamSel<true, 8> { static constexpr int NF = 2, KW = 8, PD = 4, KC = 128; };
+template <bool W4, int MF> struct StreamFallback {
+  static constexpr int NF = StreamSel<W4, MF>::NF, KW = StreamSel<W4, MF>::KW;
+  static constexpr int PD = StreamSel<W4, MF>::KC == 128 ? StreamSel<W4, MF>::PD : 2 * StreamSel<W4, MF>::PD;
+  static constexpr int KC = 128;
+};
+
+constexpr int kStreamMaxM = 128;
+constexpr int kStreamMaxSplits = 8;
+constexpr int64_t kStreamMaxWGs = 256;  // about one workgroup per CU measured best
+
+static int stream_mf(int64_t M) { return M <= 32 ? 2 : (M <= 64 ? 4 : 8); }
+
+// K split: the largest power of two (up to the cap) that keeps the grid
+// within kStreamMaxWGs workgroups and the split a multiple of the chunk
+static int stream_splits(int64_t N, int64_t K, int rows_per_wg, int kc) {
+  const int64_t blocks = (N + rows_per_wg - 1) / rows_per_wg;
+  int S = 1;
+  while (S < kStreamMaxSplits && blocks * 2 * S <= kStreamMaxWGs && K % (2ll * S * kc) == 0)
+    S *= 2;
+  return S;
+}
+
+struct StreamPlan {
+  bool fallback;
+  int rows_per_wg, kc, splits;
+};
+
+template <bool W4, int MF>
+static StreamPlan stream_plan_mf(int64_t N, int64_t K) {
+  using P = StreamSel<W4, MF>;
+  using B = StreamFallback<W4, MF>;
+  StreamPlan pl;
+  pl.fallback = K % P::KC != 0;
+  pl.rows_per_wg = pl.fallback ? 16 * B::NF * B::KW : 16 * P::NF * P::KW;
+  pl.kc = pl.fallback ? B::KC : P::KC;
+  pl.splits = stream_splits(N, K, pl.rows_per_wg, pl.kc);
+  return pl;
+}
+
+static StreamPlan stream_plan(int64_t M, int64_t N, int64_t K, bool w4) {
+  switch (stream_mf(M)) {
+    case 2: return w4 ? stream_plan_mf<true, 2>(N, K) : stream_plan_mf<false, 2>(N, K);
+    case 4: return w4 ? stream_plan_mf<true, 4>(N, K) : stream_plan_mf<false, 4>(N, K);
+    default: return w4 ? stream_plan_mf<true, 8>(N, K) : stream_plan_mf<false, 8>(N, K);
+  }
+}
+
+static bool uses_stream(int64_t M) { return M > 16 && M <= kStreamMaxM; }
+
+int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, bool w4) {
+  if (!uses_stream(M) || N <= 0 || K <= 0 || K % 128 != 0) return 0;
+  const StreamPlan pl = stream_plan(M, N, K, w4);
+  return pl.splits > 1 ? (int64_t)pl.splits * M * N * 4 : 0;
+}
+
+int64_t gemm_workspace_bytes_upto(int64_t M_max, int64_t N, int64_t K, bool w4) {
+  int64_t best = 0;
+  for (int64_t M : {(int64_t)32, (int64_t)64, (int64_t)kStreamMaxM}) {
+    const int64_t m = M < M_max ? M : M_max;
+    const int64_t b = gemm_workspace_bytes(m, N, K, w4);
+    best = b > best ? b : best;
+  }
+  return best;
+}
+
+template <int NF, int MF, int KW, int PD, bool W4, int KC, int EPI>
+static void launch_stream_cfg(const GemmArgs& a, int S, float* ws, hipStream_t st) {
+  constexpr int rows = 16 * NF * KW;
+  const dim3 grid((unsigned)((a.N + rows - 1) / rows), (unsigned)S);
+  launch((gemm_stream<NF, MF, KW, PD, W4, KC, EPI>), grid, dim3(KW * 64), 0, st, a, ws, a.K / S);
+  if (S > 1) {
+    const int64_t MN = a.M * a.N;
+    launch((gemm_combine<EPI>), dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, st, a,
+           (const float*)ws, S);
+  }
+}
+
+template <bool W4, int MF, int EPI>
+static void launch_stream_mf(const GemmArgs& a, const StreamPlan& pl, int S, float* ws,
+                             hipStream_t st) {
+  if (pl.fallback) {
+    using B = StreamFallback<W4, MF>;
+    launch_stream_cfg<B::NF, MF, B::KW, B::PD, W4, B::KC, EPI>(a, S, ws, st);
+  } else {
+    using P = StreamSel<W4, MF>;
+    launch_stream_cfg<P::NF, MF, P::KW, P::PD, W4, P::KC, EPI>(a, S, ws, st);
+  }
 }
 
 template <bool W4, int EPI>
-static pipo_status launch_epi(const GemmArgs& a, hipStream_t st) {
-  if (a.M <= 64) {
+static pipo_status launch_epi(const GemmArgs& a, float* ws, int64_t ws_bytes, hipStream_t st) {
+  if (a.M <= 16) {
     // 64 W rows per workgroup (less X traffic per W byte) once that still
     // gives enough workgroups to fill the chip, else 16
     if (a.N >= 64 * 192)
-      launch_skinny_m<4, W4, EPI>(a, st);
+      launch_skinny<4, W4, EPI>(a, st);
     else
-      launch_skinny_m<1, W4, EPI>(a, st);
+      launch_skinny<1, W4, EPI>(a, st);
+  } else if (a.M <= kStreamMaxM) {
+    const StreamPlan pl = stream_plan(a.M, a.N, a.K, W4);
+    // without room for the partial sums the K split is dropped
+    const int S = (pl.splits > 1 && ws != nullptr &&
+                   ws_bytes >= (int64_t)pl.splits * a.M * a.N * 4) ? pl.splits : 1;
+    switch (stream_mf(a.M)) {
+      case 2: launch_stream_mf<W4, 2, EPI>(a, pl, S, ws, st); break;
+      case 4: launch_stream_mf<W4, 4, EPI>(a, pl, S, ws, st); break;
+      default: launch_stream_mf<W4, 8, EPI>(a, pl, S, ws, st); break;
+    }
   } else {
-    const dim3 grid((unsigned)((a.N + kTBN - 1) / kTBN), (unsigned)((a.M + kTBM - 1) / kTBM));
-    launch((gemm_tiled<W4, EPI>), grid, dim3(kTThreads), 0, st, a);
+    const int64_t total = ((a.N + kTBN - 1) / kTBN) * ((a.M + kTBM - 1) / kTBM);
+    const int64_t per_xcd = (total + kXcds - 1) / kXcds;
+    launch((gemm_tiled<W4, EPI>), dim3((unsigned)(per_xcd * kXcds)), dim3(kTThreads), 0, st, a);
   }
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
 }
 
 template <bool W4>
-static pipo_status launch_fmt(const GemmArgs& a, int epi, hipStream_t st) {
+static pipo_status launch_fmt(const GemmArgs& a, int epi, float* ws, int64_t ws_bytes,
+                              hipStream_t st) {
   switch (epi) {
-    case EPI_F16: return launch_epi<W4, EPI_F16>(a, st);
-    case EPI_RELU_F16: return launch_epi<W4, EPI_RELU_F16>(a, st);
-    case EPI_ADD_F32: return launch_epi<W4, EPI_ADD_F32>(a, st);
-    case EPI_F32: return launch_epi<W4, EPI_F32>(a, st);
-    case EPI_QKV: return launch_epi<W4, EPI_QKV>(a, st);
+    case EPI_F16: return launch_epi<W4, EPI_F16>(a, ws, ws_bytes, st);
+    case EPI_RELU_F16: return launch_epi<W4, EPI_RELU_F16>(a, ws, ws_bytes, st);
+    case EPI_ADD_F32: return launch_epi<W4, EPI_ADD_F32>(a, ws, ws_bytes, st);
+    case EPI_F32: return launch_epi<W4, EPI_F32>(a, ws, ws_bytes, st);
+    case EPI_QKV: return launch_epi<W4, EPI_QKV>(a, ws, ws_bytes, st);
     default: set_error("gemm: unknown epilogue %d", epi); return PIPO_ERR_ARG;
   }
 }
 
-pipo_status launch_gemm(const GemmArgs& a, bool w4, int epi, hipStream_t st) {
+pipo_status launch_gemm(const GemmArgs& a, bool w4, int epi, float* workspace,
+                        int64_t workspace_bytes, hipStream_t st) {
   if (a.M <= 0 || a.N <= 0 || a.K <= 0) {
     set_error("gemm: empty shape M=%lld N=%lld K=%lld", (long long)a.M, (long long)a.N,
               (long long)a.K);
@@ -336,7 +633,8 @@ pipo_status launch_gemm(const GemmArgs& a, bool w4, int epi, hipStream_t st) {
     set_error("gemm: null operand");
     return PIPO_ERR_ARG;
   }
-  return w4 ? launch_fmt<true>(a, epi, st) : launch_fmt<false>(a, epi, st);
+  return w4 ? launch_fmt<true>(a, epi, workspace, workspace_bytes, st)
+            : launch_fmt<false>(a, epi, workspace, workspace_bytes, st);
 }
 
 }  // namespace pipo

@@ -46,9 +46,14 @@ pipo_status pipo_dev_synchronize(void) {
   return PIPO_OK;
 }
 
-static pipo_status gemm_common(GemmArgs& a, bool w4, void* out, int32_t epi, void* stream) {
+static pipo_status gemm_common(GemmArgs& a, bool w4, void* out, int32_t epi, void* workspace,
+                               int64_t workspace_bytes, void* stream) {
   if (epi < 0 || epi > PIPO_EPI_F32 || !out) {
     set_error("gemm: bad epilogue %d or NULL output", epi);
+    return PIPO_ERR_ARG;
+  }
+  if (workspace_bytes < 0) {
+    set_error("gemm: negative workspace size");
     return PIPO_ERR_ARG;
   }
   a.ldo = a.N;
@@ -56,12 +61,13 @@ static pipo_status gemm_common(GemmArgs& a, bool w4, void* out, int32_t epi, voi
     a.out16 = static_cast<uint16_t*>(out);
   else
     a.out32 = static_cast<float*>(out);
-  return launch_gemm(a, w4, epi, static_cast<hipStream_t>(stream));
+  return launch_gemm(a, w4, epi, static_cast<float*>(workspace), workspace ? workspace_bytes : 0,
+                     static_cast<hipStream_t>(stream));
 }
 
 pipo_status pipo_op_gemm_f16(const uint16_t* X, const uint16_t* W, const uint16_t* bias,
                              void* out, int64_t M, int64_t N, int64_t K, int32_t epi,
-                             void* stream) {
+                             void* workspace, int64_t workspace_bytes, void* stream) {
   clear_error();
   GemmArgs a;
   a.X = X;
@@ -70,12 +76,12 @@ pipo_status pipo_op_gemm_f16(const uint16_t* X, const uint16_t* W, const uint16_
   a.M = M;
   a.N = N;
   a.K = K;
-  return gemm_common(a, false, out, epi, stream);
+  return gemm_common(a, false, out, epi, workspace, workspace_bytes, stream);
 }
 
 pipo_status pipo_op_gemm_w4(const uint16_t* X, const uint8_t* Wq, const uint16_t* Wsm,
                             const uint16_t* bias, void* out, int64_t M, int64_t N, int64_t K,
-                            int32_t epi, void* stream) {
+                            int32_t epi, void* workspace, int64_t workspace_bytes, void* stream) {
   clear_error();
   GemmArgs a;
   a.X = X;
@@ -85,7 +91,11 @@ pipo_status pipo_op_gemm_w4(const uint16_t* X, const uint8_t* Wq, const uint16_t
   a.M = M;
   a.N = N;
   a.K = K;
-  return gemm_common(a, true, out, epi, stream);
+  return gemm_common(a, true, out, epi, workspace, workspace_bytes, stream);
+}
+
+int64_t pipo_op_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int32_t wfmt) {
+  return gemm_workspace_bytes(M, N, K, wfmt == PIPO_W_INT4_G64);
 }
 
 pipo_status pipo_op_layernorm(const float* x, const uint16_t* gamma, const uint16_t* beta,

@@ -95,3 +95,15 @@ def test_null_weights_rejected():
     with pytest.raises(B.PipoError) as e:
         B.pipo_create(c_shape(_Shape()), B.PipoHostWeights(), c_policy(max_batch=1, max_seq=4))
     assert e.value.status == -1
+
+
+def test_gemm_workspace_sizes():
+    """GEMM K splits (host-side planning only, no GPU needed) happen only for
+    16 < M <= 128 and stay within the cap of 8."""
+    for M in (1, 16, 129, 4096):
+        assert B.pipo_op_gemm_workspace_bytes(M, 100, 4096, B.PIPO_W_FP16) == 0
+    for wfmt in (B.PIPO_W_FP16, B.PIPO_W_INT4_G64):
+        for M, N, K in ((17, 130, 4096), (64, 7168, 7168), (128, 28672, 7168), (32, 5120, 20480)):
+            ws = B.pipo_op_gemm_workspace_bytes(M, N, K, wfmt)
+            assert ws % (M * N * 4) == 0 and ws // (M * N * 4) in (0, 2, 4, 8)
+        assert B.pipo_op_gemm_workspace_bytes(17, 130, 4096, wfmt) == 8 * 17 * 130 * 4

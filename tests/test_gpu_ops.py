@@ -13,7 +13,11 @@ pytestmark = pytest.mark.gpu
 GEMM_SHAPES = [(1, 50, 128), (4, 100, 256), (16, 64, 128), (33, 130, 384), (64, 96, 128),
                (65, 200, 256), (128, 128, 128), (300, 257, 512),
                # 64-row workgroups (N >= 12288), ragged N
-               (16, 12300, 256), (40, 12288, 128), (64, 12350, 128), (7, 1000, 1024)]
+               (16, 12300, 256), (40, 12288, 128), (64, 12350, 128), (7, 1000, 1024),
+               # streaming kernel: K split over workgroups (up to 8 ways), INT4
+               # chunk length not dividing K, ragged M and N
+               (17, 130, 4096), (32, 200, 2048), (50, 1000, 1280), (100, 300, 640),
+               (128, 1030, 1024), (129, 64, 256)]
 EPIS = [B.PIPO_EPI_F16, B.PIPO_EPI_RELU_F16, B.PIPO_EPI_ADD_F32, B.PIPO_EPI_F32]
 
 
@@ -21,9 +25,14 @@ def log(msg):
     print(msg, flush=True)
 
 
-def run_gemm(X, W, bias, epi, out_init=None, w4=None):
+def run_gemm(X, W, bias, epi, out_init=None, w4=None, workspace=True):
+    """One GEMM through the C ABI; `workspace` False passes none (no K split)."""
     M, K = X.shape
     N = W.shape[0] if w4 is None else w4[0].shape[0]
+    ws_bytes = B.pipo_op_gemm_workspace_bytes(M, N, K, B.PIPO_W_FP16 if w4 is None
+                                              else B.PIPO_W_INT4_G64) if workspace else 0
+    dWs = DB(ws_bytes) if ws_bytes > 0 else None
+    ws = (dWs.ptr, ws_bytes) if dWs else (None, 0)
     dX = DB.from_array(X.astype(np.float16))
     dB = DB.from_array(bias.astype(np.float16)) if bias is not None else None
     f32 = epi in (B.PIPO_EPI_ADD_F32, B.PIPO_EPI_F32)
@@ -33,10 +42,11 @@ def run_gemm(X, W, bias, epi, out_init=None, w4=None):
         dO = DB(M * N * (4 if f32 else 2))
     if w4 is None:
         dW = DB.from_array(W.astype(np.float16))
-        B.pipo_op_gemm_f16(dX.ptr, dW.ptr, dB.ptr if dB else None, dO.ptr, M, N, K, epi)
+        B.pipo_op_gemm_f16(dX.ptr, dW.ptr, dB.ptr if dB else None, dO.ptr, M, N, K, epi, *ws)
     else:
         dq, dsm = DB.from_array(w4[0]), DB.from_array(w4[1])
-        B.pipo_op_gemm_w4(dX.ptr, dq.ptr, dsm.ptr, dB.ptr if dB else None, dO.ptr, M, N, K, epi)
+        B.pipo_op_gemm_w4(dX.ptr, dq.ptr, dsm.ptr, dB.ptr if dB else None, dO.ptr, M, N, K, epi,
+                          *ws)
     B.pipo_dev_synchronize()
     return dO.to_array(np.float32 if f32 else np.float16, (M, N))
 
@@ -102,22 +112,29 @@ def test_gemm_random_vs_oracle_definition(M):
     assert np.abs(got4 - want4).max() <= 2e-3 * np.abs(want4).max()
 
 
-@pytest.mark.parametrize("M", [4, 40, 100])
+@pytest.mark.parametrize("M", [4, 40, 100, 200])
 @pytest.mark.parametrize("w4", [False, True])
-def test_gemm_row_chunks_bit_identical(M, w4):
-    """A launch over a row range of W equals those rows of the whole launch
-    (the per-element summation order depends on M and K only)."""
-    log(f"gemm chunk invariance M={M} w4={w4}")
+def test_gemm_deterministic_and_split_consistent(M, w4):
+    """Repeated calls give the same bits; the K-split result equals the
+    unsplit one up to fp32 rounding; without a split (M <= 16, M > 128, or
+    no workspace) a launch over a row range of W gives those rows bit for
+    bit (the summation order then depends on M and K only)."""
+    log(f"gemm determinism/split M={M} w4={w4}")
     rng = np.random.default_rng(5)
-    K, N = 512, 64 * 200
+    K, N = 2048, 1024
     X = (rng.standard_normal((M, K))).astype(np.float16)
     W = (rng.standard_normal((N, K)) * 0.05).astype(np.float16)
-    full = run_gemm(X, W, None, B.PIPO_EPI_F32, w4=synth.quant_int4_g64(W) if w4 else None)
-    for n0, n1 in ((0, 32), (32, 160), (160, 4096), (64 * 150, N)):
+    q = synth.quant_int4_g64(W) if w4 else None
+    a = run_gemm(X, W, None, B.PIPO_EPI_F32, w4=q)
+    b = run_gemm(X, W, None, B.PIPO_EPI_F32, w4=q)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    unsplit = run_gemm(X, W, None, B.PIPO_EPI_F32, w4=q, workspace=False)
+    assert np.abs(a - unsplit).max() <= 1e-5 * np.abs(unsplit).max()
+    for n0, n1 in ((0, 32), (32, 160), (160, 1000)):
         part = W[n0:n1]
         got = run_gemm(X, part, None, B.PIPO_EPI_F32,
-                       w4=synth.quant_int4_g64(part) if w4 else None)
-        assert np.array_equal(got.view(np.uint32), full[:, n0:n1].view(np.uint32))
+                       w4=synth.quant_int4_g64(part) if w4 else None, workspace=False)
+        assert np.array_equal(got.view(np.uint32), unsplit[:, n0:n1].view(np.uint32))
 
 
 def test_attention_workspace_reuse():
