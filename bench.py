@@ -147,7 +147,7 @@ def cpu_baseline(wl, seed, sample_layers=2, steps=3):
             return self._lnf
 
     held = Held()
-    dec = OracleDecoder(held, np.float32)
+    dec = OracleDecoder(held, np.float32, kv_int4=wl.kv_fmt == "int4")
     b, ctx = wl.batch, wl.prompt + 1
     rng = np.random.default_rng(0)
     d = shape.d_model
@@ -210,6 +210,7 @@ def main():
 
     flags = 0 if args.no_timestamps else B.PIPO_DBG_TIMESTAMPS
     dec = Decoder(hw, weights_on_host=True, embed_on_host=True, kv_on_host=wl.kv_on_host,
+                  kv_fmt=wl.kv_fmt,
                   n_weight_slots=args.slots, n_h2d_streams=args.h2d_streams,
                   chunk_bytes=args.chunk_mb << 20, max_batch=wl.batch, max_seq=max_seq,
                   debug_flags=flags)
@@ -241,8 +242,8 @@ def main():
         "config": {"workload": wl.name, "layers": shape.n_layers, "d_model": shape.d_model,
                    "batch": wl.batch, "prompt": wl.prompt,
                    "generated": 1 + W + K, "weights": f"{wl.wfmt}, pinned host, streamed",
-                   "kv_cache": "host (pinned, or pageable through pinned staging), streamed"
-                               if wl.kv_on_host else "HBM",
+                   "kv_cache": ("host (pinned, or pageable through pinned staging), streamed"
+                                if wl.kv_on_host else "HBM") + f", {wl.kv_fmt}",
                    "chunk_bytes": args.chunk_mb << 20, "slots": args.slots,
                    "h2d_streams": args.h2d_streams},
         "h2d_link": {"peak_gbps": round(peak, 2), "peak_1stream_gbps": round(peak1, 2),

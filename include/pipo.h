@@ -54,6 +54,17 @@ typedef enum {
 /* Weight storage format of the four per-layer matrices. */
 enum { PIPO_W_FP16 = 0, PIPO_W_INT4_G64 = 1 };
 
+/* KV cache storage format.  PIPO_KV_INT4_G64 (Section 2: the KV cache may
+ * be kept in 4 bits like the weights): a cached key or value row of d
+ * elements takes d/2 code bytes (element 2i in the low nibble of byte i)
+ * followed by d/64 fp16 (scale, min) pairs, one per 64 consecutive
+ * elements, 9d/16 bytes in all instead of 2d.  A new row (fp16) is
+ * quantized when it is written: per group, in fp32, scale = fp16((max -
+ * min) / 15), min = fp16(min), code = clamp(rint((x - min) / scale), 0, 15)
+ * rounding half to even (0 where scale is 0); every attention, prefill
+ * included, reads code * scale + min.  Needs d_model % 256 == 0. */
+enum { PIPO_KV_FP16 = 0, PIPO_KV_INT4_G64 = 1 };
+
 /* pipo_policy.debug_flags */
 enum {
   PIPO_DBG_POISON_SLOTS = 1,  /* fill a weight/KV slot with NaN before every refill */
@@ -126,6 +137,7 @@ typedef struct {
                                   pinned staging buffers, copied by host worker threads (the
                                   paper's multi-thread transfer, Section 3.3) */
   int32_t copy_threads;      /* host threads for staged copies (default 8) */
+  int32_t kv_fmt;            /* PIPO_KV_FP16 (default) or PIPO_KV_INT4_G64 */
 } pipo_policy;
 
 /* Per-kernel timing (filled when PIPO_DBG_TIMESTAMPS is set): each launch

@@ -85,6 +85,23 @@ pipo_status pipo_op_attn_decode(const uint16_t* q, const uint16_t* kc, const uin
 int64_t pipo_op_attn_decode_workspace_bytes(int32_t b, int32_t n_heads, int32_t head_dim,
                                             int32_t t);
 
+/* The same over an INT4 KV cache (PIPO_KV_INT4_G64 rows of 9d/16 bytes,
+ * position-major like the fp16 cache; d % 256 == 0): every key and value
+ * is read as code * scale + min (rounded once to fp16).  Same workspace. */
+pipo_status pipo_op_attn_decode_kv4(const uint16_t* q, const uint8_t* kc, const uint8_t* vc,
+                                    uint16_t* o, int32_t b, int32_t n_heads, int32_t head_dim,
+                                    int32_t t, void* workspace, int64_t workspace_bytes,
+                                    void* stream);
+
+/* INT4 KV cache rows (Section 2; the conversion is part of saving and
+ * loading the cache, Section 3.1.2): quantize `rows` fp16 rows x [rows][d]
+ * into out [rows][9d/16 bytes] with the PIPO_KV_INT4_G64 recipe (pipo.h),
+ * or expand INT4 rows back to fp16 y [rows][d].  d % 256 == 0. */
+pipo_status pipo_op_kv_quant(const uint16_t* x, uint8_t* out, int64_t rows, int64_t d,
+                             void* stream);
+pipo_status pipo_op_kv_dequant(const uint8_t* in, uint16_t* y, int64_t rows, int64_t d,
+                               void* stream);
+
 /*
  * Causal prefill attention over P positions of b sequences.
  * q: [b][P][d] fp16 (scaled); kc, vc: [>= P][b][d] position-major as

@@ -17,5 +17,6 @@ from .opt import (  # noqa: F401
     layer_norm,
     param_count,
     layer_param_count,
+    quant_kv_int4_g64,
     streamed_bytes_per_step,
 )

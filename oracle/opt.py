@@ -22,9 +22,23 @@ What is computed, and where it comes from:
   (scale, min) pair per group of 64 consecutive inputs of a row, codes
   packed two per byte with the even input in the low nibble.  The paper
   gives no recipe; this is the one the workloads define.
+* INT4 KV cache (Section 2: PIPO can keep the KV cache in 4 bits too; the
+  conversion belongs to the KV loading and saving tasks, Section 3.1.2).
+  The paper gives no recipe; the reading here: a new key or value row is
+  rounded to fp16 (activations are fp16, Section 4.1) and quantized per
+  group of 64 consecutive elements with the same asymmetric (scale, min)
+  scheme (quant_kv_int4_g64), and every attention -- prefill included --
+  reads the cache, i.e. the dequantized values.  A row's codes depend on
+  that row alone, so incremental decoding still equals full recomputation.
 
 The default arithmetic type is float32; tests that pin the oracle run it in
-float64.  Everything is vectorised numpy over whole tensors, with no
+float64.  With ``fp16_operands`` every tensor the kernels hold in fp16 is
+rounded to fp16 (Section 4.1: fp16 activations; an INT4 weight is expanded
+to an fp16 operand): the LayerNorm outputs, q, k and v, the attention
+output, the FC1 output and the expanded INT4 weights; the residual stream
+and the logits stay in the arithmetic type.  INT4 KV codes are decisions
+taken on k and v, so comparisons with an INT4 cache use this mode (the codes
+then come from the same fp16 values up to summation order).  Everything is vectorised numpy over whole tensors, with no
 blocking or fusion: a layer is LN -> QKV -> causal softmax attention ->
 out-projection + residual -> LN -> FC1 -> ReLU -> FC2 + residual.
 """
@@ -65,6 +79,33 @@ def dequant_int4_g64(q: np.ndarray, sm: np.ndarray, dtype=np.float32) -> np.ndar
     return w.reshape(N, K)
 
 
+def quant_kv_int4_g64(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """INT4 cache entry of fp16 rows x [R][d] (d a multiple of 64).
+
+    Per group of 64 consecutive elements of a row, in float32:
+    mn, mx = min, max; s = fp16((mx - mn) / 15); m = fp16(mn);
+    code = clamp(rint((x - m) / s), 0, 15) with rint rounding half to even,
+    and code = 0 where s == 0.  Returns codes [R][d/2] uint8 (element 2i in
+    the low nibble of byte i) and (s, m) pairs [R][d/64][2] fp16, the layout
+    dequant_int4_g64 reads.
+    """
+    x = np.asarray(x, dtype=np.float16).astype(np.float32)
+    R, d = x.shape
+    g = x.reshape(R, d // 64, 64)
+    mn = g.min(axis=-1)
+    mx = g.max(axis=-1)
+    s16 = ((mx - mn) / np.float32(15)).astype(np.float16)
+    m16 = mn.astype(np.float16)
+    s32 = s16.astype(np.float32)[..., None]
+    m32 = m16.astype(np.float32)[..., None]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        c = np.rint((g - m32) / s32)
+    c = np.where(s32 == 0, np.float32(0), np.clip(c, 0, 15)).astype(np.uint8).reshape(R, d)
+    codes = (c[:, 0::2] | (c[:, 1::2] << 4)).astype(np.uint8)
+    sm = np.stack([s16, m16], axis=-1)
+    return codes, sm
+
+
 def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, n_heads: int) -> np.ndarray:
     """Multi-head softmax attention of T queries over S >= T keys.
 
@@ -103,10 +144,12 @@ def param_count(n_layers: int, d: int, d_ffn: int, vocab: int, n_pos_rows: int) 
 
 def streamed_bytes_per_step(n_layers: int, d: int, d_ffn: int, vocab: int, wfmt: str,
                             stream_head: bool = True, kv_batch: int = 0,
-                            kv_len: int = 0) -> int:
+                            kv_len: int = 0, kv_fmt: str = "fp16") -> int:
     """Host-to-device bytes one decode step streams: every layer's weights,
     the tied output head, and (when the KV cache lives in host memory) each
-    layer's K and V prefix of kv_len positions for kv_batch sequences."""
+    layer's K and V prefix of kv_len positions for kv_batch sequences, a
+    row of d elements taking 2 d bytes (fp16) or d/2 + d/16 (INT4 codes and
+    one (scale, min) pair per 64)."""
     mats = 4 * d * d + 2 * d * d_ffn
     small = layer_param_count(d, d_ffn) - mats
     if wfmt == "fp16":
@@ -118,7 +161,8 @@ def streamed_bytes_per_step(n_layers: int, d: int, d_ffn: int, vocab: int, wfmt:
     total = n_layers * per_layer
     if stream_head:
         total += 2 * vocab * d
-    total += n_layers * 2 * kv_batch * kv_len * d * 2
+    row = {"fp16": 2 * d, "int4": d // 2 + d // 16}[kv_fmt]
+    total += n_layers * 2 * kv_batch * kv_len * row
     return total
 
 
@@ -134,10 +178,13 @@ class OracleDecoder:
     time, so the oracle never holds more than one layer's weights.
     """
 
-    def __init__(self, weights, dtype=np.float32):
+    def __init__(self, weights, dtype=np.float32, kv_int4: bool = False,
+                 fp16_operands: bool = False):
         self.w = weights
         self.s = weights.shape
         self.dtype = dtype
+        self.kv_int4 = kv_int4
+        self.fp16_operands = fp16_operands
         self._tok = None
         self._pos = None
         self._lnf = None
@@ -167,7 +214,7 @@ class OracleDecoder:
         out = {}
         for name, val in raw.items():
             if name in MATRICES and self.w.wfmt == "int4":
-                out[name] = dequant_int4_g64(val[0], val[1], self.dtype)
+                out[name] = self.act(dequant_int4_g64(val[0], val[1], self.dtype))
             else:
                 out[name] = self._f(val)
         return out
@@ -188,24 +235,38 @@ class OracleDecoder:
         d = self.s.d_model
         dh = d // self.s.n_heads
         eps = self.s.ln_eps
-        a = layer_norm(x, L["ln1_g"], L["ln1_b"], eps)
+        a = self.act(layer_norm(x, L["ln1_g"], L["ln1_b"], eps))
         qkv = a @ L["wqkv"].T + L["bqkv"]
-        q = qkv[:, :d] * (dh ** -0.5)
-        k = qkv[:, d:2 * d]
-        v = qkv[:, 2 * d:]
+        q = self.act(qkv[:, :d] * (dh ** -0.5))
+        k = self.kv_entry(self.act(qkv[:, d:2 * d]))
+        v = self.kv_entry(self.act(qkv[:, 2 * d:]))
         if past_k is not None:
             k = np.concatenate([past_k, k], axis=0)
             v = np.concatenate([past_v, v], axis=0)
-        o = causal_attention(q, k, v, self.s.n_heads)
+        o = self.act(causal_attention(q, k, v, self.s.n_heads))
         x = x + (o @ L["wo"].T + L["bo"])
-        a2 = layer_norm(x, L["ln2_g"], L["ln2_b"], eps)
-        hdn = np.maximum(a2 @ L["w1"].T + L["b1"], 0)
+        a2 = self.act(layer_norm(x, L["ln2_g"], L["ln2_b"], eps))
+        hdn = self.act(np.maximum(a2 @ L["w1"].T + L["b1"], 0))
         x = x + (hdn @ L["w2"].T + L["b2"])
         return x, k, v
 
+    def act(self, a: np.ndarray) -> np.ndarray:
+        """A tensor as the kernels hold it (fp16 with fp16_operands)."""
+        if not self.fp16_operands:
+            return a
+        return a.astype(np.float16).astype(self.dtype)
+
+    def kv_entry(self, a: np.ndarray) -> np.ndarray:
+        """The values the KV cache holds for new key or value rows a [T][d]:
+        a itself, or with an INT4 cache the dequantized int4 entry."""
+        if not self.kv_int4:
+            return a
+        codes, sm = quant_kv_int4_g64(a.astype(np.float16))
+        return dequant_int4_g64(codes, sm, self.dtype)
+
     def head(self, x: np.ndarray) -> np.ndarray:
         g, b = self.lnf()
-        return layer_norm(x, g, b, self.s.ln_eps) @ self.tok_emb().T
+        return self.act(layer_norm(x, g, b, self.s.ln_eps)) @ self.tok_emb().T
 
     # -- whole passes -------------------------------------------------------
     def forward(self, tokens: np.ndarray, layers: Optional[int] = None) -> np.ndarray:

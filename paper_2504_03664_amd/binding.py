@@ -25,6 +25,7 @@ STATUS_NAMES = {0: "PIPO_OK", -1: "PIPO_ERR_ARG", -2: "PIPO_ERR_OOM_DEVICE",
                 -3: "PIPO_ERR_OOM_HOST", -4: "PIPO_ERR_HIP", -5: "PIPO_ERR_STATE",
                 -6: "PIPO_ERR_UNSUPPORTED"}
 PIPO_W_FP16, PIPO_W_INT4_G64 = 0, 1
+PIPO_KV_FP16, PIPO_KV_INT4_G64 = 0, 1
 PIPO_DBG_POISON_SLOTS, PIPO_DBG_COPY_DELAY, PIPO_DBG_TIMESTAMPS = 1, 2, 4
 PIPO_DBG_KV_PAGEABLE = 8
 PIPO_EPI_F16, PIPO_EPI_RELU_F16, PIPO_EPI_ADD_F32, PIPO_EPI_F32 = 0, 1, 2, 3
@@ -56,7 +57,7 @@ class PipoPolicy(ctypes.Structure):
                 ("kv_on_host", i32), ("n_weight_slots", i32), ("n_h2d_streams", i32),
                 ("chunk_bytes", i64), ("max_batch", i32), ("max_seq", i32),
                 ("hbm_budget_bytes", i64), ("debug_flags", i32), ("copy_delay_us", i32),
-                ("pinned_budget_bytes", i64), ("copy_threads", i32)]
+                ("pinned_budget_bytes", i64), ("copy_threads", i32), ("kv_fmt", i32)]
 
 
 class PipoKernelStat(ctypes.Structure):
@@ -114,6 +115,9 @@ _SIGNATURES = {
     "pipo_op_layernorm": ([vp, vp, vp, vp, i64, i64, i64, i64, f32, vp], i32),
     "pipo_op_attn_decode": ([vp, vp, vp, vp, i32, i32, i32, i32, vp, i64, vp], i32),
     "pipo_op_attn_decode_workspace_bytes": ([i32, i32, i32, i32], i64),
+    "pipo_op_attn_decode_kv4": ([vp, vp, vp, vp, i32, i32, i32, i32, vp, i64, vp], i32),
+    "pipo_op_kv_quant": ([vp, vp, i64, i64, vp], i32),
+    "pipo_op_kv_dequant": ([vp, vp, i64, i64, vp], i32),
     "pipo_op_attn_prefill": ([vp, vp, vp, vp, i32, i32, i32, i32, vp], i32),
     "pipo_op_argmax": ([vp, vp, i64, i64, vp], i32),
     "pipo_op_copy": ([vp, vp, i64, vp], i32),
@@ -309,6 +313,20 @@ def pipo_op_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, workspace=None,
 
 def pipo_op_attn_decode_workspace_bytes(b, n_heads, head_dim, t) -> int:
     return lib().pipo_op_attn_decode_workspace_bytes(b, n_heads, head_dim, t)
+
+
+def pipo_op_attn_decode_kv4(q, kc, vc, o, b, n_heads, head_dim, t, workspace=None,
+                            workspace_bytes=0, stream=None):
+    _check(lib().pipo_op_attn_decode_kv4(q, kc, vc, o, b, n_heads, head_dim, t, workspace,
+                                         workspace_bytes, stream), "pipo_op_attn_decode_kv4")
+
+
+def pipo_op_kv_quant(x, out, rows, d, stream=None):
+    _check(lib().pipo_op_kv_quant(x, out, rows, d, stream), "pipo_op_kv_quant")
+
+
+def pipo_op_kv_dequant(src, y, rows, d, stream=None):
+    _check(lib().pipo_op_kv_dequant(src, y, rows, d, stream), "pipo_op_kv_dequant")
 
 
 def pipo_op_attn_prefill(q, kc, vc, o, b, P, n_heads, head_dim, stream=None):

@@ -34,7 +34,9 @@ __device__ __forceinline__ float wave_max(float v) {
 // keys at a time so that K and V of both are in flight together.  Groups are
 // merged by a butterfly inside the wave, waves in order through LDS.  With
 // one split the result is final; otherwise (m, l, acc[D]) goes to `part`
-// and attn_decode_combine merges the splits in split order.
+// and attn_decode_combine merges the splits in split order.  With KV4 the
+// cache rows are INT4 (d/2 code bytes, then d/64 fp16 (scale, min) pairs):
+// a lane reads its 8 codes and its group's pair and expands them to fp16.
 template <int D>
 __device__ __forceinline__ void online_merge(float& m, float& l, float (&acc)[8], float m2,
                                              float l2, const float (&acc2)[8]) {
@@ -47,10 +49,10 @@ __device__ __forceinline__ void online_merge(float& m, float& l, float (&acc)[8]
   m = M;
 }
 
-template <int D>
+template <int D, bool KV4>
 __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict__ q,
-                                                     const uint16_t* __restrict__ kc,
-                                                     const uint16_t* __restrict__ vc,
+                                                     const void* __restrict__ kc,
+                                                     const void* __restrict__ vc,
                                                      uint16_t* __restrict__ o,
                                                      float* __restrict__ part, int b, int H,
                                                      int t, int chunk) {
@@ -65,7 +67,6 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
   const int T = t + 1;
   const int p0 = sp * chunk, p1 = min(T, p0 + chunk);
   const int64_t col = (int64_t)h * D + cl * 8;
-  const int64_t row_stride = (int64_t)b * d;
 
   float qf[8];
   {
@@ -77,8 +78,21 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
 
-  const uint16_t* kbase = kc + (int64_t)bi * d + col;
-  const uint16_t* vbase = vc + (int64_t)bi * d + col;
+  // fp16: element offset of this lane's 8 values in row `bi` of position 0;
+  // INT4: byte offsets of its 4 code bytes and of its group's (scale, min)
+  const int64_t row_bytes = KV4 ? d / 2 + d / 16 : 2 * d;
+  const int64_t code_off = (int64_t)bi * row_bytes + (KV4 ? col / 2 : 2 * col);
+  const int64_t sm_off = (int64_t)bi * row_bytes + d / 2 + (col / 64) * 4;
+  const auto load_kv = [&](const void* base, int p) -> h8 {
+    const char* row = static_cast<const char*>(base) + (int64_t)p * b * row_bytes;
+    if constexpr (KV4) {
+      h2 s2, m2;
+      scale_min_pairs(*reinterpret_cast<const uint32_t*>(row + sm_off), s2, m2);
+      return dequant8(*reinterpret_cast<const uint32_t*>(row + code_off), s2, m2);
+    } else {
+      return load_h8(reinterpret_cast<const uint16_t*>(row + code_off));
+    }
+  };
   const auto visit = [&](h8 kv, h8 vv) {
     float s = 0.f;
 #pragma unroll
@@ -95,12 +109,12 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
   };
   for (int p = p0 + wave * PPW + sub; p < p1; p += 8 * PPW) {
     const int p2 = p + 4 * PPW;
-    const h8 ka = load_h8(kbase + (int64_t)p * row_stride);
-    const h8 va = load_h8(vbase + (int64_t)p * row_stride);
+    const h8 ka = load_kv(kc, p);
+    const h8 va = load_kv(vc, p);
     h8 kb2 = zero_h8(), vb2 = zero_h8();
     if (p2 < p1) {
-      kb2 = load_h8(kbase + (int64_t)p2 * row_stride);
-      vb2 = load_h8(vbase + (int64_t)p2 * row_stride);
+      kb2 = load_kv(kc, p2);
+      vb2 = load_kv(vc, p2);
     }
     visit(ka, va);
     if (p2 < p1) visit(kb2, vb2);
@@ -316,8 +330,20 @@ int64_t attn_decode_workspace_bytes(int b, int n_heads, int head_dim, int splits
   return splits > 1 ? (int64_t)b * n_heads * splits * (head_dim + 2) * 4 : 0;
 }
 
-pipo_status launch_attn_decode(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
-                               uint16_t* o, int b, int n_heads, int head_dim, int t,
+template <int D, bool KV4>
+static void launch_decode_d(const uint16_t* q, const void* kc, const void* vc, uint16_t* o, int b,
+                            int n_heads, int t, int S, int chunk, float* workspace,
+                            hipStream_t st) {
+  const dim3 grid((unsigned)n_heads, (unsigned)b, (unsigned)S);
+  launch(attn_decode_k<D, KV4>, grid, dim3(256), 0, st, q, kc, vc, o, workspace, b, n_heads, t,
+         chunk);
+  if (S > 1)
+    launch(attn_decode_combine<D>, dim3((unsigned)n_heads, (unsigned)b), dim3(D), 0, st,
+           (const float*)workspace, o, n_heads, S);
+}
+
+pipo_status launch_attn_decode(const uint16_t* q, const void* kc, const void* vc, uint16_t* o,
+                               int b, int n_heads, int head_dim, int t, bool kv4,
                                float* workspace, int64_t workspace_bytes, hipStream_t st) {
   if (b < 1 || n_heads < 1 || t < 0) {
     set_error("attn_decode: bad shape b=%d heads=%d t=%d", b, n_heads, t);
@@ -327,25 +353,21 @@ pipo_status launch_attn_decode(const uint16_t* q, const uint16_t* kc, const uint
     set_error("attn_decode: head_dim %d not supported (64 or 128)", head_dim);
     return PIPO_ERR_UNSUPPORTED;
   }
+  if (kv4 && ((int64_t)n_heads * head_dim) % 256 != 0) {
+    set_error("attn_decode: INT4 KV rows need d %% 256 == 0 (d=%d)", n_heads * head_dim);
+    return PIPO_ERR_UNSUPPORTED;
+  }
   const int T = t + 1;
   int S = attn_decode_splits(b, n_heads, t);
   if (!workspace || workspace_bytes < attn_decode_workspace_bytes(b, n_heads, head_dim, S)) S = 1;
   const int chunk = (T + S - 1) / S;
   S = (T + chunk - 1) / chunk;
-  const dim3 grid((unsigned)n_heads, (unsigned)b, (unsigned)S);
-  if (head_dim == 128) {
-    launch(attn_decode_k<128>, grid, dim3(256), 0, st, q, kc, vc, o, workspace, b, n_heads, t,
-           chunk);
-    if (S > 1)
-      hipLaunchKernelGGL(attn_decode_combine<128>, dim3((unsigned)n_heads, (unsigned)b),
-                         dim3(128), 0, st, (const float*)workspace, o, n_heads, S);
-  } else {
-    launch(attn_decode_k<64>, grid, dim3(256), 0, st, q, kc, vc, o, workspace, b, n_heads, t,
-           chunk);
-    if (S > 1)
-      hipLaunchKernelGGL(attn_decode_combine<64>, dim3((unsigned)n_heads, (unsigned)b), dim3(64),
-                         0, st, (const float*)workspace, o, n_heads, S);
-  }
+  if (head_dim == 128)
+    (kv4 ? launch_decode_d<128, true> : launch_decode_d<128, false>)(q, kc, vc, o, b, n_heads, t,
+                                                                    S, chunk, workspace, st);
+  else
+    (kv4 ? launch_decode_d<64, true> : launch_decode_d<64, false>)(q, kc, vc, o, b, n_heads, t, S,
+                                                                  chunk, workspace, st);
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
 }

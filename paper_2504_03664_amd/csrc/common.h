@@ -104,12 +104,18 @@ pipo_status launch_embed(const uint16_t* tok_rows, const int32_t* ids, const uin
 // in split order; without enough workspace it runs unsplit
 int attn_decode_splits(int b, int n_heads, int t);
 int64_t attn_decode_workspace_bytes(int b, int n_heads, int head_dim, int splits);
-pipo_status launch_attn_decode(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
-                               uint16_t* o, int b, int n_heads, int head_dim, int t,
+// kc, vc: fp16 rows, or INT4 rows (kv4; see kvcache.hip) of the cache
+pipo_status launch_attn_decode(const uint16_t* q, const void* kc, const void* vc, uint16_t* o,
+                               int b, int n_heads, int head_dim, int t, bool kv4,
                                float* workspace, int64_t workspace_bytes, hipStream_t st);
 pipo_status launch_attn_prefill(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                                 uint16_t* o, int b, int P, int n_heads, int head_dim,
                                 hipStream_t st);
+// INT4 KV rows (d/2 code bytes + d/64 fp16 (scale, min) pairs; d % 256 == 0)
+pipo_status launch_kv_quant(const uint16_t* x, uint8_t* out, int64_t rows, int64_t d,
+                            hipStream_t st);
+pipo_status launch_kv_dequant(const uint8_t* in, uint16_t* y, int64_t rows, int64_t d,
+                              hipStream_t st);
 pipo_status launch_argmax(const float* logits, int32_t* next, int64_t rows, int64_t V,
                           hipStream_t st);
 pipo_status launch_fill_u16(uint16_t* p, uint16_t value, int64_t n, hipStream_t st);

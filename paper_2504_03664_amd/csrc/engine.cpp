@@ -260,7 +260,11 @@ struct pipo_ctx {
   float* gemm_ws = nullptr;    // GEMM K-split partials
   int64_t gemm_ws_bytes = 0;
   char* kv = nullptr;          // resident cache or KV slots
-  int64_t kv_part_bytes = 0;   // max_seq * max_batch * d * 2
+  bool kv4 = false;            // INT4 cache rows (PIPO_KV_INT4_G64)
+  int64_t kv_row = 0;          // bytes of one cached key (value) row: 2 d, or 9 d / 16
+  int64_t kv_part_bytes = 0;   // max_seq * max_batch * kv_row
+  uint16_t* kst = nullptr;     // INT4 cache: fp16 staging of new (decode) or all
+  uint16_t* vst = nullptr;     //   (prefill attention) key and value rows
 
   // sequence state
   int b = 0;
@@ -378,13 +382,13 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
     }
   }
   const uint16_t* misc = base ? misc_ptr(base, c) : nullptr;
-  // KV cache of layer j
-  uint16_t *kc = nullptr, *vc = nullptr;
+  // KV cache of layer j (fp16 or INT4 rows, position-major)
+  char *kc = nullptr, *vc = nullptr;
   if (j >= 0) {
     char* kvb = c->pol.kv_on_host ? c->kv + (int64_t)op.slot * 2 * c->kv_part_bytes
                                   : c->kv + (int64_t)j * 2 * c->kv_part_bytes;
-    kc = reinterpret_cast<uint16_t*>(kvb);
-    vc = reinterpret_cast<uint16_t*>(kvb + c->kv_part_bytes);
+    kc = kvb;
+    vc = kvb + c->kv_part_bytes;
   }
   const auto gemm = [&](int seg, const uint16_t* X, const uint16_t* bias, int64_t M, int64_t N,
                         int64_t K, int epi, GemmArgs& ga) {
@@ -421,20 +425,40 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
     case kQkv: {
       GemmArgs ga;
       ga.q_out = c->q;
-      ga.k_out = kc;
-      ga.v_out = vc;
       ga.d = d;
       ga.q_scale = 1.0f / std::sqrt((float)c->dh);
       ga.rows_per_seq = p.T;
-      ga.pos0 = p.pos0;
       ga.batch = c->b;
-      return gemm(kSegWqkv, c->a, misc + 2 * d, rows, 3 * d, d, EPI_QKV, ga);
+      if (!c->kv4) {
+        ga.k_out = reinterpret_cast<uint16_t*>(kc);
+        ga.v_out = reinterpret_cast<uint16_t*>(vc);
+        ga.pos0 = p.pos0;
+        return gemm(kSegWqkv, c->a, misc + 2 * d, rows, 3 * d, d, EPI_QKV, ga);
+      }
+      // INT4 cache: the new rows go to fp16 staging (position-major from the
+      // pass's first position) and are quantized into the cache at pos0
+      ga.k_out = c->kst;
+      ga.v_out = c->vst;
+      ga.pos0 = 0;
+      PIPO_TRY(gemm(kSegWqkv, c->a, misc + 2 * d, rows, 3 * d, d, EPI_QKV, ga));
+      const int64_t at = p.pos0 * c->b * c->kv_row;
+      PIPO_TRY(launch_kv_quant(c->kst, reinterpret_cast<uint8_t*>(kc + at), rows, d, s));
+      return launch_kv_quant(c->vst, reinterpret_cast<uint8_t*>(vc + at), rows, d, s);
     }
     case kAttn:
-      if (p.prefill)
-        return launch_attn_prefill(c->q, kc, vc, c->o, c->b, (int)p.T, (int)c->H, (int)c->dh, s);
+      if (p.prefill) {
+        if (!c->kv4)
+          return launch_attn_prefill(c->q, reinterpret_cast<const uint16_t*>(kc),
+                                     reinterpret_cast<const uint16_t*>(vc), c->o, c->b, (int)p.T,
+                                     (int)c->H, (int)c->dh, s);
+        // INT4 cache: attention reads the cache, expanded to fp16 staging
+        PIPO_TRY(launch_kv_dequant(reinterpret_cast<const uint8_t*>(kc), c->kst, rows, d, s));
+        PIPO_TRY(launch_kv_dequant(reinterpret_cast<const uint8_t*>(vc), c->vst, rows, d, s));
+        return launch_attn_prefill(c->q, c->kst, c->vst, c->o, c->b, (int)p.T, (int)c->H,
+                                   (int)c->dh, s);
+      }
       return launch_attn_decode(c->q, kc, vc, c->o, c->b, (int)c->H, (int)c->dh, (int)p.pos0,
-                                c->attn_ws, c->attn_ws_bytes, s);
+                                c->kv4, c->attn_ws, c->attn_ws_bytes, s);
     case kOproj: {
       GemmArgs ga;
       ga.out32 = c->x;
@@ -490,7 +514,10 @@ static void kernel_cost(const pipo_ctx* c, const Op& op, double* bytes, double* 
   *bytes = 0;
   *flops = 0;
   switch (op.kernel) {
-    case kQkv: g(rows, 3 * d, d, 2, wbytes(3 * d, d)); break;
+    case kQkv:
+      g(rows, 3 * d, d, 2, wbytes(3 * d, d));
+      if (c->kv4) *bytes += 2 * rows * (d * 4 + c->kv_row);  // staging write, read, INT4 write
+      break;
     case kOproj: g(rows, d, d, 8, wbytes(d, d)); break;
     case kFc1: g(rows, F, d, 2, wbytes(F, d)); break;
     case kFc2: g(rows, d, F, 8, wbytes(d, F)); break;
@@ -500,10 +527,10 @@ static void kernel_cost(const pipo_ctx* c, const Op& op, double* bytes, double* 
     case kLnf: *bytes = c->b * d * 6 + d * 4; *flops = c->b * d * 8; break;
     case kAttn:
       if (p.prefill) {
-        *bytes = 4 * rows * d * 2;
+        *bytes = 4 * rows * d * 2 + (c->kv4 ? 2 * rows * (c->kv_row + d * 2) : 0);
         *flops = 4.0 * c->b * p.T * (p.T + 1) / 2 * d;
       } else {
-        *bytes = 2.0 * c->b * (p.pos0 + 1) * d * 2 + 2 * rows * d * 2;
+        *bytes = 2.0 * c->b * (p.pos0 + 1) * c->kv_row + 2 * rows * d * 2;
         *flops = 4.0 * c->b * (p.pos0 + 1) * d;
       }
       break;
@@ -606,8 +633,8 @@ static pipo_status exec_op(pipo_ctx* c, const Op& op) {
       const void* src;
       const bool h2d = op.kind == OpKind::CopyH2D;
       if (op.kv) {
-        // host cache of the layer: [K|V][max_seq][b][d] for the current batch b
-        const int64_t host_off = (int64_t)op.seg * c->pol.max_seq * c->b * c->d * 2;
+        // host cache of the layer: [K|V][max_seq][b] rows for the current batch b
+        const int64_t host_off = (int64_t)op.seg * c->pol.max_seq * c->b * c->kv_row;
         char* hptr = c->kv_host[op.layer] + host_off + op.off;
         char* dptr = c->kv + (int64_t)op.slot * 2 * c->kv_part_bytes + op.seg * c->kv_part_bytes + op.off;
         dst = h2d ? (void*)dptr : (void*)hptr;
@@ -753,6 +780,15 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
     set_error("kv_on_host requires weights_on_host");
     return PIPO_ERR_UNSUPPORTED;
   }
+  if (pol.kv_fmt != PIPO_KV_FP16 && pol.kv_fmt != PIPO_KV_INT4_G64) {
+    set_error("unknown kv_fmt %d", pol.kv_fmt);
+    return PIPO_ERR_ARG;
+  }
+  if (pol.kv_fmt == PIPO_KV_INT4_G64 && shape->d_model % 256 != 0) {
+    set_error("an INT4 KV cache needs d_model %% 256 == 0 (d_model=%d)", shape->d_model);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  c->kv4 = pol.kv_fmt == PIPO_KV_INT4_G64;
   c->w4 = pol.wfmt == PIPO_W_INT4_G64;
   c->d = shape->d_model;
   c->F = shape->d_ffn;
@@ -948,7 +984,14 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
       c->gemm_ws = (float*)p;
     }
   }
-  c->kv_part_bytes = rows * d * 2;
+  c->kv_row = c->kv4 ? d / 2 + d / 16 : 2 * d;
+  c->kv_part_bytes = rows * c->kv_row;
+  if (c->kv4) {
+    PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+    c->kst = (uint16_t*)p;
+    PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+    c->vst = (uint16_t*)p;
+  }
   const int64_t kv_units = pol.kv_on_host ? pol.n_weight_slots : L;
   PIPO_TRY(dev_alloc(c, &p, kv_units * 2 * c->kv_part_bytes));
   c->kv = (char*)p;
@@ -1148,7 +1191,7 @@ pipo_status pipo_prefill(pipo_ctx* c, const int32_t* tokens, int32_t b, int32_t 
   c->b = b;
   // tokens[b][P] -> row i * P + p, the order the kernels use
   PIPO_TRY(stage_tokens(c, tokens, (int64_t)b * P));
-  c->pass = PassInfo{true, 0, P, (int64_t)b * c->d * 2};
+  c->pass = PassInfo{true, 0, P, (int64_t)b * c->kv_row};
   PIPO_TRY(run_pass(c, logits_out, next_out, false));
   c->pos = P;
   c->have_seq = true;
@@ -1175,7 +1218,7 @@ pipo_status pipo_decode_step(pipo_ctx* c, const int32_t* tokens, float* logits_o
   PIPO_HIP_TRY(hipSetDevice(c->device));
   const auto t0 = std::chrono::steady_clock::now();
   PIPO_TRY(stage_tokens(c, tokens, c->b));
-  c->pass = PassInfo{false, c->pos, 1, (int64_t)c->b * c->d * 2};
+  c->pass = PassInfo{false, c->pos, 1, (int64_t)c->b * c->kv_row};
   PIPO_TRY(run_pass(c, logits_out, next_out, true));
   c->pos += 1;
   c->stats.decode_steps++;

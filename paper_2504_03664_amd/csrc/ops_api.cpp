@@ -119,9 +119,43 @@ pipo_status pipo_op_attn_decode(const uint16_t* q, const uint16_t* kc, const uin
     set_error("attn_decode: NULL pointer or negative workspace size");
     return PIPO_ERR_ARG;
   }
-  return launch_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t,
+  return launch_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, false,
                             static_cast<float*>(workspace), workspace_bytes,
                             static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_attn_decode_kv4(const uint16_t* q, const uint8_t* kc, const uint8_t* vc,
+                                    uint16_t* o, int32_t b, int32_t n_heads, int32_t head_dim,
+                                    int32_t t, void* workspace, int64_t workspace_bytes,
+                                    void* stream) {
+  clear_error();
+  if (!q || !kc || !vc || !o || workspace_bytes < 0) {
+    set_error("attn_decode_kv4: NULL pointer or negative workspace size");
+    return PIPO_ERR_ARG;
+  }
+  return launch_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, true,
+                            static_cast<float*>(workspace), workspace_bytes,
+                            static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_kv_quant(const uint16_t* x, uint8_t* out, int64_t rows, int64_t d,
+                             void* stream) {
+  clear_error();
+  if (!x || !out) {
+    set_error("kv_quant: NULL pointer");
+    return PIPO_ERR_ARG;
+  }
+  return launch_kv_quant(x, out, rows, d, static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_kv_dequant(const uint8_t* in, uint16_t* y, int64_t rows, int64_t d,
+                               void* stream) {
+  clear_error();
+  if (!in || !y) {
+    set_error("kv_dequant: NULL pointer");
+    return PIPO_ERR_ARG;
+  }
+  return launch_kv_dequant(in, y, rows, d, static_cast<hipStream_t>(stream));
 }
 
 int64_t pipo_op_attn_decode_workspace_bytes(int32_t b, int32_t n_heads, int32_t head_dim,

@@ -174,6 +174,7 @@ class Workload:
     gen: int
     wfmt: str            # "fp16" or "int4"
     kv_on_host: bool
+    kv_fmt: str = "fp16"  # KV cache rows: "fp16" or "int4"
 
 
 WORKLOADS = (
@@ -182,6 +183,9 @@ WORKLOADS = (
     Workload("opt-13b b32 p512 g32 int4-g64", OPT_13B, 32, 512, 32, "int4", False),
     Workload("opt-30b b64 p512 g32 fp16", OPT_30B, 64, 512, 32, "fp16", False),
     Workload("opt-30b b128 p512 g32 int4-g64 kv-host", OPT_30B, 128, 512, 32, "int4", True),
+    # the previous workload with the KV cache in INT4 as well
+    Workload("opt-30b b128 p512 g32 int4-g64 kv-host kv-int4", OPT_30B, 128, 512, 32, "int4", True,
+             "int4"),
 )
 
 

@@ -22,10 +22,13 @@ def normwise(g, o):
     return np.abs(g - o).max(axis=-1) / np.abs(o).max(axis=-1)
 
 
-def teacher_forced_check(model, wfmt, prompt, gen_tokens, gpu_logits, dtype=np.float32):
-    """Oracle logits at every generated position, fed the GPU's tokens."""
+def teacher_forced_check(model, wfmt, prompt, gen_tokens, gpu_logits, dtype=np.float32,
+                         kv_int4=False):
+    """Oracle logits at every generated position, fed the GPU's tokens.  With
+    an INT4 cache the oracle keeps fp16 activations, so that its codes are
+    decided on the same fp16 keys and values as the kernels'."""
     full = np.concatenate([prompt, gen_tokens[:, :-1]], axis=1)
-    ref = OracleDecoder(model, dtype).forward(full)
+    ref = OracleDecoder(model, dtype, kv_int4=kv_int4, fp16_operands=kv_int4).forward(full)
     P = prompt.shape[1]
     errs, agree, total, ties = [], 0, 0, 0
     for s, lg in enumerate(gpu_logits):
@@ -200,5 +203,106 @@ def test_head_dim_64_kv_on_host():
         assert err <= REL_TOL
         tr, lr = _run(hw, prompt, 9, weights_on_host=False, embed_on_host=False)
         assert np.array_equal(lr.view(np.uint32), l0.view(np.uint32))
+    finally:
+        hw.free()
+
+
+@pytest.mark.parametrize("wfmt", ["fp16", "int4"])
+def test_int4_kv_cache_parity_and_placements(wfmt):
+    """INT4 KV cache (4-layer model, head_dim 128, prompt 70): against the
+    oracle with the same cache format, and bit-identical across resident
+    weights, KV in host memory (pinned, pageable through staging, two copy
+    streams with poisoned slots)."""
+    log(f"int4 kv cache, {wfmt} weights")
+    model = synth.SyntheticOPT(SMALL, seed=13, wfmt=wfmt)
+    hw = HostWeights(SMALL, wfmt, model)
+    try:
+        prompt = synth.prompt_tokens(3, 70, SMALL.vocab, seed=8)
+        t0, l0 = _run(hw, prompt, 6, kv_fmt="int4")
+        err, agree, ties = teacher_forced_check(model, wfmt, prompt, t0, list(l0), kv_int4=True)
+        log(f"  err {err:.2e} agree {agree:.3f} ({ties} near ties)")
+        assert err <= REL_TOL
+        assert agree >= ARGMAX_MIN or ties <= 1
+        for v in (dict(weights_on_host=False, embed_on_host=False),
+                  dict(kv_on_host=True),
+                  dict(kv_on_host=True, debug_flags=B.PIPO_DBG_KV_PAGEABLE, chunk_bytes=1 << 16),
+                  dict(kv_on_host=True, n_h2d_streams=2, chunk_bytes=8192,
+                       debug_flags=B.PIPO_DBG_POISON_SLOTS)):
+            log(f"  variant {v}")
+            tk, lk = _run(hw, prompt, 6, kv_fmt="int4", **v)
+            assert np.array_equal(tk, t0)
+            assert np.array_equal(lk.view(np.uint32), l0.view(np.uint32))
+    finally:
+        hw.free()
+
+
+class _BiasKV:
+    """A synthetic model whose key and value projections are zero: every
+    key and value row is its bias, an fp16 value, so the GPU and the oracle
+    quantize identical rows and the codes cannot differ."""
+
+    def __init__(self, base):
+        self.base, self.shape, self.wfmt = base, base.shape, base.wfmt
+
+    def fill(self, layer, name, out):
+        self.base.fill(layer, name, out)
+        if name == "wqkv":
+            out[self.shape.d_model:] = 0
+        return out
+
+    def layer(self, j):
+        L = dict(self.base.layer(j))
+        w = np.array(L["wqkv"])
+        w[self.shape.d_model:] = 0
+        L["wqkv"] = w
+        return L
+
+    def tok_emb(self):
+        return self.base.tok_emb()
+
+    def pos_emb(self):
+        return self.base.pos_emb()
+
+    def lnf(self):
+        return self.base.lnf()
+
+
+def test_int4_kv_cache_exact_decisions():
+    """With the same rows quantized on both sides the INT4-cache decoder meets
+    the fp16 bar against the plain fp32 oracle with the same cache format."""
+    log("int4 kv cache, identical codes")
+    model = _BiasKV(synth.SyntheticOPT(SMALL, seed=16))
+    hw = HostWeights(SMALL, "fp16", model)
+    try:
+        prompt = synth.prompt_tokens(2, 40, SMALL.vocab, seed=10)
+        t0, l0 = _run(hw, prompt, 6, kv_fmt="int4", kv_on_host=True)
+        full = np.concatenate([prompt, t0[:, :-1]], axis=1)
+        ref = OracleDecoder(model, np.float32, kv_int4=True).forward(full)
+        for s, lg in enumerate(l0):
+            o = ref[:, 40 - 1 + s]
+            assert normwise(lg.astype(np.float64), o.astype(np.float64)).max() <= REL_TOL
+    finally:
+        hw.free()
+
+
+def test_int4_kv_cache_head_dim_64_and_bad_width():
+    shape = synth.OPTShape(3, 256, 4, 1024, vocab=512, max_pos=64)
+    log("int4 kv cache, head_dim 64")
+    model = synth.SyntheticOPT(shape, seed=14)
+    hw = HostWeights(shape, "fp16", model)
+    try:
+        prompt = synth.prompt_tokens(5, 17, shape.vocab, seed=9)
+        t0, l0 = _run(hw, prompt, 9, kv_fmt="int4", kv_on_host=True, n_weight_slots=2)
+        err, agree, ties = teacher_forced_check(model, "fp16", prompt, t0, list(l0), kv_int4=True)
+        assert err <= REL_TOL
+    finally:
+        hw.free()
+    odd = synth.OPTShape(2, 384, 3, 768, vocab=100, max_pos=16)
+    model = synth.SyntheticOPT(odd, seed=15)
+    hw = HostWeights(odd, "fp16", model)
+    try:
+        with pytest.raises(B.PipoError) as e:
+            Decoder(hw, max_batch=1, max_seq=8, kv_fmt="int4")
+        assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_UNSUPPORTED"
     finally:
         hw.free()

@@ -4,7 +4,7 @@ import numpy as np
 import pytest
 
 import synth
-from oracle import causal_attention, dequant_int4_g64, layer_norm
+from oracle import causal_attention, dequant_int4_g64, layer_norm, quant_kv_int4_g64
 from paper_2504_03664_amd import binding as B
 from paper_2504_03664_amd.binding import DeviceBuffer as DB
 
@@ -200,6 +200,79 @@ def test_attn_decode_vs_oracle(b, T, H, D, split):
     for i in range(b):
         want = causal_attention(q[i:i + 1].astype(np.float64), kc[:, i].astype(np.float64),
                                 vc[:, i].astype(np.float64), H)[0]
+        assert np.abs(got[i] - want).max() <= 5e-3 * max(1.0, np.abs(want).max())
+
+
+def _kv_rows(codes, sm):
+    """INT4 cache rows as the library stores them: each row's d/2 code bytes,
+    then its d/64 fp16 (scale, min) pairs."""
+    R = codes.shape[0]
+    return np.ascontiguousarray(np.concatenate([codes, sm.view(np.uint8).reshape(R, -1)], axis=1))
+
+
+def _kv_test_rows(rng, R, d):
+    scales = np.array([1e-3, 0.02, 1.0, 300.0])[rng.integers(0, 4, R)]
+    x = (rng.standard_normal((R, d)) * scales[:, None]).astype(np.float16)
+    if R > 3:
+        x[1, 64:128] = np.float16(-2.5)                     # constant group: scale 0
+        half = np.arange(64) % 15 + 0.5                     # min 0, max 15: scale 1, the
+        half[:2] = 0, 15                                    # rest half-way between codes
+        x[2, :64] = half.astype(np.float16)
+        x[3, :64] = (np.arange(64) % 16) * 0.125 - 1.0      # exact grid points
+    return x
+
+
+@pytest.mark.parametrize("rows,d", [(1, 256), (37, 512), (300, 768), (5, 7168)])
+def test_kv_quant_dequant_bit_exact_vs_oracle(rows, d):
+    """The GPU quantizer makes the oracle's codes, scales and mins bit for
+    bit (the same fp32 decisions); the expansion is code * scale + min
+    rounded once to fp16."""
+    log(f"kv quant rows={rows} d={d}")
+    rng = np.random.default_rng(rows + d)
+    x = _kv_test_rows(rng, rows, d)
+    codes, sm = quant_kv_int4_g64(x)
+    want = _kv_rows(codes, sm)
+    dx, dq = DB.from_array(x), DB(want.nbytes)
+    B.pipo_op_kv_quant(dx.ptr, dq.ptr, rows, d)
+    B.pipo_dev_synchronize()
+    got = dq.to_array(np.uint8, want.shape)
+    assert np.array_equal(got, want)
+    dy = DB(rows * d * 2)
+    B.pipo_op_kv_dequant(dq.ptr, dy.ptr, rows, d)
+    B.pipo_dev_synchronize()
+    back = dy.to_array(np.float16, (rows, d))
+    assert np.array_equal(back, dequant_int4_g64(codes, sm, np.float64).astype(np.float16))
+
+
+@pytest.mark.parametrize("b,T,H,D", [(1, 1, 4, 64), (3, 70, 4, 128), (2, 1000, 2, 128),
+                                     (16, 543, 8, 64)])
+@pytest.mark.parametrize("split", [False, True])
+def test_attn_decode_kv4(b, T, H, D, split):
+    """Decode attention over an INT4 cache equals, bit for bit, the fp16
+    kernel over the expanded cache, and the oracle over the dequantized one."""
+    log(f"attn_decode_kv4 b={b} T={T} H={H} D={D} split={split}")
+    rng = np.random.default_rng(T + 7 * b)
+    d = H * D
+    q, kc, vc = _attn_inputs(rng, b, T, H, D)
+    ck, sk = quant_kv_int4_g64(kc.reshape(T * b, d))
+    cv, sv = quant_kv_int4_g64(vc.reshape(T * b, d))
+    k16 = dequant_int4_g64(ck, sk, np.float64).astype(np.float16).reshape(T, b, d)
+    v16 = dequant_int4_g64(cv, sv, np.float64).astype(np.float16).reshape(T, b, d)
+    dq, dk4, dv4 = DB.from_array(q), DB.from_array(_kv_rows(ck, sk)), DB.from_array(_kv_rows(cv, sv))
+    dk, dv = DB.from_array(k16), DB.from_array(v16)
+    ws_bytes = B.pipo_op_attn_decode_workspace_bytes(b, H, D, T - 1) if split else 0
+    ws = DB(ws_bytes) if ws_bytes else None
+    w = (ws.ptr if ws else None, ws_bytes)
+    o4, o16 = DB(b * d * 2), DB(b * d * 2)
+    B.pipo_op_attn_decode_kv4(dq.ptr, dk4.ptr, dv4.ptr, o4.ptr, b, H, D, T - 1, *w)
+    B.pipo_op_attn_decode(dq.ptr, dk.ptr, dv.ptr, o16.ptr, b, H, D, T - 1, *w)
+    B.pipo_dev_synchronize()
+    got = o4.to_array(np.uint16, (b, d))
+    assert np.array_equal(got, o16.to_array(np.uint16, (b, d)))
+    got = got.view(np.float16).astype(np.float64)
+    for i in range(b):
+        want = causal_attention(q[i:i + 1].astype(np.float64), k16[:, i].astype(np.float64),
+                                v16[:, i].astype(np.float64), H)[0]
         assert np.abs(got[i] - want).max() <= 5e-3 * max(1.0, np.abs(want).max())
 
 

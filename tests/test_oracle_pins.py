@@ -12,7 +12,7 @@ import pytest
 
 import synth
 from oracle import (OracleDecoder, causal_attention, dequant_int4_g64, layer_norm,
-                    param_count, streamed_bytes_per_step)
+                    param_count, quant_kv_int4_g64, streamed_bytes_per_step)
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -212,12 +212,17 @@ def test_relu_mlp_on_second_norm():
 
 # ---------------------------------------------------------------------------
 # whole-decoder brute force and invariants
-def brute_decoder(w, tokens):
-    """Scalar-loop forward of one sequence (float64, math only)."""
+def brute_decoder(w, tokens, fp16_act=False):
+    """Scalar-loop forward of one sequence (float64, math only); with fp16_act
+    the LayerNorm outputs, q, k, v, attention output and FC1 output are
+    rounded to fp16."""
     s = w.shape
     d, H, F = s.d_model, s.n_heads, s.d_ffn
     dh = d // H
     T = len(tokens)
+
+    def r(vec):
+        return [float(np.float16(a)) for a in vec] if fp16_act else vec
 
     def ln(vec, g, b):
         mu = sum(vec) / d
@@ -229,25 +234,27 @@ def brute_decoder(w, tokens):
 
     xs = [[w.tok[tokens[p]][c] + w.pos[p + s.pos_offset][c] for c in range(d)] for p in range(T)]
     for L in w.layers:
-        qkv = [lin(L["wqkv"], L["bqkv"], ln(x, L["ln1_g"], L["ln1_b"])) for x in xs]
+        qkv = [lin(L["wqkv"], L["bqkv"], r(ln(x, L["ln1_g"], L["ln1_b"]))) for x in xs]
+        qs = [r([a / math.sqrt(dh) for a in row[:d]]) for row in qkv]
+        ks = [r(row[d:2 * d]) for row in qkv]
+        vs = [r(row[2 * d:]) for row in qkv]
         new = []
         for i in range(T):
             o = [0.0] * d
             for hh in range(H):
-                sc = [sum(qkv[i][hh * dh + c] / math.sqrt(dh) * qkv[j][d + hh * dh + c]
-                          for c in range(dh)) for j in range(i + 1)]
+                sc = [sum(qs[i][hh * dh + c] * ks[j][hh * dh + c] for c in range(dh))
+                      for j in range(i + 1)]
                 m = max(sc)
                 e = [math.exp(a - m) for a in sc]
                 for c in range(dh):
-                    o[hh * dh + c] = sum(e[j] * qkv[j][2 * d + hh * dh + c]
-                                         for j in range(i + 1)) / sum(e)
-            x = [xs[i][c] + v for c, v in enumerate(lin(L["wo"], L["bo"], o))]
-            hid = [max(a, 0.0) for a in lin(L["w1"], L["b1"], ln(x, L["ln2_g"], L["ln2_b"]))]
+                    o[hh * dh + c] = sum(e[j] * vs[j][hh * dh + c] for j in range(i + 1)) / sum(e)
+            x = [xs[i][c] + v for c, v in enumerate(lin(L["wo"], L["bo"], r(o)))]
+            hid = r([max(a, 0.0) for a in lin(L["w1"], L["b1"], r(ln(x, L["ln2_g"], L["ln2_b"])))])
             new.append([x[c] + v for c, v in enumerate(lin(L["w2"], L["b2"], hid))])
         xs = new
     out = []
     for x in xs:
-        y = ln(x, w.lnf_g, w.lnf_b)
+        y = r(ln(x, w.lnf_g, w.lnf_b))
         out.append([sum(w.tok[t][c] * y[c] for c in range(d)) for t in range(s.vocab)])
     return np.array(out)
 
@@ -258,6 +265,18 @@ def test_decoder_vs_scalar_brute_force():
     got = OracleDecoder(w, np.float64).forward(toks)
     for b in range(2):
         assert np.allclose(got[b], brute_decoder(w, list(toks[b])), rtol=1e-11, atol=1e-11)
+
+
+def test_fp16_activation_mode_vs_scalar_brute_force():
+    """The fp16-activation reading against the scalar decoder that rounds
+    the same tensors, and its distance from the all-float64 decoder."""
+    w = random_hand(d=16, h=2, F=24, seed=31)
+    toks = np.array([[3, 1, 4, 1, 5, 9]])
+    got = OracleDecoder(w, np.float64, fp16_operands=True).forward(toks)[0]
+    assert np.allclose(got, brute_decoder(w, list(toks[0]), fp16_act=True), rtol=1e-11, atol=1e-11)
+    exact = OracleDecoder(w, np.float64).forward(toks)[0]
+    rel = np.abs(got - exact).max() / np.abs(exact).max()
+    assert 0 < rel < 1e-2
 
 
 def test_incremental_decode_equals_full_recompute():
@@ -354,6 +373,38 @@ def test_int4_weights_drive_the_same_decoder():
     assert np.abs(a - b).max() < 0.25 * np.abs(a).max()
 
 
+def test_fp16_operands_expand_int4_weights_to_fp16():
+    """In the fp16-operand reading an INT4 model computes exactly as the fp16
+    model whose weights are the expanded codes rounded to fp16."""
+    shape = synth.OPTShape(2, 64, 4, 256, vocab=97, max_pos=16)
+    m4 = synth.SyntheticOPT(shape, seed=3, wfmt="int4")
+
+    class Expanded:
+        def __init__(self):
+            self.shape, self.wfmt = m4.shape, "fp16"
+
+        def layer(self, j):
+            out = dict(m4.layer(j))
+            for nm in ("wqkv", "wo", "w1", "w2"):
+                out[nm] = dequant_int4_g64(*out[nm], np.float64).astype(np.float16)
+            return out
+
+        def tok_emb(self):
+            return m4.tok_emb()
+
+        def pos_emb(self):
+            return m4.pos_emb()
+
+        def lnf(self):
+            return m4.lnf()
+
+    toks = np.array([[1, 5, 9, 13]])
+    a = OracleDecoder(m4, np.float64, fp16_operands=True).forward(toks)
+    b = OracleDecoder(Expanded(), np.float64, fp16_operands=True).forward(toks)
+    assert np.array_equal(a, b)
+    assert not np.array_equal(a, OracleDecoder(m4, np.float64).forward(toks))
+
+
 # ---------------------------------------------------------------------------
 # shapes and bytes
 def test_parameter_counts_of_opt_shapes():
@@ -387,3 +438,94 @@ def test_streamed_bytes_per_step_closed_forms():
     kv = streamed_bytes_per_step(2, 64, 256, 10, "fp16", stream_head=False, kv_batch=3, kv_len=5)
     assert kv - streamed_bytes_per_step(2, 64, 256, 10, "fp16", stream_head=False) == \
         2 * 2 * 3 * 5 * 64 * 2
+    # the same prefix as INT4 rows: d/2 code bytes and d/64 (scale, min) pairs
+    kv4 = streamed_bytes_per_step(2, 64, 256, 10, "fp16", stream_head=False, kv_batch=3, kv_len=5,
+                                  kv_fmt="int4")
+    assert kv4 - streamed_bytes_per_step(2, 64, 256, 10, "fp16", stream_head=False) == \
+        2 * 2 * 3 * 5 * (32 + 4)
+
+
+# ---------------------------------------------------------------------------
+# INT4 KV cache entries
+def test_kv_int4_grid_values_are_exact():
+    """Rows built as m + code * s (fp16-exact, each group holding codes 0 and
+    15) come back with exactly those codes, s and m, and dequantize exactly."""
+    rng = np.random.default_rng(21)
+    R, d = 5, 256
+    codes = rng.integers(0, 16, (R, d))
+    codes[:, 0::64] = 0
+    codes[:, 1::64] = 15
+    s = (2.0 ** rng.integers(-8, 0, (R, d // 64))).astype(np.float16)
+    m = (rng.integers(-64, 64, (R, d // 64)) / 64.0).astype(np.float16)
+    x = m.astype(np.float64).repeat(64, 1) + codes * s.astype(np.float64).repeat(64, 1)
+    assert np.array_equal(x.astype(np.float16).astype(np.float64), x)
+    q, sm = quant_kv_int4_g64(x.astype(np.float16))
+    assert np.array_equal(sm[..., 0], s) and np.array_equal(sm[..., 1], m)
+    assert np.array_equal(q & 0x0F, codes[:, 0::2]) and np.array_equal(q >> 4, codes[:, 1::2])
+    assert np.array_equal(dequant_int4_g64(q, sm, np.float64), x)
+
+
+def test_kv_int4_rounding_half_even_and_nibbles():
+    """Group with min 0 and max 15 (scale exactly 1): halves round to even,
+    and codes pack two per byte, even element low."""
+    row = np.zeros(64, np.float16)
+    row[:8] = [0, 15, 0.5, 1.5, 2.5, 14.5, 7.25, 7.75]
+    q, sm = quant_kv_int4_g64(row[None])
+    assert sm[0, 0, 0] == 1 and sm[0, 0, 1] == 0
+    assert list(q[0, :4]) == [0 | 15 << 4, 0 | 2 << 4, 2 | 14 << 4, 7 | 8 << 4]
+    ramp = np.arange(16, dtype=np.float16).repeat(4)          # codes 0,0,0,0,1,1,1,1,...
+    q, _ = quant_kv_int4_g64(ramp[None])
+    assert list(q[0, :4]) == [0x00, 0x00, 0x11, 0x11]
+
+
+def test_kv_int4_roundtrip_bound_monotone_constant_groups():
+    rng = np.random.default_rng(22)
+    for scale in (1e-3, 0.02, 1.0, 300.0):
+        x = (rng.standard_normal((7, 512)) * scale).astype(np.float16)
+        x[3, 64:128] = np.float16(0.375)                      # a constant group
+        q, sm = quant_kv_int4_g64(x)
+        back = dequant_int4_g64(q, sm, np.float64)
+        s = sm[..., 0].astype(np.float64).repeat(64, 1)
+        # nearest grid point: half a step, plus fp32 rounding of the division
+        err = np.abs(back - x.astype(np.float64))
+        assert (err <= 0.5 * s * (1 + 1e-6) + 1e-30).all()
+        assert np.array_equal(back[3, 64:128], x[3, 64:128].astype(np.float64))
+        c = np.empty(x.shape, np.int64)
+        c[:, 0::2], c[:, 1::2] = q & 0x0F, q >> 4
+        for r in range(x.shape[0]):
+            for g in range(x.shape[1] // 64):
+                xs, cs = x[r, 64 * g:64 * g + 64], c[r, 64 * g:64 * g + 64]
+                order = np.argsort(xs, kind="stable")
+                assert (np.diff(cs[order]) >= 0).all()       # codes never decrease with x
+
+
+@pytest.mark.parametrize("fp16_act", [False, True])
+def test_kv_int4_incremental_decode_equals_full_recompute(fp16_act):
+    w = random_hand(d=64, h=2, F=32, seed=23)
+    toks = np.array([[1, 2, 3, 4, 5, 6, 7], [7, 6, 5, 4, 3, 2, 1]])
+    dec = OracleDecoder(w, np.float64, kv_int4=True, fp16_operands=fp16_act)
+    full = dec.forward(toks)
+    assert not np.allclose(full, OracleDecoder(w, np.float64).forward(toks), rtol=1e-6)
+    P = 3
+    logits, cache = dec.prefill(toks[:, :P])
+    assert np.allclose(logits, full[:, P - 1], rtol=1e-12, atol=1e-12)
+    for t in range(P, toks.shape[1]):
+        assert np.allclose(dec.decode(cache, toks[:, t]), full[:, t], rtol=1e-12, atol=1e-12)
+
+
+def test_kv_int4_values_are_the_cached_entries():
+    """With Wk = Wv = 0 every key and value row is its bias, so the INT4-cache
+    decoder must equal the plain decoder whose biases are replaced by their
+    cache entries (and differ from the plain one with the original biases)."""
+    w = random_hand(d=64, h=2, F=32, seed=24)
+    for lw in w.layers:
+        lw["wqkv"][64:] = 0
+    toks = np.array([[1, 2, 3, 4, 5]])
+    got = OracleDecoder(w, np.float64, kv_int4=True).forward(toks)
+    plain = OracleDecoder(w, np.float64).forward(toks)
+    assert not np.allclose(got, plain, rtol=1e-9)
+    for lw in w.layers:
+        kv = lw["bqkv"][64:].reshape(2, 64).astype(np.float16)
+        q, sm = quant_kv_int4_g64(kv)
+        lw["bqkv"] = np.concatenate([lw["bqkv"][:64], dequant_int4_g64(q, sm, np.float64).ravel()])
+    assert np.allclose(got, OracleDecoder(w, np.float64).forward(toks), rtol=1e-12, atol=1e-12)
