@@ -45,7 +45,7 @@ def parse():
                     help="index into synth.WORKLOADS (default: the OPT-30B fp16 decode)")
     ap.add_argument("--chunk-mb", type=int, default=64)
     ap.add_argument("--slots", type=int, default=3)
-    ap.add_argument("--h2d-streams", type=int, default=1)
+    ap.add_argument("--h2d-streams", type=int, default=2)
     ap.add_argument("--no-timestamps", action="store_true",
                     help="skip device timestamps (no busy %% or kernel roofline)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -195,7 +195,8 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     shape = wl.shape if args.layers <= 0 else wl.shape.with_layers(args.layers)
     W, K = args.warmup, args.steps
-    max_seq = max(wl.prompt + wl.gen, wl.prompt + 1 + W + K)
+    KI = 0 if args.no_timestamps else min(K, 10)   # instrumented steps after the timed ones
+    max_seq = max(wl.prompt + wl.gen, wl.prompt + 1 + W + K + KI)
     seed = synth.DEFAULT_SEED
     log(f"workload {wl.name}: {shape.n_layers} layers, d {shape.d_model}, batch {wl.batch}")
 
@@ -208,12 +209,10 @@ def main():
     peak = max(peak1, peak2)
     log(f"H2D link peak: {peak1:.1f} GB/s (1 stream), {peak2:.1f} GB/s (2 streams)")
 
-    flags = 0 if args.no_timestamps else B.PIPO_DBG_TIMESTAMPS
     dec = Decoder(hw, weights_on_host=True, embed_on_host=True, kv_on_host=wl.kv_on_host,
                   kv_fmt=wl.kv_fmt,
                   n_weight_slots=args.slots, n_h2d_streams=args.h2d_streams,
-                  chunk_bytes=args.chunk_mb << 20, max_batch=wl.batch, max_seq=max_seq,
-                  debug_flags=flags)
+                  chunk_bytes=args.chunk_mb << 20, max_batch=wl.batch, max_seq=max_seq)
     prompt = synth.prompt_tokens(wl.batch, wl.prompt, shape.vocab, seed=1, stream=args.workload)
     t0 = time.perf_counter()
     nxt, _ = dec.prefill(prompt)
@@ -222,12 +221,27 @@ def main():
     for _ in range(W):
         nxt, _ = dec.decode(nxt)
     dec.reset_stats()
+    step_s = []
     t0 = time.perf_counter()
     for _ in range(K):
+        ts = time.perf_counter()
         nxt, _ = dec.decode(nxt)
+        step_s.append(time.perf_counter() - ts)
     dt = time.perf_counter() - t0
     st = dec.stats()
     log(f"{K} decode steps in {dt:.3f} s")
+    if KI:
+        # device timestamps around every copy and kernel, over separate
+        # steps: they add events and a stream synchronisation per step, so
+        # the throughput above is measured without them
+        dec.set_timestamps(True)
+        dec.reset_stats()
+        ti = time.perf_counter()
+        for _ in range(KI):
+            nxt, _ = dec.decode(nxt)
+        dti = time.perf_counter() - ti
+        sti = dec.stats()
+        log(f"{KI} instrumented decode steps in {dti:.3f} s")
     dec.close()
 
     value = wl.batch * K / dt
@@ -254,13 +268,21 @@ def main():
                      "roofline_tokens_per_s": round(roof, 3),
                      "frac_of_roofline": round(value / roof, 4)},
         "ttft_ms": round(ttft_ms, 1),
+        "step_ms": {"median": round(float(np.median(step_s)) * 1e3, 3),
+                    "min": round(min(step_s) * 1e3, 3), "max": round(max(step_s) * 1e3, 3),
+                    "source": "host clock around each pipo_decode_step (returns after the "
+                              "token readback; later steps' loads may already run ahead)"},
     }
-    if not args.no_timestamps and st["window_ms"] > 0:
+    if KI and sti["window_ms"] > 0:
+        st = sti
         out["gpu_busy"] = {"busy_frac": round(st["busy_ms"] / st["window_ms"], 4),
                            "copy_busy_frac": round(st["copy_busy_ms"] / st["window_ms"], 4),
                            "kernel_busy_frac": round(st["kernel_busy_ms"] / st["window_ms"], 4),
                            "window_ms": round(st["window_ms"], 2),
-                           "source": "HIP events around every copy and kernel"}
+                           "steps": KI,
+                           "instrumented_tokens_per_s": round(wl.batch * KI / dti, 3),
+                           "source": "HIP events around every copy and kernel, over "
+                                     f"{KI} decode steps after the timed ones"}
         # dominant decode kernel, grouped by kernel symbol: the GEMM epilogue is
         # a template parameter, so the out-projection and FC2 share one symbol
         gemm = gemm_family(wl.batch)

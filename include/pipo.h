@@ -124,7 +124,8 @@ typedef struct {
                                 before its attention and the new rows saved after it (a call
                                 returns with its rows saved); 0: KV cache resident in HBM */
   int32_t n_weight_slots;    /* HBM slots the layers rotate through (default 3, min 2) */
-  int32_t n_h2d_streams;     /* host-to-device copy streams (default 1, max 2) */
+  int32_t n_h2d_streams;     /* host-to-device copy streams (default 2, max 2); chunk k goes
+                                to stream k % n, so one DMA is always queued behind another */
   int64_t chunk_bytes;       /* bytes per copy chunk (default 64 MiB; rounded to 4 KiB) */
   int32_t max_batch;         /* sequences per pass (>= 1) */
   int32_t max_seq;           /* prompt + generated positions per sequence (<= max_pos) */
@@ -216,6 +217,12 @@ pipo_status pipo_decode_step(pipo_ctx* ctx, const int32_t* tokens, float* logits
 /* Copy the context's counters into *out (see pipo_stats). */
 pipo_status pipo_get_stats(pipo_ctx* ctx, pipo_stats* out);
 
+/* Turn device timestamps (PIPO_DBG_TIMESTAMPS) on or off between calls.
+ * While on, every copy and kernel is bracketed by two events and each pass
+ * ends by synchronising all of the context's streams (which stops the next
+ * call's loads from running ahead); figures recorded so far are kept. */
+pipo_status pipo_set_timestamps(pipo_ctx* ctx, int32_t on);
+
 /* Zero the counters and timelines of pipo_stats (allocation figures stay). */
 pipo_status pipo_reset_stats(pipo_ctx* ctx);
 
@@ -230,6 +237,16 @@ void pipo_destroy(pipo_ctx* ctx);
  */
 pipo_status pipo_measure_h2d_peak(int64_t bytes, int32_t iters, int32_t n_streams,
                                   double* gbps);
+
+/*
+ * The same probe with the transfer pattern of the pipeline (Section 3.3,
+ * blockwise transfer): each round copies `bytes` as consecutive copies of
+ * chunk_bytes, copy k on stream k % n_streams, timed from the first copy's
+ * start to the last one's end; best of `iters` rounds.  Used to choose
+ * pipo_policy.chunk_bytes.  Errors: ARG, OOM_HOST, OOM_DEVICE, HIP.
+ */
+pipo_status pipo_measure_h2d_chunked(int64_t bytes, int64_t chunk_bytes, int32_t iters,
+                                     int32_t n_streams, double* gbps);
 
 /* Pinned (page-locked) host memory, 4 KiB aligned; NULL on failure.
  * Matrices placed here are streamed by the copy engines without staging. */

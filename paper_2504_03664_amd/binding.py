@@ -100,7 +100,9 @@ _SIGNATURES = {
     "pipo_get_stats": ([vp, ctypes.POINTER(PipoStats)], i32),
     "pipo_reset_stats": ([vp], i32),
     "pipo_destroy": ([vp], None),
+    "pipo_set_timestamps": ([vp, i32], i32),
     "pipo_measure_h2d_peak": ([i64, i32, i32, ctypes.POINTER(f64)], i32),
+    "pipo_measure_h2d_chunked": ([i64, i64, i32, i32, ctypes.POINTER(f64)], i32),
     "pipo_host_alloc": ([sz], vp),
     "pipo_host_free": ([vp], None),
     "pipo_last_error": ([], ctypes.c_char_p),
@@ -218,6 +220,10 @@ def pipo_reset_stats(ctx: int) -> None:
     _check(lib().pipo_reset_stats(ctx), "pipo_reset_stats")
 
 
+def pipo_set_timestamps(ctx: int, on: bool) -> None:
+    _check(lib().pipo_set_timestamps(ctx, int(on)), "pipo_set_timestamps")
+
+
 def pipo_destroy(ctx: int) -> None:
     lib().pipo_destroy(ctx)
 
@@ -226,6 +232,14 @@ def pipo_measure_h2d_peak(nbytes: int, iters: int = 10, n_streams: int = 1) -> f
     g = f64()
     _check(lib().pipo_measure_h2d_peak(nbytes, iters, n_streams, ctypes.byref(g)),
            "pipo_measure_h2d_peak")
+    return g.value
+
+
+def pipo_measure_h2d_chunked(nbytes: int, chunk_bytes: int, iters: int = 5,
+                             n_streams: int = 1) -> float:
+    g = f64()
+    _check(lib().pipo_measure_h2d_chunked(nbytes, chunk_bytes, iters, n_streams, ctypes.byref(g)),
+           "pipo_measure_h2d_chunked")
     return g.value
 
 

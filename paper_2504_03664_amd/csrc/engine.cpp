@@ -762,7 +762,7 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
     return PIPO_ERR_ARG;
   }
   if (pol.n_weight_slots == 0) pol.n_weight_slots = 3;
-  if (pol.n_h2d_streams == 0) pol.n_h2d_streams = 1;
+  if (pol.n_h2d_streams == 0) pol.n_h2d_streams = 2;
   if (pol.chunk_bytes == 0) pol.chunk_bytes = 64ll << 20;
   pol.chunk_bytes = align_up(pol.chunk_bytes, 4096);
   if (pol.n_weight_slots < 2 || pol.n_weight_slots > 16 || pol.n_h2d_streams < 1 ||
@@ -1251,6 +1251,18 @@ pipo_status pipo_get_stats(pipo_ctx* c, pipo_stats* out) {
   return PIPO_OK;
 }
 
+pipo_status pipo_set_timestamps(pipo_ctx* c, int32_t on) {
+  clear_error();
+  if (!c) {
+    set_error("NULL argument");
+    return PIPO_ERR_ARG;
+  }
+  PIPO_HIP_TRY(hipSetDevice(c->device));
+  PIPO_TRY(resolve_timeline(c));
+  c->timestamps = on != 0;
+  return PIPO_OK;
+}
+
 pipo_status pipo_reset_stats(pipo_ctx* c) {
   clear_error();
   if (!c) {
@@ -1272,9 +1284,11 @@ pipo_status pipo_reset_stats(pipo_ctx* c) {
   return PIPO_OK;
 }
 
-pipo_status pipo_measure_h2d_peak(int64_t bytes, int32_t iters, int32_t n_streams, double* gbps) {
-  clear_error();
-  if (bytes <= 0 || iters < 1 || n_streams < 1 || n_streams > 2 || !gbps) {
+// `bytes` pinned -> HBM per round as consecutive copies of `chunk` bytes,
+// copy k on stream k % n_streams (the pipeline's pattern); best round
+static pipo_status measure_h2d(int64_t bytes, int64_t chunk, int32_t iters, int32_t n_streams,
+                               double* gbps) {
+  if (bytes <= 0 || chunk <= 0 || iters < 1 || n_streams < 1 || n_streams > 2 || !gbps) {
     set_error("invalid arguments");
     return PIPO_ERR_ARG;
   }
@@ -1292,7 +1306,7 @@ pipo_status pipo_measure_h2d_peak(int64_t bytes, int32_t iters, int32_t n_stream
     return PIPO_ERR_OOM_DEVICE;
   }
   hipStream_t st[2] = {};
-  hipEvent_t e0, e1, ej;
+  hipEvent_t e0 = nullptr, e1 = nullptr, ej = nullptr;
   pipo_status status = PIPO_OK;
   double best = 0;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess ||
@@ -1302,15 +1316,14 @@ pipo_status pipo_measure_h2d_peak(int64_t bytes, int32_t iters, int32_t n_stream
   }
   for (int i = 0; i < n_streams && status == PIPO_OK; ++i)
     if (hipStreamCreateWithFlags(&st[i], hipStreamNonBlocking) != hipSuccess) status = PIPO_ERR_HIP;
-  const int64_t half = pipo::align_up(bytes / n_streams, 4096);
   for (int it = 0; it <= iters && status == PIPO_OK; ++it) {  // first round warms up
     bool ok = hipEventRecord(e0, st[0]) == hipSuccess;
     if (n_streams == 2) ok = ok && hipStreamWaitEvent(st[1], e0, 0) == hipSuccess;
-    for (int i = 0; i < n_streams && ok; ++i) {
-      const int64_t a = i * half, n = std::min(bytes, a + half) - a;
-      if (n > 0)
-        ok = hipMemcpyAsync((char*)dptr + a, (char*)h + a, (size_t)n, hipMemcpyHostToDevice,
-                            st[i]) == hipSuccess;
+    int k = 0;
+    for (int64_t a = 0; a < bytes && ok; a += chunk, ++k) {
+      const int64_t n = std::min(chunk, bytes - a);
+      ok = hipMemcpyAsync((char*)dptr + a, (char*)h + a, (size_t)n, hipMemcpyHostToDevice,
+                          st[k % n_streams]) == hipSuccess;
     }
     if (n_streams == 2) {
       ok = ok && hipEventRecord(ej, st[1]) == hipSuccess &&
@@ -1328,13 +1341,29 @@ pipo_status pipo_measure_h2d_peak(int64_t bytes, int32_t iters, int32_t n_stream
   }
   for (int i = 0; i < 2; ++i)
     if (st[i]) (void)hipStreamDestroy(st[i]);
-  (void)hipEventDestroy(e0);
-  (void)hipEventDestroy(e1);
-  (void)hipEventDestroy(ej);
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (ej) (void)hipEventDestroy(ej);
   (void)hipFree(dptr);
   pipo::host_free_pinned(h);
   *gbps = best;
   return status;
+}
+
+pipo_status pipo_measure_h2d_peak(int64_t bytes, int32_t iters, int32_t n_streams, double* gbps) {
+  clear_error();
+  if (n_streams < 1) {
+    set_error("invalid arguments");
+    return PIPO_ERR_ARG;
+  }
+  return measure_h2d(bytes, pipo::align_up((bytes + n_streams - 1) / n_streams, 4096), iters,
+                     n_streams, gbps);
+}
+
+pipo_status pipo_measure_h2d_chunked(int64_t bytes, int64_t chunk_bytes, int32_t iters,
+                                     int32_t n_streams, double* gbps) {
+  clear_error();
+  return measure_h2d(bytes, chunk_bytes, iters, n_streams, gbps);
 }
 
 }  // extern "C"

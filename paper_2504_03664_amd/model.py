@@ -137,7 +137,7 @@ def c_shape(shape) -> B.PipoShape:
 
 
 def c_policy(wfmt: str = "fp16", weights_on_host: bool = True, embed_on_host: bool = True,
-             kv_on_host: bool = False, n_weight_slots: int = 3, n_h2d_streams: int = 1,
+             kv_on_host: bool = False, n_weight_slots: int = 3, n_h2d_streams: int = 0,
              chunk_bytes: int = 64 << 20, max_batch: int = 1, max_seq: int = 1,
              hbm_budget_bytes: int = 0, debug_flags: int = 0,
              copy_delay_us: int = 0, pinned_budget_bytes: int = 0,
@@ -192,6 +192,9 @@ class Decoder:
 
     def reset_stats(self) -> None:
         B.pipo_reset_stats(self.ctx)
+
+    def set_timestamps(self, on: bool) -> None:
+        B.pipo_set_timestamps(self.ctx, on)
 
     def close(self) -> None:
         if self.ctx:

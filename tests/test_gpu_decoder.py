@@ -93,6 +93,7 @@ def test_streamed_bit_identical_to_resident(opt125m):
     t0, l0 = _run(hw, prompt, 6, weights_on_host=False, embed_on_host=False)
     variants = [
         dict(),
+        dict(n_h2d_streams=1),
         dict(n_weight_slots=2, chunk_bytes=4096 * 37),
         dict(n_h2d_streams=2, chunk_bytes=1 << 20, n_weight_slots=4),
         dict(debug_flags=B.PIPO_DBG_POISON_SLOTS | B.PIPO_DBG_COPY_DELAY, copy_delay_us=200,
