@@ -123,7 +123,11 @@ typedef struct {
                                 possible, see pinned_budget_bytes), each layer's prefix loaded
                                 before its attention and the new rows saved after it (a call
                                 returns with its rows saved); 0: KV cache resident in HBM */
-  int32_t n_weight_slots;    /* HBM slots the layers rotate through (default 3, min 2) */
+  int32_t n_weight_slots;    /* HBM slots the layers rotate through (default 3, 1..16).  3: the
+                                performance-optimized pipeline (Section 3.2.3) -- loads run two
+                                units ahead; 1: the memory-efficient pipeline -- one layer's
+                                weights (and KV buffer) in HBM, a unit's load waits until the
+                                previous unit's compute (and KV save) is done */
   int32_t n_h2d_streams;     /* host-to-device copy streams (default 2, max 2); chunk k goes
                                 to stream k % n, so one DMA is always queued behind another */
   int64_t chunk_bytes;       /* bytes per copy chunk (default 64 MiB; rounded to 4 KiB) */
@@ -140,6 +144,27 @@ typedef struct {
   int32_t copy_threads;      /* host threads for staged copies (default 8) */
   int32_t kv_fmt;            /* PIPO_KV_FP16 (default) or PIPO_KV_INT4_G64 */
 } pipo_policy;
+
+/* The paper's two pipeline options (Section 3.2.3). */
+enum { PIPO_PIPE_PERFORMANCE = 0, PIPO_PIPE_MEMORY_EFFICIENT = 1 };
+
+/* What a policy costs (pipo_plan_policy, pipo_configure).  hbm_bytes is the
+ * exact sum of the device allocations pipo_create makes for the policy
+ * (activations are sized for max_batch x max_seq rows: the prefill peak). */
+typedef struct {
+  int64_t weight_bytes;        /* W: layer tensors, token and position tables, final LN */
+  int64_t kv_bytes;            /* C: KV cache of max_batch x max_seq positions, all layers */
+  int64_t hbm_bytes;           /* device memory pipo_create allocates */
+  int64_t host_kv_bytes;       /* host memory the library allocates for the KV cache */
+  int64_t h2d_bytes_per_step;  /* host-to-device bytes of a decode step at the last position */
+  int32_t pipeline;            /* PIPO_PIPE_* (memory-efficient: n_weight_slots == 1) */
+} pipo_plan;
+
+/* Resources for the automatic configuration. */
+typedef struct {
+  int64_t hbm_bytes;   /* device memory the context may use; 0: the device's free memory */
+  int64_t host_bytes;  /* host memory for a host KV cache; 0: the system's available memory */
+} pipo_resources;
 
 /* Per-kernel timing (filled when PIPO_DBG_TIMESTAMPS is set): each launch
  * is bracketed by events on the stream that runs it. */
@@ -216,6 +241,32 @@ pipo_status pipo_decode_step(pipo_ctx* ctx, const int32_t* tokens, float* logits
 
 /* Copy the context's counters into *out (see pipo_stats). */
 pipo_status pipo_get_stats(pipo_ctx* ctx, pipo_stats* out);
+
+/* Cost of a policy for a shape (no allocation, no device needed).
+ * Errors: ARG, UNSUPPORTED (as pipo_create would report them). */
+pipo_status pipo_plan_policy(const pipo_shape* shape, const pipo_policy* policy,
+                             pipo_plan* plan_out);
+
+/*
+ * Automatic configuration (Section 3.5, Eq. (1); Algorithm 2's Configure):
+ * choose where the weights, the output head and the KV cache live and which
+ * pipeline runs, for a shape, weight and KV formats, max_batch and max_seq
+ * within the given resources.  Eq. (1) puts the weights in HBM when they
+ * fit, else in host memory, and takes the performance-optimized pipeline
+ * when its peak memory fits, else the memory-efficient one; here every
+ * placement (weights and head resident or streamed, KV resident or on the
+ * host) and pipeline (3, 2 or 1 slots) is costed exactly and the one that
+ * streams the fewest bytes per decode step within the budgets wins, more
+ * slots on ties.  *policy_out gets the choice (with hbm_budget_bytes set to
+ * the budget, chunk_bytes and copy streams at their defaults) and, if
+ * plan_out is not NULL, its cost.  Errors: ARG, UNSUPPORTED, OOM_DEVICE
+ * (not even the memory-efficient pipeline fits), OOM_HOST (the KV cache
+ * fits neither in HBM nor in host memory; the paper's disk tier is not
+ * built), HIP (querying free HBM).
+ */
+pipo_status pipo_configure(const pipo_shape* shape, int32_t wfmt, int32_t kv_fmt,
+                           int32_t max_batch, int32_t max_seq, const pipo_resources* res,
+                           pipo_policy* policy_out, pipo_plan* plan_out);
 
 /* Turn device timestamps (PIPO_DBG_TIMESTAMPS) on or off between calls.
  * While on, every copy and kernel is bracketed by two events and each pass

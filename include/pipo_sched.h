@@ -21,7 +21,7 @@ extern "C" {
 
 typedef struct {
   int32_t n_layers;
-  int32_t n_slots;          /* >= 2 */
+  int32_t n_slots;          /* >= 1 (1: no unit is loaded before the previous one is done) */
   int32_t n_h2d;            /* 1 or 2 */
   int32_t layers_streamed;  /* 0/1 */
   int32_t head_streamed;    /* 0/1 */

@@ -33,6 +33,7 @@
 #include <vector>
 
 #include "common.h"
+#include "plan.h"
 #include "schedule.h"
 
 namespace pipo {
@@ -109,7 +110,6 @@ static void par_memcpy(void* dst, const void* src, size_t n) {
   for (auto& t : th) t.join();
 }
 
-static inline int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 
 // Host worker threads for copies between pageable and pinned memory (the
 // paper's multi-thread parallel transfer, Section 3.3): a copy is cut into
@@ -331,32 +331,6 @@ static hipEvent_t tevent(pipo_ctx* c) {
 
 // ---------------------------------------------------------------------------
 // validation
-static pipo_status check_shape(const pipo_shape* s) {
-  if (!s) {
-    set_error("shape is NULL");
-    return PIPO_ERR_ARG;
-  }
-  if (s->n_layers < 1 || s->d_model < 1 || s->n_heads < 1 || s->d_ffn < 1 || s->vocab < 1 ||
-      s->max_pos < 1 || s->pos_offset < 0 || !(s->ln_eps >= 0.f)) {
-    set_error("invalid shape");
-    return PIPO_ERR_ARG;
-  }
-  if (s->d_model % s->n_heads != 0) {
-    set_error("d_model %d is not a multiple of n_heads %d", s->d_model, s->n_heads);
-    return PIPO_ERR_ARG;
-  }
-  const int dh = s->d_model / s->n_heads;
-  if (dh != 64 && dh != 128) {
-    set_error("head_dim %d not supported (64 or 128)", dh);
-    return PIPO_ERR_UNSUPPORTED;
-  }
-  if (s->d_model % 128 != 0 || s->d_ffn % 128 != 0 || s->d_model > 8192) {
-    set_error("d_model %d / d_ffn %d must be multiples of 128 (d_model <= 8192)", s->d_model,
-              s->d_ffn);
-    return PIPO_ERR_UNSUPPORTED;
-  }
-  return PIPO_OK;
-}
 
 // ---------------------------------------------------------------------------
 // kernels of one op
@@ -757,37 +731,7 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   c->sh = *shape;
   c->pol = *policy;
   pipo_policy& pol = c->pol;
-  if (pol.wfmt != PIPO_W_FP16 && pol.wfmt != PIPO_W_INT4_G64) {
-    set_error("unknown weight format %d", pol.wfmt);
-    return PIPO_ERR_ARG;
-  }
-  if (pol.n_weight_slots == 0) pol.n_weight_slots = 3;
-  if (pol.n_h2d_streams == 0) pol.n_h2d_streams = 2;
-  if (pol.chunk_bytes == 0) pol.chunk_bytes = 64ll << 20;
-  pol.chunk_bytes = align_up(pol.chunk_bytes, 4096);
-  if (pol.n_weight_slots < 2 || pol.n_weight_slots > 16 || pol.n_h2d_streams < 1 ||
-      pol.n_h2d_streams > 2 || pol.max_batch < 1 || pol.max_seq < 1 || pol.chunk_bytes < 0 ||
-      pol.copy_delay_us < 0) {
-    set_error("invalid policy");
-    return PIPO_ERR_ARG;
-  }
-  if (pol.max_seq > shape->max_pos || pol.max_seq > kAttnDecodeMaxT) {
-    set_error("max_seq %d exceeds max_pos %d or the decode kernel's %d keys", pol.max_seq,
-              shape->max_pos, kAttnDecodeMaxT);
-    return PIPO_ERR_UNSUPPORTED;
-  }
-  if (pol.kv_on_host && !pol.weights_on_host) {
-    set_error("kv_on_host requires weights_on_host");
-    return PIPO_ERR_UNSUPPORTED;
-  }
-  if (pol.kv_fmt != PIPO_KV_FP16 && pol.kv_fmt != PIPO_KV_INT4_G64) {
-    set_error("unknown kv_fmt %d", pol.kv_fmt);
-    return PIPO_ERR_ARG;
-  }
-  if (pol.kv_fmt == PIPO_KV_INT4_G64 && shape->d_model % 256 != 0) {
-    set_error("an INT4 KV cache needs d_model %% 256 == 0 (d_model=%d)", shape->d_model);
-    return PIPO_ERR_UNSUPPORTED;
-  }
+  PIPO_TRY(normalize_policy(shape, &pol));
   c->kv4 = pol.kv_fmt == PIPO_KV_INT4_G64;
   c->w4 = pol.wfmt == PIPO_W_INT4_G64;
   c->d = shape->d_model;
@@ -800,32 +744,17 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   PIPO_HIP_TRY(hipGetDevice(&c->device));
   const int64_t d = c->d, F = c->F, V = c->V, L = c->L;
 
-  // unit layout
-  c->misc_bytes = (9 * d + F) * 2;
-  const auto mat = [&](int seg, int64_t N, int64_t K) {
-    if (c->w4) {
-      c->seg_bytes[seg] = N * K / 2;
-      c->seg_bytes[seg + 1] = N * (K / 64) * 4;
-    } else {
-      c->seg_bytes[seg] = N * K * 2;
-    }
-  };
-  c->seg_bytes[kSegMisc] = c->misc_bytes;
-  mat(kSegWqkv, 3 * d, d);
-  mat(kSegWo, d, d);
-  mat(kSegW1, F, d);
-  mat(kSegW2, d, F);
-  int64_t off = 0;
+  // unit layout and device allocations (plan.h: the same sizes pipo_plan_policy reports)
+  const UnitLayout ul = unit_layout(*shape, c->w4);
+  const HbmPlan hp = hbm_plan(*shape, pol);
   for (int sg = 0; sg < kNumSegs; ++sg) {
-    if (sg == kSegHead) continue;
-    c->seg_off[sg] = off;
-    off = align_up(off + c->seg_bytes[sg], 4096);
+    c->seg_bytes[sg] = ul.seg_bytes[sg];
+    c->seg_off[sg] = ul.seg_off[sg];
   }
-  c->layer_bytes = off;
-  c->head_bytes = V * d * 2;
-  c->slot_bytes = 0;
-  if (pol.weights_on_host) c->slot_bytes = c->layer_bytes;
-  if (pol.embed_on_host) c->slot_bytes = std::max(c->slot_bytes, align_up(c->head_bytes, 4096));
+  c->misc_bytes = ul.misc_bytes;
+  c->layer_bytes = ul.layer_bytes;
+  c->head_bytes = ul.head_bytes;
+  c->slot_bytes = hp.slot_bytes;
 
   // host sources: small tensors packed per layer; matrices in place when
   // they sit in pipo_host_alloc memory, else copied into a merged pinned
@@ -918,12 +847,12 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   // HBM
   const int64_t rows = (int64_t)pol.max_batch * pol.max_seq;
   void* p = nullptr;
-  if (c->slot_bytes > 0) {
-    PIPO_TRY(dev_alloc(c, &p, c->slot_bytes * pol.n_weight_slots));
+  if (hp.slots > 0) {
+    PIPO_TRY(dev_alloc(c, &p, hp.slots));
     c->slots = (char*)p;
   }
   if (!pol.weights_on_host) {
-    PIPO_TRY(dev_alloc(c, &p, c->layer_bytes * L));
+    PIPO_TRY(dev_alloc(c, &p, hp.resident));
     c->resident = (char*)p;
     for (int64_t j = 0; j < L; ++j)
       for (int sg = 0; sg < kNumSegs; ++sg)
@@ -933,67 +862,56 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
                                  hipMemcpyHostToDevice));
   }
   if (!pol.embed_on_host) {
-    PIPO_TRY(dev_alloc(c, &p, c->head_bytes));
+    PIPO_TRY(dev_alloc(c, &p, hp.tok));
     c->tok_dev = (uint16_t*)p;
     PIPO_HIP_TRY(hipMemcpy(c->tok_dev, w->tok_emb, (size_t)c->head_bytes, hipMemcpyHostToDevice));
   }
-  const int64_t pos_bytes = ((int64_t)shape->max_pos + shape->pos_offset) * d * 2;
-  PIPO_TRY(dev_alloc(c, &p, pos_bytes));
+  PIPO_TRY(dev_alloc(c, &p, hp.pos));
   c->pos_dev = (uint16_t*)p;
-  PIPO_HIP_TRY(hipMemcpy(c->pos_dev, w->pos_emb, (size_t)pos_bytes, hipMemcpyHostToDevice));
-  PIPO_TRY(dev_alloc(c, &p, d * 4));
+  PIPO_HIP_TRY(hipMemcpy(c->pos_dev, w->pos_emb, (size_t)hp.pos, hipMemcpyHostToDevice));
+  PIPO_TRY(dev_alloc(c, &p, hp.lnf));
   c->lnf_g = (uint16_t*)p;
   c->lnf_b = c->lnf_g + d;
   PIPO_HIP_TRY(hipMemcpy(c->lnf_g, w->lnf_g, (size_t)d * 2, hipMemcpyHostToDevice));
   PIPO_HIP_TRY(hipMemcpy(c->lnf_b, w->lnf_b, (size_t)d * 2, hipMemcpyHostToDevice));
-  PIPO_TRY(dev_alloc(c, &p, rows * d * 4));
+  PIPO_TRY(dev_alloc(c, &p, hp.x));
   c->x = (float*)p;
-  PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+  PIPO_TRY(dev_alloc(c, &p, hp.a));
   c->a = (uint16_t*)p;
-  PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+  PIPO_TRY(dev_alloc(c, &p, hp.q));
   c->q = (uint16_t*)p;
-  PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+  PIPO_TRY(dev_alloc(c, &p, hp.o));
   c->o = (uint16_t*)p;
-  PIPO_TRY(dev_alloc(c, &p, rows * F * 2));
+  PIPO_TRY(dev_alloc(c, &p, hp.h));
   c->h = (uint16_t*)p;
-  PIPO_TRY(dev_alloc(c, &p, (int64_t)pol.max_batch * V * 4));
+  PIPO_TRY(dev_alloc(c, &p, hp.logits));
   c->logits = (float*)p;
-  PIPO_TRY(dev_alloc(c, &p, (int64_t)pol.max_batch * 4));
+  PIPO_TRY(dev_alloc(c, &p, hp.next));
   c->next_dev = (int32_t*)p;
-  PIPO_TRY(dev_alloc(c, &p, rows * 4));
+  PIPO_TRY(dev_alloc(c, &p, hp.ids));
   c->ids_dev = (int32_t*)p;
-  if (pol.embed_on_host) {
-    PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+  if (hp.emb > 0) {
+    PIPO_TRY(dev_alloc(c, &p, hp.emb));
     c->emb_dev = (uint16_t*)p;
   }
-  c->attn_ws_bytes = attn_decode_workspace_bytes(pol.max_batch, (int)c->H, (int)c->dh,
-                                                 kAttnDecodeMaxSplits);
+  c->attn_ws_bytes = hp.attn_ws;
   PIPO_TRY(dev_alloc(c, &p, c->attn_ws_bytes));
   c->attn_ws = (float*)p;
-  {
-    // GEMM rows: b (decode) or b * P (prefill), at most max_batch * max_seq
-    const int64_t m_max = rows;
-    const int64_t shapes[5][3] = {{3 * d, d, c->w4}, {d, d, c->w4}, {F, d, c->w4},
-                                  {d, F, c->w4}, {V, d, 0}};
-    for (const auto& sh : shapes) {
-      const int64_t b = gemm_workspace_bytes_upto(m_max, sh[0], sh[1], sh[2] != 0);
-      c->gemm_ws_bytes = b > c->gemm_ws_bytes ? b : c->gemm_ws_bytes;
-    }
-    if (c->gemm_ws_bytes > 0) {
-      PIPO_TRY(dev_alloc(c, &p, c->gemm_ws_bytes));
-      c->gemm_ws = (float*)p;
-    }
+  // GEMM rows: b (decode) or b * P (prefill), at most max_batch * max_seq
+  c->gemm_ws_bytes = hp.gemm_ws;
+  if (c->gemm_ws_bytes > 0) {
+    PIPO_TRY(dev_alloc(c, &p, c->gemm_ws_bytes));
+    c->gemm_ws = (float*)p;
   }
-  c->kv_row = c->kv4 ? d / 2 + d / 16 : 2 * d;
-  c->kv_part_bytes = rows * c->kv_row;
-  if (c->kv4) {
-    PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+  c->kv_row = hp.kv_row;
+  c->kv_part_bytes = hp.kv_part;
+  if (hp.kstage > 0) {
+    PIPO_TRY(dev_alloc(c, &p, hp.kstage));
     c->kst = (uint16_t*)p;
-    PIPO_TRY(dev_alloc(c, &p, rows * d * 2));
+    PIPO_TRY(dev_alloc(c, &p, hp.kstage));
     c->vst = (uint16_t*)p;
   }
-  const int64_t kv_units = pol.kv_on_host ? pol.n_weight_slots : L;
-  PIPO_TRY(dev_alloc(c, &p, kv_units * 2 * c->kv_part_bytes));
+  PIPO_TRY(dev_alloc(c, &p, hp.kv));
   c->kv = (char*)p;
 
   // pinned staging

@@ -1,0 +1,45 @@
+// What pipo_create allocates, computed without allocating anything.  The
+// context, pipo_plan_policy and pipo_configure all size memory through
+// these functions, so a planned footprint is the real one.
+#pragma once
+
+#include "common.h"
+#include "schedule.h"
+
+namespace pipo {
+
+inline int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+pipo_status check_shape(const pipo_shape* s);
+
+// defaults (0 fields) and range checks of a policy, in place
+pipo_status normalize_policy(const pipo_shape* shape, pipo_policy* pol);
+
+// one layer unit as it sits in a weight slot: segments at 4 KiB offsets
+struct UnitLayout {
+  int64_t seg_bytes[kNumSegs] = {};
+  int64_t seg_off[kNumSegs] = {};
+  int64_t misc_bytes = 0;    // small tensors of a layer, packed
+  int64_t layer_bytes = 0;   // slot bytes of a layer unit
+  int64_t copy_bytes = 0;    // bytes a layer unit's copies move (sum of segments)
+  int64_t head_bytes = 0;    // the token table / output head
+};
+UnitLayout unit_layout(const pipo_shape& sh, bool w4);
+
+// every device allocation of a context (bytes; 0 where not allocated)
+struct HbmPlan {
+  int64_t slot_bytes = 0, slots = 0, resident = 0, tok = 0, pos = 0, lnf = 0;
+  int64_t x = 0, a = 0, q = 0, o = 0, h = 0, logits = 0, next = 0, ids = 0, emb = 0;
+  int64_t attn_ws = 0, gemm_ws = 0, kstage = 0;  // kstage: each of the K and V staging buffers
+  int64_t kv_row = 0, kv_part = 0, kv = 0;
+  int64_t total() const {
+    return slots + resident + tok + pos + lnf + x + a + q + o + h + logits + next + ids + emb +
+           attn_ws + gemm_ws + 2 * kstage + kv;
+  }
+};
+HbmPlan hbm_plan(const pipo_shape& sh, const pipo_policy& pol);  // pol normalized
+
+// host memory the library allocates for the KV cache (per layer, 4 KiB aligned)
+int64_t host_kv_bytes(const pipo_shape& sh, const pipo_policy& pol);
+
+}  // namespace pipo

@@ -10,7 +10,7 @@ extern "C" int64_t pipo_sched_trace(const pipo_sched_config* c, int32_t n_passes
                                     const int32_t* prefill, const int64_t* pos0, const int64_t* T,
                                     int64_t kv_row_bytes, char* buf, int64_t buflen) {
   if (!c || !prefill || !pos0 || !T || !buf || buflen <= 0 || n_passes < 0) return -1;
-  if (c->n_layers < 1 || c->n_slots < 2 || c->n_h2d < 1 || c->n_h2d > 2 || c->chunk_bytes <= 0)
+  if (c->n_layers < 1 || c->n_slots < 1 || c->n_h2d < 1 || c->n_h2d > 2 || c->chunk_bytes <= 0)
     return -1;
   if (c->kv_on_host && !c->layers_streamed) return -1;
   pipo::SchedConfig sc;

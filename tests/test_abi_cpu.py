@@ -81,7 +81,7 @@ def test_bad_shapes_rejected(kw, status):
 @pytest.mark.parametrize("pol,status", [
     (dict(max_batch=0), "PIPO_ERR_ARG"),
     (dict(max_seq=65), "PIPO_ERR_UNSUPPORTED"),        # beyond max_pos
-    (dict(n_weight_slots=1), "PIPO_ERR_ARG"),
+    (dict(n_weight_slots=17), "PIPO_ERR_ARG"),
     (dict(n_h2d_streams=3), "PIPO_ERR_ARG"),
     (dict(kv_on_host=True, weights_on_host=False), "PIPO_ERR_UNSUPPORTED"),
 ])

@@ -210,7 +210,7 @@ def check(ops_by_pass, flat, cfg, pass_info, kv_row):
 
 VARIANTS = list(itertools.product(
     [1, 3],            # layers
-    [2, 3, 4],         # slots
+    [1, 2, 3, 4],      # slots (1: the memory-efficient pipeline)
     [1, 2],            # h2d streams
     [(1, 1, 0), (1, 0, 0), (0, 1, 0), (1, 1, 1), (1, 0, 1)],  # layers/head streamed, kv on host
     [False, True],     # int4 segments
@@ -250,6 +250,8 @@ def test_lookahead_keeps_link_busy_across_steps():
 
 
 def test_invalid_config_rejected():
-    cfg = make_config(2, 1, 1, 1, 1, 0, False, 4096)
-    with pytest.raises(ValueError):
-        B.pipo_sched_trace(cfg, [(True, 0, 2)])
+    for bad in (make_config(2, 0, 1, 1, 1, 0, False, 4096),
+                make_config(2, 2, 3, 1, 1, 0, False, 4096),
+                make_config(0, 2, 1, 1, 1, 0, False, 4096)):
+        with pytest.raises(ValueError):
+            B.pipo_sched_trace(bad, [(True, 0, 2)])
