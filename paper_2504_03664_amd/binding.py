@@ -26,6 +26,7 @@ STATUS_NAMES = {0: "PIPO_OK", -1: "PIPO_ERR_ARG", -2: "PIPO_ERR_OOM_DEVICE",
                 -6: "PIPO_ERR_UNSUPPORTED"}
 PIPO_W_FP16, PIPO_W_INT4_G64 = 0, 1
 PIPO_KV_FP16, PIPO_KV_INT4_G64 = 0, 1
+PIPO_PIPE_PERFORMANCE, PIPO_PIPE_MEMORY_EFFICIENT = 0, 1
 PIPO_DBG_POISON_SLOTS, PIPO_DBG_COPY_DELAY, PIPO_DBG_TIMESTAMPS = 1, 2, 4
 PIPO_DBG_KV_PAGEABLE = 8
 PIPO_EPI_F16, PIPO_EPI_RELU_F16, PIPO_EPI_ADD_F32, PIPO_EPI_F32 = 0, 1, 2, 3
@@ -58,6 +59,15 @@ class PipoPolicy(ctypes.Structure):
                 ("chunk_bytes", i64), ("max_batch", i32), ("max_seq", i32),
                 ("hbm_budget_bytes", i64), ("debug_flags", i32), ("copy_delay_us", i32),
                 ("pinned_budget_bytes", i64), ("copy_threads", i32), ("kv_fmt", i32)]
+
+
+class PipoPlan(ctypes.Structure):
+    _fields_ = [("weight_bytes", i64), ("kv_bytes", i64), ("hbm_bytes", i64),
+                ("host_kv_bytes", i64), ("h2d_bytes_per_step", i64), ("pipeline", i32)]
+
+
+class PipoResources(ctypes.Structure):
+    _fields_ = [("hbm_bytes", i64), ("host_bytes", i64)]
 
 
 class PipoKernelStat(ctypes.Structure):
@@ -101,6 +111,11 @@ _SIGNATURES = {
     "pipo_reset_stats": ([vp], i32),
     "pipo_destroy": ([vp], None),
     "pipo_set_timestamps": ([vp, i32], i32),
+    "pipo_plan_policy": ([ctypes.POINTER(PipoShape), ctypes.POINTER(PipoPolicy),
+                          ctypes.POINTER(PipoPlan)], i32),
+    "pipo_configure": ([ctypes.POINTER(PipoShape), i32, i32, i32, i32,
+                        ctypes.POINTER(PipoResources), ctypes.POINTER(PipoPolicy),
+                        ctypes.POINTER(PipoPlan)], i32),
     "pipo_measure_h2d_peak": ([i64, i32, i32, ctypes.POINTER(f64)], i32),
     "pipo_measure_h2d_chunked": ([i64, i64, i32, i32, ctypes.POINTER(f64)], i32),
     "pipo_host_alloc": ([sz], vp),
@@ -218,6 +233,28 @@ def pipo_get_stats(ctx: int) -> dict:
 
 def pipo_reset_stats(ctx: int) -> None:
     _check(lib().pipo_reset_stats(ctx), "pipo_reset_stats")
+
+
+def _plan_dict(p: PipoPlan) -> dict:
+    return {name: getattr(p, name) for name, _ in PipoPlan._fields_}
+
+
+def pipo_plan_policy(shape: PipoShape, policy: PipoPolicy) -> dict:
+    plan = PipoPlan()
+    _check(lib().pipo_plan_policy(ctypes.byref(shape), ctypes.byref(policy), ctypes.byref(plan)),
+           "pipo_plan_policy")
+    return _plan_dict(plan)
+
+
+def pipo_configure(shape: PipoShape, wfmt: int, kv_fmt: int, max_batch: int, max_seq: int,
+                   hbm_bytes: int = 0, host_bytes: int = 0):
+    """Returns (PipoPolicy, plan dict)."""
+    res = PipoResources(hbm_bytes, host_bytes)
+    pol, plan = PipoPolicy(), PipoPlan()
+    _check(lib().pipo_configure(ctypes.byref(shape), wfmt, kv_fmt, max_batch, max_seq,
+                                ctypes.byref(res), ctypes.byref(pol), ctypes.byref(plan)),
+           "pipo_configure")
+    return pol, _plan_dict(plan)
 
 
 def pipo_set_timestamps(ctx: int, on: bool) -> None:

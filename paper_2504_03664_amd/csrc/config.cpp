@@ -239,8 +239,9 @@ pipo_status pipo_configure(const pipo_shape* shape, int32_t wfmt, int32_t kv_fmt
           const int64_t h = hbm_plan(*shape, pol).total();
           const int64_t k = host_kv_bytes(*shape, pol);
           if (need_hbm < 0 || h < need_hbm) need_hbm = h;
-          if (k <= host && (need_host < 0 || k < need_host)) need_host = k;
-          if (h > hbm || k > host) continue;
+          if (h > hbm) continue;
+          if (need_host < 0 || k < need_host) need_host = k;  // among those that fit in HBM
+          if (k > host) continue;
           const int64_t bytes = step_bytes(*shape, pol);
           if (best_bytes < 0 || bytes < best_bytes || (bytes == best_bytes && slots > best_slots)) {
             best = pol;
@@ -251,13 +252,14 @@ pipo_status pipo_configure(const pipo_shape* shape, int32_t wfmt, int32_t kv_fmt
   if (best_bytes < 0) {
     if (first_err != PIPO_OK && need_hbm < 0) return first_err;
     if (need_host < 0) {
-      set_error("the KV cache does not fit in %lld bytes of host memory (a disk tier would be "
-                "needed, which this library does not have)", (long long)host);
-      return PIPO_ERR_OOM_HOST;
+      set_error("even the memory-efficient pipeline needs %lld bytes of HBM (%lld available)",
+                (long long)need_hbm, (long long)hbm);
+      return PIPO_ERR_OOM_DEVICE;
     }
-    set_error("even the memory-efficient pipeline needs %lld bytes of HBM (%lld available)",
-              (long long)need_hbm, (long long)hbm);
-    return PIPO_ERR_OOM_DEVICE;
+    set_error("the KV cache needs %lld bytes of host memory (%lld available); a disk tier "
+              "would be needed, which this library does not have",
+              (long long)need_host, (long long)host);
+    return PIPO_ERR_OOM_HOST;
   }
   best.hbm_budget_bytes = hbm;
   *policy_out = best;

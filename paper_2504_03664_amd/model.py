@@ -154,11 +154,14 @@ def c_policy(wfmt: str = "fp16", weights_on_host: bool = True, embed_on_host: bo
 class Decoder:
     """One pipo context over HostWeights."""
 
-    def __init__(self, weights: HostWeights, **policy):
-        policy.setdefault("wfmt", weights.wfmt)
+    def __init__(self, weights: HostWeights, policy: Optional[B.PipoPolicy] = None, **kw):
+        """`policy` (e.g. from pipo_configure) or keyword fields for c_policy."""
         self.weights = weights
         self.vocab = weights.shape.vocab
-        self.policy = c_policy(**policy)
+        if policy is None:
+            kw.setdefault("wfmt", weights.wfmt)
+            policy = c_policy(**kw)
+        self.policy = policy
         self.ctx = B.pipo_create(c_shape(weights.shape), weights.c_weights, self.policy)
 
     def prefill(self, tokens: np.ndarray, want_logits: bool = False

@@ -6,7 +6,7 @@ import pytest
 import synth
 from oracle import OracleDecoder
 from paper_2504_03664_amd import binding as B
-from paper_2504_03664_amd.model import Decoder, HostWeights
+from paper_2504_03664_amd.model import Decoder, HostWeights, c_policy, c_shape
 
 pytestmark = pytest.mark.gpu
 
@@ -94,6 +94,7 @@ def test_streamed_bit_identical_to_resident(opt125m):
     variants = [
         dict(),
         dict(n_h2d_streams=1),
+        dict(n_weight_slots=1),
         dict(n_weight_slots=2, chunk_bytes=4096 * 37),
         dict(n_h2d_streams=2, chunk_bytes=1 << 20, n_weight_slots=4),
         dict(debug_flags=B.PIPO_DBG_POISON_SLOTS | B.PIPO_DBG_COPY_DELAY, copy_delay_us=200,
@@ -183,7 +184,9 @@ def test_small_model_parity_and_kv_on_host(wfmt):
                   dict(kv_on_host=True, debug_flags=B.PIPO_DBG_KV_PAGEABLE | B.PIPO_DBG_COPY_DELAY,
                        copy_delay_us=100, n_h2d_streams=2, chunk_bytes=3 * 4096, copy_threads=3),
                   # the first two layers pinned, the rest pageable
-                  dict(kv_on_host=True, pinned_budget_bytes=2 * (2 * 3 * 76 * 512 * 2) + 100)):
+                  dict(kv_on_host=True, pinned_budget_bytes=2 * (2 * 3 * 76 * 512 * 2) + 100),
+                  # the memory-efficient pipeline: one weight slot, one KV buffer
+                  dict(kv_on_host=True, n_weight_slots=1, chunk_bytes=1 << 18)):
             log(f"  kv on host {v}")
             tk, lk = _run(hw, prompt, 6, **v)
             assert np.array_equal(tk, t0)
@@ -305,5 +308,38 @@ def test_int4_kv_cache_head_dim_64_and_bad_width():
         with pytest.raises(B.PipoError) as e:
             Decoder(hw, max_batch=1, max_seq=8, kv_fmt="int4")
         assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_UNSUPPORTED"
+    finally:
+        hw.free()
+
+
+def test_planned_memory_is_allocated_memory_and_configured_runs():
+    """pipo_plan_policy predicts pipo_create's device allocations exactly;
+    a configuration chosen by pipo_configure under a tight HBM budget (the
+    memory-efficient pipeline) runs and matches the resident run bit for
+    bit."""
+    log("memory plan vs allocation; configured run")
+    model = synth.SyntheticOPT(SMALL, seed=17)
+    hw = HostWeights(SMALL, "fp16", model)
+    try:
+        shape = c_shape(SMALL)
+        for pol in (dict(), dict(n_weight_slots=1, kv_on_host=True),
+                    dict(weights_on_host=False, embed_on_host=False),
+                    dict(embed_on_host=False, kv_fmt="int4", n_weight_slots=2),
+                    dict(kv_on_host=True, kv_fmt="int4", max_batch=5, max_seq=33)):
+            pol = dict(dict(max_batch=3, max_seq=76), **pol)
+            want = B.pipo_plan_policy(shape, c_policy(**pol))["hbm_bytes"]
+            with Decoder(hw, **pol) as dec:
+                assert dec.stats()["hbm_bytes"] == want, pol
+        prompt = synth.prompt_tokens(3, 70, SMALL.vocab, seed=6)
+        t0, l0 = _run(hw, prompt, 6, weights_on_host=False, embed_on_host=False)
+        me = B.pipo_plan_policy(shape, c_policy(max_batch=3, max_seq=76, kv_on_host=True,
+                                                n_weight_slots=1))["hbm_bytes"]
+        pol, plan = B.pipo_configure(shape, B.PIPO_W_FP16, B.PIPO_KV_FP16, 3, 76, me, 1 << 34)
+        assert plan["pipeline"] == B.PIPO_PIPE_MEMORY_EFFICIENT and pol.n_weight_slots == 1
+        with Decoder(hw, policy=pol) as dec:
+            t1, l1 = dec.generate(prompt, 6, want_logits=True)
+            assert dec.stats()["hbm_bytes"] == plan["hbm_bytes"] <= me
+        assert np.array_equal(t1, t0)
+        assert np.array_equal(np.stack(l1).view(np.uint32), l0.view(np.uint32))
     finally:
         hw.free()
