@@ -309,7 +309,8 @@ def main():
             symbols = gemm_symbols(wl.batch, *nk[fam_key], epi[fam_key],
                                    wl.wfmt == "int4" and fam_key != "head")
         elif fam_key == "attention":
-            symbols = [f"attn_decode_k<{shape.d_model // shape.n_heads}>"]
+            kv4 = "true" if wl.kv_fmt == "int4" else "false"
+            symbols = [f"attn_decode_k<{shape.d_model // shape.n_heads}, {kv4}>"]
         symbol = " + ".join(symbols) if symbols else None
         traffic, tsrc = measured_traffic(wl.name, symbols) if symbols else (None, None)
         out["roofline"] = {"kernel": name, "symbol": symbol, "bound": "hbm",

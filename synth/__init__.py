@@ -85,7 +85,7 @@ def philox4x64_10(ctr, key) -> np.ndarray:
 # ----------------------------------------------------------------------------
 # tensor naming
 _TENSOR_CODES = {
-    "tok_emb": 1, "pos_emb": 2, "lnf_g": 3, "lnf_b": 4,
+    "tok_emb": 1, "pos_emb": 2, "lnf_g": 3, "lnf_b": 4, "lm_head": 5,
     "ln1_g": 10, "ln1_b": 11, "wqkv": 12, "bqkv": 13, "wo": 14, "bo": 15,
     "ln2_g": 16, "ln2_b": 17, "w1": 18, "b1": 19, "w2": 20, "b2": 21,
 }
@@ -159,6 +159,8 @@ class OPTShape:
         return dataclasses.replace(self, n_layers=n)
 
 
+OPTShape.family = "opt"
+
 OPT_125M = OPTShape(12, 768, 12, 3072)
 OPT_6_7B = OPTShape(32, 4096, 32, 16384)
 OPT_13B = OPTShape(40, 5120, 40, 20480)
@@ -166,9 +168,41 @@ OPT_30B = OPTShape(48, 7168, 56, 28672)
 
 
 @dataclasses.dataclass(frozen=True)
+class LlamaShape:
+    """LLaMA-3.1-style decoder: RMSNorm, grouped-query attention with rotary
+    positions (with the 3.1 frequency scaling), SwiGLU MLP, untied head."""
+    n_layers: int
+    d_model: int
+    n_heads: int
+    n_kv_heads: int
+    d_ffn: int
+    vocab: int = 128256
+    max_pos: int = 8192
+    rope_theta: float = 500000.0
+    rope_factor: float = 8.0        # 0: no frequency scaling
+    rope_low_freq_factor: float = 1.0
+    rope_high_freq_factor: float = 4.0
+    rope_orig_max_pos: int = 8192
+    ln_eps: float = 1e-5
+    family = "llama"
+    pos_offset = 0
+
+    @property
+    def head_dim(self) -> int:
+        return self.d_model // self.n_heads
+
+    def with_layers(self, n: int) -> "LlamaShape":
+        return dataclasses.replace(self, n_layers=n)
+
+
+LLAMA31_8B = LlamaShape(32, 4096, 32, 8, 14336)
+LLAMA31_70B = LlamaShape(80, 8192, 64, 8, 28672)
+
+
+@dataclasses.dataclass(frozen=True)
 class Workload:
     name: str
-    shape: OPTShape
+    shape: object         # OPTShape or LlamaShape
     batch: int
     prompt: int
     gen: int
@@ -186,6 +220,9 @@ WORKLOADS = (
     # the previous workload with the KV cache in INT4 as well
     Workload("opt-30b b128 p512 g32 int4-g64 kv-host kv-int4", OPT_30B, 128, 512, 32, "int4", True,
              "int4"),
+    # the paper's other dense family (Section 4.1): LLaMA3.1-8B shape
+    Workload("llama3.1-8b b16 p512 g32 fp16", LLAMA31_8B, 16, 512, 32, "fp16", False),
+    Workload("llama3.1-8b b32 p512 g32 int4-g64", LLAMA31_8B, 32, 512, 32, "int4", False),
 )
 
 
@@ -263,3 +300,37 @@ class SyntheticOPT:
             else:
                 out[name] = self.tensor(j, name)
         return out
+
+
+class SyntheticLlama(SyntheticOPT):
+    """Random-init LLaMA-3.1-shaped weights (same streams and encodings as
+    SyntheticOPT): RMSNorm weights 1, no biases, q/k/v stacked in ``wqkv``
+    ([(h + 2 h_kv) head_dim][d]), gate and up stacked in ``w1`` ([2 d_ffn][d],
+    gate rows first), untied ``lm_head``; no position table."""
+
+    def __init__(self, shape: "LlamaShape", seed: int = DEFAULT_SEED, wfmt: str = "fp16",
+                 std: float = WEIGHT_STD):
+        super().__init__(shape, seed=seed, wfmt=wfmt, zero_bias=True, std=std)
+
+    def layer_shapes(self) -> Dict[str, tuple]:
+        s = self.shape
+        d, F, dh = s.d_model, s.d_ffn, s.head_dim
+        return {"ln1_g": (d,), "wqkv": ((s.n_heads + 2 * s.n_kv_heads) * dh, d), "wo": (d, d),
+                "ln2_g": (d,), "w1": (2 * F, d), "w2": (d, F)}
+
+    def tensor(self, layer: int, name: str) -> np.ndarray:
+        if layer < 0 and name in ("tok_emb", "lm_head"):
+            shp = (self.shape.vocab, self.shape.d_model)
+            return self.fill(layer, name, np.empty(shp, dtype=np.float16))
+        if layer < 0 and name == "lnf_g":
+            return self.fill(layer, name, np.empty(self.shape.d_model, dtype=np.float16))
+        return super().tensor(layer, name)
+
+    def lm_head(self) -> np.ndarray:
+        return self.tensor(-1, "lm_head")
+
+    def pos_emb(self):
+        return None
+
+    def lnf(self):
+        return self.tensor(-1, "lnf_g"), None
