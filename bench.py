@@ -1,5 +1,5 @@
 #!/usr/bin/env python3
-"""Decode throughput of the pipelined-offloading OPT decoder on one MI355X.
+"""Decode throughput of the pipelined-offloading decoder on one MI355X.
 
 One step = one decode step of the whole batch: every layer's weights and the
 output head stream from pinned host memory into rotating HBM slots while the
@@ -9,9 +9,11 @@ progress goes to stderr.
 
     python bench.py [--steps K] [--warmup W] [--workload I]
 
-Default workload: OPT-6.7B shape (32 layers, d 4096, 32 heads, FFN 16384),
-fp16 weights, batch 16, prompt 512, 32 generated tokens (1 from the prefill
-plus warmup + steps decode steps), KV cache in HBM.
+Default workload: OPT-30B shape (48 layers, d 7168, 56 heads, FFN 28672),
+fp16 weights, batch 64, prompt 512, 32 generated tokens (1 from the prefill
+plus warmup + steps decode steps), KV cache in HBM.  --workload picks
+another entry of synth.WORKLOADS (OPT shapes, INT4 weights and caches, the
+KV cache in host memory, LLaMA-3.1-8B shapes).
 """
 from __future__ import annotations
 
@@ -119,20 +121,23 @@ def cpu_baseline(wl, seed, sample_layers=2, steps=3):
     (KV prefix filled with synthetic values), plus the output head, scaled
     to all layers."""
     import synth
-    from oracle import OracleDecoder
+    from oracle import decoder_for
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         blas_threads = None
     shape = wl.shape.with_layers(sample_layers)
-    gen = synth.SyntheticOPT(shape, seed=seed, wfmt=wl.wfmt)
+    gen = synth.synthetic_model(shape, seed=seed, wfmt=wl.wfmt)
+    llama = getattr(shape, "family", "opt") == "llama"
 
     class Held:  # the sample's weights, drawn once (drawing is not the oracle's work)
         def __init__(self):
             self.shape, self.wfmt = gen.shape, gen.wfmt
             self._layers = [gen.layer(j) for j in range(sample_layers)]
-            self._tok, self._pos, self._lnf = gen.tok_emb(), gen.pos_emb(), gen.lnf()
+            self._tok, self._lnf = gen.tok_emb(), gen.lnf()
+            self._pos = None if llama else gen.pos_emb()
+            self._head = gen.lm_head() if llama else None
 
         def layer(self, j):
             return self._layers[j]
@@ -143,16 +148,20 @@ def cpu_baseline(wl, seed, sample_layers=2, steps=3):
         def pos_emb(self):
             return self._pos
 
+        def lm_head(self):
+            return self._head
+
         def lnf(self):
             return self._lnf
 
     held = Held()
-    dec = OracleDecoder(held, np.float32, kv_int4=wl.kv_fmt == "int4")
+    dec = decoder_for(held, np.float32, kv_int4=wl.kv_fmt == "int4")
     b, ctx = wl.batch, wl.prompt + 1
     rng = np.random.default_rng(0)
     d = shape.d_model
-    cache = [[(rng.standard_normal((ctx, d), dtype=np.float32),
-               rng.standard_normal((ctx, d), dtype=np.float32)) for _ in range(b)]
+    dkv = shape.n_kv_heads * shape.head_dim if llama else d   # width of a cached row
+    cache = [[(rng.standard_normal((ctx, dkv), dtype=np.float32),
+               rng.standard_normal((ctx, dkv), dtype=np.float32)) for _ in range(b)]
              for _ in range(sample_layers)]
     toks = synth.prompt_tokens(b, 1, shape.vocab, seed=9)[:, 0]
     fresh = lambda: [[(k, v) for k, v in layer] for layer in cache]  # noqa: E731
@@ -201,7 +210,7 @@ def main():
     log(f"workload {wl.name}: {shape.n_layers} layers, d {shape.d_model}, batch {wl.batch}")
 
     t0 = time.time()
-    hw = HostWeights(shape, wl.wfmt, synth.SyntheticOPT(shape, seed=seed, wfmt=wl.wfmt))
+    hw = HostWeights(shape, wl.wfmt, synth.synthetic_model(shape, seed=seed, wfmt=wl.wfmt))
     log(f"weights drawn into pinned host memory in {time.time() - t0:.1f} s")
 
     peak1 = B.pipo_measure_h2d_peak(1 << 30, 10, 1)
@@ -286,9 +295,14 @@ def main():
         # dominant decode kernel, grouped by kernel symbol: the GEMM epilogue is
         # a template parameter, so the out-projection and FC2 share one symbol
         gemm = gemm_family(wl.batch)
+        llama = getattr(shape, "family", "opt") == "llama"
+        # LLaMA: FC1 is the gate/up GEMM (fp16 out) followed by the SwiGLU kernel,
+        # QKV is followed by the rotary kernel
+        fc1_label = f"{gemm}<f16>+swiglu (fc1)" if llama else f"{gemm}<relu_f16> (fc1)"
+        qkv_label = f"{gemm}<qkv>+rope (qkv)" if llama else f"{gemm}<qkv> (qkv)"
         families = {f"{gemm}<add_f32> (oproj+fc2)": ("oproj_decode", "fc2_decode"),
-                    f"{gemm}<relu_f16> (fc1)": ("fc1_decode",),
-                    f"{gemm}<qkv> (qkv)": ("qkv_decode",),
+                    fc1_label: ("fc1_decode",),
+                    qkv_label: ("qkv_decode",),
                     f"{gemm}<f32> (head)": ("head_decode",),
                     "attn_decode_k+combine (attention)": ("attn_decode",)}
         fam = {}
@@ -300,17 +314,19 @@ def main():
         name, ks = max(fam.items(), key=lambda kv: kv[1]["total_ms"])
         avg_ms = ks["total_ms"] / ks["launches"]
         ach = ks["alg_bytes"] / (ks["total_ms"] * 1e-3) / 1e9
-        epi = {"oproj": 2, "fc1": 1, "qkv": 4, "head": 3}
+        epi = {"oproj": 2, "fc1": 0 if llama else 1, "qkv": 4, "head": 3}
         fam_key = name.split("(")[1].split("+")[0].rstrip(")")
         symbols = None
+        d, F, dh = shape.d_model, shape.d_ffn, shape.d_model // shape.n_heads
+        hkv = shape.n_kv_heads if llama else shape.n_heads
         if fam_key in epi:
-            d, F = shape.d_model, shape.d_ffn
-            nk = {"oproj": (d, d), "fc1": (F, d), "qkv": (3 * d, d), "head": (shape.vocab, d)}
+            nk = {"oproj": (d, d), "fc1": (2 * F if llama else F, d),
+                  "qkv": (d + 2 * hkv * dh, d), "head": (shape.vocab, d)}
             symbols = gemm_symbols(wl.batch, *nk[fam_key], epi[fam_key],
                                    wl.wfmt == "int4" and fam_key != "head")
         elif fam_key == "attention":
             kv4 = "true" if wl.kv_fmt == "int4" else "false"
-            symbols = [f"attn_decode_k<{shape.d_model // shape.n_heads}, {kv4}>"]
+            symbols = [f"attn_decode_k<{dh}, {shape.n_heads // hkv}, {kv4}>"]
         symbol = " + ".join(symbols) if symbols else None
         traffic, tsrc = measured_traffic(wl.name, symbols) if symbols else (None, None)
         out["roofline"] = {"kernel": name, "symbol": symbol, "bound": "hbm",

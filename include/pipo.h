@@ -18,6 +18,10 @@
  *   - loading runs ahead of computation so that two or more layers are
  *     resident (Section 3.2.3, performance-optimized pipeline);
  *   - INT4 weights are consumed directly by the GEMM (Section 3.4).
+ * A second model family, LLaMA 3.1 (the paper's other evaluated models,
+ * Section 4.1; memory model of Section 3.5), runs through the same
+ * pipeline: RMSNorm, grouped-query attention with rotary positions,
+ * a SwiGLU MLP, untied output head, no biases (see pipo_shape).
  * The lifecycle follows the paper's workflow (Algorithm 2): pipo_create
  * initialises the model data, the transfer machinery and the schedule;
  * pipo_prefill and pipo_decode_step run the generation loop.
@@ -73,13 +77,44 @@ enum {
   PIPO_DBG_KV_PAGEABLE = 8    /* keep the host KV cache in pageable memory (staged copies) */
 };
 
+/* Model families (pipo_shape.family).
+ *  PIPO_FAMILY_OPT: pre-LN blocks with LayerNorm (gain and bias), learned
+ *    positions added to the token embedding, multi-head attention, biases on
+ *    every projection, ReLU MLP (w1 [d_ffn][d], w2 [d][d_ffn]), final
+ *    LayerNorm, output head tied to the token table.
+ *  PIPO_FAMILY_LLAMA: pre-norm blocks with RMSNorm (y = x / sqrt(mean(x^2) +
+ *    eps) * g); q, k, v without biases; rotary positions on q and k, pairing
+ *    element i with i + head_dim/2 of every head at angle p * w_i, w_i =
+ *    rope_theta^(-2i/head_dim), with the LLaMA 3.1 frequency scaling when
+ *    rope_factor > 0 (a component whose wavelength 2 pi / w_i exceeds
+ *    rope_orig_max_pos / rope_low_freq_factor is divided by rope_factor, one
+ *    shorter than rope_orig_max_pos / rope_high_freq_factor is kept, in
+ *    between w' = (1 - s) w / rope_factor + s w with s = (rope_orig_max_pos
+ *    / wavelength - low) / (high - low)); keys are cached after rotation;
+ *    grouped-query attention (query head h reads key/value head h / (n_heads
+ *    / n_kv_heads)); SwiGLU MLP h = silu(x w_gate^T) * (x w_up^T) with gate
+ *    and up stacked in w1 [2 d_ffn][d] (gate rows first), then h w2^T;
+ *    final RMSNorm; untied output head (pipo_host_weights.lm_head).
+ * Both: q is scaled by head_dim^-1/2, causal softmax attention, greedy
+ * decoding. */
+enum { PIPO_FAMILY_OPT = 0, PIPO_FAMILY_LLAMA = 1 };
+
 /* Decoder shape.  Constraints: d_model = n_heads * head_dim with head_dim
- * 64 or 128; d_model and d_ffn multiples of 128; vocab >= 1. */
+ * 64 or 128; d_model and d_ffn multiples of 128; vocab >= 1; n_heads a
+ * multiple of n_kv_heads, 1, 2, 4 or 8 query heads per key/value head.
+ * The fields after ln_eps are zero for OPT. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, d_ffn, vocab;
-  int32_t max_pos;      /* positions the learned table covers (rows = max_pos + pos_offset) */
-  int32_t pos_offset;   /* row of position 0 in the position table (2 for OPT) */
-  float ln_eps;         /* LayerNorm epsilon (1e-5) */
+  int32_t max_pos;      /* OPT: positions the learned table covers (rows = max_pos +
+                           pos_offset); LLaMA: longest sequence the rotary table covers */
+  int32_t pos_offset;   /* OPT: row of position 0 in the position table (2); LLaMA: unused */
+  float ln_eps;         /* LayerNorm / RMSNorm epsilon (1e-5) */
+  int32_t family;       /* PIPO_FAMILY_OPT (0) or PIPO_FAMILY_LLAMA */
+  int32_t n_kv_heads;   /* key/value heads; 0 means n_heads (OPT: must be 0 or n_heads) */
+  float rope_theta;     /* LLaMA: rotary base (500000 for LLaMA 3.1) */
+  float rope_factor;    /* LLaMA: 3.1 frequency scaling factor (8), 0 for none */
+  float rope_low_freq_factor, rope_high_freq_factor;  /* LLaMA 3.1: 1 and 4 */
+  int32_t rope_orig_max_pos;  /* LLaMA 3.1: 8192 (used when rope_factor > 0) */
 } pipo_shape;
 
 /* One group-wise INT4 matrix W[N][K]: W[n][k] = code * scale + min, one
@@ -90,7 +125,10 @@ typedef struct {
   const uint16_t* scale_min;  /* [N][K/64][2] fp16: {scale, min} */
 } pipo_q4;
 
-/* Host tensors of one layer (caller-owned; read, never written). */
+/* Host tensors of one layer (caller-owned; read, never written).  With
+ * dkv = n_kv_heads * head_dim (= d without grouped-query attention) and
+ * F = d_ffn.  LLaMA uses only ln1_g, ln2_g and the matrices (the bias and
+ * LayerNorm-bias pointers are ignored). */
 typedef struct {
   const uint16_t *ln1_g, *ln1_b;   /* [d] */
   const uint16_t *bqkv;            /* [3d]: q, k, v biases */
@@ -98,18 +136,19 @@ typedef struct {
   const uint16_t *ln2_g, *ln2_b;   /* [d] */
   const uint16_t *b1;              /* [d_ffn] */
   const uint16_t *b2;              /* [d] */
-  const uint16_t *wqkv;            /* [3d][d] rows: q, k, v       (PIPO_W_FP16) */
-  const uint16_t *wo;              /* [d][d]                      (PIPO_W_FP16) */
-  const uint16_t *w1;              /* [d_ffn][d]                  (PIPO_W_FP16) */
-  const uint16_t *w2;              /* [d][d_ffn]                  (PIPO_W_FP16) */
-  pipo_q4 qqkv, qo, q1, q2;        /* same matrices               (PIPO_W_INT4_G64) */
+  const uint16_t *wqkv;            /* [d + 2 dkv][d] rows: q, k, v          (PIPO_W_FP16) */
+  const uint16_t *wo;              /* [d][d]                                (PIPO_W_FP16) */
+  const uint16_t *w1;              /* OPT [F][d]; LLaMA [2F][d] gate, up    (PIPO_W_FP16) */
+  const uint16_t *w2;              /* [d][F]                                (PIPO_W_FP16) */
+  pipo_q4 qqkv, qo, q1, q2;        /* same matrices                         (PIPO_W_INT4_G64) */
 } pipo_layer_host;
 
 typedef struct {
-  const uint16_t* tok_emb;   /* [vocab][d]; also the output head (tied) */
-  const uint16_t* pos_emb;   /* [max_pos + pos_offset][d] */
-  const uint16_t *lnf_g, *lnf_b;   /* final LayerNorm [d] */
+  const uint16_t* tok_emb;   /* [vocab][d]; OPT: also the output head (tied) */
+  const uint16_t* pos_emb;   /* OPT: [max_pos + pos_offset][d]; LLaMA: unused */
+  const uint16_t *lnf_g, *lnf_b;   /* final norm [d] (LLaMA: lnf_b unused) */
   const pipo_layer_host* layers;   /* [n_layers] */
+  const uint16_t* lm_head;   /* LLaMA: output head [vocab][d]; OPT: unused */
 } pipo_host_weights;
 
 /* Offload policy (the paper's (S_off, S_pipe) pair, Algorithm 2, made
@@ -118,7 +157,7 @@ typedef struct {
   int32_t wfmt;              /* PIPO_W_FP16 or PIPO_W_INT4_G64 */
   int32_t weights_on_host;   /* 1: stream every layer each pass; 0: all layers resident in HBM */
   int32_t embed_on_host;     /* 1: stream the output head each pass, gather embeddings on the
-                                host; 0: token table resident in HBM */
+                                host; 0: token table (and an untied head) resident in HBM */
   int32_t kv_on_host;        /* 1: KV cache in library-owned host memory (pinned where
                                 possible, see pinned_budget_bytes), each layer's prefix loaded
                                 before its attention and the new rows saved after it (a call
@@ -152,7 +191,8 @@ enum { PIPO_PIPE_PERFORMANCE = 0, PIPO_PIPE_MEMORY_EFFICIENT = 1 };
  * exact sum of the device allocations pipo_create makes for the policy
  * (activations are sized for max_batch x max_seq rows: the prefill peak). */
 typedef struct {
-  int64_t weight_bytes;        /* W: layer tensors, token and position tables, final LN */
+  int64_t weight_bytes;        /* W: layer tensors, token and position tables (or token table
+                                  and untied head), final norm */
   int64_t kv_bytes;            /* C: KV cache of max_batch x max_seq positions, all layers */
   int64_t hbm_bytes;           /* device memory pipo_create allocates */
   int64_t host_kv_bytes;       /* host memory the library allocates for the KV cache */

@@ -111,6 +111,64 @@ pipo_status pipo_op_attn_prefill(const uint16_t* q, const uint16_t* kc, const ui
                                  uint16_t* o, int32_t b, int32_t P, int32_t n_heads,
                                  int32_t head_dim, void* stream);
 
+/* --- LLaMA-family operations (PIPO_FAMILY_LLAMA in pipo.h) --- */
+
+/* Grouped-query decode attention: q [b][n_heads * head_dim], cache rows of
+ * n_kv_heads * head_dim (fp16, or PIPO_KV_INT4_G64 rows when kv_fmt says
+ * so, then n_kv_heads * head_dim % 256 == 0); query head h reads key/value
+ * head h / (n_heads / n_kv_heads), 1, 2, 4 or 8 query heads per key/value
+ * head.  One workgroup serves all query heads of a key/value head, so each
+ * cached row is read once.  Workspace as for pipo_op_attn_decode, sized by
+ * pipo_op_attn_decode_gqa_workspace_bytes. */
+pipo_status pipo_op_attn_decode_gqa(const uint16_t* q, const void* kc, const void* vc,
+                                    uint16_t* o, int32_t b, int32_t n_heads, int32_t n_kv_heads,
+                                    int32_t head_dim, int32_t t, int32_t kv_fmt, void* workspace,
+                                    int64_t workspace_bytes, void* stream);
+int64_t pipo_op_attn_decode_gqa_workspace_bytes(int32_t b, int32_t n_heads, int32_t n_kv_heads,
+                                                int32_t head_dim, int32_t t);
+
+/* Grouped-query causal prefill attention (layouts as pipo_op_attn_prefill,
+ * cache rows of n_kv_heads * head_dim). */
+pipo_status pipo_op_attn_prefill_gqa(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                                     uint16_t* o, int32_t b, int32_t P, int32_t n_heads,
+                                     int32_t n_kv_heads, int32_t head_dim, void* stream);
+
+/* RMSNorm: y[r][:] = x[src] / sqrt(mean(x[src]^2) + eps) * gamma with
+ * src = r*src_stride + src_offset; x fp32, y fp16, statistics in fp32. */
+pipo_status pipo_op_rmsnorm(const float* x, const uint16_t* gamma, uint16_t* y, int64_t rows,
+                            int64_t d, int64_t src_stride, int64_t src_offset, float eps,
+                            void* stream);
+
+/*
+ * Rotary positions, in place (pipo.h, PIPO_FAMILY_LLAMA).  Row m (m < M)
+ * is sequence m / rows_per_seq at position pos0 + m % rows_per_seq.
+ * q: [M][n_heads * head_dim] fp16, each head rotated and then multiplied by
+ * q_scale; k: rows (kpos0 + m % rows_per_seq) * batch + m / rows_per_seq of
+ * [.][n_kv_heads * head_dim] fp16 (a position-major cache, or with kpos0 = 0
+ * a staging buffer), rotated.  cos_sin: device fp32 [positions][head_dim/2]
+ * [2] = (cos, sin) of p * w_i (pipo_rope_table).  head_dim 64 or 128.
+ */
+pipo_status pipo_op_rope(uint16_t* q, uint16_t* k, const float* cos_sin, int64_t M,
+                         int64_t rows_per_seq, int64_t pos0, int64_t kpos0, int64_t batch,
+                         int32_t n_heads, int32_t n_kv_heads, int32_t head_dim, float q_scale,
+                         void* stream);
+
+/* The rotary table of a LLaMA shape on the host: out[p][i][2] = (cos, sin)
+ * of p * w_i (w_i as in pipo.h, with the 3.1 scaling when rope_factor >
+ * 0), computed in double and stored as fp32, for p < n_pos and i <
+ * head_dim / 2.  `out` holds n_pos * head_dim floats.  Errors: ARG. */
+pipo_status pipo_rope_table(const pipo_shape* shape, int32_t n_pos, float* out);
+
+/* SwiGLU: h[m][i] = silu(gu[m][i]) * gu[m][F + i], silu(g) = g / (1 +
+ * exp(-g)), in fp32; gu [M][2F], h [M][F] fp16, F % 8 == 0. */
+pipo_status pipo_op_swiglu(const uint16_t* gu, uint16_t* h, int64_t M, int64_t F, void* stream);
+
+/* Embedding: x[r][:] = tok_table[ids[r]] (+ pos_table[pos0 + r % rows_per_seq
+ * + pos_offset] when pos_table is not NULL), fp32 x [rows][d]. */
+pipo_status pipo_op_embed(const int32_t* ids, const uint16_t* tok_table, const uint16_t* pos_table,
+                          float* x, int64_t rows, int64_t d, int64_t rows_per_seq, int64_t pos0,
+                          int64_t pos_offset, void* stream);
+
 /* next[r] = index of the largest logits[r][:] (ties: lowest index). */
 pipo_status pipo_op_argmax(const float* logits, int32_t* next, int64_t rows, int64_t V,
                            void* stream);

@@ -29,4 +29,5 @@ from .llama import (  # noqa: F401
     llama_param_count,
     rms_norm,
     rope_frequencies,
+    swiglu,
 )

@@ -78,6 +78,11 @@ def apply_rope(x: np.ndarray, positions: np.ndarray, freqs: np.ndarray) -> np.nd
     return np.concatenate([a * c - b * s, b * c + a * s], axis=-1).reshape(T, width)
 
 
+def swiglu(gate: np.ndarray, up: np.ndarray) -> np.ndarray:
+    """silu(gate) * up with silu(g) = g / (1 + exp(-g))."""
+    return gate / (1 + np.exp(-gate)) * up
+
+
 def gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, n_heads: int,
                   n_kv_heads: int) -> np.ndarray:
     """T queries [T][h*dh] (already scaled) over S >= T keys and values
@@ -201,7 +206,7 @@ class LlamaDecoder:
         gu = a2 @ L["w1"].T
         F = s.d_ffn
         gate, up = gu[:, :F], gu[:, F:]
-        hdn = self.act(gate / (1 + np.exp(-gate)) * up)
+        hdn = self.act(swiglu(gate, up))
         x = x + hdn @ L["w2"].T
         return x, k, v
 

@@ -25,6 +25,7 @@ STATUS_NAMES = {0: "PIPO_OK", -1: "PIPO_ERR_ARG", -2: "PIPO_ERR_OOM_DEVICE",
                 -3: "PIPO_ERR_OOM_HOST", -4: "PIPO_ERR_HIP", -5: "PIPO_ERR_STATE",
                 -6: "PIPO_ERR_UNSUPPORTED"}
 PIPO_W_FP16, PIPO_W_INT4_G64 = 0, 1
+PIPO_FAMILY_OPT, PIPO_FAMILY_LLAMA = 0, 1
 PIPO_KV_FP16, PIPO_KV_INT4_G64 = 0, 1
 PIPO_PIPE_PERFORMANCE, PIPO_PIPE_MEMORY_EFFICIENT = 0, 1
 PIPO_DBG_POISON_SLOTS, PIPO_DBG_COPY_DELAY, PIPO_DBG_TIMESTAMPS = 1, 2, 4
@@ -35,7 +36,10 @@ PIPO_MAX_KERNEL_STATS = 16
 
 class PipoShape(ctypes.Structure):
     _fields_ = [("n_layers", i32), ("d_model", i32), ("n_heads", i32), ("d_ffn", i32),
-                ("vocab", i32), ("max_pos", i32), ("pos_offset", i32), ("ln_eps", f32)]
+                ("vocab", i32), ("max_pos", i32), ("pos_offset", i32), ("ln_eps", f32),
+                ("family", i32), ("n_kv_heads", i32), ("rope_theta", f32), ("rope_factor", f32),
+                ("rope_low_freq_factor", f32), ("rope_high_freq_factor", f32),
+                ("rope_orig_max_pos", i32)]
 
 
 class PipoQ4(ctypes.Structure):
@@ -50,7 +54,7 @@ class PipoLayerHost(ctypes.Structure):
 
 class PipoHostWeights(ctypes.Structure):
     _fields_ = [("tok_emb", vp), ("pos_emb", vp), ("lnf_g", vp), ("lnf_b", vp),
-                ("layers", ctypes.POINTER(PipoLayerHost))]
+                ("layers", ctypes.POINTER(PipoLayerHost)), ("lm_head", vp)]
 
 
 class PipoPolicy(ctypes.Structure):
@@ -138,6 +142,14 @@ _SIGNATURES = {
     "pipo_op_attn_prefill": ([vp, vp, vp, vp, i32, i32, i32, i32, vp], i32),
     "pipo_op_argmax": ([vp, vp, i64, i64, vp], i32),
     "pipo_op_copy": ([vp, vp, i64, vp], i32),
+    "pipo_op_attn_decode_gqa": ([vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, i64, vp], i32),
+    "pipo_op_attn_decode_gqa_workspace_bytes": ([i32, i32, i32, i32, i32], i64),
+    "pipo_op_attn_prefill_gqa": ([vp, vp, vp, vp, i32, i32, i32, i32, i32, vp], i32),
+    "pipo_op_rmsnorm": ([vp, vp, vp, i64, i64, i64, i64, f32, vp], i32),
+    "pipo_op_rope": ([vp, vp, vp, i64, i64, i64, i64, i64, i32, i32, i32, f32, vp], i32),
+    "pipo_rope_table": ([ctypes.POINTER(PipoShape), i32, vp], i32),
+    "pipo_op_swiglu": ([vp, vp, i64, i64, vp], i32),
+    "pipo_op_embed": ([vp, vp, vp, vp, i64, i64, i64, i64, i64, vp], i32),
     "pipo_sched_trace": ([ctypes.POINTER(PipoSchedConfig), i32, vp, vp, vp, i64, vp, i64], i64),
 }
 
@@ -391,6 +403,52 @@ def pipo_op_argmax(logits, nxt, rows, V, stream=None):
 
 def pipo_op_copy(dst, src, nbytes, stream=None):
     _check(lib().pipo_op_copy(dst, src, nbytes, stream), "pipo_op_copy")
+
+
+def pipo_op_attn_decode_gqa(q, kc, vc, o, b, n_heads, n_kv_heads, head_dim, t, kv_fmt,
+                            workspace=None, workspace_bytes=0, stream=None):
+    _check(lib().pipo_op_attn_decode_gqa(q, kc, vc, o, b, n_heads, n_kv_heads, head_dim, t,
+                                         kv_fmt, workspace, workspace_bytes, stream),
+           "pipo_op_attn_decode_gqa")
+
+
+def pipo_op_attn_decode_gqa_workspace_bytes(b, n_heads, n_kv_heads, head_dim, t) -> int:
+    return int(lib().pipo_op_attn_decode_gqa_workspace_bytes(b, n_heads, n_kv_heads, head_dim,
+                                                             t))
+
+
+def pipo_op_attn_prefill_gqa(q, kc, vc, o, b, P, n_heads, n_kv_heads, head_dim, stream=None):
+    _check(lib().pipo_op_attn_prefill_gqa(q, kc, vc, o, b, P, n_heads, n_kv_heads, head_dim,
+                                          stream), "pipo_op_attn_prefill_gqa")
+
+
+def pipo_op_rmsnorm(x, g, y, rows, d, src_stride, src_offset, eps, stream=None):
+    _check(lib().pipo_op_rmsnorm(x, g, y, rows, d, src_stride, src_offset, eps, stream),
+           "pipo_op_rmsnorm")
+
+
+def pipo_op_rope(q, k, cos_sin, M, rows_per_seq, pos0, kpos0, batch, n_heads, n_kv_heads,
+                 head_dim, q_scale, stream=None):
+    _check(lib().pipo_op_rope(q, k, cos_sin, M, rows_per_seq, pos0, kpos0, batch, n_heads,
+                              n_kv_heads, head_dim, q_scale, stream), "pipo_op_rope")
+
+
+def pipo_rope_table(shape: PipoShape, n_pos: int) -> np.ndarray:
+    """[n_pos][head_dim/2][2] float32 (cos, sin) table the library uses."""
+    dh = shape.d_model // shape.n_heads
+    out = np.zeros((n_pos, dh // 2, 2), dtype=np.float32)
+    _check(lib().pipo_rope_table(ctypes.byref(shape), n_pos, _ptr(out)), "pipo_rope_table")
+    return out
+
+
+def pipo_op_swiglu(gu, h, M, F, stream=None):
+    _check(lib().pipo_op_swiglu(gu, h, M, F, stream), "pipo_op_swiglu")
+
+
+def pipo_op_embed(ids, tok_table, pos_table, x, rows, d, rows_per_seq, pos0, pos_offset,
+                  stream=None):
+    _check(lib().pipo_op_embed(ids, tok_table, pos_table, x, rows, d, rows_per_seq, pos0,
+                               pos_offset, stream), "pipo_op_embed")
 
 
 # ---------------------------------------------------------------------------

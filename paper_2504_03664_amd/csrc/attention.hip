@@ -1,6 +1,7 @@
 // Causal softmax attention over a position-major KV cache: row p * b + i
-// of K (or V) holds sequence i's key (value) at position p, all heads side
-// by side.  This is the layout the copy engine streams when the cache lives
+// of K (or V) holds sequence i's key (value) at position p, all key/value
+// heads side by side.  With grouped-query attention, query head h reads
+// key/value head h / (H / Hkv).  This is the layout the copy engine streams when the cache lives
 // in host memory: a layer's prefix 0..t-1 is one contiguous range.
 //
 //   attn_decode:  one new query per (sequence, head) against keys 0..t.
@@ -27,17 +28,19 @@ __device__ __forceinline__ float wave_max(float v) {
 }
 
 // ---------------------------------------------------------------------------
-// decode: grid (heads, b, splits), 256 threads.  Split z of a (sequence,
+// decode: grid (key/value heads, b, splits), 256 threads.  A workgroup
+// serves the G = H / Hkv query heads that share key/value head kh, so each
+// cached row is read from HBM once per step.  Split z of a (sequence, kv
 // head) covers keys [z * chunk, min(T, (z + 1) * chunk)).  A key is handled
-// by D/8 lanes (8 dims each); every lane group keeps its own online softmax
-// state (running max m, sum l, 8 accumulators) over the keys it visits, two
-// keys at a time so that K and V of both are in flight together.  Groups are
-// merged by a butterfly inside the wave, waves in order through LDS.  With
-// one split the result is final; otherwise (m, l, acc[D]) goes to `part`
-// and attn_decode_combine merges the splits in split order.  With KV4 the
-// cache rows are INT4 (d/2 code bytes, then d/64 fp16 (scale, min) pairs):
-// a lane reads its 8 codes and its group's pair and expands them to fp16.
-template <int D>
+// by D/8 lanes (8 dims each); every lane group keeps, per query head, its
+// own online softmax state (running max m, sum l, 8 accumulators) over the
+// keys it visits, two keys at a time so that K and V of both are in flight
+// together.  Groups are merged by a butterfly inside the wave, waves in
+// order through LDS.  With one split the result is final; otherwise (m, l,
+// acc[D]) of each query head goes to `part` and attn_decode_combine merges
+// the splits in split order.  With KV4 the cache rows are INT4 (dkv/2 code
+// bytes, then dkv/64 fp16 (scale, min) pairs): a lane reads its 8 codes and
+// its group's pair and expands them to fp16.
 __device__ __forceinline__ void online_merge(float& m, float& l, float (&acc)[8], float m2,
                                              float l2, const float (&acc2)[8]) {
   const float M = fmaxf(m, m2);
@@ -49,40 +52,47 @@ __device__ __forceinline__ void online_merge(float& m, float& l, float (&acc)[8]
   m = M;
 }
 
-template <int D, bool KV4>
+template <int D, int G, bool KV4>
 __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict__ q,
                                                      const void* __restrict__ kc,
                                                      const void* __restrict__ vc,
                                                      uint16_t* __restrict__ o,
-                                                     float* __restrict__ part, int b, int H,
+                                                     float* __restrict__ part, int b, int Hkv,
                                                      int t, int chunk) {
-  __shared__ float wm[4], wl[4];
-  __shared__ float wacc[4][D];
+  __shared__ float wm[G][4], wl[G][4];
+  __shared__ float wacc[G][4][D];
   constexpr int LPP = D / 8;     // lanes per key
   constexpr int PPW = 64 / LPP;  // keys per wave per pass
-  const int h = blockIdx.x, bi = blockIdx.y, sp = blockIdx.z, S = gridDim.z;
+  const int kh = blockIdx.x, bi = blockIdx.y, sp = blockIdx.z, S = gridDim.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sub = lane / LPP, cl = lane % LPP;
-  const int64_t d = (int64_t)H * D;
+  const int H = Hkv * G;
+  const int64_t d = (int64_t)H * D, dkv = (int64_t)Hkv * D;
   const int T = t + 1;
   const int p0 = sp * chunk, p1 = min(T, p0 + chunk);
-  const int64_t col = (int64_t)h * D + cl * 8;
+  const int64_t kcol = (int64_t)kh * D + cl * 8;
 
-  float qf[8];
-  {
-    const h8 qv = load_h8(q + (int64_t)bi * d + col);
+  float qf[G][8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) qf[i] = (float)qv[i];
+  for (int g = 0; g < G; ++g) {
+    const h8 qv = load_h8(q + (int64_t)bi * d + (int64_t)(kh * G + g) * D + cl * 8);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) qf[g][i] = (float)qv[i];
   }
-  float m = -INFINITY, l = 0.f, acc[8];
+  float m[G], l[G], acc[G][8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+  for (int g = 0; g < G; ++g) {
+    m[g] = -INFINITY;
+    l[g] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[g][i] = 0.f;
+  }
 
-  // fp16: element offset of this lane's 8 values in row `bi` of position 0;
+  // fp16: byte offset of this lane's 8 values in row `bi` of position 0;
   // INT4: byte offsets of its 4 code bytes and of its group's (scale, min)
-  const int64_t row_bytes = KV4 ? d / 2 + d / 16 : 2 * d;
-  const int64_t code_off = (int64_t)bi * row_bytes + (KV4 ? col / 2 : 2 * col);
-  const int64_t sm_off = (int64_t)bi * row_bytes + d / 2 + (col / 64) * 4;
+  const int64_t row_bytes = KV4 ? dkv / 2 + dkv / 16 : 2 * dkv;
+  const int64_t code_off = (int64_t)bi * row_bytes + (KV4 ? kcol / 2 : 2 * kcol);
+  const int64_t sm_off = (int64_t)bi * row_bytes + dkv / 2 + (kcol / 64) * 4;
   const auto load_kv = [&](const void* base, int p) -> h8 {
     const char* row = static_cast<const char*>(base) + (int64_t)p * b * row_bytes;
     if constexpr (KV4) {
@@ -94,18 +104,27 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
     }
   };
   const auto visit = [&](h8 kv, h8 vv) {
-    float s = 0.f;
+    float kf[8], vf[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) s += qf[i] * (float)kv[i];
+    for (int i = 0; i < 8; ++i) {
+      kf[i] = (float)kv[i];
+      vf[i] = (float)vv[i];
+    }
 #pragma unroll
-    for (int off = LPP / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
-    const float mn = fmaxf(m, s);
-    const float alpha = expf(m - mn);
-    const float e = expf(s - mn);
-    l = l * alpha + e;
+    for (int g = 0; g < G; ++g) {
+      float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = acc[i] * alpha + e * (float)vv[i];
-    m = mn;
+      for (int i = 0; i < 8; ++i) s += qf[g][i] * kf[i];
+#pragma unroll
+      for (int off = LPP / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+      const float mn = fmaxf(m[g], s);
+      const float alpha = expf(m[g] - mn);
+      const float e = expf(s - mn);
+      l[g] = l[g] * alpha + e;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[g][i] = acc[g][i] * alpha + e * vf[i];
+      m[g] = mn;
+    }
   };
   for (int p = p0 + wave * PPW + sub; p < p1; p += 8 * PPW) {
     const int p2 = p + 4 * PPW;
@@ -122,40 +141,47 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
   // merge the lane groups of the wave (butterfly over the group index)
 #pragma unroll
   for (int off = LPP; off < 64; off <<= 1) {
-    float acc2[8];
-    const float m2 = __shfl_xor(m, off, 64);
-    const float l2 = __shfl_xor(l, off, 64);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc2[i] = __shfl_xor(acc[i], off, 64);
-    online_merge<D>(m, l, acc, m2, l2, acc2);
+    for (int g = 0; g < G; ++g) {
+      float acc2[8];
+      const float m2 = __shfl_xor(m[g], off, 64);
+      const float l2 = __shfl_xor(l[g], off, 64);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc2[i] = __shfl_xor(acc[g][i], off, 64);
+      online_merge(m[g], l[g], acc[g], m2, l2, acc2);
+    }
   }
   if (sub == 0) {
-    if (cl == 0) {
-      wm[wave] = m;
-      wl[wave] = l;
-    }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) wacc[wave][cl * 8 + i] = acc[i];
+    for (int g = 0; g < G; ++g) {
+      if (cl == 0) {
+        wm[g][wave] = m[g];
+        wl[g][wave] = l[g];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) wacc[g][wave][cl * 8 + i] = acc[g][i];
+    }
   }
   __syncthreads();
-  for (int c = tid; c < D; c += 256) {
-    float M = wm[0], L = wl[0], A = wacc[0][c];
+  for (int c = tid; c < G * D; c += 256) {
+    const int g = c / D, cc = c % D, h = kh * G + g;
+    float M = wm[g][0], L = wl[g][0], A = wacc[g][0][cc];
 #pragma unroll
     for (int w = 1; w < 4; ++w) {
-      const float m2 = wm[w];
+      const float m2 = wm[g][w];
       const float Mn = fmaxf(M, m2);
       const float a1 = M == -INFINITY ? 0.f : expf(M - Mn);
       const float a2 = m2 == -INFINITY ? 0.f : expf(m2 - Mn);
-      L = L * a1 + wl[w] * a2;
-      A = A * a1 + wacc[w][c] * a2;
+      L = L * a1 + wl[g][w] * a2;
+      A = A * a1 + wacc[g][w][cc] * a2;
       M = Mn;
     }
     if (S == 1) {
-      o[(int64_t)bi * d + (int64_t)h * D + c] = f2h(A / L);
+      o[(int64_t)bi * d + (int64_t)h * D + cc] = f2h(A / L);
     } else {
       float* pp = part + (((int64_t)bi * H + h) * S + sp) * (D + 2);
-      pp[c] = A;
-      if (c == 0) {
+      pp[cc] = A;
+      if (cc == 0) {
         pp[D] = M;
         pp[D + 1] = L;
       }
@@ -193,7 +219,7 @@ __global__ __launch_bounds__(256) void attn_prefill_k(const uint16_t* __restrict
                                                       const uint16_t* __restrict__ kc,
                                                       const uint16_t* __restrict__ vc,
                                                       uint16_t* __restrict__ o, int b, int P,
-                                                      int H) {
+                                                      int H, int Hkv) {
   constexpr int KB = 64;
   constexpr int KROW = D + 8;
   constexpr int VROW = KB + 8;
@@ -203,7 +229,8 @@ __global__ __launch_bounds__(256) void attn_prefill_k(const uint16_t* __restrict
   __shared__ __attribute__((aligned(16))) uint16_t Ps[4][16 * PROW];
 
   const int qb = blockIdx.x, h = blockIdx.y, bi = blockIdx.z;
-  const int64_t d = (int64_t)H * D;
+  const int64_t d = (int64_t)H * D, dkv = (int64_t)Hkv * D;
+  const int kh = h / (H / Hkv);  // key/value head of query head h
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, g = lane >> 4;
   const int q0 = qb * 64 + wave * 16;
@@ -231,7 +258,7 @@ __global__ __launch_bounds__(256) void attn_prefill_k(const uint16_t* __restrict
     for (int c = tid; c < KB * (D / 8); c += 256) {
       const int key = c / (D / 8), col = (c % (D / 8)) * 8;
       const int kp = kb * KB + key;
-      const int64_t off = ((int64_t)kp * b + bi) * d + (int64_t)h * D + col;
+      const int64_t off = ((int64_t)kp * b + bi) * dkv + (int64_t)kh * D + col;
       const h8 kv = kp < P ? load_h8(kc + off) : zero_h8();
       const h8 vv = kp < P ? load_h8(vc + off) : zero_h8();
       *reinterpret_cast<h8*>(&Ks[key * KROW + col]) = kv;
@@ -316,10 +343,10 @@ __global__ __launch_bounds__(256) void attn_prefill_k(const uint16_t* __restrict
 }
 
 // ---------------------------------------------------------------------------
-int attn_decode_splits(int b, int n_heads, int t) {
+int attn_decode_splits(int b, int n_kv_heads, int t) {
   // enough workgroups to fill the chip, at least 64 keys per split
   const int T = t + 1;
-  int S = (2048 + b * n_heads - 1) / (b * n_heads);
+  int S = (2048 + b * n_kv_heads - 1) / (b * n_kv_heads);
   S = std::min(S, std::max(1, T / 64));
   S = std::min(S, kAttnDecodeMaxSplits);
   const int chunk = (T + S - 1) / S;
@@ -330,64 +357,89 @@ int64_t attn_decode_workspace_bytes(int b, int n_heads, int head_dim, int splits
   return splits > 1 ? (int64_t)b * n_heads * splits * (head_dim + 2) * 4 : 0;
 }
 
-template <int D, bool KV4>
-static void launch_decode_d(const uint16_t* q, const void* kc, const void* vc, uint16_t* o, int b,
-                            int n_heads, int t, int S, int chunk, float* workspace,
+template <int D, int G, bool KV4>
+static void launch_decode_g(const uint16_t* q, const void* kc, const void* vc, uint16_t* o,
+                            int b, int Hkv, int t, int S, int chunk, float* workspace,
                             hipStream_t st) {
-  const dim3 grid((unsigned)n_heads, (unsigned)b, (unsigned)S);
-  launch(attn_decode_k<D, KV4>, grid, dim3(256), 0, st, q, kc, vc, o, workspace, b, n_heads, t,
+  const dim3 grid((unsigned)Hkv, (unsigned)b, (unsigned)S);
+  launch(attn_decode_k<D, G, KV4>, grid, dim3(256), 0, st, q, kc, vc, o, workspace, b, Hkv, t,
          chunk);
   if (S > 1)
-    launch(attn_decode_combine<D>, dim3((unsigned)n_heads, (unsigned)b), dim3(D), 0, st,
-           (const float*)workspace, o, n_heads, S);
+    launch(attn_decode_combine<D>, dim3((unsigned)(Hkv * G), (unsigned)b), dim3(D), 0, st,
+           (const float*)workspace, o, Hkv * G, S);
+}
+
+template <int D, bool KV4>
+static void launch_decode_d(const uint16_t* q, const void* kc, const void* vc, uint16_t* o, int b,
+                            int Hkv, int G, int t, int S, int chunk, float* workspace,
+                            hipStream_t st) {
+  switch (G) {
+    case 1: launch_decode_g<D, 1, KV4>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, st); break;
+    case 2: launch_decode_g<D, 2, KV4>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, st); break;
+    case 4: launch_decode_g<D, 4, KV4>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, st); break;
+    default: launch_decode_g<D, 8, KV4>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, st); break;
+  }
+}
+
+static pipo_status check_heads(const char* what, int n_heads, int n_kv_heads, int head_dim) {
+  if (head_dim != 64 && head_dim != 128) {
+    set_error("%s: head_dim %d not supported (64 or 128)", what, head_dim);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  if (n_kv_heads < 1 || n_heads % n_kv_heads != 0) {
+    set_error("%s: %d query heads are not a multiple of %d key/value heads", what, n_heads,
+              n_kv_heads);
+    return PIPO_ERR_ARG;
+  }
+  const int G = n_heads / n_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8) {
+    set_error("%s: %d query heads per key/value head not supported (1, 2, 4, 8)", what, G);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  return PIPO_OK;
 }
 
 pipo_status launch_attn_decode(const uint16_t* q, const void* kc, const void* vc, uint16_t* o,
-                               int b, int n_heads, int head_dim, int t, bool kv4,
+                               int b, int n_heads, int n_kv_heads, int head_dim, int t, bool kv4,
                                float* workspace, int64_t workspace_bytes, hipStream_t st) {
   if (b < 1 || n_heads < 1 || t < 0) {
     set_error("attn_decode: bad shape b=%d heads=%d t=%d", b, n_heads, t);
     return PIPO_ERR_ARG;
   }
-  if (head_dim != 64 && head_dim != 128) {
-    set_error("attn_decode: head_dim %d not supported (64 or 128)", head_dim);
+  PIPO_TRY(check_heads("attn_decode", n_heads, n_kv_heads, head_dim));
+  if (kv4 && ((int64_t)n_kv_heads * head_dim) % 256 != 0) {
+    set_error("attn_decode: INT4 KV rows need a width %% 256 == 0 (%d)", n_kv_heads * head_dim);
     return PIPO_ERR_UNSUPPORTED;
   }
-  if (kv4 && ((int64_t)n_heads * head_dim) % 256 != 0) {
-    set_error("attn_decode: INT4 KV rows need d %% 256 == 0 (d=%d)", n_heads * head_dim);
-    return PIPO_ERR_UNSUPPORTED;
-  }
+  const int G = n_heads / n_kv_heads;
   const int T = t + 1;
-  int S = attn_decode_splits(b, n_heads, t);
+  int S = attn_decode_splits(b, n_kv_heads, t);
   if (!workspace || workspace_bytes < attn_decode_workspace_bytes(b, n_heads, head_dim, S)) S = 1;
   const int chunk = (T + S - 1) / S;
   S = (T + chunk - 1) / chunk;
   if (head_dim == 128)
-    (kv4 ? launch_decode_d<128, true> : launch_decode_d<128, false>)(q, kc, vc, o, b, n_heads, t,
-                                                                    S, chunk, workspace, st);
+    (kv4 ? launch_decode_d<128, true> : launch_decode_d<128, false>)(
+        q, kc, vc, o, b, n_kv_heads, G, t, S, chunk, workspace, st);
   else
-    (kv4 ? launch_decode_d<64, true> : launch_decode_d<64, false>)(q, kc, vc, o, b, n_heads, t, S,
-                                                                  chunk, workspace, st);
+    (kv4 ? launch_decode_d<64, true> : launch_decode_d<64, false>)(
+        q, kc, vc, o, b, n_kv_heads, G, t, S, chunk, workspace, st);
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
 }
 
 pipo_status launch_attn_prefill(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
-                                uint16_t* o, int b, int P, int n_heads, int head_dim,
-                                hipStream_t st) {
+                                uint16_t* o, int b, int P, int n_heads, int n_kv_heads,
+                                int head_dim, hipStream_t st) {
   if (b < 1 || n_heads < 1 || P < 1) {
     set_error("attn_prefill: bad shape b=%d P=%d heads=%d", b, P, n_heads);
     return PIPO_ERR_ARG;
   }
+  PIPO_TRY(check_heads("attn_prefill", n_heads, n_kv_heads, head_dim));
   const dim3 grid((unsigned)((P + 63) / 64), (unsigned)n_heads, (unsigned)b);
-  if (head_dim == 128) {
-    launch(attn_prefill_k<128>, grid, dim3(256), 0, st, q, kc, vc, o, b, P, n_heads);
-  } else if (head_dim == 64) {
-    launch(attn_prefill_k<64>, grid, dim3(256), 0, st, q, kc, vc, o, b, P, n_heads);
-  } else {
-    set_error("attn_prefill: head_dim %d not supported (64 or 128)", head_dim);
-    return PIPO_ERR_UNSUPPORTED;
-  }
+  if (head_dim == 128)
+    launch(attn_prefill_k<128>, grid, dim3(256), 0, st, q, kc, vc, o, b, P, n_heads, n_kv_heads);
+  else
+    launch(attn_prefill_k<64>, grid, dim3(256), 0, st, q, kc, vc, o, b, P, n_heads, n_kv_heads);
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
 }

@@ -74,11 +74,13 @@ struct GemmArgs {
   uint16_t* out16 = nullptr;      // [M][ldo]
   float* out32 = nullptr;         // [M][ldo]
   int64_t ldo = 0;
-  // EPI_QKV: row m is sequence m / rows_per_seq at position pos0 + m % rows_per_seq
+  // EPI_QKV: row m is sequence m / rows_per_seq at position pos0 + m % rows_per_seq;
+  // output columns [0, d) are q, the next dkv k, the last dkv v (dkv = d
+  // without grouped-query attention)
   uint16_t* q_out = nullptr;      // [M][d]
-  uint16_t* k_out = nullptr;      // cache rows (p * batch + seq), [.][d]
+  uint16_t* k_out = nullptr;      // cache rows (p * batch + seq), [.][dkv]
   uint16_t* v_out = nullptr;
-  int64_t d = 0;
+  int64_t d = 0, dkv = 0;
   float q_scale = 1.f;
   int64_t rows_per_seq = 1, pos0 = 0, batch = 1;
 };
@@ -95,22 +97,38 @@ int64_t gemm_workspace_bytes_upto(int64_t M_max, int64_t N, int64_t K, bool w4);
 pipo_status launch_layernorm(const float* x, const uint16_t* g, const uint16_t* b, uint16_t* y,
                              int64_t rows, int64_t d, int64_t src_stride, int64_t src_offset,
                              float eps, hipStream_t st);
+// y = x / sqrt(mean(x^2) + eps) * g (RMSNorm), same row addressing as LayerNorm
+pipo_status launch_rmsnorm(const float* x, const uint16_t* g, uint16_t* y, int64_t rows,
+                           int64_t d, int64_t src_stride, int64_t src_offset, float eps,
+                           hipStream_t st);
+// pos_table may be null (no learned positions)
 pipo_status launch_embed(const uint16_t* tok_rows, const int32_t* ids, const uint16_t* tok_table,
                          const uint16_t* pos_table, float* x, int64_t rows, int64_t d,
                          int64_t rows_per_seq, int64_t pos0, int64_t pos_offset, hipStream_t st);
+// rotary positions, in place: q rows [M][H * D] (then scaled by q_scale) and
+// k rows at cache row (kpos0 + m % rows_per_seq) * batch + m / rows_per_seq of
+// [.][Hkv * D]; row m sits at position pos0 + m % rows_per_seq, whose
+// (cos, sin) pairs are cs[pos][D / 2][2]
+pipo_status launch_rope(uint16_t* q, uint16_t* k, const float* cs, int64_t M,
+                        int64_t rows_per_seq, int64_t pos0, int64_t kpos0, int64_t batch, int H,
+                        int Hkv, int D, float q_scale, hipStream_t st);
+// h[m][i] = silu(gu[m][i]) * gu[m][F + i]
+pipo_status launch_swiglu(const uint16_t* gu, uint16_t* h, int64_t M, int64_t F, hipStream_t st);
 // decode attention splits the keys of a (sequence, head) over several
 // workgroups when there are few of them; the splits' partial results go to
 // `workspace` (attn_decode_workspace_bytes) and a second kernel merges them
 // in split order; without enough workspace it runs unsplit
-int attn_decode_splits(int b, int n_heads, int t);
+// Query head h reads key/value head h / (n_heads / n_kv_heads); cache rows
+// hold the n_kv_heads heads side by side.
+int attn_decode_splits(int b, int n_kv_heads, int t);
 int64_t attn_decode_workspace_bytes(int b, int n_heads, int head_dim, int splits);
 // kc, vc: fp16 rows, or INT4 rows (kv4; see kvcache.hip) of the cache
 pipo_status launch_attn_decode(const uint16_t* q, const void* kc, const void* vc, uint16_t* o,
-                               int b, int n_heads, int head_dim, int t, bool kv4,
+                               int b, int n_heads, int n_kv_heads, int head_dim, int t, bool kv4,
                                float* workspace, int64_t workspace_bytes, hipStream_t st);
 pipo_status launch_attn_prefill(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
-                                uint16_t* o, int b, int P, int n_heads, int head_dim,
-                                hipStream_t st);
+                                uint16_t* o, int b, int P, int n_heads, int n_kv_heads,
+                                int head_dim, hipStream_t st);
 // INT4 KV rows (d/2 code bytes + d/64 fp16 (scale, min) pairs; d % 256 == 0)
 pipo_status launch_kv_quant(const uint16_t* x, uint8_t* out, int64_t rows, int64_t d,
                             hipStream_t st);

@@ -5,6 +5,7 @@
 #include <unistd.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <vector>
 
@@ -36,7 +37,70 @@ pipo_status check_shape(const pipo_shape* s) {
               s->d_ffn);
     return PIPO_ERR_UNSUPPORTED;
   }
+  if (s->family != PIPO_FAMILY_OPT && s->family != PIPO_FAMILY_LLAMA) {
+    set_error("unknown model family %d", s->family);
+    return PIPO_ERR_ARG;
+  }
+  const int hkv = (int)kv_heads(*s);
+  if (s->n_kv_heads < 0 || s->n_heads % hkv != 0) {
+    set_error("n_heads %d is not a multiple of n_kv_heads %d", s->n_heads, s->n_kv_heads);
+    return PIPO_ERR_ARG;
+  }
+  const int group = s->n_heads / hkv;
+  if (group != 1 && group != 2 && group != 4 && group != 8) {
+    set_error("%d query heads per key/value head not supported (1, 2, 4, 8)", group);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  if (s->family == PIPO_FAMILY_OPT && group != 1) {
+    set_error("the OPT family has no grouped-query attention (n_kv_heads %d)", s->n_kv_heads);
+    return PIPO_ERR_ARG;
+  }
+  if (s->family == PIPO_FAMILY_LLAMA) {
+    if (!(s->rope_theta > 0.f) || !(s->rope_factor >= 0.f)) {
+      set_error("invalid rotary base %g or scaling factor %g", (double)s->rope_theta,
+                (double)s->rope_factor);
+      return PIPO_ERR_ARG;
+    }
+    if (s->rope_factor > 0.f &&
+        !(s->rope_low_freq_factor > 0.f && s->rope_high_freq_factor > s->rope_low_freq_factor &&
+          s->rope_orig_max_pos > 0)) {
+      set_error("invalid rotary scaling: low %g, high %g, original length %d",
+                (double)s->rope_low_freq_factor, (double)s->rope_high_freq_factor,
+                s->rope_orig_max_pos);
+      return PIPO_ERR_ARG;
+    }
+  }
   return PIPO_OK;
+}
+
+// Rotary angles (the LLaMA 3.1 reading of the family): w_i = theta^(-2i/D);
+// with scaling, a wavelength 2 pi / w above orig / low is divided by the
+// factor, one below orig / high is kept, and in between the two are blended
+// linearly in orig / wavelength.  Angles and their sines in double.
+void rope_table(const pipo_shape& s, int64_t n_pos, float* out) {
+  const int D = s.d_model / s.n_heads, half = D / 2;
+  std::vector<double> w((size_t)half);
+  for (int i = 0; i < half; ++i) {
+    double wi = std::pow((double)s.rope_theta, -2.0 * i / D);
+    if (s.rope_factor > 0.f) {
+      const double factor = s.rope_factor, lo = s.rope_low_freq_factor,
+                   hi = s.rope_high_freq_factor, orig = s.rope_orig_max_pos;
+      const double wavelen = 2.0 * M_PI / wi;
+      if (wavelen > orig / lo) {
+        wi /= factor;
+      } else if (wavelen >= orig / hi) {
+        const double sm = (orig / wavelen - lo) / (hi - lo);
+        wi = (1.0 - sm) * wi / factor + sm * wi;
+      }
+    }
+    w[(size_t)i] = wi;
+  }
+  for (int64_t p = 0; p < n_pos; ++p)
+    for (int i = 0; i < half; ++i) {
+      const double ang = (double)p * w[(size_t)i];
+      out[(p * half + i) * 2] = (float)std::cos(ang);
+      out[(p * half + i) * 2 + 1] = (float)std::sin(ang);
+    }
 }
 
 pipo_status normalize_policy(const pipo_shape* shape, pipo_policy* p) {
@@ -68,8 +132,9 @@ pipo_status normalize_policy(const pipo_shape* shape, pipo_policy* p) {
     set_error("unknown kv_fmt %d", pol.kv_fmt);
     return PIPO_ERR_ARG;
   }
-  if (pol.kv_fmt == PIPO_KV_INT4_G64 && shape->d_model % 256 != 0) {
-    set_error("an INT4 KV cache needs d_model %% 256 == 0 (d_model=%d)", shape->d_model);
+  if (pol.kv_fmt == PIPO_KV_INT4_G64 && kv_width(*shape) % 256 != 0) {
+    set_error("an INT4 KV cache needs rows of a multiple of 256 elements (%lld)",
+              (long long)kv_width(*shape));
     return PIPO_ERR_UNSUPPORTED;
   }
   return PIPO_OK;
@@ -78,7 +143,19 @@ pipo_status normalize_policy(const pipo_shape* shape, pipo_policy* p) {
 UnitLayout unit_layout(const pipo_shape& sh, bool w4) {
   UnitLayout u;
   const int64_t d = sh.d_model, F = sh.d_ffn, V = sh.vocab;
-  u.misc_bytes = (9 * d + F) * 2;
+  if (is_llama(sh)) {
+    u.misc_count[kLn1G] = d;
+    u.misc_count[kLn2G] = d;
+  } else {
+    const int64_t cnt[kNumMisc] = {d, d, 3 * d, d, d, d, F, d};
+    for (int i = 0; i < kNumMisc; ++i) u.misc_count[i] = cnt[i];
+  }
+  int64_t elems = 0;
+  for (int i = 0; i < kNumMisc; ++i) {
+    u.misc_off[i] = elems;
+    elems += u.misc_count[i];
+  }
+  u.misc_bytes = elems * 2;
   const auto mat = [&](int seg, int64_t N, int64_t K) {
     if (w4) {
       u.seg_bytes[seg] = N * K / 2;
@@ -88,9 +165,9 @@ UnitLayout unit_layout(const pipo_shape& sh, bool w4) {
     }
   };
   u.seg_bytes[kSegMisc] = u.misc_bytes;
-  mat(kSegWqkv, 3 * d, d);
+  mat(kSegWqkv, qkv_rows(sh), d);
   mat(kSegWo, d, d);
-  mat(kSegW1, F, d);
+  mat(kSegW1, fc1_rows(sh), d);
   mat(kSegW2, d, F);
   int64_t off = 0;
   for (int sg = 0; sg < kNumSegs; ++sg) {
@@ -115,24 +192,31 @@ HbmPlan hbm_plan(const pipo_shape& sh, const pipo_policy& pol) {
   p.slots = p.slot_bytes * pol.n_weight_slots;
   p.resident = pol.weights_on_host ? 0 : u.layer_bytes * L;
   p.tok = pol.embed_on_host ? 0 : u.head_bytes;
-  p.pos = ((int64_t)sh.max_pos + sh.pos_offset) * d * 2;
+  const bool llama = is_llama(sh);
+  p.head = llama && !pol.embed_on_host ? u.head_bytes : 0;  // untied head
+  p.pos = llama ? 0 : ((int64_t)sh.max_pos + sh.pos_offset) * d * 2;
+  p.rope = llama ? (int64_t)pol.max_seq * (d / sh.n_heads) * 4 : 0;
   p.lnf = d * 4;
   p.x = rows * d * 4;
   p.a = rows * d * 2;
   p.q = rows * d * 2;
   p.o = rows * d * 2;
   p.h = rows * F * 2;
+  p.gu = llama ? rows * 2 * F * 2 : 0;  // gate and up outputs before SwiGLU
   p.logits = (int64_t)pol.max_batch * V * 4;
   p.next = (int64_t)pol.max_batch * 4;
   p.ids = rows * 4;
   p.emb = pol.embed_on_host ? rows * d * 2 : 0;
   p.attn_ws = attn_decode_workspace_bytes(pol.max_batch, sh.n_heads, (int)(d / sh.n_heads),
                                           kAttnDecodeMaxSplits);
-  const int64_t shapes[5][3] = {{3 * d, d, w4}, {d, d, w4}, {F, d, w4}, {d, F, w4}, {V, d, 0}};
+  const int64_t shapes[5][3] = {
+      {qkv_rows(sh), d, w4}, {d, d, w4}, {fc1_rows(sh), d, w4}, {d, F, w4}, {V, d, 0}};
   for (const auto& s : shapes)
     p.gemm_ws = std::max(p.gemm_ws, gemm_workspace_bytes_upto(rows, s[0], s[1], s[2] != 0));
-  p.kstage = kv4 ? rows * d * 2 : 0;
-  p.kv_row = kv4 ? d / 2 + d / 16 : 2 * d;
+  const int64_t dkv = kv_width(sh);
+  // INT4 cache: new rows are staged in fp16 (and rotated there) before quantization
+  p.kstage = kv4 ? rows * dkv * 2 : 0;
+  p.kv_row = kv4 ? dkv / 2 + dkv / 16 : 2 * dkv;
   p.kv_part = rows * p.kv_row;
   p.kv = (pol.kv_on_host ? pol.n_weight_slots : L) * 2 * p.kv_part;
   return p;
@@ -160,8 +244,10 @@ static void fill_plan(const pipo_shape& sh, const pipo_policy& pol, pipo_plan* o
   const UnitLayout u = unit_layout(sh, pol.wfmt == PIPO_W_INT4_G64);
   const HbmPlan p = hbm_plan(sh, pol);
   std::memset(out, 0, sizeof *out);
-  out->weight_bytes = (int64_t)sh.n_layers * u.copy_bytes + u.head_bytes +
-                      ((int64_t)sh.max_pos + sh.pos_offset) * sh.d_model * 2 + 4 * sh.d_model;
+  out->weight_bytes =
+      (int64_t)sh.n_layers * u.copy_bytes + u.head_bytes +
+      (is_llama(sh) ? u.head_bytes + 2 * sh.d_model
+                    : ((int64_t)sh.max_pos + sh.pos_offset) * sh.d_model * 2 + 4 * sh.d_model);
   out->kv_bytes = (int64_t)sh.n_layers * 2 * p.kv_part;
   out->hbm_bytes = p.total();
   out->host_kv_bytes = host_kv_bytes(sh, pol);
@@ -174,6 +260,17 @@ static void fill_plan(const pipo_shape& sh, const pipo_policy& pol, pipo_plan* o
 using namespace pipo;
 
 extern "C" {
+
+pipo_status pipo_rope_table(const pipo_shape* shape, int32_t n_pos, float* out) {
+  clear_error();
+  PIPO_TRY(check_shape(shape));
+  if (!out || n_pos < 0 || shape->family != PIPO_FAMILY_LLAMA) {
+    set_error("rope_table: NULL output, negative n_pos or not a LLaMA shape");
+    return PIPO_ERR_ARG;
+  }
+  rope_table(*shape, n_pos, out);
+  return PIPO_OK;
+}
 
 pipo_status pipo_plan_policy(const pipo_shape* shape, const pipo_policy* policy,
                              pipo_plan* plan_out) {

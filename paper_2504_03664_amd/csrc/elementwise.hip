@@ -1,6 +1,7 @@
-// Row-wise kernels of the decoder: LayerNorm, embedding, greedy argmax, and
-// a fill used to poison weight slots.  The residual stream x is fp32; the
-// LayerNorm output that feeds the next GEMM is fp16.
+// Row-wise kernels of the decoder: LayerNorm and RMSNorm, embedding, rotary
+// positions, the SwiGLU gate, greedy argmax, and a fill used to poison
+// weight slots.  The residual stream x is fp32; the normalised output that
+// feeds the next GEMM is fp16.
 #include <cfloat>
 #include <climits>
 
@@ -22,11 +23,13 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
   return ((red[0] + red[1]) + red[2]) + red[3];
 }
 
-// y[r] = (x[src] - mean) / sqrt(var + eps) * gamma + beta, two passes over
-// the row held in registers (d <= 256 * 4 * kLnMaxVec)
+// LayerNorm: y[r] = (x[src] - mean) / sqrt(var + eps) * gamma + beta, two
+// passes over the row held in registers (d <= 256 * 4 * kLnMaxVec).
+// RMSNorm (RMS): y[r] = x[src] / sqrt(mean(x^2) + eps) * gamma.
 constexpr int kLnMaxVec = 8;
 
-__global__ __launch_bounds__(256) void layernorm_k(const float* __restrict__ x,
+template <bool RMS>
+__global__ __launch_bounds__(256) void norm_k(const float* __restrict__ x,
                                                    const uint16_t* __restrict__ gamma,
                                                    const uint16_t* __restrict__ beta,
                                                    uint16_t* __restrict__ y, int64_t d,
@@ -45,7 +48,7 @@ __global__ __launch_bounds__(256) void layernorm_k(const float* __restrict__ x,
     v[i] = c < nv ? xr[c] : f4v{0.f, 0.f, 0.f, 0.f};
     s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
   }
-  const float mean = block_sum256(s, red) / (float)d;
+  const float mean = RMS ? 0.f : block_sum256(s, red) / (float)d;
   float sq = 0.f;
 #pragma unroll
   for (int i = 0; i < kLnMaxVec; ++i) {
@@ -69,8 +72,12 @@ __global__ __launch_bounds__(256) void layernorm_k(const float* __restrict__ x,
 #pragma unroll
       for (int e = 0; e < 4; e += 2) {
         const int64_t k = 4 * (int64_t)c + e;
-        const float a0 = (v[i][e] - mean) * rstd * h2f(gamma[k]) + h2f(beta[k]);
-        const float a1 = (v[i][e + 1] - mean) * rstd * h2f(gamma[k + 1]) + h2f(beta[k + 1]);
+        float a0 = (v[i][e] - mean) * rstd * h2f(gamma[k]);
+        float a1 = (v[i][e + 1] - mean) * rstd * h2f(gamma[k + 1]);
+        if constexpr (!RMS) {
+          a0 += h2f(beta[k]);
+          a1 += h2f(beta[k + 1]);
+        }
         packed[e / 2] = (uint32_t)f2h(a0) | ((uint32_t)f2h(a1) << 16);
       }
       *reinterpret_cast<u32x2*>(yr + 4 * (int64_t)c) = packed;
@@ -79,7 +86,8 @@ __global__ __launch_bounds__(256) void layernorm_k(const float* __restrict__ x,
 }
 
 // x[r][:] = tok(r) + pos_table[pos0 + r % rows_per_seq + pos_offset], with
-// tok(r) = tok_rows[r] (gathered on the host) or tok_table[ids[r]]
+// tok(r) = tok_rows[r] (gathered on the host) or tok_table[ids[r]]; without
+// a position table x[r][:] = tok(r)
 __global__ __launch_bounds__(256) void embed_k(const uint16_t* __restrict__ tok_rows,
                                                const int32_t* __restrict__ ids,
                                                const uint16_t* __restrict__ tok_table,
@@ -89,8 +97,84 @@ __global__ __launch_bounds__(256) void embed_k(const uint16_t* __restrict__ tok_
                                                int64_t pos_offset) {
   const int64_t r = blockIdx.x;
   const uint16_t* tr = tok_rows ? tok_rows + r * d : tok_table + (int64_t)ids[r] * d;
+  if (!pos_table) {
+    for (int64_t c = threadIdx.x; c < d; c += 256) x[r * d + c] = h2f(tr[c]);
+    return;
+  }
   const uint16_t* pr = pos_table + (pos0 + r % rows_per_seq + pos_offset) * d;
   for (int64_t c = threadIdx.x; c < d; c += 256) x[r * d + c] = h2f(tr[c]) + h2f(pr[c]);
+}
+
+// Rotary positions.  Each thread turns 4 consecutive pairs (i, i + D/2) of
+// one head of one row: (a, b) -> (a cos - b sin, b cos + a sin), in fp32 from
+// fp16 and back (q also times q_scale before its one rounding).  Items of a
+// row: the H query heads, then the Hkv key heads, D/8 items per head.
+__global__ __launch_bounds__(256) void rope_k(uint16_t* __restrict__ q, uint16_t* __restrict__ k,
+                                              const float* __restrict__ cs, int64_t M,
+                                              int64_t rows_per_seq, int64_t pos0, int64_t kpos0,
+                                              int64_t batch, int H, int Hkv, int D,
+                                              float q_scale) {
+  const int per_head = D / 8, per_row = (H + Hkv) * per_head;
+  const int64_t item = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (item >= M * per_row) return;
+  const int64_t m = item / per_row;
+  const int r = (int)(item % per_row);
+  const int hh = r / per_head, i = 4 * (r % per_head);
+  const int64_t p = m % rows_per_seq, seq = m / rows_per_seq;
+  uint16_t* base;
+  float sc;
+  if (hh < H) {
+    base = q + m * ((int64_t)H * D) + (int64_t)hh * D;
+    sc = q_scale;
+  } else {
+    base = k + ((kpos0 + p) * batch + seq) * ((int64_t)Hkv * D) + (int64_t)(hh - H) * D;
+    sc = 1.f;
+  }
+  const float* c = cs + (pos0 + p) * D + 2 * i;  // D/2 (cos, sin) pairs per position
+  const u32x2 av = *reinterpret_cast<const u32x2*>(base + i);
+  const u32x2 bv = *reinterpret_cast<const u32x2*>(base + i + D / 2);
+  u32x2 ao, bo;
+#pragma unroll
+  for (int w = 0; w < 2; ++w) {
+    uint32_t ra = 0, rb = 0;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int j = 2 * w + e;
+      const float a = h2f((uint16_t)(av[w] >> (16 * e)));
+      const float b = h2f((uint16_t)(bv[w] >> (16 * e)));
+      const float co = c[2 * j], si = c[2 * j + 1];
+      ra |= (uint32_t)f2h((a * co - b * si) * sc) << (16 * e);
+      rb |= (uint32_t)f2h((b * co + a * si) * sc) << (16 * e);
+    }
+    ao[w] = ra;
+    bo[w] = rb;
+  }
+  *reinterpret_cast<u32x2*>(base + i) = ao;
+  *reinterpret_cast<u32x2*>(base + i + D / 2) = bo;
+}
+
+// SwiGLU: h[m][i] = silu(g) * u with g = gu[m][i], u = gu[m][F + i] and
+// silu(g) = g / (1 + exp(-g)), in fp32; 8 elements per thread
+__global__ __launch_bounds__(256) void swiglu_k(const uint16_t* __restrict__ gu,
+                                                uint16_t* __restrict__ h, int64_t M, int64_t F) {
+  const int64_t per_row = F / 8;
+  const int64_t item = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (item >= M * per_row) return;
+  const int64_t m = item / per_row, i = 8 * (item % per_row);
+  const h8 g = load_h8(gu + m * 2 * F + i);
+  const h8 u = load_h8(gu + m * 2 * F + F + i);
+  u32x4 out;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    uint32_t r = 0;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const float gv = (float)g[2 * w + e], uv = (float)u[2 * w + e];
+      r |= (uint32_t)f2h(gv / (1.f + expf(-gv)) * uv) << (16 * e);
+    }
+    out[w] = r;
+  }
+  *reinterpret_cast<u32x4*>(h + m * F + i) = out;
 }
 
 // greedy token: largest logit, ties to the lowest index (NaNs are skipped)
@@ -157,8 +241,49 @@ pipo_status launch_layernorm(const float* x, const uint16_t* g, const uint16_t* 
     set_error("layernorm: unsupported rows=%lld d=%lld", (long long)rows, (long long)d);
     return PIPO_ERR_UNSUPPORTED;
   }
-  launch(layernorm_k, dim3((unsigned)rows), dim3(256), 0, st, x, g, b, y, d,
-                     src_stride, src_offset, eps);
+  launch(norm_k<false>, dim3((unsigned)rows), dim3(256), 0, st, x, g, b, y, d, src_stride,
+         src_offset, eps);
+  PIPO_HIP_TRY(hipGetLastError());
+  return PIPO_OK;
+}
+
+pipo_status launch_rmsnorm(const float* x, const uint16_t* g, uint16_t* y, int64_t rows,
+                           int64_t d, int64_t src_stride, int64_t src_offset, float eps,
+                           hipStream_t st) {
+  if (rows < 1 || d < 4 || d % 4 != 0 || d > 256 * 4 * kLnMaxVec) {
+    set_error("rmsnorm: unsupported rows=%lld d=%lld", (long long)rows, (long long)d);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  launch(norm_k<true>, dim3((unsigned)rows), dim3(256), 0, st, x, g, (const uint16_t*)nullptr, y,
+         d, src_stride, src_offset, eps);
+  PIPO_HIP_TRY(hipGetLastError());
+  return PIPO_OK;
+}
+
+pipo_status launch_rope(uint16_t* q, uint16_t* k, const float* cs, int64_t M,
+                        int64_t rows_per_seq, int64_t pos0, int64_t kpos0, int64_t batch, int H,
+                        int Hkv, int D, float q_scale, hipStream_t st) {
+  if (M < 1) return PIPO_OK;
+  if ((D != 64 && D != 128) || H < 1 || Hkv < 1 || rows_per_seq < 1 || batch < 1 || pos0 < 0 ||
+      kpos0 < 0 || M > rows_per_seq * batch) {
+    set_error("rope: unsupported shape M=%lld head_dim=%d heads=%d/%d", (long long)M, D, H, Hkv);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  const int64_t items = M * (H + Hkv) * (D / 8);
+  launch(rope_k, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st, q, k, cs, M,
+         rows_per_seq, pos0, kpos0, batch, H, Hkv, D, q_scale);
+  PIPO_HIP_TRY(hipGetLastError());
+  return PIPO_OK;
+}
+
+pipo_status launch_swiglu(const uint16_t* gu, uint16_t* h, int64_t M, int64_t F, hipStream_t st) {
+  if (M < 1) return PIPO_OK;
+  if (F < 8 || F % 8 != 0) {
+    set_error("swiglu: F=%lld is not a multiple of 8", (long long)F);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  const int64_t items = M * (F / 8);
+  launch(swiglu_k, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st, gu, h, M, F);
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
 }

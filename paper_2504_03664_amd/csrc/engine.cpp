@@ -212,6 +212,8 @@ struct pipo_ctx {
   pipo_shape sh{};
   pipo_policy pol{};
   int64_t d = 0, F = 0, V = 0, L = 0, H = 0, dh = 0;
+  int64_t Hkv = 0, dkv = 0;    // key/value heads and the width of a cached row
+  bool llama = false;          // PIPO_FAMILY_LLAMA
   bool w4 = false;
   int device = 0;
   hipStream_t st[kNumStreams] = {};
@@ -221,6 +223,7 @@ struct pipo_ctx {
   int64_t seg_off[kNumSegs] = {};
   int64_t seg_bytes[kNumSegs] = {};
   int64_t layer_bytes = 0, head_bytes = 0, slot_bytes = 0, misc_bytes = 0;
+  int64_t misc_off[kNumMisc] = {}, misc_count[kNumMisc] = {};
 
   // host side
   std::vector<std::vector<const void*>> layer_src;  // [L][seg] host pointer
@@ -243,7 +246,9 @@ struct pipo_ctx {
   char* slots = nullptr;
   char* resident = nullptr;
   uint16_t* tok_dev = nullptr;
+  uint16_t* head_dev = nullptr;  // untied output head, when resident
   uint16_t* pos_dev = nullptr;
+  float* rope_dev = nullptr;     // rotary (cos, sin) table [max_seq][dh/2][2]
   uint16_t* lnf_g = nullptr;
   uint16_t* lnf_b = nullptr;
   float* x = nullptr;
@@ -251,6 +256,7 @@ struct pipo_ctx {
   uint16_t* q = nullptr;
   uint16_t* o = nullptr;
   uint16_t* h = nullptr;
+  uint16_t* gu = nullptr;        // SwiGLU gate and up outputs [rows][2F]
   float* logits = nullptr;
   int32_t* next_dev = nullptr;
   int32_t* ids_dev = nullptr;
@@ -261,7 +267,7 @@ struct pipo_ctx {
   int64_t gemm_ws_bytes = 0;
   char* kv = nullptr;          // resident cache or KV slots
   bool kv4 = false;            // INT4 cache rows (PIPO_KV_INT4_G64)
-  int64_t kv_row = 0;          // bytes of one cached key (value) row: 2 d, or 9 d / 16
+  int64_t kv_row = 0;          // bytes of one cached key (value) row: 2 dkv, or 9 dkv / 16
   int64_t kv_part_bytes = 0;   // max_seq * max_batch * kv_row
   uint16_t* kst = nullptr;     // INT4 cache: fp16 staging of new (decode) or all
   uint16_t* vst = nullptr;     //   (prefill attention) key and value rows
@@ -338,6 +344,11 @@ static const uint16_t* misc_ptr(const char* base, const pipo_ctx* c) {
   return reinterpret_cast<const uint16_t*>(base + c->seg_off[kSegMisc]);
 }
 
+// one small tensor of the packed block, or null where the family has none
+static const uint16_t* misc_tensor(const uint16_t* misc, const pipo_ctx* c, int which) {
+  return misc && c->misc_count[which] > 0 ? misc + c->misc_off[which] : nullptr;
+}
+
 static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
   hipStream_t s = c->st[kCompute];
   const PassInfo& p = c->pass;
@@ -352,10 +363,11 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
     } else if (j >= 0) {
       base = c->resident + (int64_t)j * c->layer_bytes;
     } else {
-      base = reinterpret_cast<const char*>(c->tok_dev);
+      base = reinterpret_cast<const char*>(c->llama ? c->head_dev : c->tok_dev);
     }
   }
-  const uint16_t* misc = base ? misc_ptr(base, c) : nullptr;
+  const uint16_t* misc = base && j >= 0 ? misc_ptr(base, c) : nullptr;
+  const auto small = [&](int which) { return misc_tensor(misc, c, which); };
   // KV cache of layer j (fp16 or INT4 rows, position-major)
   char *kc = nullptr, *vc = nullptr;
   if (j >= 0) {
@@ -386,7 +398,7 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
                                     hipMemcpyHostToDevice, s));
         c->stats.n_copies++;
         return launch_embed(c->emb_dev, nullptr, nullptr, c->pos_dev, c->x, rows, d, p.T, p.pos0,
-                            c->sh.pos_offset, s);
+                            c->sh.pos_offset, s);  // pos_dev is null for LLaMA
       }
       PIPO_HIP_TRY(hipMemcpyAsync(c->ids_dev, c->ids_stage, (size_t)(rows * 4),
                                   hipMemcpyHostToDevice, s));
@@ -395,72 +407,89 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
                           c->sh.pos_offset, s);
     }
     case kLn1:
-      return launch_layernorm(c->x, misc, misc + d, c->a, rows, d, 1, 0, c->sh.ln_eps, s);
+      if (c->llama)
+        return launch_rmsnorm(c->x, small(kLn1G), c->a, rows, d, 1, 0, c->sh.ln_eps, s);
+      return launch_layernorm(c->x, small(kLn1G), small(kLn1B), c->a, rows, d, 1, 0,
+                              c->sh.ln_eps, s);
     case kQkv: {
       GemmArgs ga;
       ga.q_out = c->q;
       ga.d = d;
-      ga.q_scale = 1.0f / std::sqrt((float)c->dh);
+      ga.dkv = c->dkv;
+      // OPT scales q in the epilogue; LLaMA scales it with the rotation
+      const float q_scale = 1.0f / std::sqrt((float)c->dh);
+      ga.q_scale = c->llama ? 1.f : q_scale;
       ga.rows_per_seq = p.T;
       ga.batch = c->b;
-      if (!c->kv4) {
-        ga.k_out = reinterpret_cast<uint16_t*>(kc);
-        ga.v_out = reinterpret_cast<uint16_t*>(vc);
-        ga.pos0 = p.pos0;
-        return gemm(kSegWqkv, c->a, misc + 2 * d, rows, 3 * d, d, EPI_QKV, ga);
-      }
-      // INT4 cache: the new rows go to fp16 staging (position-major from the
-      // pass's first position) and are quantized into the cache at pos0
-      ga.k_out = c->kst;
-      ga.v_out = c->vst;
-      ga.pos0 = 0;
-      PIPO_TRY(gemm(kSegWqkv, c->a, misc + 2 * d, rows, 3 * d, d, EPI_QKV, ga));
+      // fp16 cache: k and v rows go straight to the cache at pos0.  INT4
+      // cache: they go to fp16 staging (position-major from the pass's first
+      // position) and are quantized into the cache at pos0.
+      ga.k_out = c->kv4 ? c->kst : reinterpret_cast<uint16_t*>(kc);
+      ga.v_out = c->kv4 ? c->vst : reinterpret_cast<uint16_t*>(vc);
+      ga.pos0 = c->kv4 ? 0 : p.pos0;
+      PIPO_TRY(gemm(kSegWqkv, c->a, small(kBqkv), rows, d + 2 * c->dkv, d, EPI_QKV, ga));
+      if (c->llama)  // rotary positions on q and on the new keys, where they were written
+        PIPO_TRY(launch_rope(c->q, ga.k_out, c->rope_dev, rows, p.T, p.pos0, ga.pos0, c->b,
+                             (int)c->H, (int)c->Hkv, (int)c->dh, q_scale, s));
+      if (!c->kv4) return PIPO_OK;
       const int64_t at = p.pos0 * c->b * c->kv_row;
-      PIPO_TRY(launch_kv_quant(c->kst, reinterpret_cast<uint8_t*>(kc + at), rows, d, s));
-      return launch_kv_quant(c->vst, reinterpret_cast<uint8_t*>(vc + at), rows, d, s);
+      PIPO_TRY(launch_kv_quant(c->kst, reinterpret_cast<uint8_t*>(kc + at), rows, c->dkv, s));
+      return launch_kv_quant(c->vst, reinterpret_cast<uint8_t*>(vc + at), rows, c->dkv, s);
     }
     case kAttn:
       if (p.prefill) {
         if (!c->kv4)
           return launch_attn_prefill(c->q, reinterpret_cast<const uint16_t*>(kc),
                                      reinterpret_cast<const uint16_t*>(vc), c->o, c->b, (int)p.T,
-                                     (int)c->H, (int)c->dh, s);
+                                     (int)c->H, (int)c->Hkv, (int)c->dh, s);
         // INT4 cache: attention reads the cache, expanded to fp16 staging
-        PIPO_TRY(launch_kv_dequant(reinterpret_cast<const uint8_t*>(kc), c->kst, rows, d, s));
-        PIPO_TRY(launch_kv_dequant(reinterpret_cast<const uint8_t*>(vc), c->vst, rows, d, s));
+        PIPO_TRY(
+            launch_kv_dequant(reinterpret_cast<const uint8_t*>(kc), c->kst, rows, c->dkv, s));
+        PIPO_TRY(
+            launch_kv_dequant(reinterpret_cast<const uint8_t*>(vc), c->vst, rows, c->dkv, s));
         return launch_attn_prefill(c->q, c->kst, c->vst, c->o, c->b, (int)p.T, (int)c->H,
-                                   (int)c->dh, s);
+                                   (int)c->Hkv, (int)c->dh, s);
       }
-      return launch_attn_decode(c->q, kc, vc, c->o, c->b, (int)c->H, (int)c->dh, (int)p.pos0,
-                                c->kv4, c->attn_ws, c->attn_ws_bytes, s);
+      return launch_attn_decode(c->q, kc, vc, c->o, c->b, (int)c->H, (int)c->Hkv, (int)c->dh,
+                                (int)p.pos0, c->kv4, c->attn_ws, c->attn_ws_bytes, s);
     case kOproj: {
       GemmArgs ga;
       ga.out32 = c->x;
       ga.ldo = d;
-      return gemm(kSegWo, c->o, misc + 5 * d, rows, d, d, EPI_ADD_F32, ga);
+      return gemm(kSegWo, c->o, small(kBo), rows, d, d, EPI_ADD_F32, ga);
     }
     case kLn2:
-      return launch_layernorm(c->x, misc + 6 * d, misc + 7 * d, c->a, rows, d, 1, 0, c->sh.ln_eps,
-                              s);
+      if (c->llama)
+        return launch_rmsnorm(c->x, small(kLn2G), c->a, rows, d, 1, 0, c->sh.ln_eps, s);
+      return launch_layernorm(c->x, small(kLn2G), small(kLn2B), c->a, rows, d, 1, 0,
+                              c->sh.ln_eps, s);
     case kFc1: {
       GemmArgs ga;
+      if (c->llama) {  // gate and up in one GEMM, then the SwiGLU gate
+        ga.out16 = c->gu;
+        ga.ldo = 2 * F;
+        PIPO_TRY(gemm(kSegW1, c->a, nullptr, rows, 2 * F, d, EPI_F16, ga));
+        return launch_swiglu(c->gu, c->h, rows, F, s);
+      }
       ga.out16 = c->h;
       ga.ldo = F;
-      return gemm(kSegW1, c->a, misc + 8 * d, rows, F, d, EPI_RELU_F16, ga);
+      return gemm(kSegW1, c->a, small(kB1), rows, F, d, EPI_RELU_F16, ga);
     }
     case kFc2: {
       GemmArgs ga;
       ga.out32 = c->x;
       ga.ldo = d;
-      return gemm(kSegW2, c->h, misc + 8 * d + F, rows, d, F, EPI_ADD_F32, ga);
+      return gemm(kSegW2, c->h, small(kB2), rows, d, F, EPI_ADD_F32, ga);
     }
     case kLnf:
+      if (c->llama)
+        return launch_rmsnorm(c->x, c->lnf_g, c->a, c->b, d, p.T, p.T - 1, c->sh.ln_eps, s);
       return launch_layernorm(c->x, c->lnf_g, c->lnf_b, c->a, c->b, d, p.T, p.T - 1, c->sh.ln_eps,
                               s);
     case kHead: {
       GemmArgs ga;
       ga.X = c->a;
-      ga.W = reinterpret_cast<const uint16_t*>(base);  // slot offset 0, or the resident table
+      ga.W = reinterpret_cast<const uint16_t*>(base);  // slot offset 0, or the resident head
       ga.M = c->b;
       ga.N = c->V;
       ga.K = d;
@@ -480,28 +509,41 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
 static void kernel_cost(const pipo_ctx* c, const Op& op, double* bytes, double* flops) {
   const PassInfo& p = c->pass;
   const double rows = (double)c->b * p.T, d = (double)c->d, F = (double)c->F, V = (double)c->V;
+  const double dkv = (double)c->dkv;
   const auto wbytes = [&](double N, double K) { return c->w4 ? N * K / 2 + N * K / 16 : N * K * 2; };
+  // weights once, X once, Y once (bias only where the family has one)
   const auto g = [&](double M, double N, double K, double out_bytes, double wb) {
-    *bytes = wb + M * K * 2 + M * N * out_bytes + N * 2;
+    *bytes = wb + M * K * 2 + M * N * out_bytes + (c->llama ? 0 : N * 2);
     *flops = 2 * M * N * K;
   };
   *bytes = 0;
   *flops = 0;
   switch (op.kernel) {
-    case kQkv:
-      g(rows, 3 * d, d, 2, wbytes(3 * d, d));
-      if (c->kv4) *bytes += 2 * rows * (d * 4 + c->kv_row);  // staging write, read, INT4 write
+    case kQkv: {
+      const double N = d + 2 * dkv;
+      g(rows, N, d, 2, wbytes(N, d));
+      if (c->llama) *bytes += rows * (d + dkv) * 4;            // rotation: read and write q, k
+      if (c->kv4) *bytes += 2 * rows * (dkv * 4 + c->kv_row);  // staging write, read, INT4 write
       break;
+    }
     case kOproj: g(rows, d, d, 8, wbytes(d, d)); break;
-    case kFc1: g(rows, F, d, 2, wbytes(F, d)); break;
+    case kFc1:
+      if (c->llama) {
+        g(rows, 2 * F, d, 2, wbytes(2 * F, d));
+        *bytes += rows * F * 6;  // SwiGLU: read gate and up, write h
+      } else {
+        g(rows, F, d, 2, wbytes(F, d));
+      }
+      break;
     case kFc2: g(rows, d, F, 8, wbytes(d, F)); break;
     case kHead: g(c->b, V, d, 4, V * d * 2); break;
     case kLn1:
     case kLn2: *bytes = rows * d * 6 + d * 4; *flops = rows * d * 8; break;
     case kLnf: *bytes = c->b * d * 6 + d * 4; *flops = c->b * d * 8; break;
     case kAttn:
+      // K and V once (per key/value head), q and o once
       if (p.prefill) {
-        *bytes = 4 * rows * d * 2 + (c->kv4 ? 2 * rows * (c->kv_row + d * 2) : 0);
+        *bytes = 2 * rows * (d + dkv) * 2 + (c->kv4 ? 2 * rows * (c->kv_row + dkv * 2) : 0);
         *flops = 4.0 * c->b * p.T * (p.T + 1) / 2 * d;
       } else {
         *bytes = 2.0 * c->b * (p.pos0 + 1) * c->kv_row + 2 * rows * d * 2;
@@ -724,7 +766,9 @@ static void destroy_ctx(pipo_ctx* c) {
 static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* w,
                               const pipo_policy* policy, pipo_ctx* c) {
   PIPO_TRY(check_shape(shape));
-  if (!w || !policy || !w->tok_emb || !w->pos_emb || !w->lnf_g || !w->lnf_b || !w->layers) {
+  const bool llama = is_llama(*shape);
+  if (!w || !policy || !w->tok_emb || !w->lnf_g || !w->layers ||
+      (llama ? !w->lm_head : (!w->pos_emb || !w->lnf_b))) {
     set_error("weights or policy incomplete");
     return PIPO_ERR_ARG;
   }
@@ -740,6 +784,9 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   c->L = shape->n_layers;
   c->H = shape->n_heads;
   c->dh = c->d / c->H;
+  c->Hkv = kv_heads(*shape);
+  c->dkv = kv_width(*shape);
+  c->llama = llama;
   c->timestamps = (pol.debug_flags & PIPO_DBG_TIMESTAMPS) != 0;
   PIPO_HIP_TRY(hipGetDevice(&c->device));
   const int64_t d = c->d, F = c->F, V = c->V, L = c->L;
@@ -752,6 +799,10 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
     c->seg_off[sg] = ul.seg_off[sg];
   }
   c->misc_bytes = ul.misc_bytes;
+  for (int i = 0; i < kNumMisc; ++i) {
+    c->misc_off[i] = ul.misc_off[i];
+    c->misc_count[i] = ul.misc_count[i];
+  }
   c->layer_bytes = ul.layer_bytes;
   c->head_bytes = ul.head_bytes;
   c->slot_bytes = hp.slot_bytes;
@@ -765,16 +816,16 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   PIPO_TRY(pin_alloc(c, &misc_all, L * c->misc_bytes));
   for (int64_t j = 0; j < L; ++j) {
     const pipo_layer_host& lw = w->layers[j];
-    const uint16_t* small[8] = {lw.ln1_g, lw.ln1_b, lw.bqkv, lw.bo, lw.ln2_g, lw.ln2_b, lw.b1, lw.b2};
-    const int64_t cnt[8] = {d, d, 3 * d, d, d, d, F, d};
-    char* dst = (char*)misc_all + j * c->misc_bytes;
-    for (int i = 0; i < 8; ++i) {
+    const uint16_t* small[kNumMisc] = {lw.ln1_g, lw.ln1_b, lw.bqkv, lw.bo,
+                                       lw.ln2_g, lw.ln2_b, lw.b1,   lw.b2};
+    uint16_t* dst = reinterpret_cast<uint16_t*>((char*)misc_all + j * c->misc_bytes);
+    for (int i = 0; i < kNumMisc; ++i) {
+      if (c->misc_count[i] == 0) continue;  // not part of this family
       if (!small[i]) {
         set_error("layer %lld: small tensor %d is NULL", (long long)j, i);
         return PIPO_ERR_ARG;
       }
-      std::memcpy(dst, small[i], (size_t)cnt[i] * 2);
-      dst += cnt[i] * 2;
+      std::memcpy(dst + c->misc_off[i], small[i], (size_t)c->misc_count[i] * 2);
     }
     c->layer_src[j][kSegMisc] = (char*)misc_all + j * c->misc_bytes;
     const void* mats[8];
@@ -818,11 +869,12 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
     }
   }
   c->tok_host = w->tok_emb;
-  c->head_src = w->tok_emb;
-  if (pol.embed_on_host && !is_registered_pinned(w->tok_emb, (size_t)c->head_bytes)) {
+  const uint16_t* head_host = llama ? w->lm_head : w->tok_emb;  // OPT ties the head
+  c->head_src = head_host;
+  if (pol.embed_on_host && !is_registered_pinned(head_host, (size_t)c->head_bytes)) {
     void* t = nullptr;
     PIPO_TRY(pin_alloc(c, &t, c->head_bytes));
-    par_memcpy(t, w->tok_emb, (size_t)c->head_bytes);
+    par_memcpy(t, head_host, (size_t)c->head_bytes);
     c->head_src = t;
   }
 
@@ -866,14 +918,30 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
     c->tok_dev = (uint16_t*)p;
     PIPO_HIP_TRY(hipMemcpy(c->tok_dev, w->tok_emb, (size_t)c->head_bytes, hipMemcpyHostToDevice));
   }
-  PIPO_TRY(dev_alloc(c, &p, hp.pos));
-  c->pos_dev = (uint16_t*)p;
-  PIPO_HIP_TRY(hipMemcpy(c->pos_dev, w->pos_emb, (size_t)hp.pos, hipMemcpyHostToDevice));
+  if (hp.head > 0) {
+    PIPO_TRY(dev_alloc(c, &p, hp.head));
+    c->head_dev = (uint16_t*)p;
+    PIPO_HIP_TRY(
+        hipMemcpy(c->head_dev, w->lm_head, (size_t)c->head_bytes, hipMemcpyHostToDevice));
+  }
+  if (hp.pos > 0) {
+    PIPO_TRY(dev_alloc(c, &p, hp.pos));
+    c->pos_dev = (uint16_t*)p;
+    PIPO_HIP_TRY(hipMemcpy(c->pos_dev, w->pos_emb, (size_t)hp.pos, hipMemcpyHostToDevice));
+  }
+  if (hp.rope > 0) {
+    PIPO_TRY(dev_alloc(c, &p, hp.rope));
+    c->rope_dev = (float*)p;
+    std::vector<float> table((size_t)(hp.rope / 4));
+    rope_table(*shape, pol.max_seq, table.data());
+    PIPO_HIP_TRY(hipMemcpy(c->rope_dev, table.data(), (size_t)hp.rope, hipMemcpyHostToDevice));
+  }
   PIPO_TRY(dev_alloc(c, &p, hp.lnf));
   c->lnf_g = (uint16_t*)p;
   c->lnf_b = c->lnf_g + d;
   PIPO_HIP_TRY(hipMemcpy(c->lnf_g, w->lnf_g, (size_t)d * 2, hipMemcpyHostToDevice));
-  PIPO_HIP_TRY(hipMemcpy(c->lnf_b, w->lnf_b, (size_t)d * 2, hipMemcpyHostToDevice));
+  if (!llama)
+    PIPO_HIP_TRY(hipMemcpy(c->lnf_b, w->lnf_b, (size_t)d * 2, hipMemcpyHostToDevice));
   PIPO_TRY(dev_alloc(c, &p, hp.x));
   c->x = (float*)p;
   PIPO_TRY(dev_alloc(c, &p, hp.a));
@@ -884,6 +952,10 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   c->o = (uint16_t*)p;
   PIPO_TRY(dev_alloc(c, &p, hp.h));
   c->h = (uint16_t*)p;
+  if (hp.gu > 0) {
+    PIPO_TRY(dev_alloc(c, &p, hp.gu));
+    c->gu = (uint16_t*)p;
+  }
   PIPO_TRY(dev_alloc(c, &p, hp.logits));
   c->logits = (float*)p;
   PIPO_TRY(dev_alloc(c, &p, hp.next));

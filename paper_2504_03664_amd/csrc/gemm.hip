@@ -44,10 +44,10 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int64_t m, int64_t n
     const int64_t crow = pos * a.batch + seq;
     if (n < a.d) {
       a.q_out[m * a.d + n] = f2h(v * a.q_scale);
-    } else if (n < 2 * a.d) {
-      a.k_out[crow * a.d + (n - a.d)] = f2h(v);
+    } else if (n < a.d + a.dkv) {
+      a.k_out[crow * a.dkv + (n - a.d)] = f2h(v);
     } else {
-      a.v_out[crow * a.d + (n - 2 * a.d)] = f2h(v);
+      a.v_out[crow * a.dkv + (n - a.d - a.dkv)] = f2h(v);
     }
   }
 }
@@ -631,6 +631,11 @@ pipo_status launch_gemm(const GemmArgs& a, bool w4, int epi, float* workspace,
   }
   if (a.X == nullptr || (w4 ? (a.Wq == nullptr || a.Wsm == nullptr) : a.W == nullptr)) {
     set_error("gemm: null operand");
+    return PIPO_ERR_ARG;
+  }
+  if (epi == EPI_QKV && (a.dkv <= 0 || a.N != a.d + 2 * a.dkv)) {
+    set_error("gemm: QKV output of %lld columns for d=%lld dkv=%lld", (long long)a.N,
+              (long long)a.d, (long long)a.dkv);
     return PIPO_ERR_ARG;
   }
   return w4 ? launch_fmt<true>(a, epi, workspace, workspace_bytes, st)

@@ -119,7 +119,7 @@ pipo_status pipo_op_attn_decode(const uint16_t* q, const uint16_t* kc, const uin
     set_error("attn_decode: NULL pointer or negative workspace size");
     return PIPO_ERR_ARG;
   }
-  return launch_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, false,
+  return launch_attn_decode(q, kc, vc, o, b, n_heads, n_heads, head_dim, t, false,
                             static_cast<float*>(workspace), workspace_bytes,
                             static_cast<hipStream_t>(stream));
 }
@@ -133,7 +133,7 @@ pipo_status pipo_op_attn_decode_kv4(const uint16_t* q, const uint8_t* kc, const 
     set_error("attn_decode_kv4: NULL pointer or negative workspace size");
     return PIPO_ERR_ARG;
   }
-  return launch_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, true,
+  return launch_attn_decode(q, kc, vc, o, b, n_heads, n_heads, head_dim, t, true,
                             static_cast<float*>(workspace), workspace_bytes,
                             static_cast<hipStream_t>(stream));
 }
@@ -172,8 +172,87 @@ pipo_status pipo_op_attn_prefill(const uint16_t* q, const uint16_t* kc, const ui
     set_error("attn_prefill: NULL pointer");
     return PIPO_ERR_ARG;
   }
-  return launch_attn_prefill(q, kc, vc, o, b, P, n_heads, head_dim,
+  return launch_attn_prefill(q, kc, vc, o, b, P, n_heads, n_heads, head_dim,
                              static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_attn_decode_gqa(const uint16_t* q, const void* kc, const void* vc,
+                                    uint16_t* o, int32_t b, int32_t n_heads, int32_t n_kv_heads,
+                                    int32_t head_dim, int32_t t, int32_t kv_fmt, void* workspace,
+                                    int64_t workspace_bytes, void* stream) {
+  clear_error();
+  if (!q || !kc || !vc || !o || workspace_bytes < 0 ||
+      (kv_fmt != PIPO_KV_FP16 && kv_fmt != PIPO_KV_INT4_G64)) {
+    set_error("attn_decode_gqa: NULL pointer, negative workspace size or unknown kv_fmt");
+    return PIPO_ERR_ARG;
+  }
+  return launch_attn_decode(q, kc, vc, o, b, n_heads, n_kv_heads, head_dim, t,
+                            kv_fmt == PIPO_KV_INT4_G64, static_cast<float*>(workspace),
+                            workspace_bytes, static_cast<hipStream_t>(stream));
+}
+
+int64_t pipo_op_attn_decode_gqa_workspace_bytes(int32_t b, int32_t n_heads, int32_t n_kv_heads,
+                                                int32_t head_dim, int32_t t) {
+  if (b < 1 || n_heads < 1 || n_kv_heads < 1 || t < 0 || head_dim < 1) return 0;
+  return attn_decode_workspace_bytes(b, n_heads, head_dim, attn_decode_splits(b, n_kv_heads, t));
+}
+
+pipo_status pipo_op_attn_prefill_gqa(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                                     uint16_t* o, int32_t b, int32_t P, int32_t n_heads,
+                                     int32_t n_kv_heads, int32_t head_dim, void* stream) {
+  clear_error();
+  if (!q || !kc || !vc || !o) {
+    set_error("attn_prefill_gqa: NULL pointer");
+    return PIPO_ERR_ARG;
+  }
+  return launch_attn_prefill(q, kc, vc, o, b, P, n_heads, n_kv_heads, head_dim,
+                             static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_rmsnorm(const float* x, const uint16_t* gamma, uint16_t* y, int64_t rows,
+                            int64_t d, int64_t src_stride, int64_t src_offset, float eps,
+                            void* stream) {
+  clear_error();
+  if (!x || !gamma || !y || src_stride < 1 || src_offset < 0 || src_offset >= src_stride) {
+    set_error("rmsnorm: bad arguments");
+    return PIPO_ERR_ARG;
+  }
+  return launch_rmsnorm(x, gamma, y, rows, d, src_stride, src_offset, eps,
+                        static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_rope(uint16_t* q, uint16_t* k, const float* cos_sin, int64_t M,
+                         int64_t rows_per_seq, int64_t pos0, int64_t kpos0, int64_t batch,
+                         int32_t n_heads, int32_t n_kv_heads, int32_t head_dim, float q_scale,
+                         void* stream) {
+  clear_error();
+  if (!q || !k || !cos_sin) {
+    set_error("rope: NULL pointer");
+    return PIPO_ERR_ARG;
+  }
+  return launch_rope(q, k, cos_sin, M, rows_per_seq, pos0, kpos0, batch, n_heads, n_kv_heads,
+                     head_dim, q_scale, static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_swiglu(const uint16_t* gu, uint16_t* h, int64_t M, int64_t F, void* stream) {
+  clear_error();
+  if (!gu || !h) {
+    set_error("swiglu: NULL pointer");
+    return PIPO_ERR_ARG;
+  }
+  return launch_swiglu(gu, h, M, F, static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_embed(const int32_t* ids, const uint16_t* tok_table, const uint16_t* pos_table,
+                          float* x, int64_t rows, int64_t d, int64_t rows_per_seq, int64_t pos0,
+                          int64_t pos_offset, void* stream) {
+  clear_error();
+  if (!ids || !tok_table || !x || rows_per_seq < 1 || pos0 < 0 || pos_offset < 0) {
+    set_error("embed: bad arguments");
+    return PIPO_ERR_ARG;
+  }
+  return launch_embed(nullptr, ids, tok_table, pos_table, x, rows, d, rows_per_seq, pos0,
+                      pos_offset, static_cast<hipStream_t>(stream));
 }
 
 pipo_status pipo_op_argmax(const float* logits, int32_t* next, int64_t rows, int64_t V,

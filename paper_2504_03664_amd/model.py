@@ -5,8 +5,8 @@ pipo_decode_step.  Nothing here computes any part of the decoder.
 Host layout (data merging, Section 3.3 of the paper): each layer's four
 matrices -- fp16, or INT4 codes each followed by its (scale, min) pairs --
 share one pinned region at 4 KiB-aligned offsets, so the copy engine streams
-them without staging; the token table (also the output head) has a pinned
-region of its own.
+them without staging; the output head (the token table for OPT, the untied
+head for LLaMA) has a pinned region of its own.
 """
 from __future__ import annotations
 
@@ -31,21 +31,26 @@ def _pinned_view(ptr: int, nbytes: int) -> np.ndarray:
 
 class HostWeights:
     """Decoder weights in host memory, filled by a provider with
-    ``fill(layer, name, out)`` (fp16 tensors, layer -1 for embeddings and
-    the final LayerNorm) and ``fill_int4(layer, name, q, sm)``.
+    ``layer_shapes()`` (the tensors of one layer and their shapes),
+    ``fill(layer, name, out)`` (fp16 tensors, layer -1 for embeddings, the
+    head and the final norm) and ``fill_int4(layer, name, q, sm)``.  The
+    shape's ``family`` ("opt" or "llama") says which tensors exist.
 
     ``pinned_matrices`` puts the layer matrices in pipo_host_alloc memory
-    (streamed in place); ``pinned_head`` does the same for the token table.
+    (streamed in place); ``pinned_head`` does the same for the output head.
     """
 
     def __init__(self, shape, wfmt: str, provider, pinned_matrices: bool = True,
                  pinned_head: bool = True):
         assert wfmt in ("fp16", "int4")
         self.shape, self.wfmt = shape, wfmt
-        d, F, V, L = shape.d_model, shape.d_ffn, shape.vocab, shape.n_layers
+        d, V, L = shape.d_model, shape.vocab, shape.n_layers
+        self.llama = getattr(shape, "family", "opt") == "llama"
         self._pinned: List[int] = []
         self._keep: List[object] = []
-        dims = {"wqkv": (3 * d, d), "wo": (d, d), "w1": (F, d), "w2": (d, F)}
+        layer_shapes = provider.layer_shapes()
+        dims = {nm: layer_shapes[nm] for nm in MATRIX_SHAPES}
+        small = {nm: layer_shapes[nm][0] for nm in SMALL if nm in layer_shapes}
         self.layers: List[Dict[str, object]] = []
         c_layers = (B.PipoLayerHost * L)()
         for j in range(L):
@@ -85,13 +90,11 @@ class HostWeights:
                     provider.fill(j, nm, mats[nm])
                 else:
                     provider.fill_int4(j, nm, mats[nm][0], mats[nm][1])
-            small = {"ln1_g": d, "ln1_b": d, "bqkv": 3 * d, "bo": d, "ln2_g": d, "ln2_b": d,
-                     "b1": F, "b2": d}
             for nm, n in small.items():
                 mats[nm] = provider.fill(j, nm, np.empty(n, np.float16))
             self.layers.append(mats)
             cl = c_layers[j]
-            for nm in SMALL:
+            for nm in small:
                 setattr(cl, nm, mats[nm].ctypes.data)
             for nm, qn in zip(MATRIX_SHAPES, ("qqkv", "qo", "q1", "q2")):
                 if wfmt == "fp16":
@@ -101,25 +104,39 @@ class HostWeights:
                     q4.q = mats[nm][0].ctypes.data
                     q4.scale_min = mats[nm][1].ctypes.data
         self.c_layers = c_layers
-        if pinned_head:
+
+        def table(pinned: bool) -> np.ndarray:
+            if not pinned:
+                return np.empty((V, d), np.float16)
             ptr = B.pipo_host_alloc(V * d * 2)
             self._pinned.append(ptr)
-            self.tok_emb = _pinned_view(ptr, V * d * 2).view(np.float16).reshape(V, d)
-        else:
-            self.tok_emb = np.empty((V, d), np.float16)
-        provider.fill(-1, "tok_emb", self.tok_emb)
-        self.pos_emb = provider.fill(-1, "pos_emb",
-                                     np.empty((shape.max_pos + shape.pos_offset, d), np.float16))
+            return _pinned_view(ptr, V * d * 2).view(np.float16).reshape(V, d)
+
+        # the streamed output head gets the pinned region: the token table
+        # (tied) for OPT, the untied head for LLaMA
+        self.tok_emb = provider.fill(-1, "tok_emb", table(pinned_head and not self.llama))
         self.lnf_g = provider.fill(-1, "lnf_g", np.empty(d, np.float16))
-        self.lnf_b = provider.fill(-1, "lnf_b", np.empty(d, np.float16))
-        self.c_weights = B.PipoHostWeights(self.tok_emb.ctypes.data, self.pos_emb.ctypes.data,
-                                           self.lnf_g.ctypes.data, self.lnf_b.ctypes.data,
-                                           ctypes.cast(c_layers, ctypes.POINTER(B.PipoLayerHost)))
+        if self.llama:
+            self.lm_head = provider.fill(-1, "lm_head", table(pinned_head))
+            self.pos_emb = self.lnf_b = None
+        else:
+            self.lm_head = None
+            self.pos_emb = provider.fill(
+                -1, "pos_emb", np.empty((shape.max_pos + shape.pos_offset, d), np.float16))
+            self.lnf_b = provider.fill(-1, "lnf_b", np.empty(d, np.float16))
+
+        def addr(a: Optional[np.ndarray]) -> Optional[int]:
+            return None if a is None else a.ctypes.data
+
+        self.c_weights = B.PipoHostWeights(addr(self.tok_emb), addr(self.pos_emb),
+                                           addr(self.lnf_g), addr(self.lnf_b),
+                                           ctypes.cast(c_layers, ctypes.POINTER(B.PipoLayerHost)),
+                                           addr(self.lm_head))
 
     def free(self):
         """Release the pinned regions (after every context using them is destroyed)."""
         self.layers = []
-        self.tok_emb = None
+        self.tok_emb = self.lm_head = None
         for p in self._pinned:
             B.pipo_host_free(p)
         self._pinned = []
@@ -132,8 +149,18 @@ class HostWeights:
 
 
 def c_shape(shape) -> B.PipoShape:
-    return B.PipoShape(shape.n_layers, shape.d_model, shape.n_heads, shape.d_ffn, shape.vocab,
-                       shape.max_pos, shape.pos_offset, shape.ln_eps)
+    """The C shape of an OPTShape or LlamaShape."""
+    c = B.PipoShape(shape.n_layers, shape.d_model, shape.n_heads, shape.d_ffn, shape.vocab,
+                    shape.max_pos, shape.pos_offset, shape.ln_eps)
+    if getattr(shape, "family", "opt") == "llama":
+        c.family = B.PIPO_FAMILY_LLAMA
+        c.n_kv_heads = shape.n_kv_heads
+        c.rope_theta = shape.rope_theta
+        c.rope_factor = shape.rope_factor
+        c.rope_low_freq_factor = shape.rope_low_freq_factor
+        c.rope_high_freq_factor = shape.rope_high_freq_factor
+        c.rope_orig_max_pos = shape.rope_orig_max_pos
+    return c
 
 
 def c_policy(wfmt: str = "fp16", weights_on_host: bool = True, embed_on_host: bool = True,

@@ -240,15 +240,16 @@ class SyntheticOPT:
     fp16 tensors are returned as float16 arrays.  With ``wfmt == "int4"`` the
     four per-layer matrices come as ``{name: (q, sm)}`` int4 codes of the same
     fp16 draw; embeddings, LayerNorm parameters and biases stay fp16.
-    LayerNorm gamma is 1 and beta 0; biases are N(0, std) unless
+    LayerNorm gamma is 1 (or 1 + N(0, gain_std), rounded to fp16, so that
+    tests can tell the norms apart) and beta 0; biases are N(0, std) unless
     ``zero_bias``.
     """
 
     def __init__(self, shape: OPTShape, seed: int = DEFAULT_SEED, wfmt: str = "fp16",
-                 zero_bias: bool = False, std: float = WEIGHT_STD):
+                 zero_bias: bool = False, std: float = WEIGHT_STD, gain_std: float = 0.0):
         assert wfmt in ("fp16", "int4")
         self.shape, self.seed, self.wfmt = shape, seed, wfmt
-        self.zero_bias, self.std = zero_bias, std
+        self.zero_bias, self.std, self.gain_std = zero_bias, std, gain_std
 
     # shapes of every tensor of one layer
     def layer_shapes(self) -> Dict[str, tuple]:
@@ -260,7 +261,11 @@ class SyntheticOPT:
     def fill(self, layer: int, name: str, out: np.ndarray) -> np.ndarray:
         """Write fp16 tensor (layer, name) into ``out``."""
         if name.endswith("_g"):
-            out[...] = np.float16(1.0)
+            if self.gain_std > 0:
+                z = normal_f16(self.seed, tensor_key(layer, name), out.size, self.gain_std)
+                out[...] = (z.astype(np.float32) + 1).reshape(out.shape).astype(np.float16)
+            else:
+                out[...] = np.float16(1.0)
         elif name.endswith("_b") and name.startswith("ln"):
             out[...] = np.float16(0.0)
         elif name.startswith("b") and self.zero_bias:
@@ -309,8 +314,8 @@ class SyntheticLlama(SyntheticOPT):
     gate rows first), untied ``lm_head``; no position table."""
 
     def __init__(self, shape: "LlamaShape", seed: int = DEFAULT_SEED, wfmt: str = "fp16",
-                 std: float = WEIGHT_STD):
-        super().__init__(shape, seed=seed, wfmt=wfmt, zero_bias=True, std=std)
+                 std: float = WEIGHT_STD, gain_std: float = 0.0):
+        super().__init__(shape, seed=seed, wfmt=wfmt, zero_bias=True, std=std, gain_std=gain_std)
 
     def layer_shapes(self) -> Dict[str, tuple]:
         s = self.shape
@@ -334,3 +339,10 @@ class SyntheticLlama(SyntheticOPT):
 
     def lnf(self):
         return self.tensor(-1, "lnf_g"), None
+
+
+def synthetic_model(shape, seed: int = DEFAULT_SEED, wfmt: str = "fp16", **kw):
+    """The random-init weight provider of the shape's family."""
+    if getattr(shape, "family", "opt") == "llama":
+        return SyntheticLlama(shape, seed=seed, wfmt=wfmt, **kw)
+    return SyntheticOPT(shape, seed=seed, wfmt=wfmt, **kw)

@@ -261,6 +261,9 @@ class _BiasKV:
         L["wqkv"] = w
         return L
 
+    def layer_shapes(self):
+        return self.base.layer_shapes()
+
     def tok_emb(self):
         return self.base.tok_emb()
 

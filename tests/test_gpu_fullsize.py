@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 import synth
-from oracle import OracleDecoder
+from oracle import decoder_for
 from paper_2504_03664_amd.model import Decoder, HostWeights
 
 pytestmark = pytest.mark.gpu
@@ -47,8 +47,8 @@ def check_rows(model, prompt, toks, logits, rows, layers=None, kv_int4=False, to
     """Teacher-forced oracle logits for `rows` at every generated position;
     every argmax disagreement must be a near tie (gap <= tol * max |logit|)."""
     full = np.concatenate([prompt[rows], toks[rows, :-1]], axis=1)
-    ref = OracleDecoder(model, np.float32, kv_int4=kv_int4,
-                        fp16_operands=kv_int4).forward(full, layers=layers)
+    ref = decoder_for(model, np.float32, kv_int4=kv_int4,
+                      fp16_operands=kv_int4).forward(full, layers=layers)
     P = prompt.shape[1]
     worst, agree, total = 0.0, 0, 0
     for i, r in enumerate(rows):
@@ -88,6 +88,33 @@ def test_full_depth_sampled_rows(widx):
     worst, agree = check_rows(model, prompt, toks, logits, rows)
     log(f"  max normwise error {worst:.3e}, argmax agreement {agree:.4f}")
     assert worst <= REL_TOL and agree >= 0.99
+
+
+@pytest.mark.parametrize("widx", [6, 7])
+def test_llama8b_full_depth_sampled_rows(widx):
+    """LLaMA-3.1-8B shape (32 layers, d 4096, 32/8 heads, FFN 14336, vocab
+    128256) at full depth, fp16 batch 16 or INT4 batch 32, prompt 512, 32
+    tokens: GPU batch rows 0 and b-1 against the oracle at every position."""
+    wl = _workload(widx)
+    log(f"full size {wl.name}: drawing weights")
+    model = synth.SyntheticLlama(wl.shape, seed=synth.DEFAULT_SEED, wfmt=wl.wfmt)
+    hw = HostWeights(wl.shape, wl.wfmt, model)
+    try:
+        prompt = synth.prompt_tokens(wl.batch, wl.prompt, wl.shape.vocab, seed=1, stream=widx)
+        log("  GPU generation")
+        toks, logits = run_gpu(hw, wl, prompt, wl.gen)
+    finally:
+        hw.free()
+    rows = [0, wl.batch - 1]
+    log(f"  oracle on rows {rows} ({wl.shape.n_layers} layers)")
+    worst, agree = check_rows(model, prompt, toks, logits, rows)
+    log(f"  max normwise error {worst:.3e}, argmax agreement {agree:.4f}")
+    # At this shape the oracle's own two readings (fp32 activations, or
+    # fp16-rounded operands as the kernels hold them) differ by 6.2e-3
+    # normwise, and with 128256 random-weight logits the top two are as
+    # close as 3.7e-3 of the largest: argmax flips at near ties are expected
+    # (each one is checked to be a near tie above).
+    assert worst <= REL_TOL and agree >= 0.95
 
 
 def test_opt30b_layer_slice():
