@@ -74,7 +74,9 @@ enum {
   PIPO_DBG_POISON_SLOTS = 1,  /* fill a weight/KV slot with NaN before every refill */
   PIPO_DBG_COPY_DELAY = 2,    /* host-side sleep of copy_delay_us before every chunk copy */
   PIPO_DBG_TIMESTAMPS = 4,    /* record device timestamps of copies and kernels (stats) */
-  PIPO_DBG_KV_PAGEABLE = 8    /* keep the host KV cache in pageable memory (staged copies) */
+  PIPO_DBG_KV_PAGEABLE = 8,   /* keep the host KV cache in pageable memory (staged copies) */
+  PIPO_DBG_SEGMENT_COPIES = 16  /* copy each tensor of a layer on its own, even where the
+                                   layer's matrices could be copied as one merged range */
 };
 
 /* Model families (pipo_shape.family).

@@ -31,6 +31,10 @@ typedef struct {
   int64_t chunk_bytes;      /* > 0 */
   int64_t layer_seg_bytes[10]; /* bytes of the 10 segments of a layer unit (head entry unused) */
   int64_t head_bytes;
+  int32_t merged;           /* 0/1: copy a layer's matrix segments (1..8) as one byte range
+                               from segment 1's slot offset, in chunks that may span
+                               segments; segment 0 is copied alone */
+  int64_t layer_seg_off[10]; /* slot offsets of the segments (used when merged) */
 } pipo_sched_config;
 
 /*
@@ -42,7 +46,8 @@ typedef struct {
  * kind: 0 copy-h2d, 1 copy-d2h, 2 wait, 3 record, 4 kernel, 5 delay,
  *       6 poison, 7 readback;  stream: 0 compute, 1-2 h2d, 3 d2h;
  * kernel: 0 embed, 1 ln1, 2 qkv, 3 attn, 4 oproj, 5 ln2, 6 fc1, 7 fc2,
- *         8 lnf, 9 head, 10 argmax.
+ *         8 lnf, 9 head, 10 argmax.  A merged weight copy names segment 1;
+ * its off counts from that segment's slot offset.
  * Returns the number of bytes written (excluding the final NUL), or -1 if
  * the arguments are invalid or buf is too small.
  */

@@ -29,7 +29,7 @@ PIPO_FAMILY_OPT, PIPO_FAMILY_LLAMA = 0, 1
 PIPO_KV_FP16, PIPO_KV_INT4_G64 = 0, 1
 PIPO_PIPE_PERFORMANCE, PIPO_PIPE_MEMORY_EFFICIENT = 0, 1
 PIPO_DBG_POISON_SLOTS, PIPO_DBG_COPY_DELAY, PIPO_DBG_TIMESTAMPS = 1, 2, 4
-PIPO_DBG_KV_PAGEABLE = 8
+PIPO_DBG_KV_PAGEABLE, PIPO_DBG_SEGMENT_COPIES = 8, 16
 PIPO_EPI_F16, PIPO_EPI_RELU_F16, PIPO_EPI_ADD_F32, PIPO_EPI_F32 = 0, 1, 2, 3
 PIPO_MAX_KERNEL_STATS = 16
 
@@ -93,7 +93,8 @@ class PipoStats(ctypes.Structure):
 class PipoSchedConfig(ctypes.Structure):
     _fields_ = [("n_layers", i32), ("n_slots", i32), ("n_h2d", i32), ("layers_streamed", i32),
                 ("head_streamed", i32), ("kv_on_host", i32), ("poison", i32), ("delay", i32),
-                ("chunk_bytes", i64), ("layer_seg_bytes", i64 * 10), ("head_bytes", i64)]
+                ("chunk_bytes", i64), ("layer_seg_bytes", i64 * 10), ("head_bytes", i64),
+                ("merged", i32), ("layer_seg_off", i64 * 10)]
 
 
 class PipoError(RuntimeError):

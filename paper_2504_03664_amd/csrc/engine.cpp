@@ -887,8 +887,30 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   c->scfg.head_streamed = pol.embed_on_host != 0;
   c->scfg.kv_on_host = pol.kv_on_host != 0;
   c->scfg.chunk_bytes = pol.chunk_bytes;
-  for (int sg = 0; sg < kNumSegs; ++sg) c->scfg.layer_seg_bytes[sg] = c->seg_bytes[sg];
+  for (int sg = 0; sg < kNumSegs; ++sg) {
+    c->scfg.layer_seg_bytes[sg] = c->seg_bytes[sg];
+    c->scfg.layer_seg_off[sg] = c->seg_off[sg];
+  }
   c->scfg.layer_seg_bytes[kSegHead] = 0;
+  // merged copies when every layer's matrices sit in one pinned allocation
+  // at the slot's relative offsets (caller regions from pipo_host_alloc laid
+  // out that way, or the library's merged regions)
+  if (pol.weights_on_host && !(pol.debug_flags & PIPO_DBG_SEGMENT_COPIES)) {
+    int last = kSegWqkv;
+    for (int sg = kSegWqkv; sg < kSegHead; ++sg)
+      if (c->seg_bytes[sg] > 0) last = sg;
+    const int64_t span = c->seg_off[last] + c->seg_bytes[last] - c->seg_off[kSegWqkv];
+    bool merged = true;
+    for (int64_t j = 0; j < L && merged; ++j) {
+      const char* base = static_cast<const char*>(c->layer_src[j][kSegWqkv]);
+      for (int sg = kSegWqkv; sg < kSegHead; ++sg)
+        if (c->seg_bytes[sg] > 0 && static_cast<const char*>(c->layer_src[j][sg]) - base !=
+                                        c->seg_off[sg] - c->seg_off[kSegWqkv])
+          merged = false;
+      if (merged && !is_registered_pinned(base, (size_t)span)) merged = false;
+    }
+    c->scfg.merged = merged;
+  }
   c->scfg.head_bytes = c->head_bytes;
   c->scfg.poison = (pol.debug_flags & PIPO_DBG_POISON_SLOTS) != 0;
   c->scfg.delay = (pol.debug_flags & PIPO_DBG_COPY_DELAY) != 0;

@@ -24,6 +24,16 @@ extern "C" int64_t pipo_sched_trace(const pipo_sched_config* c, int32_t n_passes
   for (int i = 0; i < pipo::kNumSegs; ++i) sc.layer_seg_bytes[i] = c->layer_seg_bytes[i];
   sc.layer_seg_bytes[pipo::kSegHead] = 0;
   sc.head_bytes = c->head_bytes;
+  sc.merged = c->merged != 0;
+  for (int i = 0; i < pipo::kNumSegs; ++i) sc.layer_seg_off[i] = c->layer_seg_off[i];
+  if (sc.merged) {  // segments must follow each other in slot order without overlap
+    int64_t end = sc.layer_seg_off[pipo::kSegWqkv];
+    for (int i = pipo::kSegWqkv; i < pipo::kSegHead; ++i) {
+      if (sc.layer_seg_bytes[i] <= 0) continue;
+      if (sc.layer_seg_off[i] < end) return -1;
+      end = sc.layer_seg_off[i] + sc.layer_seg_bytes[i];
+    }
+  }
   sc.poison = c->poison != 0;
   sc.delay = c->delay != 0;
   pipo::Scheduler sched(sc);

@@ -55,25 +55,26 @@ void Scheduler::issue_weights(int64_t g, std::vector<Op>& out) {
     }
   }
   int chunk_no = 0;
-  for (int seg = 0; seg < kNumSegs; ++seg) {
-    const int64_t bytes = layer >= 0 ? (seg == kSegHead ? 0 : cfg_.layer_seg_bytes[seg])
-                                     : (seg == kSegHead ? cfg_.head_bytes : 0);
-    uint8_t& mask = seg_streams_[(size_t)s * kNumSegs + seg];
-    mask = 0;
-    if (bytes <= 0) continue;
-    for (int64_t off = 0; off < bytes; off += cfg_.chunk_bytes) {
-      const int st = chunk_no++ % n;
-      if (cfg_.delay) out.push_back(make(OpKind::Delay, kH2D0 + st));
-      Op c = make(OpKind::CopyH2D, kH2D0 + st);
-      c.unit = g;
-      c.layer = layer;
-      c.slot = s;
-      c.seg = seg;
-      c.off = off;
-      c.bytes = std::min(cfg_.chunk_bytes, bytes - off);
-      out.push_back(c);
-      mask |= (uint8_t)(1u << st);
-    }
+  const auto seg_bytes = [&](int seg) -> int64_t {
+    return layer >= 0 ? (seg == kSegHead ? 0 : cfg_.layer_seg_bytes[seg])
+                      : (seg == kSegHead ? cfg_.head_bytes : 0);
+  };
+  const auto copy = [&](int seg, int64_t off, int64_t bytes) {
+    const int st = chunk_no++ % n;
+    if (cfg_.delay) out.push_back(make(OpKind::Delay, kH2D0 + st));
+    Op c = make(OpKind::CopyH2D, kH2D0 + st);
+    c.unit = g;
+    c.layer = layer;
+    c.slot = s;
+    c.seg = seg;
+    c.off = off;
+    c.bytes = bytes;
+    out.push_back(c);
+    return st;
+  };
+  // ready events of a segment, on every stream that carried part of it
+  const auto record = [&](int seg) {
+    const uint8_t mask = seg_streams_[(size_t)s * kNumSegs + seg];
     for (int st = 0; st < n; ++st) {
       if (!(mask & (1u << st))) continue;
       Op r = make(OpKind::Record, kH2D0 + st);
@@ -82,6 +83,40 @@ void Scheduler::issue_weights(int64_t g, std::vector<Op>& out) {
       r.slot = s;
       r.seg = seg;
       out.push_back(r);
+    }
+  };
+  for (int seg = 0; seg < kNumSegs; ++seg) seg_streams_[(size_t)s * kNumSegs + seg] = 0;
+  const bool merged = cfg_.merged && layer >= 0;
+  for (int seg = 0; seg < kNumSegs; ++seg) {
+    if (merged && seg != kSegMisc) continue;
+    const int64_t bytes = seg_bytes(seg);
+    if (bytes <= 0) continue;
+    for (int64_t off = 0; off < bytes; off += cfg_.chunk_bytes)
+      seg_streams_[(size_t)s * kNumSegs + seg] |=
+          (uint8_t)(1u << copy(seg, off, std::min(cfg_.chunk_bytes, bytes - off)));
+    record(seg);
+  }
+  if (!merged) return;
+  // the matrix segments as one range from the first one's slot offset; a
+  // chunk marks every segment it overlaps, and a segment's ready events are
+  // recorded right after the chunk that holds its last byte
+  const int64_t base = cfg_.layer_seg_off[kSegWqkv];
+  int64_t end = 0;
+  for (int seg = kSegWqkv; seg < kSegHead; ++seg)
+    if (seg_bytes(seg) > 0) end = cfg_.layer_seg_off[seg] + seg_bytes(seg) - base;
+  int next_rec = kSegWqkv;
+  for (int64_t off = 0; off < end; off += cfg_.chunk_bytes) {
+    const int64_t len = std::min(cfg_.chunk_bytes, end - off);
+    const int st = copy(kSegWqkv, off, len);
+    for (int seg = kSegWqkv; seg < kSegHead; ++seg) {
+      const int64_t a = cfg_.layer_seg_off[seg] - base, b = a + seg_bytes(seg);
+      if (seg_bytes(seg) > 0 && a < off + len && b > off)
+        seg_streams_[(size_t)s * kNumSegs + seg] |= (uint8_t)(1u << st);
+    }
+    for (; next_rec < kSegHead; ++next_rec) {
+      if (seg_bytes(next_rec) <= 0) continue;
+      if (cfg_.layer_seg_off[next_rec] - base + seg_bytes(next_rec) > off + len) break;
+      record(next_rec);
     }
   }
 }

@@ -60,7 +60,8 @@ struct Op {
   int64_t unit = -1;   // unit instance g (-1: resident weights)
   int layer = -1;      // layer index, -1 for the head
   int slot = -1;       // weight/KV slot of the unit instance
-  int seg = -1;        // CopyH2D of weights: segment; KV copies: 0 = K, 1 = V
+  int seg = -1;        // CopyH2D of weights: segment (a merged copy names its first
+                       // segment, `off` may run past its end); KV copies: 0 = K, 1 = V
   bool kv = false;     // copy of KV-cache rows
   int64_t off = 0;     // byte offset inside the segment (weights) or KV part
   int64_t bytes = 0;
@@ -76,6 +77,12 @@ struct SchedConfig {
   int64_t chunk_bytes = 64ll << 20;
   int64_t layer_seg_bytes[kNumSegs] = {};  // bytes of each segment of a layer unit
   int64_t head_bytes = 0;
+  // merged copies: a layer's matrix segments sit in host memory at the same
+  // relative offsets as in the slot (layer_seg_off), so they are copied as
+  // one byte range in chunks that may span segments (fewer, larger copies;
+  // Section 3.3, data merging).  The small-tensor segment is copied alone.
+  bool merged = false;
+  int64_t layer_seg_off[kNumSegs] = {};
   bool poison = false;
   bool delay = false;
 };

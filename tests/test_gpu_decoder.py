@@ -101,12 +101,34 @@ def test_streamed_bit_identical_to_resident(opt125m):
              n_h2d_streams=2, chunk_bytes=1 << 21),
         dict(embed_on_host=False),
         dict(weights_on_host=False, embed_on_host=True),
+        # one copy per tensor instead of merged ranges spanning a layer's matrices
+        dict(debug_flags=B.PIPO_DBG_SEGMENT_COPIES),
+        dict(debug_flags=B.PIPO_DBG_SEGMENT_COPIES, n_h2d_streams=2, chunk_bytes=4096 * 37),
     ]
     for v in variants:
         log(f"streamed variant {v}")
         t1, l1 = _run(hw, prompt, 6, **v)
         assert np.array_equal(t1, t0)
         assert np.array_equal(l1.view(np.uint32), l0.view(np.uint32))
+
+
+def test_merged_copies_are_fewer(opt125m):
+    """A layer's matrices, laid out in one pinned region at the slot's
+    offsets, stream as one range: fewer copies than one per tensor, the
+    same bytes up to the padding between tensors."""
+    wl, model, hw = opt125m
+    prompt = synth.prompt_tokens(4, 32, wl.shape.vocab, seed=3)
+    st = {}
+    for name, flags in (("merged", 0), ("segments", B.PIPO_DBG_SEGMENT_COPIES)):
+        with Decoder(hw, max_batch=4, max_seq=40, chunk_bytes=1 << 30, debug_flags=flags) as dec:
+            dec.prefill(prompt)
+            dec.reset_stats()
+            dec.decode(np.zeros(4, np.int32))
+            st[name] = dec.stats()
+    L = wl.shape.n_layers
+    assert st["segments"]["n_copies"] - st["merged"]["n_copies"] == L * 3   # 5 copies -> 2
+    pad = st["merged"]["h2d_weight_bytes"] - st["segments"]["h2d_weight_bytes"]
+    assert 0 <= pad < L * 3 * 4096
 
 
 def test_new_prefill_resets_sequences(opt125m):

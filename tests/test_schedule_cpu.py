@@ -13,7 +13,9 @@ simulated timeline must satisfy the orderings the pipeline relies on
   previous token's save of that layer completed, the save reads rows only
   after the QKV projection wrote them, and a KV buffer is overwritten only
   after its previous contents were read and saved;
-* every tensor is streamed exactly once per pass, in full.
+* every tensor is streamed exactly once per pass, in full (also when a
+  layer's matrices are copied as one merged range whose chunks span
+  tensors).
 """
 import itertools
 import random
@@ -35,7 +37,7 @@ LAYER_KERNELS = [K_LN1, K_QKV, K_ATTN, K_OPROJ, K_LN2, K_FC1, K_FC2]
 
 
 def make_config(n_layers, n_slots, n_h2d, layers_streamed, head_streamed, kv_on_host, w4,
-                chunk, poison=False, delay=False):
+                chunk, poison=False, delay=False, merged=False):
     cfg = B.PipoSchedConfig()
     cfg.n_layers, cfg.n_slots, cfg.n_h2d = n_layers, n_slots, n_h2d
     cfg.layers_streamed, cfg.head_streamed, cfg.kv_on_host = layers_streamed, head_streamed, kv_on_host
@@ -47,10 +49,33 @@ def make_config(n_layers, n_slots, n_h2d, layers_streamed, head_streamed, kv_on_
         seg[s] = n * 65536 if not w4 else n * 16384
         if w4:
             seg[s + 1] = n * 2048
+    off = 0
     for i in range(10):
         cfg.layer_seg_bytes[i] = seg[i]
+        if i != SEG_HEAD:   # slot layout: segments at 4 KiB-aligned offsets
+            cfg.layer_seg_off[i] = off
+            off = (off + seg[i] + 4095) // 4096 * 4096
+    cfg.merged = int(merged)
     cfg.head_bytes = 200 * 1024
     return cfg
+
+
+def split_merged(cfg, c):
+    """The per-segment pieces of a weight copy: a merged copy (named after
+    segment 1, offset from its slot offset) covers every segment it
+    overlaps; padding between segments belongs to none."""
+    if not cfg.merged or c["layer"] < 0 or c["seg"] == SEG_MISC:
+        return [c]
+    base = cfg.layer_seg_off[SEG_WQKV]
+    a0, a1 = c["off"], c["off"] + c["bytes"]
+    pieces = []
+    for seg in range(SEG_WQKV, SEG_HEAD):
+        n = cfg.layer_seg_bytes[seg]
+        lo = cfg.layer_seg_off[seg] - base
+        x0, x1 = max(a0, lo), min(a1, lo + n)
+        if n > 0 and x0 < x1:
+            pieces.append(dict(c, seg=seg, off=x0 - lo, bytes=x1 - x0))
+    return pieces
 
 
 def parse(text):
@@ -117,8 +142,23 @@ def check(ops_by_pass, flat, cfg, pass_info, kv_row):
     kvsave = [o for o in flat if o["kind"] == COPY_D2H]
     poisons = [o for o in flat if o["kind"] == POISON]
     copies_of = defaultdict(list)
+    merged_of = defaultdict(list)
     for c in wcopies:
-        copies_of[(c["unit"], c["seg"])].append(c)
+        for piece in split_merged(cfg, c):
+            copies_of[(c["unit"], piece["seg"])].append(piece)
+        if cfg.merged and c["layer"] >= 0 and c["seg"] != SEG_MISC:
+            assert c["seg"] == SEG_WQKV
+            merged_of[c["unit"]].append(c)
+    # a merged range is copied once, in order-independent chunks of at most
+    # chunk_bytes, from the first matrix to the end of the last
+    last = max(s for s in range(SEG_WQKV, SEG_HEAD) if cfg.layer_seg_bytes[s] > 0)
+    span = cfg.layer_seg_off[last] + cfg.layer_seg_bytes[last] - cfg.layer_seg_off[SEG_WQKV]
+    for g, cs in merged_of.items():
+        pos = 0
+        for c in sorted(cs, key=lambda c: c["off"]):
+            assert c["off"] == pos and 0 < c["bytes"] <= cfg.chunk_bytes
+            pos += c["bytes"]
+        assert pos == span
 
     # RAW on weights
     for k in kernels:
@@ -214,20 +254,21 @@ VARIANTS = list(itertools.product(
     [1, 2],            # h2d streams
     [(1, 1, 0), (1, 0, 0), (0, 1, 0), (1, 1, 1), (1, 0, 1)],  # layers/head streamed, kv on host
     [False, True],     # int4 segments
+    [False, True],     # merged copies of a layer's matrices
 ))
 
 
-@pytest.mark.parametrize("L,S,nh,mode,w4", VARIANTS)
-def test_schedule_orderings(L, S, nh, mode, w4):
+@pytest.mark.parametrize("L,S,nh,mode,w4,merged", VARIANTS)
+def test_schedule_orderings(L, S, nh, mode, w4, merged):
     ls, hs, kvh = mode
-    rng = random.Random(hash((L, S, nh, mode, w4)) & 0xFFFF)
+    rng = random.Random(hash((L, S, nh, mode, w4, merged)) & 0xFFFF)
     P, G = 5, 4
     passes = [(True, 0, P)] + [(False, P + i, 1) for i in range(G)] + \
              [(True, 0, 3)] + [(False, 3, 1)]
     kv_row = 4096
-    for chunk in (32 * 1024, 1 << 30):
+    for chunk in (32 * 1024, 50 * 1024, 1 << 30):
         cfg = make_config(L, S, nh, ls, hs, kvh, w4, chunk, poison=(chunk < 1 << 30),
-                          delay=(nh == 2))
+                          delay=(nh == 2), merged=merged)
         text = B.pipo_sched_trace(cfg, passes, kv_row_bytes=kv_row)
         for trial in range(6):
             ops_by_pass = split_passes(parse(text))
