@@ -326,7 +326,9 @@ def main():
                                    wl.wfmt == "int4" and fam_key != "head")
         elif fam_key == "attention":
             kv4 = "true" if wl.kv_fmt == "int4" else "false"
-            symbols = [f"attn_decode_k<{dh}, {shape.n_heads // hkv}, {kv4}>"]
+            G = shape.n_heads // hkv
+            hp = 1 if G > 1 else (4 if hkv % 4 == 0 else (2 if hkv % 2 == 0 else 1))
+            symbols = [f"attn_decode_k<{dh}, {G}, {hp}, {kv4}>"]
         symbol = " + ".join(symbols) if symbols else None
         traffic, tsrc = measured_traffic(wl.name, symbols) if symbols else (None, None)
         out["roofline"] = {"kernel": name, "symbol": symbol, "bound": "hbm",

@@ -28,19 +28,22 @@ __device__ __forceinline__ float wave_max(float v) {
 }
 
 // ---------------------------------------------------------------------------
-// decode: grid (key/value heads, b, splits), 256 threads.  A workgroup
-// serves the G = H / Hkv query heads that share key/value head kh, so each
-// cached row is read from HBM once per step.  Split z of a (sequence, kv
-// head) covers keys [z * chunk, min(T, (z + 1) * chunk)).  A key is handled
-// by D/8 lanes (8 dims each); every lane group keeps, per query head, its
-// own online softmax state (running max m, sum l, 8 accumulators) over the
-// keys it visits, two keys at a time so that K and V of both are in flight
-// together.  Groups are merged by a butterfly inside the wave, waves in
-// order through LDS.  With one split the result is final; otherwise (m, l,
-// acc[D]) of each query head goes to `part` and attn_decode_combine merges
-// the splits in split order.  With KV4 the cache rows are INT4 (dkv/2 code
-// bytes, then dkv/64 fp16 (scale, min) pairs): a lane reads its 8 codes and
-// its group's pair and expands them to fp16.
+// decode: grid (key/value head groups, b, splits), 256 threads.  A workgroup
+// serves HP adjacent key/value heads of one sequence and the G = H / Hkv
+// query heads that read each of them (HP > 1 only without grouping, G = 1),
+// so each cached row is read from HBM once per step and a key's HP heads
+// are one contiguous HP * D * 2-byte read.  Split z of a (sequence, head
+// group) covers keys [z * chunk, min(T, (z + 1) * chunk)).  A key's head is
+// handled by D/8 lanes (8 dims each); every lane group keeps, per query
+// head, its own online softmax state (running max m, sum l, 8 accumulators)
+// over the keys it visits, two keys at a time so that K and V of both are
+// in flight together (the second one's index is clamped, so the loads are
+// unconditional).  Groups are merged by a butterfly inside the wave, waves
+// in order through LDS.  With one split the result is final; otherwise (m,
+// l, acc[D]) of each query head goes to `part` and attn_decode_combine
+// merges the splits in split order.  With KV4 the cache rows are INT4
+// (dkv/2 code bytes, then dkv/64 fp16 (scale, min) pairs): a lane reads its
+// 8 codes and its group's pair and expands them to fp16.
 __device__ __forceinline__ void online_merge(float& m, float& l, float (&acc)[8], float m2,
                                              float l2, const float (&acc2)[8]) {
   const float M = fmaxf(m, m2);
@@ -52,30 +55,34 @@ __device__ __forceinline__ void online_merge(float& m, float& l, float (&acc)[8]
   m = M;
 }
 
-template <int D, int G, bool KV4>
+template <int D, int G, int HP, bool KV4>
 __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict__ q,
                                                      const void* __restrict__ kc,
                                                      const void* __restrict__ vc,
                                                      uint16_t* __restrict__ o,
                                                      float* __restrict__ part, int b, int Hkv,
                                                      int t, int chunk) {
-  __shared__ float wm[G][4], wl[G][4];
-  __shared__ float wacc[G][4][D];
-  constexpr int LPP = D / 8;     // lanes per key
-  constexpr int PPW = 64 / LPP;  // keys per wave per pass
-  const int kh = blockIdx.x, bi = blockIdx.y, sp = blockIdx.z, S = gridDim.z;
+  static_assert(G == 1 || HP == 1, "several heads per workgroup only without grouping");
+  constexpr int LPP = D / 8;      // lanes per head of a key
+  constexpr int LPK = HP * LPP;   // lanes per key
+  constexpr int PPW = 64 / LPK;   // keys per wave per pass
+  constexpr int NQ = HP * G;      // query heads of the workgroup
+  __shared__ float wm[4][NQ], wl[4][NQ];
+  __shared__ float wacc[4][NQ * D];
+  const int kb = blockIdx.x, bi = blockIdx.y, sp = blockIdx.z, S = gridDim.z;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int sub = lane / LPP, cl = lane % LPP;
+  const int sub = lane / LPK, cl = lane % LPK, hl = cl / LPP, cd = (cl % LPP) * 8;
   const int H = Hkv * G;
   const int64_t d = (int64_t)H * D, dkv = (int64_t)Hkv * D;
   const int T = t + 1;
   const int p0 = sp * chunk, p1 = min(T, p0 + chunk);
-  const int64_t kcol = (int64_t)kh * D + cl * 8;
+  const int kh = kb * HP + hl;                    // this lane's key/value head
+  const int64_t kcol = (int64_t)kh * D + cd;
 
   float qf[G][8];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    const h8 qv = load_h8(q + (int64_t)bi * d + (int64_t)(kh * G + g) * D + cl * 8);
+    const h8 qv = load_h8(q + (int64_t)bi * d + (int64_t)(kh * G + g) * D + cd);
 #pragma unroll
     for (int i = 0; i < 8; ++i) qf[g][i] = (float)qv[i];
   }
@@ -127,20 +134,17 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
     }
   };
   for (int p = p0 + wave * PPW + sub; p < p1; p += 8 * PPW) {
-    const int p2 = p + 4 * PPW;
+    const int p2 = min(p + 4 * PPW, p1 - 1);
     const h8 ka = load_kv(kc, p);
     const h8 va = load_kv(vc, p);
-    h8 kb2 = zero_h8(), vb2 = zero_h8();
-    if (p2 < p1) {
-      kb2 = load_kv(kc, p2);
-      vb2 = load_kv(vc, p2);
-    }
+    const h8 kb2 = load_kv(kc, p2);
+    const h8 vb2 = load_kv(vc, p2);
     visit(ka, va);
-    if (p2 < p1) visit(kb2, vb2);
+    if (p + 4 * PPW < p1) visit(kb2, vb2);
   }
   // merge the lane groups of the wave (butterfly over the group index)
 #pragma unroll
-  for (int off = LPP; off < 64; off <<= 1) {
+  for (int off = LPK; off < 64; off <<= 1) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       float acc2[8];
@@ -154,26 +158,27 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
   if (sub == 0) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      if (cl == 0) {
-        wm[g][wave] = m[g];
-        wl[g][wave] = l[g];
+      const int j = hl * G + g;  // query head within the workgroup
+      if (cd == 0) {
+        wm[wave][j] = m[g];
+        wl[wave][j] = l[g];
       }
 #pragma unroll
-      for (int i = 0; i < 8; ++i) wacc[g][wave][cl * 8 + i] = acc[g][i];
+      for (int i = 0; i < 8; ++i) wacc[wave][j * D + cd + i] = acc[g][i];
     }
   }
   __syncthreads();
-  for (int c = tid; c < G * D; c += 256) {
-    const int g = c / D, cc = c % D, h = kh * G + g;
-    float M = wm[g][0], L = wl[g][0], A = wacc[g][0][cc];
+  for (int c = tid; c < NQ * D; c += 256) {
+    const int j = c / D, cc = c % D, h = kb * NQ + j;
+    float M = wm[0][j], L = wl[0][j], A = wacc[0][c];
 #pragma unroll
     for (int w = 1; w < 4; ++w) {
-      const float m2 = wm[g][w];
+      const float m2 = wm[w][j];
       const float Mn = fmaxf(M, m2);
       const float a1 = M == -INFINITY ? 0.f : expf(M - Mn);
       const float a2 = m2 == -INFINITY ? 0.f : expf(m2 - Mn);
-      L = L * a1 + wl[g][w] * a2;
-      A = A * a1 + wacc[g][w][cc] * a2;
+      L = L * a1 + wl[w][j] * a2;
+      A = A * a1 + wacc[w][c] * a2;
       M = Mn;
     }
     if (S == 1) {
@@ -343,10 +348,17 @@ __global__ __launch_bounds__(256) void attn_prefill_k(const uint16_t* __restrict
 }
 
 // ---------------------------------------------------------------------------
-int attn_decode_splits(int b, int n_kv_heads, int t) {
-  // enough workgroups to fill the chip, at least 64 keys per split
+int attn_decode_heads_per_wg(int n_heads, int n_kv_heads) {
+  if (n_heads != n_kv_heads) return 1;
+  return n_heads % 4 == 0 ? 4 : (n_heads % 2 == 0 ? 2 : 1);
+}
+
+int attn_decode_splits(int b, int n_heads, int n_kv_heads, int t) {
+  // at least kAttnDecodeMinWGs workgroups (three per CU: fewer leave HBM
+  // idle, more only add merge traffic), at least 64 keys per split
   const int T = t + 1;
-  int S = (2048 + b * n_kv_heads - 1) / (b * n_kv_heads);
+  const int wgs = b * (n_kv_heads / attn_decode_heads_per_wg(n_heads, n_kv_heads));
+  int S = (kAttnDecodeMinWGs + wgs - 1) / wgs;
   S = std::min(S, std::max(1, T / 64));
   S = std::min(S, kAttnDecodeMaxSplits);
   const int chunk = (T + S - 1) / S;
@@ -357,13 +369,13 @@ int64_t attn_decode_workspace_bytes(int b, int n_heads, int head_dim, int splits
   return splits > 1 ? (int64_t)b * n_heads * splits * (head_dim + 2) * 4 : 0;
 }
 
-template <int D, int G, bool KV4>
+template <int D, int G, int HP, bool KV4>
 static void launch_decode_g(const uint16_t* q, const void* kc, const void* vc, uint16_t* o,
                             int b, int Hkv, int t, int S, int chunk, float* workspace,
                             hipStream_t st) {
-  const dim3 grid((unsigned)Hkv, (unsigned)b, (unsigned)S);
-  launch(attn_decode_k<D, G, KV4>, grid, dim3(256), 0, st, q, kc, vc, o, workspace, b, Hkv, t,
-         chunk);
+  const dim3 grid((unsigned)(Hkv / HP), (unsigned)b, (unsigned)S);
+  launch(attn_decode_k<D, G, HP, KV4>, grid, dim3(256), 0, st, q, kc, vc, o, workspace, b, Hkv,
+         t, chunk);
   if (S > 1)
     launch(attn_decode_combine<D>, dim3((unsigned)(Hkv * G), (unsigned)b), dim3(D), 0, st,
            (const float*)workspace, o, Hkv * G, S);
@@ -371,14 +383,19 @@ static void launch_decode_g(const uint16_t* q, const void* kc, const void* vc, u
 
 template <int D, bool KV4>
 static void launch_decode_d(const uint16_t* q, const void* kc, const void* vc, uint16_t* o, int b,
-                            int Hkv, int G, int t, int S, int chunk, float* workspace,
+                            int Hkv, int G, int HP, int t, int S, int chunk, float* workspace,
                             hipStream_t st) {
-  switch (G) {
-    case 1: launch_decode_g<D, 1, KV4>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, st); break;
-    case 2: launch_decode_g<D, 2, KV4>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, st); break;
-    case 4: launch_decode_g<D, 4, KV4>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, st); break;
-    default: launch_decode_g<D, 8, KV4>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, st); break;
-  }
+#define PIPO_DECODE_CASE(g, hp)                                                         \
+  if (G == g && HP == hp)                                                               \
+    return launch_decode_g<D, g, hp, KV4>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, \
+                                          st);
+  PIPO_DECODE_CASE(1, 4)
+  PIPO_DECODE_CASE(1, 2)
+  PIPO_DECODE_CASE(1, 1)
+  PIPO_DECODE_CASE(2, 1)
+  PIPO_DECODE_CASE(4, 1)
+  PIPO_DECODE_CASE(8, 1)
+#undef PIPO_DECODE_CASE
 }
 
 static pipo_status check_heads(const char* what, int n_heads, int n_kv_heads, int head_dim) {
@@ -412,17 +429,18 @@ pipo_status launch_attn_decode(const uint16_t* q, const void* kc, const void* vc
     return PIPO_ERR_UNSUPPORTED;
   }
   const int G = n_heads / n_kv_heads;
+  const int HP = attn_decode_heads_per_wg(n_heads, n_kv_heads);
   const int T = t + 1;
-  int S = attn_decode_splits(b, n_kv_heads, t);
+  int S = attn_decode_splits(b, n_heads, n_kv_heads, t);
   if (!workspace || workspace_bytes < attn_decode_workspace_bytes(b, n_heads, head_dim, S)) S = 1;
   const int chunk = (T + S - 1) / S;
   S = (T + chunk - 1) / chunk;
   if (head_dim == 128)
     (kv4 ? launch_decode_d<128, true> : launch_decode_d<128, false>)(
-        q, kc, vc, o, b, n_kv_heads, G, t, S, chunk, workspace, st);
+        q, kc, vc, o, b, n_kv_heads, G, HP, t, S, chunk, workspace, st);
   else
     (kv4 ? launch_decode_d<64, true> : launch_decode_d<64, false>)(
-        q, kc, vc, o, b, n_kv_heads, G, t, S, chunk, workspace, st);
+        q, kc, vc, o, b, n_kv_heads, G, HP, t, S, chunk, workspace, st);
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
 }
