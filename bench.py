@@ -52,6 +52,9 @@ def parse():
                     help="skip device timestamps (no busy %% or kernel roofline)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", type=int, default=0, help="override layer count (testing only)")
+    ap.add_argument("--disk-dir", default=None,
+                    help="directory of the disk tier's file (disk workloads; default: the "
+                         "system's temporary directory)")
     return ap.parse_args()
 
 
@@ -218,10 +221,21 @@ def main():
     peak = max(peak1, peak2)
     log(f"H2D link peak: {peak1:.1f} GB/s (1 stream), {peak2:.1f} GB/s (2 streams)")
 
+    disk = None
+    if wl.weights_on_disk:
+        import tempfile
+        disk_dir = args.disk_dir or tempfile.gettempdir()
+        dpeak, direct = B.pipo_measure_disk_read(disk_dir, 4 << 30, args.chunk_mb << 20, 8, 2)
+        log(f"disk read peak in {disk_dir}: {dpeak:.2f} GB/s (direct I/O: {direct})")
+        disk = {"dir": disk_dir, "peak_gbps": dpeak, "direct_io": direct}
+        t0 = time.time()
     dec = Decoder(hw, weights_on_host=True, embed_on_host=True, kv_on_host=wl.kv_on_host,
-                  kv_fmt=wl.kv_fmt,
+                  kv_fmt=wl.kv_fmt, weights_on_disk=wl.weights_on_disk,
+                  disk_dir=disk["dir"] if disk else None,
                   n_weight_slots=args.slots, n_h2d_streams=args.h2d_streams,
                   chunk_bytes=args.chunk_mb << 20, max_batch=wl.batch, max_seq=max_seq)
+    if disk:
+        log(f"disk tier file written in {time.time() - t0:.1f} s")
     prompt = synth.prompt_tokens(wl.batch, wl.prompt, shape.vocab, seed=1, stream=args.workload)
     t0 = time.perf_counter()
     nxt, _ = dec.prefill(prompt)
@@ -264,7 +278,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "layers": shape.n_layers, "d_model": shape.d_model,
                    "batch": wl.batch, "prompt": wl.prompt,
-                   "generated": 1 + W + K, "weights": f"{wl.wfmt}, pinned host, streamed",
+                   "generated": 1 + W + K,
+                   "weights": f"{wl.wfmt}, " + ("layers in the disk tier's file (disk -> pinned "
+                                                "-> HBM), head pinned host" if wl.weights_on_disk
+                                                else "pinned host") + ", streamed",
                    "kv_cache": ("host (pinned, or pageable through pinned staging), streamed"
                                 if wl.kv_on_host else "HBM") + f", {wl.kv_fmt}",
                    "chunk_bytes": args.chunk_mb << 20, "slots": args.slots,
@@ -277,6 +294,17 @@ def main():
                      "roofline_tokens_per_s": round(roof, 3),
                      "frac_of_roofline": round(value / roof, 4)},
         "ttft_ms": round(ttft_ms, 1),
+        **({"disk": {"peak_gbps": round(disk["peak_gbps"], 2), "direct_io": disk["direct_io"],
+                     "bytes_per_step": int(st["disk_read_bytes"] / K),
+                     "sustained_gbps": round(st["disk_read_bytes"] / dt / 1e9, 2),
+                     "frac_of_peak": round(st["disk_read_bytes"] / dt / 1e9 / disk["peak_gbps"], 4),
+                     "read_ms_per_step": round(st["disk_read_ms"] / K, 1),
+                     "roofline_tokens_per_s": round(
+                         wl.batch * disk["peak_gbps"] * 1e9 / (st["disk_read_bytes"] / K), 3),
+                     "frac_of_roofline": round(
+                         value / (wl.batch * disk["peak_gbps"] * 1e9 / (st["disk_read_bytes"] / K)),
+                         4)}}
+           if disk else {}),
         "step_ms": {"median": round(float(np.median(step_s)) * 1e3, 3),
                     "min": round(min(step_s) * 1e3, 3), "max": round(max(step_s) * 1e3, 3),
                     "source": "host clock around each pipo_decode_step (returns after the "

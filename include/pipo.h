@@ -52,7 +52,8 @@ typedef enum {
   PIPO_ERR_OOM_HOST = -3,     /* pinned host allocation failed */
   PIPO_ERR_HIP = -4,          /* a HIP runtime call failed */
   PIPO_ERR_STATE = -5,        /* call not valid in the context's state */
-  PIPO_ERR_UNSUPPORTED = -6   /* shape or policy outside what the kernels support */
+  PIPO_ERR_UNSUPPORTED = -6,  /* shape or policy outside what the kernels support */
+  PIPO_ERR_IO = -7            /* a file operation of the disk tier failed */
 } pipo_status;
 
 /* Weight storage format of the four per-layer matrices. */
@@ -182,8 +183,20 @@ typedef struct {
                                   that are not pinned live in pageable memory and move through
                                   pinned staging buffers, copied by host worker threads (the
                                   paper's multi-thread transfer, Section 3.3) */
-  int32_t copy_threads;      /* host threads for staged copies (default 8) */
+  int32_t copy_threads;      /* host threads for staged copies and disk reads (default 8) */
   int32_t kv_fmt;            /* PIPO_KV_FP16 (default) or PIPO_KV_INT4_G64 */
+  int32_t weights_on_disk;   /* 1: the disk tier (Section 3.1.1 offloads to CPU memory or disk;
+                                Section 3.3's blockwise transfer): pipo_create writes every
+                                layer unit to a library-owned file in disk_dir (removed when the
+                                context is destroyed; the caller's layer tensors are read only
+                                during pipo_create) and each pass streams the layers disk ->
+                                pinned staging -> HBM in chunk_bytes pieces, read by
+                                copy_threads threads with direct I/O where the file system
+                                allows it, the next chunk's read overlapping the previous
+                                chunk's DMA.  Requires weights_on_host.  The output head stays
+                                in host memory (embed_on_host) or HBM. */
+  int32_t reserved0;         /* 0 */
+  const char* disk_dir;      /* directory of the disk tier's file (NULL: the working directory) */
 } pipo_policy;
 
 /* The paper's two pipeline options (Section 3.2.3). */
@@ -200,12 +213,19 @@ typedef struct {
   int64_t host_kv_bytes;       /* host memory the library allocates for the KV cache */
   int64_t h2d_bytes_per_step;  /* host-to-device bytes of a decode step at the last position */
   int32_t pipeline;            /* PIPO_PIPE_* (memory-efficient: n_weight_slots == 1) */
+  int32_t reserved0;
+  int64_t host_weight_bytes;   /* weights that live in host memory (streamed layers unless on
+                                  disk, streamed head) plus the disk tier's staging buffers */
+  int64_t disk_bytes;          /* the disk tier's file (0 without it) */
+  int64_t disk_bytes_per_step; /* bytes a decode step reads from disk */
 } pipo_plan;
 
 /* Resources for the automatic configuration. */
 typedef struct {
   int64_t hbm_bytes;   /* device memory the context may use; 0: the device's free memory */
-  int64_t host_bytes;  /* host memory for a host KV cache; 0: the system's available memory */
+  int64_t host_bytes;  /* host memory for the weights kept there and a host KV cache; 0: the
+                          system's available memory */
+  int64_t disk_bytes;  /* disk space for the disk tier; 0: no disk tier */
 } pipo_resources;
 
 /* Per-kernel timing (filled when PIPO_DBG_TIMESTAMPS is set): each launch
@@ -236,6 +256,8 @@ typedef struct {
   double kernel_busy_ms;     /* union of compute-stream kernel intervals inside the window */
   double busy_ms;            /* union of both */
   int64_t staged_bytes;      /* bytes that went through the pinned staging buffers */
+  int64_t disk_read_bytes;   /* bytes read from the disk tier's file */
+  double disk_read_ms;       /* host wall time spent in those reads */
   int64_t hbm_bytes;         /* HBM the context holds */
   int64_t pinned_host_bytes; /* pinned host memory the context holds */
   int32_t n_kernel_stats;
@@ -294,17 +316,19 @@ pipo_status pipo_plan_policy(const pipo_shape* shape, const pipo_policy* policy,
  * choose where the weights, the output head and the KV cache live and which
  * pipeline runs, for a shape, weight and KV formats, max_batch and max_seq
  * within the given resources.  Eq. (1) puts the weights in HBM when they
- * fit, else in host memory, and takes the performance-optimized pipeline
- * when its peak memory fits, else the memory-efficient one; here every
- * placement (weights and head resident or streamed, KV resident or on the
- * host) and pipeline (3, 2 or 1 slots) is costed exactly and the one that
- * streams the fewest bytes per decode step within the budgets wins, more
- * slots on ties.  *policy_out gets the choice (with hbm_budget_bytes set to
- * the budget, chunk_bytes and copy streams at their defaults) and, if
+ * fit, else in host memory, else on disk, and takes the performance-
+ * optimized pipeline when its peak memory fits, else the memory-efficient
+ * one; here every placement (weights and head resident or streamed, the
+ * streamed layers in host memory or on disk when res->disk_bytes allows,
+ * KV resident or on the host) and pipeline (3, 2 or 1 slots) is costed
+ * exactly and the one that streams the fewest bytes per decode step within
+ * the budgets wins; on ties host memory before disk, then more slots.
+ * *policy_out gets the choice (with hbm_budget_bytes set to the budget,
+ * chunk_bytes and copy streams at their defaults, disk_dir NULL) and, if
  * plan_out is not NULL, its cost.  Errors: ARG, UNSUPPORTED, OOM_DEVICE
- * (not even the memory-efficient pipeline fits), OOM_HOST (the KV cache
- * fits neither in HBM nor in host memory; the paper's disk tier is not
- * built), HIP (querying free HBM).
+ * (not even the memory-efficient pipeline fits), OOM_HOST (what must stay
+ * in host memory does not fit, even with the layers on disk), HIP
+ * (querying free HBM).
  */
 pipo_status pipo_configure(const pipo_shape* shape, int32_t wfmt, int32_t kv_fmt,
                            int32_t max_batch, int32_t max_seq, const pipo_resources* res,
@@ -340,6 +364,18 @@ pipo_status pipo_measure_h2d_peak(int64_t bytes, int32_t iters, int32_t n_stream
  */
 pipo_status pipo_measure_h2d_chunked(int64_t bytes, int64_t chunk_bytes, int32_t iters,
                                      int32_t n_streams, double* gbps);
+
+/*
+ * Disk probe for the disk tier: write a file of `bytes` in `dir` (removed
+ * again), then read it `iters` times in chunk_bytes pieces with n_threads
+ * threads the way the disk tier does (direct I/O where the file system
+ * allows it, through a pageable buffer) and return the best rate in *gbps
+ * (1e9 bytes per second) and whether direct I/O was used in *direct (may be
+ * NULL).  Host memory only; no GPU needed.  Errors: ARG, IO, OOM_HOST.
+ */
+pipo_status pipo_measure_disk_read(const char* dir, int64_t bytes, int64_t chunk_bytes,
+                                   int32_t n_threads, int32_t iters, double* gbps,
+                                   int32_t* direct);
 
 /* Pinned (page-locked) host memory, 4 KiB aligned; NULL on failure.
  * Matrices placed here are streamed by the copy engines without staging. */

@@ -23,7 +23,7 @@ vp, sz = ctypes.c_void_p, ctypes.c_size_t
 PIPO_OK = 0
 STATUS_NAMES = {0: "PIPO_OK", -1: "PIPO_ERR_ARG", -2: "PIPO_ERR_OOM_DEVICE",
                 -3: "PIPO_ERR_OOM_HOST", -4: "PIPO_ERR_HIP", -5: "PIPO_ERR_STATE",
-                -6: "PIPO_ERR_UNSUPPORTED"}
+                -6: "PIPO_ERR_UNSUPPORTED", -7: "PIPO_ERR_IO"}
 PIPO_W_FP16, PIPO_W_INT4_G64 = 0, 1
 PIPO_FAMILY_OPT, PIPO_FAMILY_LLAMA = 0, 1
 PIPO_KV_FP16, PIPO_KV_INT4_G64 = 0, 1
@@ -62,16 +62,19 @@ class PipoPolicy(ctypes.Structure):
                 ("kv_on_host", i32), ("n_weight_slots", i32), ("n_h2d_streams", i32),
                 ("chunk_bytes", i64), ("max_batch", i32), ("max_seq", i32),
                 ("hbm_budget_bytes", i64), ("debug_flags", i32), ("copy_delay_us", i32),
-                ("pinned_budget_bytes", i64), ("copy_threads", i32), ("kv_fmt", i32)]
+                ("pinned_budget_bytes", i64), ("copy_threads", i32), ("kv_fmt", i32),
+                ("weights_on_disk", i32), ("reserved0", i32), ("disk_dir", ctypes.c_char_p)]
 
 
 class PipoPlan(ctypes.Structure):
     _fields_ = [("weight_bytes", i64), ("kv_bytes", i64), ("hbm_bytes", i64),
-                ("host_kv_bytes", i64), ("h2d_bytes_per_step", i64), ("pipeline", i32)]
+                ("host_kv_bytes", i64), ("h2d_bytes_per_step", i64), ("pipeline", i32),
+                ("reserved0", i32), ("host_weight_bytes", i64), ("disk_bytes", i64),
+                ("disk_bytes_per_step", i64)]
 
 
 class PipoResources(ctypes.Structure):
-    _fields_ = [("hbm_bytes", i64), ("host_bytes", i64)]
+    _fields_ = [("hbm_bytes", i64), ("host_bytes", i64), ("disk_bytes", i64)]
 
 
 class PipoKernelStat(ctypes.Structure):
@@ -84,7 +87,8 @@ class PipoStats(ctypes.Structure):
                 ("d2h_bytes", i64), ("n_copies", i64), ("n_kernels", i64),
                 ("decode_steps", i64), ("decode_wall_ms", f64), ("prefill_wall_ms", f64),
                 ("window_ms", f64), ("copy_busy_ms", f64), ("kernel_busy_ms", f64),
-                ("busy_ms", f64), ("staged_bytes", i64), ("hbm_bytes", i64),
+                ("busy_ms", f64), ("staged_bytes", i64), ("disk_read_bytes", i64),
+                ("disk_read_ms", f64), ("hbm_bytes", i64),
                 ("pinned_host_bytes", i64),
                 ("n_kernel_stats", i32),
                 ("kernels", PipoKernelStat * PIPO_MAX_KERNEL_STATS)]
@@ -123,6 +127,8 @@ _SIGNATURES = {
                         ctypes.POINTER(PipoPlan)], i32),
     "pipo_measure_h2d_peak": ([i64, i32, i32, ctypes.POINTER(f64)], i32),
     "pipo_measure_h2d_chunked": ([i64, i64, i32, i32, ctypes.POINTER(f64)], i32),
+    "pipo_measure_disk_read": ([ctypes.c_char_p, i64, i64, i32, i32, ctypes.POINTER(f64),
+                                ctypes.POINTER(i32)], i32),
     "pipo_host_alloc": ([sz], vp),
     "pipo_host_free": ([vp], None),
     "pipo_last_error": ([], ctypes.c_char_p),
@@ -260,9 +266,9 @@ def pipo_plan_policy(shape: PipoShape, policy: PipoPolicy) -> dict:
 
 
 def pipo_configure(shape: PipoShape, wfmt: int, kv_fmt: int, max_batch: int, max_seq: int,
-                   hbm_bytes: int = 0, host_bytes: int = 0):
+                   hbm_bytes: int = 0, host_bytes: int = 0, disk_bytes: int = 0):
     """Returns (PipoPolicy, plan dict)."""
-    res = PipoResources(hbm_bytes, host_bytes)
+    res = PipoResources(hbm_bytes, host_bytes, disk_bytes)
     pol, plan = PipoPolicy(), PipoPlan()
     _check(lib().pipo_configure(ctypes.byref(shape), wfmt, kv_fmt, max_batch, max_seq,
                                 ctypes.byref(res), ctypes.byref(pol), ctypes.byref(plan)),
@@ -291,6 +297,16 @@ def pipo_measure_h2d_chunked(nbytes: int, chunk_bytes: int, iters: int = 5,
     _check(lib().pipo_measure_h2d_chunked(nbytes, chunk_bytes, iters, n_streams, ctypes.byref(g)),
            "pipo_measure_h2d_chunked")
     return g.value
+
+
+def pipo_measure_disk_read(directory: str, nbytes: int, chunk_bytes: int = 64 << 20,
+                           n_threads: int = 8, iters: int = 2) -> Tuple[float, bool]:
+    """(GB/s, direct I/O used) of the disk tier's read pattern in `directory`."""
+    g, direct = f64(), i32()
+    _check(lib().pipo_measure_disk_read(directory.encode(), nbytes, chunk_bytes, n_threads,
+                                        iters, ctypes.byref(g), ctypes.byref(direct)),
+           "pipo_measure_disk_read")
+    return g.value, bool(direct.value)
 
 
 def pipo_host_alloc(nbytes: int) -> int:

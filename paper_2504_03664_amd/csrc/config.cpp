@@ -128,6 +128,14 @@ pipo_status normalize_policy(const pipo_shape* shape, pipo_policy* p) {
     set_error("kv_on_host requires weights_on_host");
     return PIPO_ERR_UNSUPPORTED;
   }
+  if (pol.weights_on_disk && !pol.weights_on_host) {
+    set_error("weights_on_disk requires weights_on_host (the layers stream every pass)");
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  if (pol.copy_threads < 0 || pol.copy_threads > 64) {
+    set_error("copy_threads %d outside [0, 64]", pol.copy_threads);
+    return PIPO_ERR_ARG;
+  }
   if (pol.kv_fmt != PIPO_KV_FP16 && pol.kv_fmt != PIPO_KV_INT4_G64) {
     set_error("unknown kv_fmt %d", pol.kv_fmt);
     return PIPO_ERR_ARG;
@@ -228,6 +236,27 @@ int64_t host_kv_bytes(const pipo_shape& sh, const pipo_policy& pol) {
   return (int64_t)sh.n_layers * align_up(2 * p.kv_part, 4096);
 }
 
+int64_t staging_bytes(const pipo_policy& pol) {
+  int64_t n = 0;
+  if (pol.kv_on_host || pol.weights_on_disk) n += kStageH2DBufs;
+  if (pol.kv_on_host) n += kStageD2HBufs;
+  if (pol.weights_on_disk) n += 1;  // the pageable chunk direct I/O goes through
+  return n * pol.chunk_bytes;
+}
+
+int64_t host_weight_bytes(const pipo_shape& sh, const pipo_policy& pol) {
+  const UnitLayout u = unit_layout(sh, pol.wfmt == PIPO_W_INT4_G64);
+  int64_t bytes = staging_bytes(pol);
+  if (pol.weights_on_host && !pol.weights_on_disk) bytes += (int64_t)sh.n_layers * u.copy_bytes;
+  if (pol.embed_on_host) bytes += u.head_bytes;
+  return bytes;
+}
+
+int64_t disk_file_bytes(const pipo_shape& sh, const pipo_policy& pol) {
+  if (!pol.weights_on_disk) return 0;
+  return (int64_t)sh.n_layers * unit_layout(sh, pol.wfmt == PIPO_W_INT4_G64).layer_bytes;
+}
+
 // bytes one decode step moves host -> device at the last position
 static int64_t step_bytes(const pipo_shape& sh, const pipo_policy& pol) {
   const UnitLayout u = unit_layout(sh, pol.wfmt == PIPO_W_INT4_G64);
@@ -253,6 +282,10 @@ static void fill_plan(const pipo_shape& sh, const pipo_policy& pol, pipo_plan* o
   out->host_kv_bytes = host_kv_bytes(sh, pol);
   out->h2d_bytes_per_step = step_bytes(sh, pol);
   out->pipeline = pol.n_weight_slots >= 2 ? PIPO_PIPE_PERFORMANCE : PIPO_PIPE_MEMORY_EFFICIENT;
+  out->host_weight_bytes = host_weight_bytes(sh, pol);
+  out->disk_bytes = disk_file_bytes(sh, pol);
+  // each layer unit is read whole (4 KiB-aligned pieces) once per pass
+  out->disk_bytes_per_step = out->disk_bytes;
 }
 
 }  // namespace pipo
@@ -295,8 +328,8 @@ pipo_status pipo_configure(const pipo_shape* shape, int32_t wfmt, int32_t kv_fmt
     set_error("NULL argument");
     return PIPO_ERR_ARG;
   }
-  int64_t hbm = res->hbm_bytes, host = res->host_bytes;
-  if (hbm < 0 || host < 0) {
+  int64_t hbm = res->hbm_bytes, host = res->host_bytes, disk = res->disk_bytes;
+  if (hbm < 0 || host < 0 || disk < 0) {
     set_error("negative resource size");
     return PIPO_ERR_ARG;
   }
@@ -308,44 +341,53 @@ pipo_status pipo_configure(const pipo_shape* shape, int32_t wfmt, int32_t kv_fmt
   if (host == 0) host = (int64_t)sysconf(_SC_AVPHYS_PAGES) * (int64_t)sysconf(_SC_PAGESIZE);
 
   // Eq. (1) generalised: among the placements that fit (weights and head
-  // resident or streamed, KV resident or in host memory) and the two
-  // pipelines, take the one that streams the fewest bytes per decode step;
-  // at equal bytes, the performance-optimized pipeline (more slots).
+  // resident or streamed, streamed layers in host memory or on disk, KV
+  // resident or in host memory) and the two pipelines, take the one that
+  // streams the fewest bytes per decode step; at equal bytes host memory
+  // before disk, then the performance-optimized pipeline (more slots).
   pipo_policy best{};
   int64_t best_bytes = -1, best_slots = 0, need_hbm = -1, need_host = -1;
+  int best_disk = 0;
   pipo_status first_err = PIPO_OK;
   for (int w_host = 0; w_host <= 1; ++w_host)
-    for (int e_host = 0; e_host <= 1; ++e_host)
-      for (int kv_host = 0; kv_host <= w_host; ++kv_host)
-        for (int slots : {3, 2, 1}) {
-          if (!w_host && !e_host && slots != 3) continue;  // nothing streams: slots unused
-          pipo_policy pol{};
-          pol.wfmt = wfmt;
-          pol.kv_fmt = kv_fmt;
-          pol.weights_on_host = w_host;
-          pol.embed_on_host = e_host;
-          pol.kv_on_host = kv_host;
-          pol.n_weight_slots = slots;
-          pol.max_batch = max_batch;
-          pol.max_seq = max_seq;
-          const pipo_status st = normalize_policy(shape, &pol);
-          if (st != PIPO_OK) {
-            if (first_err == PIPO_OK) first_err = st;
-            continue;
+    for (int on_disk = 0; on_disk <= (w_host && disk > 0 ? 1 : 0); ++on_disk)
+      for (int e_host = 0; e_host <= 1; ++e_host)
+        for (int kv_host = 0; kv_host <= w_host; ++kv_host)
+          for (int slots : {3, 2, 1}) {
+            if (!w_host && !e_host && slots != 3) continue;  // nothing streams: slots unused
+            pipo_policy pol{};
+            pol.wfmt = wfmt;
+            pol.kv_fmt = kv_fmt;
+            pol.weights_on_host = w_host;
+            pol.weights_on_disk = on_disk;
+            pol.embed_on_host = e_host;
+            pol.kv_on_host = kv_host;
+            pol.n_weight_slots = slots;
+            pol.max_batch = max_batch;
+            pol.max_seq = max_seq;
+            const pipo_status st = normalize_policy(shape, &pol);
+            if (st != PIPO_OK) {
+              if (first_err == PIPO_OK) first_err = st;
+              continue;
+            }
+            const int64_t h = hbm_plan(*shape, pol).total();
+            const int64_t k = host_kv_bytes(*shape, pol) + host_weight_bytes(*shape, pol);
+            if (need_hbm < 0 || h < need_hbm) need_hbm = h;
+            if (h > hbm) continue;
+            if (need_host < 0 || k < need_host) need_host = k;  // among those that fit in HBM
+            if (k > host || disk_file_bytes(*shape, pol) > disk) continue;
+            const int64_t bytes = step_bytes(*shape, pol);
+            const bool better =
+                best_bytes < 0 || bytes < best_bytes ||
+                (bytes == best_bytes &&
+                 (on_disk < best_disk || (on_disk == best_disk && slots > best_slots)));
+            if (better) {
+              best = pol;
+              best_bytes = bytes;
+              best_slots = slots;
+              best_disk = on_disk;
+            }
           }
-          const int64_t h = hbm_plan(*shape, pol).total();
-          const int64_t k = host_kv_bytes(*shape, pol);
-          if (need_hbm < 0 || h < need_hbm) need_hbm = h;
-          if (h > hbm) continue;
-          if (need_host < 0 || k < need_host) need_host = k;  // among those that fit in HBM
-          if (k > host) continue;
-          const int64_t bytes = step_bytes(*shape, pol);
-          if (best_bytes < 0 || bytes < best_bytes || (bytes == best_bytes && slots > best_slots)) {
-            best = pol;
-            best_bytes = bytes;
-            best_slots = slots;
-          }
-        }
   if (best_bytes < 0) {
     if (first_err != PIPO_OK && need_hbm < 0) return first_err;
     if (need_host < 0) {
@@ -353,9 +395,9 @@ pipo_status pipo_configure(const pipo_shape* shape, int32_t wfmt, int32_t kv_fmt
                 (long long)need_hbm, (long long)hbm);
       return PIPO_ERR_OOM_DEVICE;
     }
-    set_error("the KV cache needs %lld bytes of host memory (%lld available); a disk tier "
-              "would be needed, which this library does not have",
-              (long long)need_host, (long long)host);
+    set_error("%lld bytes must stay in host memory (%lld available) even with the layers on "
+              "disk (%lld bytes of disk allowed)",
+              (long long)need_host, (long long)host, (long long)disk);
     return PIPO_ERR_OOM_HOST;
   }
   best.hbm_budget_bytes = hbm;

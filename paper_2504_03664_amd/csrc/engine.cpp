@@ -17,9 +17,13 @@
 //   host - pinned: packed small tensors per layer, copies of matrices the
 //          caller did not place in pinned memory, embedding staging, token
 //          readback, KV cache per layer [K|V][max_seq][b][d] (KV on host).
+#include <fcntl.h>
+#include <unistd.h>
+
 #include <algorithm>
 #include <atomic>
 #include <chrono>
+#include <cerrno>
 #include <cmath>
 #include <condition_variable>
 #include <cstdarg>
@@ -139,6 +143,49 @@ class CopyPool {
       if (b > a) std::memset((char*)dst + a, v, b - a);
     });
   }
+  // n bytes of file `fd` at `off` into dst, one 4 KiB-aligned piece per
+  // thread (direct I/O needs aligned offsets and lengths; off and n are
+  // multiples of 4 KiB).  With `bounce` (pageable, 4 KiB aligned, n bytes)
+  // each thread reads its piece there and copies it to dst: direct I/O
+  // cannot target pinned device-mapped pages.  False on an error or a
+  // short file.
+  bool pread_all(int fd, void* dst, size_t n, int64_t off, char* bounce) {
+    std::atomic<bool> ok{true};
+    run([&, dst, n, off, bounce](int i) {
+      const size_t per = (n / n_ + 4095) / 4096 * 4096;
+      const size_t a = std::min(n, i * per), b = (i == n_ - 1) ? n : std::min(n, a + per);
+      char* to = bounce ? bounce : (char*)dst;
+      for (size_t p = a; p < b && ok.load();) {
+        const ssize_t r = ::pread(fd, to + p, b - p, off + (int64_t)p);
+        if (r < 0 && errno == EINTR) continue;
+        if (r <= 0) {
+          ok = false;
+          break;
+        }
+        p += (size_t)r;
+      }
+      if (bounce && ok.load() && b > a) std::memcpy((char*)dst + a, bounce + a, b - a);
+    });
+    return ok.load();
+  }
+  // the same for writing n bytes of src at `off`
+  bool pwrite_all(int fd, const void* src, size_t n, int64_t off) {
+    std::atomic<bool> ok{true};
+    run([&, src, n, off](int i) {
+      const size_t per = (n / n_ + 4095) / 4096 * 4096;
+      const size_t a = std::min(n, i * per), b = (i == n_ - 1) ? n : std::min(n, a + per);
+      for (size_t p = a; p < b && ok.load();) {
+        const ssize_t r = ::pwrite(fd, (const char*)src + p, b - p, off + (int64_t)p);
+        if (r < 0 && errno == EINTR) continue;
+        if (r <= 0) {
+          ok = false;
+          break;
+        }
+        p += (size_t)r;
+      }
+    });
+    return ok.load();
+  }
 
  private:
   void run(const std::function<void(int)>& fn) {
@@ -239,6 +286,9 @@ struct pipo_ctx {
   std::vector<char*> kv_pageable;                   // pageable regions to free
   StagingRing stage_h2d, stage_d2h;
   CopyPool* pool = nullptr;
+  int disk_fd = -1;                                 // disk tier: layer units in slot layout
+  bool disk_direct = false;                         //   opened with O_DIRECT
+  char* disk_bounce = nullptr;                      //   pageable chunk for direct I/O
 
   // device side
   std::vector<void*> dev;
@@ -599,6 +649,39 @@ static pipo_status staged_h2d(pipo_ctx* c, void* dst, const void* src, int64_t b
   return PIPO_OK;
 }
 
+// disk tier: `bytes` of the layer file at file_off (4 KiB aligned) into HBM
+// at dst through the H2D staging ring; each piece is read whole by the copy
+// threads (rounded up to 4 KiB, which stays inside the file: layer units are
+// 4 KiB-aligned) before its DMA is queued, so the next piece's read overlaps
+// the previous piece's DMA
+static pipo_status disk_h2d(pipo_ctx* c, void* dst, int64_t file_off, int64_t bytes,
+                            hipStream_t s, hipEvent_t first) {
+  StagingRing& r = c->stage_h2d;
+  for (int64_t off = 0; off < bytes; off += r.buf_bytes) {
+    const int64_t n = std::min(r.buf_bytes, bytes - off);
+    const int64_t nr = align_up(n, 4096);
+    const int b = r.next;
+    r.next = (r.next + 1) % (int)r.buf.size();
+    if (r.busy[b]) PIPO_HIP_TRY(hipEventSynchronize(r.ev[b]));
+    const auto t0 = std::chrono::steady_clock::now();
+    if (!c->pool->pread_all(c->disk_fd, r.buf[b], (size_t)nr, file_off + off,
+                            c->disk_direct ? c->disk_bounce : nullptr)) {
+      set_error("disk tier: reading %lld bytes at %lld failed: %s", (long long)nr,
+                (long long)(file_off + off), std::strerror(errno));
+      return PIPO_ERR_IO;
+    }
+    c->stats.disk_read_ms +=
+        std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    c->stats.disk_read_bytes += nr;
+    if (off == 0 && first) PIPO_HIP_TRY(hipEventRecord(first, s));
+    PIPO_HIP_TRY(hipMemcpyAsync((char*)dst + off, r.buf[b], (size_t)n, hipMemcpyHostToDevice, s));
+    PIPO_HIP_TRY(hipEventRecord(r.ev[b], s));
+    r.busy[b] = true;
+    c->stats.staged_bytes += n;
+  }
+  return PIPO_OK;
+}
+
 static pipo_status staged_d2h(pipo_ctx* c, void* dst, const void* src, int64_t bytes,
                               hipStream_t s, hipEvent_t first) {
   StagingRing& r = c->stage_d2h;
@@ -667,7 +750,10 @@ static pipo_status exec_op(pipo_ctx* c, const Op& op) {
         e0 = tevent(c);
         e1 = tevent(c);
       }
-      if (op.kv && !c->kv_pinned[op.layer]) {
+      if (!op.kv && op.layer >= 0 && c->disk_fd >= 0) {
+        const int64_t file_off = (int64_t)op.layer * c->layer_bytes + c->seg_off[op.seg] + op.off;
+        PIPO_TRY(disk_h2d(c, dst, file_off, op.bytes, s, e0));
+      } else if (op.kv && !c->kv_pinned[op.layer]) {
         PIPO_TRY(h2d ? staged_h2d(c, dst, src, op.bytes, s, e0)
                      : staged_d2h(c, dst, src, op.bytes, s, e0));
       } else {
@@ -752,6 +838,8 @@ static void destroy_ctx(pipo_ctx* c) {
   for (StagingRing* r : {&c->stage_h2d, &c->stage_d2h})
     for (auto e : r->ev) (void)hipEventDestroy(e);
   delete c->pool;
+  if (c->disk_fd >= 0) ::close(c->disk_fd);  // the file was unlinked when it was created
+  std::free(c->disk_bounce);
   for (char* p : c->kv_pageable) std::free(p);
   for (auto e : c->ev) (void)hipEventDestroy(e);
   for (auto e : c->tpool) (void)hipEventDestroy(e);
@@ -761,6 +849,69 @@ static void destroy_ctx(pipo_ctx* c) {
   for (void* p : c->pinned) host_free_pinned(p);
   delete c->sched;
   delete c;
+}
+
+// The disk tier's file: every layer unit in slot layout (small tensors,
+// then the matrices at their 4 KiB-aligned offsets, zero padding), layer j
+// at j * layer_bytes.  Created in disk_dir and unlinked at once, so it
+// disappears with the context (or the process); opened for direct I/O
+// where the file system allows it, so that reads come from the device.
+static pipo_status write_disk_tier(pipo_ctx* c) {
+  const std::string dir = c->pol.disk_dir && c->pol.disk_dir[0] ? c->pol.disk_dir : ".";
+  std::string path = dir + "/pipo_weights_XXXXXX";
+  int fd = ::mkstemp(&path[0]);
+  if (fd < 0) {
+    set_error("disk tier: cannot create a file in %s: %s", dir.c_str(), std::strerror(errno));
+    return PIPO_ERR_IO;
+  }
+  const int fd_direct = ::open(path.c_str(), O_RDWR | O_DIRECT);
+  if (fd_direct >= 0) {
+    ::close(fd);
+    fd = fd_direct;
+    c->disk_direct = true;
+  }
+  ::unlink(path.c_str());
+  c->disk_fd = fd;
+  c->disk_bounce = static_cast<char*>(std::aligned_alloc(4096, (size_t)c->pol.chunk_bytes));
+  if (!c->disk_bounce) {
+    set_error("disk tier: host allocation of %lld bytes failed", (long long)c->pol.chunk_bytes);
+    return PIPO_ERR_OOM_HOST;
+  }
+  const int64_t total = c->L * c->layer_bytes;
+  const int rc = ::posix_fallocate(fd, 0, (off_t)total);
+  if (rc != 0) {
+    set_error("disk tier: cannot reserve %lld bytes in %s: %s", (long long)total, dir.c_str(),
+              std::strerror(rc));
+    return PIPO_ERR_IO;
+  }
+  char* buf = c->disk_bounce;  // pageable: direct I/O cannot use pinned pages
+  const int64_t piece = c->pol.chunk_bytes;
+  for (int64_t j = 0; j < c->L; ++j) {
+    for (int64_t o = 0; o < c->layer_bytes; o += piece) {
+      const int64_t n = std::min(piece, c->layer_bytes - o);
+      int64_t cursor = o;  // [o, cursor) is filled
+      for (int sg = 0; sg < kNumSegs; ++sg) {
+        if (sg == kSegHead || c->seg_bytes[sg] == 0) continue;
+        const int64_t lo = std::max(o, c->seg_off[sg]);
+        const int64_t hi = std::min(o + n, c->seg_off[sg] + c->seg_bytes[sg]);
+        if (lo >= hi) continue;
+        if (lo > cursor) std::memset(buf + (cursor - o), 0, (size_t)(lo - cursor));
+        c->pool->copy(buf + (lo - o),
+                      static_cast<const char*>(c->layer_src[j][sg]) + (lo - c->seg_off[sg]),
+                      (size_t)(hi - lo));
+        cursor = hi;
+      }
+      if (cursor < o + n) std::memset(buf + (cursor - o), 0, (size_t)(o + n - cursor));
+      if (!c->pool->pwrite_all(fd, buf, (size_t)n, j * c->layer_bytes + o)) {
+        set_error("disk tier: writing %lld bytes to %s failed: %s", (long long)n, dir.c_str(),
+                  std::strerror(errno));
+        return PIPO_ERR_IO;
+      }
+    }
+    for (int sg = 0; sg < kNumSegs; ++sg)
+      if (sg != kSegMisc) c->layer_src[j][sg] = nullptr;  // caller memory: not kept
+  }
+  return PIPO_OK;
 }
 
 static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* w,
@@ -810,7 +961,9 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   // host sources: small tensors packed per layer; matrices in place when
   // they sit in pipo_host_alloc memory, else copied into a merged pinned
   // region per layer (data merging, Section 3.3)
-  const bool need_host = pol.weights_on_host != 0;
+  // layer matrices that stream from host memory must be pinned; with the
+  // disk tier they are only read once, to write the file
+  const bool need_host = pol.weights_on_host != 0 && !pol.weights_on_disk;
   c->layer_src.assign((size_t)L, std::vector<const void*>(kNumSegs, nullptr));
   void* misc_all = nullptr;
   PIPO_TRY(pin_alloc(c, &misc_all, L * c->misc_bytes));
@@ -895,7 +1048,9 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   // merged copies when every layer's matrices sit in one pinned allocation
   // at the slot's relative offsets (caller regions from pipo_host_alloc laid
   // out that way, or the library's merged regions)
-  if (pol.weights_on_host && !(pol.debug_flags & PIPO_DBG_SEGMENT_COPIES)) {
+  if (pol.weights_on_disk && !(pol.debug_flags & PIPO_DBG_SEGMENT_COPIES)) {
+    c->scfg.merged = true;  // the file holds every unit in slot layout
+  } else if (pol.weights_on_host && !(pol.debug_flags & PIPO_DBG_SEGMENT_COPIES)) {
     int last = kSegWqkv;
     for (int sg = kSegWqkv; sg < kSegHead; ++sg)
       if (c->seg_bytes[sg] > 0) last = sg;
@@ -1017,18 +1172,13 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   c->ids_stage = (int32_t*)p;
   PIPO_TRY(pin_alloc(c, &p, (int64_t)pol.max_batch * 4));
   c->next_stage = (int32_t*)p;
-  if (pol.kv_on_host) {
-    // One region per layer.  Layers are pinned while the budget and the
-    // system allow (the copy engines stream those directly); the rest live
-    // in pageable memory and go through pinned staging rings, which are
-    // allocated first, with 1 GiB of pinned memory held back meanwhile so
-    // that the KV layers do not take the last of what the system grants.
-    const int64_t per_layer = align_up(2 * c->kv_part_bytes, 4096);
-    const bool force_pageable = (pol.debug_flags & PIPO_DBG_KV_PAGEABLE) != 0;
+  if (pol.kv_on_host || pol.weights_on_disk) {
+    // pinned staging rings (disk reads and pageable KV layers) and the copy threads
     c->pool = new CopyPool(pol.copy_threads > 0 ? pol.copy_threads : 8);
     const int64_t buf_bytes = pol.chunk_bytes;
-    for (auto [ring, n] : {std::pair<StagingRing*, int>{&c->stage_h2d, 16},
-                           std::pair<StagingRing*, int>{&c->stage_d2h, 8}}) {
+    for (auto [ring, n] :
+         {std::pair<StagingRing*, int>{&c->stage_h2d, kStageH2DBufs},
+          std::pair<StagingRing*, int>{&c->stage_d2h, pol.kv_on_host ? kStageD2HBufs : 0}}) {
       ring->buf_bytes = buf_bytes;
       ring->buf.assign((size_t)n, nullptr);
       ring->ev.assign((size_t)n, nullptr);
@@ -1041,6 +1191,16 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
         PIPO_HIP_TRY(hipEventCreateWithFlags(&ring->ev[(size_t)i], hipEventDisableTiming));
       }
     }
+  }
+  if (pol.weights_on_disk) PIPO_TRY(write_disk_tier(c));
+  if (pol.kv_on_host) {
+    // One region per layer.  Layers are pinned while the budget and the
+    // system allow (the copy engines stream those directly); the rest live
+    // in pageable memory and go through the pinned staging rings, with 1 GiB
+    // of pinned memory held back meanwhile so that the KV layers do not take
+    // the last of what the system grants.
+    const int64_t per_layer = align_up(2 * c->kv_part_bytes, 4096);
+    const bool force_pageable = (pol.debug_flags & PIPO_DBG_KV_PAGEABLE) != 0;
     void* reserve = force_pageable ? nullptr : host_alloc_pinned((size_t)1 << 30);
     c->kv_host.assign((size_t)L, nullptr);
     c->kv_pinned.assign((size_t)L, false);
@@ -1376,6 +1536,68 @@ pipo_status pipo_measure_h2d_chunked(int64_t bytes, int64_t chunk_bytes, int32_t
                                      int32_t n_streams, double* gbps) {
   clear_error();
   return measure_h2d(bytes, chunk_bytes, iters, n_streams, gbps);
+}
+
+pipo_status pipo_measure_disk_read(const char* dir, int64_t bytes, int64_t chunk_bytes,
+                                   int32_t n_threads, int32_t iters, double* gbps,
+                                   int32_t* direct) {
+  clear_error();
+  if (!gbps || bytes <= 0 || chunk_bytes <= 0 || n_threads < 1 || n_threads > 64 || iters < 1) {
+    set_error("measure_disk_read: bad arguments");
+    return PIPO_ERR_ARG;
+  }
+  chunk_bytes = align_up(chunk_bytes, 4096);
+  bytes = align_up(bytes, chunk_bytes);
+  const std::string d = dir && dir[0] ? dir : ".";
+  std::string path = d + "/pipo_probe_XXXXXX";
+  int fd = ::mkstemp(&path[0]);
+  if (fd < 0) {
+    set_error("measure_disk_read: cannot create a file in %s: %s", d.c_str(), std::strerror(errno));
+    return PIPO_ERR_IO;
+  }
+  const int fdd = ::open(path.c_str(), O_RDWR | O_DIRECT);
+  bool is_direct = false;
+  if (fdd >= 0) {
+    ::close(fd);
+    fd = fdd;
+    is_direct = true;
+  }
+  ::unlink(path.c_str());
+  char* buf = static_cast<char*>(std::aligned_alloc(4096, (size_t)chunk_bytes));
+  char* bounce = static_cast<char*>(std::aligned_alloc(4096, (size_t)chunk_bytes));
+  pipo_status st = PIPO_OK;
+  if (!buf || !bounce) {
+    set_error("measure_disk_read: host allocation failed");
+    st = PIPO_ERR_OOM_HOST;
+  }
+  CopyPool pool(n_threads);
+  if (st == PIPO_OK) {
+    std::memset(buf, 0x5a, (size_t)chunk_bytes);
+    for (int64_t off = 0; off < bytes && st == PIPO_OK; off += chunk_bytes)
+      if (!pool.pwrite_all(fd, buf, (size_t)chunk_bytes, off)) {
+        set_error("measure_disk_read: writing %s failed: %s", d.c_str(), std::strerror(errno));
+        st = PIPO_ERR_IO;
+      }
+  }
+  double best = 0;
+  for (int it = 0; it < iters && st == PIPO_OK; ++it) {
+    const auto t0 = std::chrono::steady_clock::now();
+    for (int64_t off = 0; off < bytes && st == PIPO_OK; off += chunk_bytes)
+      if (!pool.pread_all(fd, buf, (size_t)chunk_bytes, off, is_direct ? bounce : nullptr)) {
+        set_error("measure_disk_read: reading %s failed: %s", d.c_str(), std::strerror(errno));
+        st = PIPO_ERR_IO;
+      }
+    const double sec =
+        std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+    best = std::max(best, (double)bytes / sec / 1e9);
+  }
+  ::close(fd);
+  std::free(buf);
+  std::free(bounce);
+  if (st != PIPO_OK) return st;
+  *gbps = best;
+  if (direct) *direct = is_direct ? 1 : 0;
+  return PIPO_OK;
 }
 
 }  // extern "C"

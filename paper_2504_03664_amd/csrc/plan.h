@@ -59,4 +59,16 @@ HbmPlan hbm_plan(const pipo_shape& sh, const pipo_policy& pol);  // pol normaliz
 // host memory the library allocates for the KV cache (per layer, 4 KiB aligned)
 int64_t host_kv_bytes(const pipo_shape& sh, const pipo_policy& pol);
 
+// pinned staging rings (pageable host KV layers, disk tier) and the disk
+// tier's pageable direct-I/O chunk: buffers of chunk_bytes
+constexpr int kStageH2DBufs = 16, kStageD2HBufs = 8;
+int64_t staging_bytes(const pipo_policy& pol);
+
+// weights kept in host memory (streamed layers unless on disk, streamed head)
+// plus the staging rings
+int64_t host_weight_bytes(const pipo_shape& sh, const pipo_policy& pol);
+
+// the disk tier's file: every layer unit in slot layout
+int64_t disk_file_bytes(const pipo_shape& sh, const pipo_policy& pol);
+
 }  // namespace pipo

@@ -168,14 +168,17 @@ def c_policy(wfmt: str = "fp16", weights_on_host: bool = True, embed_on_host: bo
              chunk_bytes: int = 64 << 20, max_batch: int = 1, max_seq: int = 1,
              hbm_budget_bytes: int = 0, debug_flags: int = 0,
              copy_delay_us: int = 0, pinned_budget_bytes: int = 0,
-             copy_threads: int = 0, kv_fmt: str = "fp16") -> B.PipoPolicy:
+             copy_threads: int = 0, kv_fmt: str = "fp16", weights_on_disk: bool = False,
+             disk_dir: Optional[str] = None) -> B.PipoPolicy:
     assert wfmt in ("fp16", "int4") and kv_fmt in ("fp16", "int4")
     return B.PipoPolicy(B.PIPO_W_FP16 if wfmt == "fp16" else B.PIPO_W_INT4_G64,
                         int(weights_on_host), int(embed_on_host), int(kv_on_host),
                         n_weight_slots, n_h2d_streams, chunk_bytes, max_batch, max_seq,
                         hbm_budget_bytes, debug_flags, copy_delay_us, pinned_budget_bytes,
                         copy_threads,
-                        B.PIPO_KV_FP16 if kv_fmt == "fp16" else B.PIPO_KV_INT4_G64)
+                        B.PIPO_KV_FP16 if kv_fmt == "fp16" else B.PIPO_KV_INT4_G64,
+                        int(weights_on_disk), 0,
+                        disk_dir.encode() if disk_dir is not None else None)
 
 
 class Decoder:

@@ -209,6 +209,7 @@ class Workload:
     wfmt: str            # "fp16" or "int4"
     kv_on_host: bool
     kv_fmt: str = "fp16"  # KV cache rows: "fp16" or "int4"
+    weights_on_disk: bool = False  # layers streamed from the disk tier's file
 
 
 WORKLOADS = (
@@ -223,6 +224,9 @@ WORKLOADS = (
     # the paper's other dense family (Section 4.1): LLaMA3.1-8B shape
     Workload("llama3.1-8b b16 p512 g32 fp16", LLAMA31_8B, 16, 512, 32, "fp16", False),
     Workload("llama3.1-8b b32 p512 g32 int4-g64", LLAMA31_8B, 32, 512, 32, "int4", False),
+    # the OPT-30B decode with the layers on disk (Section 3.1.1's third tier)
+    Workload("opt-30b b64 p512 g32 fp16 disk", OPT_30B, 64, 512, 32, "fp16", False,
+             weights_on_disk=True),
 )
 
 

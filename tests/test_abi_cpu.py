@@ -107,3 +107,17 @@ def test_gemm_workspace_sizes():
             ws = B.pipo_op_gemm_workspace_bytes(M, N, K, wfmt)
             assert ws % (M * N * 4) == 0 and ws // (M * N * 4) in (0, 2, 4, 8)
         assert B.pipo_op_gemm_workspace_bytes(17, 130, 4096, wfmt) == 8 * 17 * 130 * 4
+
+
+def test_disk_probe_runs_without_a_gpu(tmp_path):
+    """The disk tier's read pattern (direct I/O through a pageable chunk,
+    several threads) on a small file; the probe removes its file."""
+    gbps, direct = B.pipo_measure_disk_read(str(tmp_path), 8 << 20, 1 << 20, 3, 1)
+    assert gbps > 0
+    assert list(tmp_path.iterdir()) == []
+    with pytest.raises(B.PipoError) as e:
+        B.pipo_measure_disk_read(str(tmp_path / "missing"), 1 << 20)
+    assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_IO"
+    with pytest.raises(B.PipoError) as e:
+        B.pipo_measure_disk_read(str(tmp_path), 1 << 20, n_threads=0)
+    assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_ARG"

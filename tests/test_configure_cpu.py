@@ -118,3 +118,40 @@ def test_more_memory_never_streams_more():
             assert p["h2d_bytes_per_step"] <= last
         last = p["h2d_bytes_per_step"]
     assert last == b * 4
+
+
+def test_disk_tier_plan():
+    """The disk tier's file holds every layer unit (slot layout); a step reads
+    it once; the layers leave host memory, the head and the staging ring
+    stay; the link carries the same bytes as from host memory."""
+    b, s = 64, 544
+    host = plan(OPT30, max_batch=b, max_seq=s)
+    disk = plan(OPT30, max_batch=b, max_seq=s, weights_on_disk=True)
+    L, d, F, V = OPT30.n_layers, OPT30.d_model, OPT30.d_ffn, OPT30.vocab
+    layer_copy = (12 * d * d + 13 * d) * 2                       # fp16 tensors of a layer
+    assert disk["disk_bytes"] == disk["disk_bytes_per_step"]
+    assert 0 <= disk["disk_bytes"] - L * layer_copy < L * 5 * 4096   # 4 KiB-aligned segments
+    assert disk["h2d_bytes_per_step"] == host["h2d_bytes_per_step"]
+    ring = (16 + 1) * (64 << 20)                      # pinned ring + the direct-I/O chunk
+    assert host["host_weight_bytes"] == L * layer_copy + V * d * 2
+    assert disk["host_weight_bytes"] == V * d * 2 + ring
+    assert disk["hbm_bytes"] == host["hbm_bytes"] and host["disk_bytes"] == 0
+    with pytest.raises(B.PipoError) as e:
+        plan(OPT30, max_batch=b, max_seq=s, weights_on_host=False, weights_on_disk=True)
+    assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_UNSUPPORTED"
+
+
+def test_configure_puts_the_layers_on_disk_only_when_host_memory_is_short():
+    """Eq. (1)'s third tier: weights that fit neither in HBM nor in host
+    memory go to disk; with enough host memory the disk is not used."""
+    b, s = 64, 544
+    conf = lambda host, disk: B.pipo_configure(c_shape(OPT30), 0, 0, b, s, 80 * GB, host,  # noqa: E731
+                                               disk)
+    pol, p = conf(512 * GB, 200 * GB)
+    assert pol.weights_on_host and not pol.weights_on_disk and p["disk_bytes"] == 0
+    pol, p = conf(16 * GB, 200 * GB)                 # 60 GB of layers do not fit on the host
+    assert pol.weights_on_disk and p["disk_bytes"] > 0
+    assert p["host_weight_bytes"] + p["host_kv_bytes"] <= 16 * GB
+    with pytest.raises(B.PipoError) as e:            # no room on disk either
+        conf(16 * GB, 30 * GB)
+    assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_OOM_HOST"

@@ -131,6 +131,48 @@ def test_merged_copies_are_fewer(opt125m):
     assert 0 <= pad < L * 3 * 4096
 
 
+def test_disk_tier_bit_identical(opt125m, tmp_path):
+    """Layers streamed from the disk tier's file (disk -> pinned staging ->
+    HBM) give the resident run's tokens and logits bit for bit, across
+    pipelines; a decode step reads each layer unit once."""
+    wl, model, hw = opt125m
+    prompt = synth.prompt_tokens(4, 32, wl.shape.vocab, seed=3)
+    log("disk tier vs resident")
+    t0, l0 = _run(hw, prompt, 6, weights_on_host=False, embed_on_host=False)
+    for v in (dict(),
+              dict(n_weight_slots=1),
+              dict(n_h2d_streams=2, chunk_bytes=4096 * 37, copy_threads=3),
+              dict(chunk_bytes=1 << 20, debug_flags=B.PIPO_DBG_SEGMENT_COPIES),
+              dict(kv_on_host=True, n_weight_slots=2, embed_on_host=False),
+              dict(debug_flags=B.PIPO_DBG_POISON_SLOTS, copy_threads=1)):
+        log(f"  disk variant {v}")
+        t1, l1 = _run(hw, prompt, 6, weights_on_disk=True, disk_dir=str(tmp_path), **v)
+        assert np.array_equal(t1, t0)
+        assert np.array_equal(l1.view(np.uint32), l0.view(np.uint32))
+    assert list(tmp_path.iterdir()) == []           # the file goes with the context
+    pol = dict(max_batch=4, max_seq=40, weights_on_disk=True, disk_dir=str(tmp_path))
+    want = B.pipo_plan_policy(c_shape(wl.shape), c_policy(**pol))
+    with Decoder(hw, **pol) as dec:
+        dec.prefill(prompt)
+        dec.decode(np.zeros(4, np.int32))
+        dec.reset_stats()
+        dec.decode(np.zeros(4, np.int32))
+        st = dec.stats()
+    assert st["disk_read_bytes"] == want["disk_bytes_per_step"]
+    assert st["hbm_bytes"] == want["hbm_bytes"]
+
+
+def test_disk_tier_errors(opt125m, tmp_path):
+    wl, model, hw = opt125m
+    with pytest.raises(B.PipoError) as e:
+        Decoder(hw, max_batch=1, max_seq=8, weights_on_disk=True,
+                disk_dir=str(tmp_path / "missing"))
+    assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_IO"
+    with pytest.raises(B.PipoError) as e:
+        Decoder(hw, max_batch=1, max_seq=8, weights_on_disk=True, weights_on_host=False)
+    assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_UNSUPPORTED"
+
+
 def test_new_prefill_resets_sequences(opt125m):
     wl, model, hw = opt125m
     pa = synth.prompt_tokens(2, 20, wl.shape.vocab, seed=4)

@@ -97,6 +97,22 @@ def test_llama_streamed_parity_and_resident_identity(shape, wfmt):
         hw.free()
 
 
+def test_llama_int4_disk_tier(tmp_path):
+    """INT4 LLaMA layers streamed from the disk tier, bit-identical to the
+    resident run."""
+    model = _model(SMALL128, seed=25, wfmt="int4")
+    hw = HostWeights(SMALL128, "int4", model)
+    try:
+        prompt = synth.prompt_tokens(2, 40, SMALL128.vocab, seed=7)
+        t0, l0 = _run(hw, prompt, 5, weights_on_host=False, embed_on_host=False)
+        t1, l1 = _run(hw, prompt, 5, weights_on_disk=True, disk_dir=str(tmp_path),
+                      chunk_bytes=1 << 20)
+        assert np.array_equal(t1, t0)
+        assert np.array_equal(l1.view(np.uint32), l0.view(np.uint32))
+    finally:
+        hw.free()
+
+
 @pytest.mark.parametrize("wfmt", ["fp16", "int4"])
 def test_llama_int4_kv_cache(wfmt):
     """INT4 cache rows (keys quantized after their rotation) against the
