@@ -68,17 +68,18 @@ def gemm_family(M):
     return "gemm_skinny" if M <= 16 else ("gemm_stream" if M <= 128 else "gemm_tiled")
 
 
-def gemm_symbols(M, N, K, epi, w4):
+def gemm_symbols(M, N, K, epi, w4, frag):
     """Kernel symbols one GEMM launches: skinny (M <= 16; 64 W rows per
     workgroup when N >= 12288), streaming (16 < M <= 128; K split into the
     largest power of two <= 8 keeping the grid within 256 workgroups, plus
-    its combine kernel), or tiled."""
+    its combine kernel), or tiled; `frag`: W in fragment order."""
     b = "true" if w4 else "false"
+    pk = "true" if frag else "false"
     if M <= 16:
         nf = 4 if N >= 64 * 192 else 1
-        return [f"gemm_skinny<{nf}, 1, 8, 2, {b}, {epi}>(GemmArgs)"]
+        return [f"gemm_skinny<{nf}, 1, 8, 2, {b}, {epi}, {pk}>(GemmArgs)"]
     if M > 128:
-        return [f"gemm_tiled<{b}, {epi}>(GemmArgs)"]
+        return [f"gemm_tiled<{b}, {epi}, {pk}>(GemmArgs)"]
     mf = 2 if M <= 32 else (4 if M <= 64 else 8)
     nf, kw, pd, kc = _STREAM_SEL[(w4, mf)]
     if K % kc:
@@ -87,7 +88,7 @@ def gemm_symbols(M, N, K, epi, w4):
     S = 1
     while S < 8 and blocks * 2 * S <= 256 and K % (2 * S * kc) == 0:
         S *= 2
-    syms = [f"gemm_stream<{nf}, {mf}, {kw}, {pd}, {b}, {kc}, {epi}>(GemmArgs, float*, long)"]
+    syms = [f"gemm_stream<{nf}, {mf}, {kw}, {pd}, {b}, {kc}, {epi}, {pk}>(GemmArgs, float*, long)"]
     if S > 1:
         syms.append(f"gemm_combine<{epi}>(GemmArgs, float const*, int)")
     return syms
@@ -350,8 +351,10 @@ def main():
         if fam_key in epi:
             nk = {"oproj": (d, d), "fc1": (2 * F if llama else F, d),
                   "qkv": (d + 2 * hkv * dh, d), "head": (shape.vocab, d)}
+            # layer matrices stream in fragment order (HostWeights' default),
+            # the output head is row-major
             symbols = gemm_symbols(wl.batch, *nk[fam_key], epi[fam_key],
-                                   wl.wfmt == "int4" and fam_key != "head")
+                                   wl.wfmt == "int4" and fam_key != "head", fam_key != "head")
         elif fam_key == "attention":
             kv4 = "true" if wl.kv_fmt == "int4" else "false"
             G = shape.n_heads // hkv

@@ -146,12 +146,31 @@ typedef struct {
   pipo_q4 qqkv, qo, q1, q2;        /* same matrices                         (PIPO_W_INT4_G64) */
 } pipo_layer_host;
 
+/* Layout of the four layer matrices in pipo_host_weights (pipo_host_weights.layout).
+ *  PIPO_LAYOUT_ROW_MAJOR: W[N][K] row-major; INT4 as pipo_q4 describes.
+ *  PIPO_LAYOUT_FRAGMENT: the layout the decode kernels read fastest (one
+ *    contiguous 1 KiB per wave load; pipo_pack_f16 / pipo_pack_w4 produce
+ *    it): fp16 W in blocks of 16 rows x 32 k, block (rg, kb) at halves
+ *    512 (rg K/32 + kb), inside which the 16 bytes at 16 (r + 16 g) hold
+ *    W[16 rg + r][32 kb + 8 g .. + 7]; INT4 codes in blocks of 16 rows x
+ *    128 k, block (rg, kb) at byte 1024 (rg K/128 + kb), the 16 bytes at
+ *    16 (r + 16 g) holding row 16 rg + r's codes for k = 128 kb + 32 g ..
+ *    + 31 (nibble order as row-major); (scale, min) pairs in 32-pair
+ *    blocks, pair 32 (rg K/128 + kb) + 2 r + j = row 16 rg + r, group
+ *    2 kb + j.  Every layer matrix has N % 16 == 0 and K % 128 == 0.
+ * With row-major input the library converts what it copies (its own
+ * pinned regions, resident HBM copies, the disk tier's file); matrices it
+ * would stream in place from pipo_host_alloc memory keep the row-major
+ * layout for the whole context.  The output head is always row-major. */
+enum { PIPO_LAYOUT_ROW_MAJOR = 0, PIPO_LAYOUT_FRAGMENT = 1 };
+
 typedef struct {
   const uint16_t* tok_emb;   /* [vocab][d]; OPT: also the output head (tied) */
   const uint16_t* pos_emb;   /* OPT: [max_pos + pos_offset][d]; LLaMA: unused */
   const uint16_t *lnf_g, *lnf_b;   /* final norm [d] (LLaMA: lnf_b unused) */
   const pipo_layer_host* layers;   /* [n_layers] */
   const uint16_t* lm_head;   /* LLaMA: output head [vocab][d]; OPT: unused */
+  int32_t layout;            /* PIPO_LAYOUT_* of the layer matrices */
 } pipo_host_weights;
 
 /* Offload policy (the paper's (S_off, S_pipe) pair, Algorithm 2, made
@@ -376,6 +395,15 @@ pipo_status pipo_measure_h2d_chunked(int64_t bytes, int64_t chunk_bytes, int32_t
 pipo_status pipo_measure_disk_read(const char* dir, int64_t bytes, int64_t chunk_bytes,
                                    int32_t n_threads, int32_t iters, double* gbps,
                                    int32_t* direct);
+
+/* Row-major -> PIPO_LAYOUT_FRAGMENT on the host (caller buffers, not
+ * overlapping): fp16 W[N][K] into out (N*K halves), or INT4 codes and
+ * (scale, min) pairs into q_out (N*K/2 bytes) and scale_min_out (N*K/32
+ * halves).  Errors: ARG (NULL, aliasing, N % 16, K % 32 (fp16) or K % 128
+ * (INT4) not 0). */
+pipo_status pipo_pack_f16(const uint16_t* W, uint16_t* out, int64_t N, int64_t K);
+pipo_status pipo_pack_w4(const uint8_t* q, const uint16_t* scale_min, uint8_t* q_out,
+                         uint16_t* scale_min_out, int64_t N, int64_t K);
 
 /* Pinned (page-locked) host memory, 4 KiB aligned; NULL on failure.
  * Matrices placed here are streamed by the copy engines without staging. */

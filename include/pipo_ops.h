@@ -56,6 +56,17 @@ pipo_status pipo_op_gemm_w4(const uint16_t* X, const uint8_t* Wq, const uint16_t
                             int32_t epi, void* workspace, int64_t workspace_bytes,
                             void* stream);
 
+/* The same two GEMMs with W (or Wq, Wsm) in PIPO_LAYOUT_FRAGMENT order
+ * (pipo.h; N % 16 == 0): same kernels, same summation order, so the result
+ * equals the row-major call bit for bit. */
+pipo_status pipo_op_gemm_f16_frag(const uint16_t* X, const uint16_t* W, const uint16_t* bias,
+                                  void* out, int64_t M, int64_t N, int64_t K, int32_t epi,
+                                  void* workspace, int64_t workspace_bytes, void* stream);
+pipo_status pipo_op_gemm_w4_frag(const uint16_t* X, const uint8_t* Wq, const uint16_t* Wsm,
+                                 const uint16_t* bias, void* out, int64_t M, int64_t N,
+                                 int64_t K, int32_t epi, void* workspace,
+                                 int64_t workspace_bytes, void* stream);
+
 /* Workspace bytes the GEMM of this shape uses to split K (0: never splits).
  * wfmt: PIPO_W_FP16 or PIPO_W_INT4_G64. */
 int64_t pipo_op_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int32_t wfmt);

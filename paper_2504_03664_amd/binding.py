@@ -26,6 +26,7 @@ STATUS_NAMES = {0: "PIPO_OK", -1: "PIPO_ERR_ARG", -2: "PIPO_ERR_OOM_DEVICE",
                 -6: "PIPO_ERR_UNSUPPORTED", -7: "PIPO_ERR_IO"}
 PIPO_W_FP16, PIPO_W_INT4_G64 = 0, 1
 PIPO_FAMILY_OPT, PIPO_FAMILY_LLAMA = 0, 1
+PIPO_LAYOUT_ROW_MAJOR, PIPO_LAYOUT_FRAGMENT = 0, 1
 PIPO_KV_FP16, PIPO_KV_INT4_G64 = 0, 1
 PIPO_PIPE_PERFORMANCE, PIPO_PIPE_MEMORY_EFFICIENT = 0, 1
 PIPO_DBG_POISON_SLOTS, PIPO_DBG_COPY_DELAY, PIPO_DBG_TIMESTAMPS = 1, 2, 4
@@ -54,7 +55,7 @@ class PipoLayerHost(ctypes.Structure):
 
 class PipoHostWeights(ctypes.Structure):
     _fields_ = [("tok_emb", vp), ("pos_emb", vp), ("lnf_g", vp), ("lnf_b", vp),
-                ("layers", ctypes.POINTER(PipoLayerHost)), ("lm_head", vp)]
+                ("layers", ctypes.POINTER(PipoLayerHost)), ("lm_head", vp), ("layout", i32)]
 
 
 class PipoPolicy(ctypes.Structure):
@@ -140,6 +141,10 @@ _SIGNATURES = {
     "pipo_op_gemm_f16": ([vp, vp, vp, vp, i64, i64, i64, i32, vp, i64, vp], i32),
     "pipo_op_gemm_w4": ([vp, vp, vp, vp, vp, i64, i64, i64, i32, vp, i64, vp], i32),
     "pipo_op_gemm_workspace_bytes": ([i64, i64, i64, i32], i64),
+    "pipo_op_gemm_f16_frag": ([vp, vp, vp, vp, i64, i64, i64, i32, vp, i64, vp], i32),
+    "pipo_op_gemm_w4_frag": ([vp, vp, vp, vp, vp, i64, i64, i64, i32, vp, i64, vp], i32),
+    "pipo_pack_f16": ([vp, vp, i64, i64], i32),
+    "pipo_pack_w4": ([vp, vp, vp, vp, i64, i64], i32),
     "pipo_op_layernorm": ([vp, vp, vp, vp, i64, i64, i64, i64, f32, vp], i32),
     "pipo_op_attn_decode": ([vp, vp, vp, vp, i32, i32, i32, i32, vp, i64, vp], i32),
     "pipo_op_attn_decode_workspace_bytes": ([i32, i32, i32, i32], i64),
@@ -373,6 +378,42 @@ def pipo_op_gemm_w4(X, Wq, Wsm, bias, out, M, N, K, epi, workspace=None, workspa
                     stream=None):
     _check(lib().pipo_op_gemm_w4(X, Wq, Wsm, bias, out, M, N, K, epi, workspace,
                                  workspace_bytes, stream), "pipo_op_gemm_w4")
+
+
+def pipo_op_gemm_f16_frag(X, W, bias, out, M, N, K, epi, workspace=None, workspace_bytes=0,
+                          stream=None):
+    _check(lib().pipo_op_gemm_f16_frag(X, W, bias, out, M, N, K, epi, workspace,
+                                       workspace_bytes, stream), "pipo_op_gemm_f16_frag")
+
+
+def pipo_op_gemm_w4_frag(X, Wq, Wsm, bias, out, M, N, K, epi, workspace=None, workspace_bytes=0,
+                         stream=None):
+    _check(lib().pipo_op_gemm_w4_frag(X, Wq, Wsm, bias, out, M, N, K, epi, workspace,
+                                      workspace_bytes, stream), "pipo_op_gemm_w4_frag")
+
+
+def pipo_pack_f16(W: np.ndarray, out: Optional[np.ndarray] = None) -> np.ndarray:
+    """Row-major fp16 W [N][K] -> PIPO_LAYOUT_FRAGMENT (flat, N*K halves)."""
+    W = np.ascontiguousarray(W)
+    N, K = W.shape
+    if out is None:
+        out = np.empty(N * K, dtype=W.dtype)
+    _check(lib().pipo_pack_f16(_ptr(W), _ptr(out), N, K), "pipo_pack_f16")
+    return out
+
+
+def pipo_pack_w4(q: np.ndarray, sm: np.ndarray, q_out: Optional[np.ndarray] = None,
+                 sm_out: Optional[np.ndarray] = None):
+    """Row-major INT4 (q [N][K/2], sm [N][K/64][2]) -> PIPO_LAYOUT_FRAGMENT."""
+    q, sm = np.ascontiguousarray(q), np.ascontiguousarray(sm)
+    N, K = q.shape[0], q.shape[1] * 2
+    if q_out is None:
+        q_out = np.empty(q.size, dtype=np.uint8)
+    if sm_out is None:
+        sm_out = np.empty(sm.size, dtype=sm.dtype)
+    _check(lib().pipo_pack_w4(_ptr(q), _ptr(sm), _ptr(q_out), _ptr(sm_out), N, K),
+           "pipo_pack_w4")
+    return q_out, sm_out
 
 
 def pipo_op_gemm_workspace_bytes(M, N, K, wfmt) -> int:

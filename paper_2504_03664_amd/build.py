@@ -27,7 +27,7 @@ ARCH = "gfx950"
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall",
              "-Wno-unused-result"]
-SOURCES = ["gemm.hip", "attention.hip", "kvcache.hip", "elementwise.hip", "engine.cpp", "config.cpp", "ops_api.cpp",
+SOURCES = ["gemm.hip", "attention.hip", "kvcache.hip", "elementwise.hip", "engine.cpp", "config.cpp", "pack.cpp", "ops_api.cpp",
            "schedule.cpp", "sched_capi.cpp"]
 SCHED_SOURCES = ["schedule.cpp", "sched_capi.cpp"]
 

@@ -71,6 +71,7 @@ struct GemmArgs {
   const uint16_t* Wsm = nullptr;  // [N][K/64][2] fp16 (scale, min)
   const uint16_t* bias = nullptr; // [N] fp16 or null
   int64_t M = 0, N = 0, K = 0;
+  bool packed = false;            // W (or Wq, Wsm) in fragment order (device.h)
   uint16_t* out16 = nullptr;      // [M][ldo]
   float* out32 = nullptr;         // [M][ldo]
   int64_t ldo = 0;

@@ -91,6 +91,41 @@ __device__ __forceinline__ h8 interleave_h8(h8 x) {
   return __builtin_bit_cast(h8, o);
 }
 
+// Weight addressing, row-major or fragment order (PK).  In fragment order a
+// 16-row x 32-k block of an fp16 matrix is 512 contiguous halves in MFMA
+// operand order: lane slot L = r + 16 g (16 bytes) holds row r, k = 8 g ..
+// 8 g + 7 of the block; blocks follow each other by k, then by row group,
+// so the 64 lanes of a wave read 1 KiB contiguous per load.  INT4 codes:
+// a 16-row x 128-k block is 1 KiB, lane slot r + 16 g holds row r's codes
+// for k = 32 g .. 32 g + 31 (byte j: codes 2j, 2j+1 as in a row-major row);
+// its (scale, min) pairs are 32 u32, row r's two groups at 2 r, 2 r + 1.
+// Fragment order needs N % 16 == 0 (and K % 128 == 0 for INT4).
+template <bool PK>
+__device__ __forceinline__ int64_t w16_index(int64_t n, int64_t k, int64_t K) {
+  if constexpr (PK)
+    return ((n >> 4) * (K >> 5) + (k >> 5)) * 512 + (((n & 15) + 16 * ((k >> 3) & 3)) << 3) +
+           (k & 7);
+  else
+    return n * K + k;
+}
+// byte of INT4 codes (k, k + 1), k even
+template <bool PK>
+__device__ __forceinline__ int64_t w4_byte(int64_t n, int64_t k, int64_t K) {
+  if constexpr (PK)
+    return ((n >> 4) * (K >> 7) + (k >> 7)) * 1024 + (((n & 15) + 16 * ((k >> 5) & 3)) << 4) +
+           ((k & 31) >> 1);
+  else
+    return n * (K / 2) + k / 2;
+}
+// u32 index of the (scale, min) pair of the group holding k
+template <bool PK>
+__device__ __forceinline__ int64_t w4_sm(int64_t n, int64_t k, int64_t K) {
+  if constexpr (PK)
+    return ((n >> 4) * (K >> 7) + (k >> 7)) * 32 + (n & 15) * 2 + ((k >> 6) & 1);
+  else
+    return n * (K / 64) + k / 64;
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_shfl_xor(T v, int mask) {
   return __shfl_xor(v, mask, 64);

@@ -37,6 +37,7 @@
 #include <vector>
 
 #include "common.h"
+#include "pack.h"
 #include "plan.h"
 #include "schedule.h"
 
@@ -262,6 +263,8 @@ struct pipo_ctx {
   int64_t Hkv = 0, dkv = 0;    // key/value heads and the width of a cached row
   bool llama = false;          // PIPO_FAMILY_LLAMA
   bool w4 = false;
+  bool packed = false;         // layer matrices in HBM are in fragment order
+  bool pack_on_copy = false;   // row-major input, converted wherever the library copies it
   int device = 0;
   hipStream_t st[kNumStreams] = {};
   std::vector<hipEvent_t> ev;
@@ -274,6 +277,7 @@ struct pipo_ctx {
 
   // host side
   std::vector<std::vector<const void*>> layer_src;  // [L][seg] host pointer
+  std::vector<std::vector<bool>> layer_copied;      // [L][seg] in the library's own region
   const void* head_src = nullptr;
   const uint16_t* tok_host = nullptr;               // for the host-side gather
   std::vector<void*> pinned;                        // library-owned pinned buffers
@@ -433,6 +437,7 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
     ga.M = M;
     ga.N = N;
     ga.K = K;
+    ga.packed = c->packed;
     if (c->w4) {
       ga.Wq = reinterpret_cast<const uint8_t*>(base + c->seg_off[seg]);
       ga.Wsm = reinterpret_cast<const uint16_t*>(base + c->seg_off[seg + 1]);
@@ -851,6 +856,38 @@ static void destroy_ctx(pipo_ctx* c) {
   delete c;
 }
 
+// (N, K) of the matrix a segment belongs to
+static void seg_matrix(const pipo_ctx* c, int sg, int64_t* N, int64_t* K) {
+  const int m = (sg - kSegWqkv) / 2;
+  const int64_t rows[4] = {qkv_rows(c->sh), c->d, fc1_rows(c->sh), c->d};
+  const int64_t cols[4] = {c->d, c->d, c->d, c->F};
+  *N = rows[m];
+  *K = cols[m];
+}
+
+// a matrix segment converted from row-major to fragment order into dst
+static void pack_segment(const pipo_ctx* c, int sg, const void* src, void* dst) {
+  int64_t N, K;
+  seg_matrix(c, sg, &N, &K);
+  if (!c->w4)
+    pack_f16(static_cast<const uint16_t*>(src), static_cast<uint16_t*>(dst), N, K);
+  else if ((sg - kSegWqkv) % 2 == 0)
+    pack_w4_codes(static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), N, K);
+  else
+    pack_w4_scale_min(static_cast<const uint16_t*>(src), static_cast<uint16_t*>(dst), N, K);
+}
+
+// the bytes of segment sg of layer j as they go to HBM (converted into tmp
+// when the library converts what it copies)
+static const char* seg_bytes_for_device(const pipo_ctx* c, int64_t j, int sg,
+                                        std::vector<char>& tmp) {
+  const char* src = static_cast<const char*>(c->layer_src[j][sg]);
+  if (!c->pack_on_copy || sg == kSegMisc || src == nullptr || c->layer_copied[j][sg]) return src;
+  tmp.resize((size_t)c->seg_bytes[sg]);
+  pack_segment(c, sg, src, tmp.data());
+  return tmp.data();
+}
+
 // The disk tier's file: every layer unit in slot layout (small tensors,
 // then the matrices at their 4 KiB-aligned offsets, zero padding), layer j
 // at j * layer_bytes.  Created in disk_dir and unlinked at once, so it
@@ -886,7 +923,12 @@ static pipo_status write_disk_tier(pipo_ctx* c) {
   }
   char* buf = c->disk_bounce;  // pageable: direct I/O cannot use pinned pages
   const int64_t piece = c->pol.chunk_bytes;
+  std::vector<std::vector<char>> tmp((size_t)kNumSegs);
   for (int64_t j = 0; j < c->L; ++j) {
+    const char* seg_src[kNumSegs] = {};
+    for (int sg = 0; sg < kNumSegs; ++sg)
+      if (sg != kSegHead && c->seg_bytes[sg] > 0)
+        seg_src[sg] = seg_bytes_for_device(c, j, sg, tmp[(size_t)sg]);
     for (int64_t o = 0; o < c->layer_bytes; o += piece) {
       const int64_t n = std::min(piece, c->layer_bytes - o);
       int64_t cursor = o;  // [o, cursor) is filled
@@ -896,9 +938,7 @@ static pipo_status write_disk_tier(pipo_ctx* c) {
         const int64_t hi = std::min(o + n, c->seg_off[sg] + c->seg_bytes[sg]);
         if (lo >= hi) continue;
         if (lo > cursor) std::memset(buf + (cursor - o), 0, (size_t)(lo - cursor));
-        c->pool->copy(buf + (lo - o),
-                      static_cast<const char*>(c->layer_src[j][sg]) + (lo - c->seg_off[sg]),
-                      (size_t)(hi - lo));
+        c->pool->copy(buf + (lo - o), seg_src[sg] + (lo - c->seg_off[sg]), (size_t)(hi - lo));
         cursor = hi;
       }
       if (cursor < o + n) std::memset(buf + (cursor - o), 0, (size_t)(o + n - cursor));
@@ -965,6 +1005,41 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   // disk tier they are only read once, to write the file
   const bool need_host = pol.weights_on_host != 0 && !pol.weights_on_disk;
   c->layer_src.assign((size_t)L, std::vector<const void*>(kNumSegs, nullptr));
+  c->layer_copied.assign((size_t)L, std::vector<bool>(kNumSegs, false));
+  const auto layer_mats = [&](int64_t j, const void* (&mats)[8]) {
+    const pipo_layer_host& lw = w->layers[j];
+    if (c->w4) {
+      const pipo_q4* q4[4] = {&lw.qqkv, &lw.qo, &lw.q1, &lw.q2};
+      for (int i = 0; i < 4; ++i) {
+        mats[2 * i] = q4[i]->q;
+        mats[2 * i + 1] = q4[i]->scale_min;
+      }
+    } else {
+      const uint16_t* m16[4] = {lw.wqkv, lw.wo, lw.w1, lw.w2};
+      for (int i = 0; i < 4; ++i) {
+        mats[2 * i] = m16[i];
+        mats[2 * i + 1] = nullptr;
+      }
+    }
+  };
+  // Layout: fragment order unless row-major matrices would be streamed in
+  // place from pinned caller memory (then everything stays row-major)
+  if (w->layout != PIPO_LAYOUT_ROW_MAJOR && w->layout != PIPO_LAYOUT_FRAGMENT) {
+    set_error("unknown weight layout %d", w->layout);
+    return PIPO_ERR_ARG;
+  }
+  bool in_place_row_major = false;
+  if (w->layout == PIPO_LAYOUT_ROW_MAJOR && need_host)
+    for (int64_t j = 0; j < L && !in_place_row_major; ++j) {
+      const void* mats[8];
+      layer_mats(j, mats);
+      for (int i = 0; i < 8; ++i)
+        if (c->seg_bytes[kSegWqkv + i] > 0 && mats[i] &&
+            is_registered_pinned(mats[i], (size_t)c->seg_bytes[kSegWqkv + i]))
+          in_place_row_major = true;
+    }
+  c->packed = w->layout == PIPO_LAYOUT_FRAGMENT || !in_place_row_major;
+  c->pack_on_copy = c->packed && w->layout == PIPO_LAYOUT_ROW_MAJOR;
   void* misc_all = nullptr;
   PIPO_TRY(pin_alloc(c, &misc_all, L * c->misc_bytes));
   for (int64_t j = 0; j < L; ++j) {
@@ -982,19 +1057,7 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
     }
     c->layer_src[j][kSegMisc] = (char*)misc_all + j * c->misc_bytes;
     const void* mats[8];
-    if (c->w4) {
-      const pipo_q4* q4[4] = {&lw.qqkv, &lw.qo, &lw.q1, &lw.q2};
-      for (int i = 0; i < 4; ++i) {
-        mats[2 * i] = q4[i]->q;
-        mats[2 * i + 1] = q4[i]->scale_min;
-      }
-    } else {
-      const uint16_t* m16[4] = {lw.wqkv, lw.wo, lw.w1, lw.w2};
-      for (int i = 0; i < 4; ++i) {
-        mats[2 * i] = m16[i];
-        mats[2 * i + 1] = nullptr;
-      }
-    }
+    layer_mats(j, mats);
     int64_t copy_bytes = 0;
     for (int i = 0; i < 8; ++i) {
       const int sg = kSegWqkv + i;
@@ -1015,8 +1078,12 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
         const int sg = kSegWqkv + i;
         if (c->seg_bytes[sg] == 0 || is_registered_pinned(mats[i], (size_t)c->seg_bytes[sg]))
           continue;
-        par_memcpy((char*)merged + o2, mats[i], (size_t)c->seg_bytes[sg]);
+        if (c->pack_on_copy)
+          pack_segment(c, sg, mats[i], (char*)merged + o2);
+        else
+          par_memcpy((char*)merged + o2, mats[i], (size_t)c->seg_bytes[sg]);
         c->layer_src[j][sg] = (char*)merged + o2;
+        c->layer_copied[j][sg] = true;  // already in the device layout
         o2 = align_up(o2 + c->seg_bytes[sg], 4096);
       }
     }
@@ -1083,11 +1150,12 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   if (!pol.weights_on_host) {
     PIPO_TRY(dev_alloc(c, &p, hp.resident));
     c->resident = (char*)p;
+    std::vector<char> tmp;
     for (int64_t j = 0; j < L; ++j)
       for (int sg = 0; sg < kNumSegs; ++sg)
         if (c->seg_bytes[sg] > 0 && sg != kSegHead)
           PIPO_HIP_TRY(hipMemcpy(c->resident + j * c->layer_bytes + c->seg_off[sg],
-                                 c->layer_src[j][sg], (size_t)c->seg_bytes[sg],
+                                 seg_bytes_for_device(c, j, sg, tmp), (size_t)c->seg_bytes[sg],
                                  hipMemcpyHostToDevice));
   }
   if (!pol.embed_on_host) {

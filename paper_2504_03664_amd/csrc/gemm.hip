@@ -63,7 +63,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int64_t m, int64_t n
 // of the 16 lanes of a row covers 64 contiguous bytes (k = 32 i + 8 g), INT4
 // codes as 32 consecutive k per lane (k = 32 g + 8 i).  Wave partials are
 // added in LDS in wave order, then the epilogue runs.
-template <int NF, int MF, int KW, int UNR, bool W4>
+template <int NF, int MF, int KW, int UNR, bool W4, bool PK>
 struct SkinnyStep {
   u32x4 w[NF][4];  // fp16: four 8-half chunks; int4: w[f][0] holds 32 codes
   uint32_t sm[NF];
@@ -79,14 +79,14 @@ struct SkinnyStep {
       const bool ok = n < a.N;
       if constexpr (W4) {
         const int64_t kb = s * 128 + 32 * g;
-        w[f][0] = ok ? *reinterpret_cast<const u32x4*>(a.Wq + n * (K / 2) + kb / 2)
+        w[f][0] = ok ? *reinterpret_cast<const u32x4*>(a.Wq + w4_byte<PK>(n, kb, K))
                      : u32x4{0, 0, 0, 0};
-        sm[f] = ok ? *reinterpret_cast<const uint32_t*>(a.Wsm + (n * (K / 64) + kb / 64) * 2) : 0u;
+        sm[f] = ok ? *reinterpret_cast<const uint32_t*>(a.Wsm + w4_sm<PK>(n, kb, K) * 2) : 0u;
       } else {
-        const uint16_t* p = a.W + n * K + s * 128;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          w[f][i] = ok ? *reinterpret_cast<const u32x4*>(p + koff(i, g)) : u32x4{0, 0, 0, 0};
+          w[f][i] = ok ? *reinterpret_cast<const u32x4*>(a.W + w16_index<PK>(n, s * 128 + koff(i, g), K))
+                       : u32x4{0, 0, 0, 0};
       }
     }
 #pragma unroll
@@ -120,7 +120,7 @@ struct SkinnyStep {
   }
 };
 
-template <int NF, int MF, int KW, int UNR, bool W4, int EPI>
+template <int NF, int MF, int KW, int UNR, bool W4, int EPI, bool PK>
 __global__ __launch_bounds__(KW * 64) void gemm_skinny(GemmArgs a) {
   __shared__ f4 red[KW][NF][MF][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -135,7 +135,7 @@ __global__ __launch_bounds__(KW * 64) void gemm_skinny(GemmArgs a) {
     for (int mf = 0; mf < MF; ++mf) acc[f][mf] = f4{0.f, 0.f, 0.f, 0.f};
 
   for (int64_t s = wave; s < nsteps; s += UNR * KW) {
-    SkinnyStep<NF, MF, KW, UNR, W4> st[UNR];
+    SkinnyStep<NF, MF, KW, UNR, W4, PK> st[UNR];
 #pragma unroll
     for (int u = 0; u < UNR; ++u)
       if (s + u * KW < nsteps) st[u].load(a, n0, s + u * KW, r, g);
@@ -190,7 +190,7 @@ struct StreamCfg {
 
 __device__ __forceinline__ int64_t clamp_hi(int64_t v, int64_t hi) { return v < hi ? v : hi; }
 
-template <int NF, int MF, int KW, int PD, bool W4, int KC, int EPI>
+template <int NF, int MF, int KW, int PD, bool W4, int KC, int EPI, bool PK>
 __global__ __launch_bounds__(KW * 64) void gemm_stream(GemmArgs a, float* part, int64_t kper) {
   using C = StreamCfg<NF, MF, KW, PD, W4, KC>;
   __shared__ __attribute__((aligned(16))) uint16_t Xs[2][C::kXRows * C::kXLd];
@@ -217,13 +217,13 @@ __global__ __launch_bounds__(KW * 64) void gemm_stream(GemmArgs a, float* part, 
 #pragma unroll
         for (int t = 0; t < KC / 128; ++t) {
           const int64_t kb = k0 + 128 * t + 32 * g;
-          F.w[f][t] = *reinterpret_cast<const u32x4*>(a.Wq + wrow[f] * (K / 2) + kb / 2);
-          F.sm[f][t] = *reinterpret_cast<const uint32_t*>(a.Wsm + (wrow[f] * (K / 64) + kb / 64) * 2);
+          F.w[f][t] = *reinterpret_cast<const u32x4*>(a.Wq + w4_byte<PK>(wrow[f], kb, K));
+          F.sm[f][t] = *reinterpret_cast<const uint32_t*>(a.Wsm + w4_sm<PK>(wrow[f], kb, K) * 2);
         }
       } else {
 #pragma unroll
         for (int i = 0; i < C::kWRegs; ++i)
-          F.w[f][i] = *reinterpret_cast<const u32x4*>(a.W + wrow[f] * K + k0 + 32 * i + 8 * g);
+          F.w[f][i] = *reinterpret_cast<const u32x4*>(a.W + w16_index<PK>(wrow[f], k0 + 32 * i + 8 * g, K));
       }
     }
   };
@@ -337,7 +337,7 @@ constexpr int kTThreads = 256;  // 2 x 2 waves of 64 x 64
 constexpr int kXcds = 8;        // accelerator complex dies of an MI355X, each with its own L2
 constexpr int kTGroupM = 8;
 
-template <bool W4, int EPI>
+template <bool W4, int EPI, bool PK>
 __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
   constexpr int LDS_ROW = kTBK + kTPad;  // halves
   __shared__ __attribute__((aligned(16))) uint16_t As[2][kTBM * LDS_ROW];
@@ -367,6 +367,12 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
 
   // global -> register staging: A and fp16 B take 4 chunks of 8 halves per
   // thread (row = c / 8, col = 8 (c % 8)); INT4 B takes one 32-code chunk.
+  // With B in fragment order a wave's 64 chunks are one 16-row x 32-k
+  // block (1 KiB contiguous; INT4: 32 threads read a 512-byte half block).
+  const auto b_row = [](int c) { return PK ? ((c >> 7) << 4) + (c & 15) : c >> 3; };
+  const auto b_col = [](int c) { return PK ? ((c >> 6) & 1) * 32 + ((c >> 4) & 3) * 8 : (c & 7) * 8; };
+  const auto b_row_w4 = [](int t, int64_t) { return PK ? ((t >> 5) << 4) + (t & 15) : t >> 1; };
+  const auto b_half_w4 = [](int t, int64_t) { return PK ? (t >> 4) & 1 : t & 1; };
   h8 ra[4], rb[4];
   const auto load_tile = [&](int64_t kt) {
 #pragma unroll
@@ -377,12 +383,12 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
       ra[i] = m < a.M ? load_h8(a.X + m * K + kt * kTBK + col) : zero_h8();
     }
     if constexpr (W4) {
-      const int row = tid >> 1, half = tid & 1;
+      const int row = b_row_w4(tid, kt), half = b_half_w4(tid, kt);
       const int64_t n = n0 + row;
       if (n < a.N) {
-        const u32x4 codes =
-            *reinterpret_cast<const u32x4*>(a.Wq + n * (K / 2) + kt * (kTBK / 2) + half * 16);
-        const uint32_t smw = *reinterpret_cast<const uint32_t*>(a.Wsm + (n * (K / 64) + kt) * 2);
+        const int64_t kc = kt * kTBK + half * 32;
+        const u32x4 codes = *reinterpret_cast<const u32x4*>(a.Wq + w4_byte<PK>(n, kc, K));
+        const uint32_t smw = *reinterpret_cast<const uint32_t*>(a.Wsm + w4_sm<PK>(n, kc, K) * 2);
         h2 s2, m2;
         scale_min_pairs(smw, s2, m2);
 #pragma unroll
@@ -395,9 +401,9 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int c = tid + i * kTThreads;
-        const int row = c >> 3, col = (c & 7) * 8;
+        const int row = b_row(c), col = b_col(c);
         const int64_t n = n0 + row;
-        rb[i] = n < a.N ? load_h8(a.W + n * K + kt * kTBK + col) : zero_h8();
+        rb[i] = n < a.N ? load_h8(a.W + w16_index<PK>(n, kt * kTBK + col, K)) : zero_h8();
       }
     }
   };
@@ -409,7 +415,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
       *reinterpret_cast<h8*>(&As[buf][row * LDS_ROW + col]) = ra[i];
     }
     if constexpr (W4) {
-      const int row = tid >> 1, half = tid & 1;
+      const int row = b_row_w4(tid, 0), half = b_half_w4(tid, 0);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         *reinterpret_cast<h8*>(&Bs[buf][row * LDS_ROW + half * 32 + 8 * i]) = rb[i];
@@ -417,8 +423,7 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int c = tid + i * kTThreads;
-        const int row = c >> 3, col = (c & 7) * 8;
-        *reinterpret_cast<h8*>(&Bs[buf][row * LDS_ROW + col]) = rb[i];
+        *reinterpret_cast<h8*>(&Bs[buf][b_row(c) * LDS_ROW + b_col(c)]) = rb[i];
       }
     }
   };
@@ -471,11 +476,11 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
 template <int MF> struct SkinnyCfg;
 template <> struct SkinnyCfg<1> { static constexpr int KW = 8, UNR = 2; };
 
-template <int NF, bool W4, int EPI>
+template <int NF, bool W4, int EPI, bool PK>
 static void launch_skinny(const GemmArgs& a, hipStream_t st) {
   using C = SkinnyCfg<1>;
   const dim3 grid((unsigned)((a.N + 16 * NF - 1) / (16 * NF)));
-  launch((gemm_skinny<NF, 1, C::KW, C::UNR, W4, EPI>), grid, dim3(C::KW * 64), 0, st, a);
+  launch((gemm_skinny<NF, 1, C::KW, C::UNR, W4, EPI, PK>), grid, dim3(C::KW * 64), 0, st, a);
 }
 
 // streaming configurations by (W format, 16-row blocks of X): rows per
@@ -553,11 +558,12 @@ int64_t gemm_workspace_bytes_upto(int64_t M_max, int64_t N, int64_t K, bool w4) 
   return best;
 }
 
-template <int NF, int MF, int KW, int PD, bool W4, int KC, int EPI>
+template <int NF, int MF, int KW, int PD, bool W4, int KC, int EPI, bool PK>
 static void launch_stream_cfg(const GemmArgs& a, int S, float* ws, hipStream_t st) {
   constexpr int rows = 16 * NF * KW;
   const dim3 grid((unsigned)((a.N + rows - 1) / rows), (unsigned)S);
-  launch((gemm_stream<NF, MF, KW, PD, W4, KC, EPI>), grid, dim3(KW * 64), 0, st, a, ws, a.K / S);
+  launch((gemm_stream<NF, MF, KW, PD, W4, KC, EPI, PK>), grid, dim3(KW * 64), 0, st, a, ws,
+         a.K / S);
   if (S > 1) {
     const int64_t MN = a.M * a.N;
     launch((gemm_combine<EPI>), dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, st, a,
@@ -565,55 +571,56 @@ static void launch_stream_cfg(const GemmArgs& a, int S, float* ws, hipStream_t s
   }
 }
 
-template <bool W4, int MF, int EPI>
+template <bool W4, int MF, int EPI, bool PK>
 static void launch_stream_mf(const GemmArgs& a, const StreamPlan& pl, int S, float* ws,
                              hipStream_t st) {
   if (pl.fallback) {
     using B = StreamFallback<W4, MF>;
-    launch_stream_cfg<B::NF, MF, B::KW, B::PD, W4, B::KC, EPI>(a, S, ws, st);
+    launch_stream_cfg<B::NF, MF, B::KW, B::PD, W4, B::KC, EPI, PK>(a, S, ws, st);
   } else {
     using P = StreamSel<W4, MF>;
-    launch_stream_cfg<P::NF, MF, P::KW, P::PD, W4, P::KC, EPI>(a, S, ws, st);
+    launch_stream_cfg<P::NF, MF, P::KW, P::PD, W4, P::KC, EPI, PK>(a, S, ws, st);
   }
 }
 
-template <bool W4, int EPI>
+template <bool W4, int EPI, bool PK>
 static pipo_status launch_epi(const GemmArgs& a, float* ws, int64_t ws_bytes, hipStream_t st) {
   if (a.M <= 16) {
     // 64 W rows per workgroup (less X traffic per W byte) once that still
     // gives enough workgroups to fill the chip, else 16
     if (a.N >= 64 * 192)
-      launch_skinny<4, W4, EPI>(a, st);
+      launch_skinny<4, W4, EPI, PK>(a, st);
     else
-      launch_skinny<1, W4, EPI>(a, st);
+      launch_skinny<1, W4, EPI, PK>(a, st);
   } else if (a.M <= kStreamMaxM) {
     const StreamPlan pl = stream_plan(a.M, a.N, a.K, W4);
     // without room for the partial sums the K split is dropped
     const int S = (pl.splits > 1 && ws != nullptr &&
                    ws_bytes >= (int64_t)pl.splits * a.M * a.N * 4) ? pl.splits : 1;
     switch (stream_mf(a.M)) {
-      case 2: launch_stream_mf<W4, 2, EPI>(a, pl, S, ws, st); break;
-      case 4: launch_stream_mf<W4, 4, EPI>(a, pl, S, ws, st); break;
-      default: launch_stream_mf<W4, 8, EPI>(a, pl, S, ws, st); break;
+      case 2: launch_stream_mf<W4, 2, EPI, PK>(a, pl, S, ws, st); break;
+      case 4: launch_stream_mf<W4, 4, EPI, PK>(a, pl, S, ws, st); break;
+      default: launch_stream_mf<W4, 8, EPI, PK>(a, pl, S, ws, st); break;
     }
   } else {
     const int64_t total = ((a.N + kTBN - 1) / kTBN) * ((a.M + kTBM - 1) / kTBM);
     const int64_t per_xcd = (total + kXcds - 1) / kXcds;
-    launch((gemm_tiled<W4, EPI>), dim3((unsigned)(per_xcd * kXcds)), dim3(kTThreads), 0, st, a);
+    launch((gemm_tiled<W4, EPI, PK>), dim3((unsigned)(per_xcd * kXcds)), dim3(kTThreads), 0, st,
+           a);
   }
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
 }
 
-template <bool W4>
+template <bool W4, bool PK>
 static pipo_status launch_fmt(const GemmArgs& a, int epi, float* ws, int64_t ws_bytes,
                               hipStream_t st) {
   switch (epi) {
-    case EPI_F16: return launch_epi<W4, EPI_F16>(a, ws, ws_bytes, st);
-    case EPI_RELU_F16: return launch_epi<W4, EPI_RELU_F16>(a, ws, ws_bytes, st);
-    case EPI_ADD_F32: return launch_epi<W4, EPI_ADD_F32>(a, ws, ws_bytes, st);
-    case EPI_F32: return launch_epi<W4, EPI_F32>(a, ws, ws_bytes, st);
-    case EPI_QKV: return launch_epi<W4, EPI_QKV>(a, ws, ws_bytes, st);
+    case EPI_F16: return launch_epi<W4, EPI_F16, PK>(a, ws, ws_bytes, st);
+    case EPI_RELU_F16: return launch_epi<W4, EPI_RELU_F16, PK>(a, ws, ws_bytes, st);
+    case EPI_ADD_F32: return launch_epi<W4, EPI_ADD_F32, PK>(a, ws, ws_bytes, st);
+    case EPI_F32: return launch_epi<W4, EPI_F32, PK>(a, ws, ws_bytes, st);
+    case EPI_QKV: return launch_epi<W4, EPI_QKV, PK>(a, ws, ws_bytes, st);
     default: set_error("gemm: unknown epilogue %d", epi); return PIPO_ERR_ARG;
   }
 }
@@ -638,8 +645,15 @@ pipo_status launch_gemm(const GemmArgs& a, bool w4, int epi, float* workspace,
               (long long)a.d, (long long)a.dkv);
     return PIPO_ERR_ARG;
   }
-  return w4 ? launch_fmt<true>(a, epi, workspace, workspace_bytes, st)
-            : launch_fmt<false>(a, epi, workspace, workspace_bytes, st);
+  if (a.packed && a.N % 16 != 0) {
+    set_error("gemm: fragment-ordered W needs N %% 16 == 0 (N=%lld)", (long long)a.N);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  if (a.packed)
+    return w4 ? launch_fmt<true, true>(a, epi, workspace, workspace_bytes, st)
+              : launch_fmt<false, true>(a, epi, workspace, workspace_bytes, st);
+  return w4 ? launch_fmt<true, false>(a, epi, workspace, workspace_bytes, st)
+            : launch_fmt<false, false>(a, epi, workspace, workspace_bytes, st);
 }
 
 }  // namespace pipo

@@ -94,6 +94,38 @@ pipo_status pipo_op_gemm_w4(const uint16_t* X, const uint8_t* Wq, const uint16_t
   return gemm_common(a, true, out, epi, workspace, workspace_bytes, stream);
 }
 
+pipo_status pipo_op_gemm_f16_frag(const uint16_t* X, const uint16_t* W, const uint16_t* bias,
+                                  void* out, int64_t M, int64_t N, int64_t K, int32_t epi,
+                                  void* workspace, int64_t workspace_bytes, void* stream) {
+  clear_error();
+  GemmArgs a;
+  a.X = X;
+  a.W = W;
+  a.bias = bias;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.packed = true;
+  return gemm_common(a, false, out, epi, workspace, workspace_bytes, stream);
+}
+
+pipo_status pipo_op_gemm_w4_frag(const uint16_t* X, const uint8_t* Wq, const uint16_t* Wsm,
+                                 const uint16_t* bias, void* out, int64_t M, int64_t N,
+                                 int64_t K, int32_t epi, void* workspace,
+                                 int64_t workspace_bytes, void* stream) {
+  clear_error();
+  GemmArgs a;
+  a.X = X;
+  a.Wq = Wq;
+  a.Wsm = Wsm;
+  a.bias = bias;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.packed = true;
+  return gemm_common(a, true, out, epi, workspace, workspace_bytes, stream);
+}
+
 int64_t pipo_op_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int32_t wfmt) {
   return gemm_workspace_bytes(M, N, K, wfmt == PIPO_W_INT4_G64);
 }

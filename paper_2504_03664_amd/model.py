@@ -38,12 +38,18 @@ class HostWeights:
 
     ``pinned_matrices`` puts the layer matrices in pipo_host_alloc memory
     (streamed in place); ``pinned_head`` does the same for the output head.
+    ``layout`` "fragment" stores the pinned matrices in the order the decode
+    kernels read fastest (converted by the library's pipo_pack_* from the
+    provider's row-major tensors); "row_major" keeps them as drawn.  Matrices
+    outside pinned memory are always row-major (the library converts its
+    copies).
     """
 
     def __init__(self, shape, wfmt: str, provider, pinned_matrices: bool = True,
-                 pinned_head: bool = True):
-        assert wfmt in ("fp16", "int4")
+                 pinned_head: bool = True, layout: str = "fragment"):
+        assert wfmt in ("fp16", "int4") and layout in ("fragment", "row_major")
         self.shape, self.wfmt = shape, wfmt
+        self.layout = layout if pinned_matrices else "row_major"
         d, V, L = shape.d_model, shape.vocab, shape.n_layers
         self.llama = getattr(shape, "family", "opt") == "llama"
         self._pinned: List[int] = []
@@ -86,7 +92,17 @@ class HostWeights:
                                 (np.empty((N, K // 2), np.uint8),
                                  np.empty((N, K // 64, 2), np.float16)))
             for nm in MATRIX_SHAPES:
-                if wfmt == "fp16":
+                N, K = dims[nm]
+                if self.layout == "fragment":   # draw row-major, store in fragment order
+                    if wfmt == "fp16":
+                        B.pipo_pack_f16(provider.fill(j, nm, np.empty((N, K), np.float16)),
+                                        mats[nm].reshape(-1))
+                    else:
+                        q = np.empty((N, K // 2), np.uint8)
+                        sm = np.empty((N, K // 64, 2), np.float16)
+                        provider.fill_int4(j, nm, q, sm)
+                        B.pipo_pack_w4(q, sm, mats[nm][0].reshape(-1), mats[nm][1].reshape(-1))
+                elif wfmt == "fp16":
                     provider.fill(j, nm, mats[nm])
                 else:
                     provider.fill_int4(j, nm, mats[nm][0], mats[nm][1])
@@ -131,7 +147,9 @@ class HostWeights:
         self.c_weights = B.PipoHostWeights(addr(self.tok_emb), addr(self.pos_emb),
                                            addr(self.lnf_g), addr(self.lnf_b),
                                            ctypes.cast(c_layers, ctypes.POINTER(B.PipoLayerHost)),
-                                           addr(self.lm_head))
+                                           addr(self.lm_head),
+                                           B.PIPO_LAYOUT_FRAGMENT if self.layout == "fragment"
+                                           else B.PIPO_LAYOUT_ROW_MAJOR)
 
     def free(self):
         """Release the pinned regions (after every context using them is destroyed)."""

@@ -121,3 +121,45 @@ def test_disk_probe_runs_without_a_gpu(tmp_path):
     with pytest.raises(B.PipoError) as e:
         B.pipo_measure_disk_read(str(tmp_path), 1 << 20, n_threads=0)
     assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_ARG"
+
+
+def _frag_f16_reference(W):
+    """Fragment order as pipo.h defines it: block (rg, kb) of 16 rows x 32 k,
+    inside which slot r + 16 g holds row r, k = 8 g .. 8 g + 7."""
+    N, K = W.shape
+    out = np.empty(N * K, W.dtype)
+    for rg in range(N // 16):
+        for kb in range(K // 32):
+            base = (rg * (K // 32) + kb) * 512
+            for r in range(16):
+                for g in range(4):
+                    out[base + (r + 16 * g) * 8:base + (r + 16 * g) * 8 + 8] = \
+                        W[16 * rg + r, 32 * kb + 8 * g:32 * kb + 8 * g + 8]
+    return out
+
+
+def test_pack_f16_matches_the_layout_definition():
+    rng = np.random.default_rng(0)
+    for N, K in ((16, 32), (48, 128), (32, 256)):
+        W = rng.integers(0, 1 << 16, size=(N, K)).astype(np.uint16)
+        got = B.pipo_pack_f16(W)
+        assert np.array_equal(got, _frag_f16_reference(W))
+        assert sorted(got.tolist()) == sorted(W.reshape(-1).tolist())   # a permutation
+
+
+def test_pack_w4_matches_the_layout_definition():
+    rng = np.random.default_rng(1)
+    N, K = 32, 256
+    q = rng.integers(0, 256, size=(N, K // 2)).astype(np.uint8)
+    sm = rng.integers(0, 1 << 16, size=(N, K // 64, 2)).astype(np.uint16)
+    gq, gsm = B.pipo_pack_w4(q, sm)
+    for n in range(N):
+        for k in range(0, K, 2):   # codes (k, k+1) share a byte
+            byte = (n // 16 * (K // 128) + k // 128) * 1024 + \
+                (n % 16 + 16 * ((k % 128) // 32)) * 16 + (k % 32) // 2
+            assert gq[byte] == q[n, k // 2]
+        for grp in range(K // 64):
+            pair = (n // 16 * (K // 128) + grp // 2) * 32 + (n % 16) * 2 + grp % 2
+            assert gsm[2 * pair] == sm[n, grp, 0] and gsm[2 * pair + 1] == sm[n, grp, 1]
+    with pytest.raises(B.PipoError):
+        B.pipo_pack_w4(q[:, :40], sm[:, :1])   # K = 80 is not a multiple of 128

@@ -259,6 +259,28 @@ def test_small_model_parity_and_kv_on_host(wfmt):
         hw.free()
 
 
+@pytest.mark.parametrize("wfmt", ["fp16", "int4"])
+def test_weight_layouts_bit_identical(wfmt):
+    """Row-major matrices streamed in place (row-major kernels), row-major
+    matrices the library converts into its own regions, and caller
+    matrices already in fragment order: the same tokens and logits."""
+    model = synth.SyntheticOPT(SMALL, seed=18, wfmt=wfmt)
+    prompt = synth.prompt_tokens(3, 37, SMALL.vocab, seed=11)
+    runs = []
+    for kw in (dict(layout="fragment"), dict(layout="row_major"),
+               dict(pinned_matrices=False)):
+        log(f"layout {wfmt} {kw}")
+        hw = HostWeights(SMALL, wfmt, model, **kw)
+        try:
+            runs.append(_run(hw, prompt, 5))
+            runs.append(_run(hw, prompt, 5, weights_on_host=False, embed_on_host=False))
+        finally:
+            hw.free()
+    for t, l in runs[1:]:
+        assert np.array_equal(t, runs[0][0])
+        assert np.array_equal(l.view(np.uint32), runs[0][1].view(np.uint32))
+
+
 def test_head_dim_64_kv_on_host():
     shape = synth.OPTShape(3, 256, 4, 1024, vocab=512, max_pos=64)
     log("head_dim 64, kv on host")

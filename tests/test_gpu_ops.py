@@ -25,8 +25,10 @@ def log(msg):
     print(msg, flush=True)
 
 
-def run_gemm(X, W, bias, epi, out_init=None, w4=None, workspace=True):
-    """One GEMM through the C ABI; `workspace` False passes none (no K split)."""
+def run_gemm(X, W, bias, epi, out_init=None, w4=None, workspace=True, frag=False):
+    """One GEMM through the C ABI; `workspace` False passes none (no K split);
+    `frag` packs W into fragment order (library packer) and calls the
+    fragment-order entry point."""
     M, K = X.shape
     N = W.shape[0] if w4 is None else w4[0].shape[0]
     ws_bytes = B.pipo_op_gemm_workspace_bytes(M, N, K, B.PIPO_W_FP16 if w4 is None
@@ -41,12 +43,15 @@ def run_gemm(X, W, bias, epi, out_init=None, w4=None, workspace=True):
     else:
         dO = DB(M * N * (4 if f32 else 2))
     if w4 is None:
-        dW = DB.from_array(W.astype(np.float16))
-        B.pipo_op_gemm_f16(dX.ptr, dW.ptr, dB.ptr if dB else None, dO.ptr, M, N, K, epi, *ws)
+        W16 = W.astype(np.float16)
+        dW = DB.from_array(B.pipo_pack_f16(W16) if frag else W16)
+        op = B.pipo_op_gemm_f16_frag if frag else B.pipo_op_gemm_f16
+        op(dX.ptr, dW.ptr, dB.ptr if dB else None, dO.ptr, M, N, K, epi, *ws)
     else:
-        dq, dsm = DB.from_array(w4[0]), DB.from_array(w4[1])
-        B.pipo_op_gemm_w4(dX.ptr, dq.ptr, dsm.ptr, dB.ptr if dB else None, dO.ptr, M, N, K, epi,
-                          *ws)
+        q, sm = B.pipo_pack_w4(*w4) if frag else w4
+        dq, dsm = DB.from_array(q), DB.from_array(sm)
+        op = B.pipo_op_gemm_w4_frag if frag else B.pipo_op_gemm_w4
+        op(dX.ptr, dq.ptr, dsm.ptr, dB.ptr if dB else None, dO.ptr, M, N, K, epi, *ws)
     B.pipo_dev_synchronize()
     return dO.to_array(np.float32 if f32 else np.float16, (M, N))
 
@@ -110,6 +115,26 @@ def test_gemm_random_vs_oracle_definition(M):
     want4 = X.astype(np.float64) @ dequant_int4_g64(q, sm, np.float64).T + bias.astype(np.float64)
     # the kernel rounds each expanded weight to fp16 (relative 2^-11)
     assert np.abs(got4 - want4).max() <= 2e-3 * np.abs(want4).max()
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 64, 128), (16, 12288, 256), (7, 1008, 1024),
+                                   (33, 144, 384), (64, 1024, 4096), (128, 1040, 1024),
+                                   (129, 64, 256), (300, 272, 512)])
+@pytest.mark.parametrize("w4", [False, True])
+def test_gemm_fragment_order_equals_row_major(M, N, K, w4):
+    """W in fragment order (skinny, streaming with K splits, and tiled
+    kernels): the same products in the same order, bit for bit."""
+    log(f"gemm fragment order M={M} N={N} K={K} w4={w4}")
+    rng = np.random.default_rng(M + N + K + w4)
+    X = rng.standard_normal((M, K)).astype(np.float16)
+    W = (rng.standard_normal((N, K)) * 0.05).astype(np.float16)
+    bias = (rng.standard_normal(N) * 0.05).astype(np.float16)
+    q = synth.quant_int4_g64(W) if w4 else None
+    for epi in (B.PIPO_EPI_F32, B.PIPO_EPI_RELU_F16):
+        a = run_gemm(X, W, bias, epi, w4=q)
+        b = run_gemm(X, W, bias, epi, w4=q, frag=True)
+        assert np.array_equal(a.view(np.uint16 if a.dtype == np.float16 else np.uint32),
+                              b.view(np.uint16 if b.dtype == np.float16 else np.uint32))
 
 
 @pytest.mark.parametrize("M", [4, 40, 100, 200])
