@@ -342,7 +342,16 @@ def main():
                                                                   "alg_bytes", "alg_flops")}
         name, ks = max(fam.items(), key=lambda kv: kv[1]["total_ms"])
         avg_ms = ks["total_ms"] / ks["launches"]
-        ach = ks["alg_bytes"] / (ks["total_ms"] * 1e-3) / 1e9
+        # the kernel's own roofline: HBM unless its arithmetic intensity
+        # (algorithmic flops per algorithmic byte) exceeds the machine balance
+        # of the fp16 MFMA peak over the HBM peak
+        mfma_bound = ks["alg_flops"] > ks["alg_bytes"] * MFMA_F16_PEAK_TFLOPS / (HBM_PEAK_GBPS / 1e3)
+        if mfma_bound:
+            ach = ks["alg_flops"] / (ks["total_ms"] * 1e-3) / 1e12
+            peak, unit = MFMA_F16_PEAK_TFLOPS, "TFLOP/s"
+        else:
+            ach = ks["alg_bytes"] / (ks["total_ms"] * 1e-3) / 1e9
+            peak, unit = HBM_PEAK_GBPS, "GB/s"
         epi = {"oproj": 2, "fc1": 0 if llama else 1, "qkv": 4, "head": 3}
         fam_key = name.split("(")[1].split("+")[0].rstrip(")")
         symbols = None
@@ -362,9 +371,11 @@ def main():
             symbols = [f"attn_decode_k<{dh}, {G}, {hp}, {kv4}>"]
         symbol = " + ".join(symbols) if symbols else None
         traffic, tsrc = measured_traffic(wl.name, symbols) if symbols else (None, None)
-        out["roofline"] = {"kernel": name, "symbol": symbol, "bound": "hbm",
-                           "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                           "frac": round(ach / HBM_PEAK_GBPS, 4),
+        out["roofline"] = {"kernel": name, "symbol": symbol,
+                           "bound": "mfma" if mfma_bound else "hbm",
+                           "achieved": round(ach, 1), "peak": peak, "unit": unit,
+                           "frac": round(ach / peak, 4),
+                           "intensity_flop_per_byte": round(ks["alg_flops"] / ks["alg_bytes"], 2),
                            "launches": ks["launches"], "avg_launch_us": round(avg_ms * 1e3, 2),
                            "alg_bytes_per_launch": int(ks["alg_bytes"] / ks["launches"]),
                            "traffic": int(traffic) if traffic else None,

@@ -194,6 +194,135 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
   }
 }
 
+// decode over an INT4 cache without grouping (G = 1): the same structure
+// as attn_decode_k, but a lane holds 32 elements of a key's head (one
+// 16-byte load of codes and one (scale, min) pair instead of four 4-byte
+// loads for 8 elements each), so a wave issues a quarter of the load
+// instructions per byte; D/32 lanes per head of a key.
+template <int D, int HP>
+__global__ __launch_bounds__(256) void attn_decode_kv4_k(const uint16_t* __restrict__ q,
+                                                         const void* __restrict__ kc,
+                                                         const void* __restrict__ vc,
+                                                         uint16_t* __restrict__ o,
+                                                         float* __restrict__ part, int b, int H,
+                                                         int t, int chunk) {
+  constexpr int EPL = 32;            // elements per lane
+  constexpr int LPP = D / EPL;       // lanes per head of a key
+  constexpr int LPK = HP * LPP;      // lanes per key
+  constexpr int PPW = 64 / LPK;      // keys per wave per pass
+  __shared__ float wm[4][HP], wl[4][HP];
+  __shared__ float wacc[4][HP * D];
+  const int kb = blockIdx.x, bi = blockIdx.y, sp = blockIdx.z, S = gridDim.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sub = lane / LPK, cl = lane % LPK, hl = cl / LPP, cd = (cl % LPP) * EPL;
+  const int64_t d = (int64_t)H * D;
+  const int T = t + 1;
+  const int p0 = sp * chunk, p1 = min(T, p0 + chunk);
+  const int64_t col = (int64_t)(kb * HP + hl) * D + cd;
+
+  float qf[EPL];
+#pragma unroll
+  for (int j = 0; j < EPL / 8; ++j) {
+    const h8 qv = load_h8(q + (int64_t)bi * d + col + 8 * j);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) qf[8 * j + i] = (float)qv[i];
+  }
+  float m = -INFINITY, l = 0.f, acc[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
+
+  const int64_t row_bytes = d / 2 + d / 16;
+  const int64_t code_off = (int64_t)bi * row_bytes + col / 2;            // 16-byte aligned
+  const int64_t sm_off = (int64_t)bi * row_bytes + d / 2 + (col / 64) * 4;
+  struct Row {
+    u32x4 codes;
+    uint32_t sm;
+  };
+  const auto load_row = [&](const void* base, int p) -> Row {
+    const char* row = static_cast<const char*>(base) + (int64_t)p * b * row_bytes;
+    return Row{*reinterpret_cast<const u32x4*>(row + code_off),
+               *reinterpret_cast<const uint32_t*>(row + sm_off)};
+  };
+  const auto visit = [&](const Row& kr, const Row& vr) {
+    h2 ks, km, vs, vm;
+    scale_min_pairs(kr.sm, ks, km);
+    scale_min_pairs(vr.sm, vs, vm);
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const h8 kv = dequant8(kr.codes[j], ks, km);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += qf[8 * j + i] * (float)kv[i];
+    }
+#pragma unroll
+    for (int off = LPP / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+    const float mn = fmaxf(m, s);
+    const float alpha = expf(m - mn);
+    const float e = expf(s - mn);
+    l = l * alpha + e;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const h8 vv = dequant8(vr.codes[j], vs, vm);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[8 * j + i] = acc[8 * j + i] * alpha + e * (float)vv[i];
+    }
+    m = mn;
+  };
+  for (int p = p0 + wave * PPW + sub; p < p1; p += 8 * PPW) {
+    const int p2 = min(p + 4 * PPW, p1 - 1);
+    const Row ka = load_row(kc, p), va = load_row(vc, p);
+    const Row kb2 = load_row(kc, p2), vb2 = load_row(vc, p2);
+    visit(ka, va);
+    if (p + 4 * PPW < p1) visit(kb2, vb2);
+  }
+  // merge the key slots of the wave, then the waves through LDS
+#pragma unroll
+  for (int off = LPK; off < 64; off <<= 1) {
+    const float m2 = __shfl_xor(m, off, 64);
+    const float l2 = __shfl_xor(l, off, 64);
+    const float M = fmaxf(m, m2);
+    const float a1 = m == -INFINITY ? 0.f : expf(m - M);
+    const float a2 = m2 == -INFINITY ? 0.f : expf(m2 - M);
+    l = l * a1 + l2 * a2;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) acc[i] = acc[i] * a1 + __shfl_xor(acc[i], off, 64) * a2;
+    m = M;
+  }
+  if (sub == 0) {
+    if (cd == 0) {
+      wm[wave][hl] = m;
+      wl[wave][hl] = l;
+    }
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) wacc[wave][hl * D + cd + i] = acc[i];
+  }
+  __syncthreads();
+  for (int c = tid; c < HP * D; c += 256) {
+    const int j = c / D, cc = c % D, h = kb * HP + j;
+    float M = wm[0][j], L = wl[0][j], A = wacc[0][c];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      const float m2 = wm[w][j];
+      const float Mn = fmaxf(M, m2);
+      const float a1 = M == -INFINITY ? 0.f : expf(M - Mn);
+      const float a2 = m2 == -INFINITY ? 0.f : expf(m2 - Mn);
+      L = L * a1 + wl[w][j] * a2;
+      A = A * a1 + wacc[w][c] * a2;
+      M = Mn;
+    }
+    if (S == 1) {
+      o[(int64_t)bi * d + (int64_t)h * D + cc] = f2h(A / L);
+    } else {
+      float* pp = part + (((int64_t)bi * H + h) * S + sp) * (D + 2);
+      pp[cc] = A;
+      if (cc == 0) {
+        pp[D] = M;
+        pp[D + 1] = L;
+      }
+    }
+  }
+}
+
 // merge the splits of each (sequence, head) in split order
 template <int D>
 __global__ __launch_bounds__(D) void attn_decode_combine(const float* __restrict__ part,
@@ -381,10 +510,29 @@ static void launch_decode_g(const uint16_t* q, const void* kc, const void* vc, u
            (const float*)workspace, o, Hkv * G, S);
 }
 
+template <int D, int HP>
+static void launch_decode_kv4(const uint16_t* q, const void* kc, const void* vc, uint16_t* o,
+                              int b, int H, int t, int S, int chunk, float* workspace,
+                              hipStream_t st) {
+  const dim3 grid((unsigned)(H / HP), (unsigned)b, (unsigned)S);
+  launch(attn_decode_kv4_k<D, HP>, grid, dim3(256), 0, st, q, kc, vc, o, workspace, b, H, t,
+         chunk);
+  if (S > 1)
+    launch(attn_decode_combine<D>, dim3((unsigned)H, (unsigned)b), dim3(D), 0, st,
+           (const float*)workspace, o, H, S);
+}
+
 template <int D, bool KV4>
 static void launch_decode_d(const uint16_t* q, const void* kc, const void* vc, uint16_t* o, int b,
                             int Hkv, int G, int HP, int t, int S, int chunk, float* workspace,
                             hipStream_t st) {
+  if constexpr (KV4) {  // INT4 rows without grouping: 32 elements per lane
+    if (G == 1) {
+      if (HP == 4) return launch_decode_kv4<D, 4>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, st);
+      if (HP == 2) return launch_decode_kv4<D, 2>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, st);
+      return launch_decode_kv4<D, 1>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, st);
+    }
+  }
 #define PIPO_DECODE_CASE(g, hp)                                                         \
   if (G == g && HP == hp)                                                               \
     return launch_decode_g<D, g, hp, KV4>(q, kc, vc, o, b, Hkv, t, S, chunk, workspace, \

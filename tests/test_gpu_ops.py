@@ -272,11 +272,13 @@ def test_kv_quant_dequant_bit_exact_vs_oracle(rows, d):
 
 
 @pytest.mark.parametrize("b,T,H,D", [(1, 1, 4, 64), (3, 70, 4, 128), (2, 1000, 2, 128),
-                                     (16, 543, 8, 64)])
+                                     (16, 543, 8, 64), (4, 600, 56, 128), (3, 129, 6, 128),
+                                     (2, 300, 12, 64)])
 @pytest.mark.parametrize("split", [False, True])
 def test_attn_decode_kv4(b, T, H, D, split):
-    """Decode attention over an INT4 cache equals, bit for bit, the fp16
-    kernel over the expanded cache, and the oracle over the dequantized one."""
+    """Decode attention over an INT4 cache (32 elements per lane, its own
+    summation order) matches the fp16 kernel over the expanded cache to
+    fp32 rounding, and the oracle over the dequantized cache."""
     log(f"attn_decode_kv4 b={b} T={T} H={H} D={D} split={split}")
     rng = np.random.default_rng(T + 7 * b)
     d = H * D
@@ -294,9 +296,9 @@ def test_attn_decode_kv4(b, T, H, D, split):
     B.pipo_op_attn_decode_kv4(dq.ptr, dk4.ptr, dv4.ptr, o4.ptr, b, H, D, T - 1, *w)
     B.pipo_op_attn_decode(dq.ptr, dk.ptr, dv.ptr, o16.ptr, b, H, D, T - 1, *w)
     B.pipo_dev_synchronize()
-    got = o4.to_array(np.uint16, (b, d))
-    assert np.array_equal(got, o16.to_array(np.uint16, (b, d)))
-    got = got.view(np.float16).astype(np.float64)
+    got = o4.to_array(np.float16, (b, d)).astype(np.float64)
+    ref16 = o16.to_array(np.float16, (b, d)).astype(np.float64)
+    assert np.abs(got - ref16).max() <= 2e-3 * max(1.0, np.abs(ref16).max())
     for i in range(b):
         want = causal_attention(q[i:i + 1].astype(np.float64), k16[:, i].astype(np.float64),
                                 v16[:, i].astype(np.float64), H)[0]
