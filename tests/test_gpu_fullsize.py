@@ -18,6 +18,11 @@ from paper_2504_03664_amd.model import Decoder, HostWeights
 pytestmark = pytest.mark.gpu
 
 REL_TOL = 2e-2
+# Argmax: every disagreement must be a near tie (check_rows asserts it); of
+# the 64 sampled positions at most 5 % may disagree.  Kernels that only
+# reorder fp32 sums flip exact near ties (an OPT-13B INT4 run at 1.3e-3
+# normwise error had one such flip in 64), so a 99 % bar would demand zero.
+ARGMAX_MIN = 0.95
 # INT4 KV cache: a code moves by a whole step when a key or value crosses a
 # decision boundary, so implementations that differ only in summation order
 # differ by far more than with an fp16 cache.  At the OPT-30B slice two
@@ -87,7 +92,7 @@ def test_full_depth_sampled_rows(widx):
     log(f"  oracle on rows {rows} ({wl.shape.n_layers} layers)")
     worst, agree = check_rows(model, prompt, toks, logits, rows)
     log(f"  max normwise error {worst:.3e}, argmax agreement {agree:.4f}")
-    assert worst <= REL_TOL and agree >= 0.99
+    assert worst <= REL_TOL and agree >= ARGMAX_MIN
 
 
 @pytest.mark.parametrize("widx", [6, 7])
@@ -114,7 +119,7 @@ def test_llama8b_full_depth_sampled_rows(widx):
     # normwise, and with 128256 random-weight logits the top two are as
     # close as 3.7e-3 of the largest: argmax flips at near ties are expected
     # (each one is checked to be a near tie above).
-    assert worst <= REL_TOL and agree >= 0.95
+    assert worst <= REL_TOL and agree >= ARGMAX_MIN
 
 
 def test_opt30b_layer_slice():
@@ -133,7 +138,7 @@ def test_opt30b_layer_slice():
         hw.free()
     worst, agree = check_rows(model, prompt, toks, logits, [0, wl.batch - 1])
     log(f"  max normwise error {worst:.3e}, argmax agreement {agree:.4f}")
-    assert worst <= REL_TOL and agree >= 0.99
+    assert worst <= REL_TOL and agree >= ARGMAX_MIN
 
 
 @pytest.mark.parametrize("widx", [4, 5])
@@ -156,7 +161,7 @@ def test_opt30b_full_offload_layer_slice(widx):
     tol = KV4_TOL if kv4 else REL_TOL
     worst, agree = check_rows(model, prompt, toks, logits, [0, wl.batch - 1], kv_int4=kv4, tol=tol)
     log(f"  max normwise error {worst:.3e}, argmax agreement {agree:.4f}")
-    assert worst <= tol and agree >= (0.9 if kv4 else 0.99)
+    assert worst <= tol and agree >= (0.9 if kv4 else ARGMAX_MIN)
 
 
 def test_opt67b_rows_independent_of_batch():
