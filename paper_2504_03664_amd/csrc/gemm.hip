@@ -237,13 +237,15 @@ __global__ __launch_bounds__(KW * 64) void gemm_stream(GemmArgs a, float* part, 
       xr[j] = load_h8(a.X + clamp_hi(row, a.M - 1) * K + k0 + col);
     }
   };
+  // INT4: X is stored already permuted to the codes' interleaved order
+  // (once per workgroup rather than once per wave and use)
   const auto store_x = [&](int b) {
 #pragma unroll
     for (int j = 0; j < C::kXPerThread; ++j) {
       const int e = tid + j * C::kThreads;
       if (e < C::kXH8) {
         const int row = e / (KC / 8), col = (e % (KC / 8)) * 8;
-        *reinterpret_cast<h8*>(&Xs[b][row * C::kXLd + col]) = xr[j];
+        *reinterpret_cast<h8*>(&Xs[b][row * C::kXLd + col]) = W4 ? interleave_h8(xr[j]) : xr[j];
       }
     }
   };
@@ -265,10 +267,8 @@ __global__ __launch_bounds__(KW * 64) void gemm_stream(GemmArgs a, float* part, 
         const int kl = 128 * t + (W4 ? 32 * g + 8 * i : 32 * i + 8 * g);
         h8 xv[MF];
 #pragma unroll
-        for (int mf = 0; mf < MF; ++mf) {
+        for (int mf = 0; mf < MF; ++mf)
           xv[mf] = *reinterpret_cast<const h8*>(&Xs[b][(16 * mf + r) * C::kXLd + kl]);
-          if constexpr (W4) xv[mf] = interleave_h8(xv[mf]);
-        }
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
           const h8 wv = W4 ? dequant8_interleaved(F.w[f][t][i], s2[f], m2[f])
