@@ -180,9 +180,17 @@ pipo_status pipo_op_embed(const int32_t* ids, const uint16_t* tok_table, const u
                           float* x, int64_t rows, int64_t d, int64_t rows_per_seq, int64_t pos0,
                           int64_t pos_offset, void* stream);
 
-/* next[r] = index of the largest logits[r][:] (ties: lowest index). */
+/* next[r] = index of the largest logits[r][:] (ties: lowest index, NaNs
+ * skipped; a row of NaNs gives 0).  rows <= 65535. */
 pipo_status pipo_op_argmax(const float* logits, int32_t* next, int64_t rows, int64_t V,
                            void* stream);
+/* The same with a row split over several workgroups whose candidates a
+ * second kernel merges (same result); workspace (device, caller-owned,
+ * contents arbitrary) of pipo_op_argmax_workspace_bytes(rows, V) bytes, or
+ * less / NULL for the single-pass kernel. */
+pipo_status pipo_op_argmax_ws(const float* logits, int32_t* next, int64_t rows, int64_t V,
+                              void* workspace, int64_t workspace_bytes, void* stream);
+int64_t pipo_op_argmax_workspace_bytes(int64_t rows, int64_t V);
 
 /* Plain device-to-device copy kernel: reads and writes `bytes` once
  * (multiple of 16, 16-byte aligned pointers).  Not part of the decoder: it

@@ -153,6 +153,8 @@ _SIGNATURES = {
     "pipo_op_kv_dequant": ([vp, vp, i64, i64, vp], i32),
     "pipo_op_attn_prefill": ([vp, vp, vp, vp, i32, i32, i32, i32, vp], i32),
     "pipo_op_argmax": ([vp, vp, i64, i64, vp], i32),
+    "pipo_op_argmax_ws": ([vp, vp, i64, i64, vp, i64, vp], i32),
+    "pipo_op_argmax_workspace_bytes": ([i64, i64], i64),
     "pipo_op_copy": ([vp, vp, i64, vp], i32),
     "pipo_op_attn_decode_gqa": ([vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp, i64, vp], i32),
     "pipo_op_attn_decode_gqa_workspace_bytes": ([i32, i32, i32, i32, i32], i64),
@@ -457,6 +459,15 @@ def pipo_op_attn_prefill(q, kc, vc, o, b, P, n_heads, head_dim, stream=None):
 
 def pipo_op_argmax(logits, nxt, rows, V, stream=None):
     _check(lib().pipo_op_argmax(logits, nxt, rows, V, stream), "pipo_op_argmax")
+
+
+def pipo_op_argmax_ws(logits, nxt, rows, V, workspace=None, workspace_bytes=0, stream=None):
+    _check(lib().pipo_op_argmax_ws(logits, nxt, rows, V, workspace, workspace_bytes, stream),
+           "pipo_op_argmax_ws")
+
+
+def pipo_op_argmax_workspace_bytes(rows, V) -> int:
+    return int(lib().pipo_op_argmax_workspace_bytes(rows, V))
 
 
 def pipo_op_copy(dst, src, nbytes, stream=None):

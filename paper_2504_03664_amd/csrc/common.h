@@ -138,8 +138,12 @@ pipo_status launch_kv_quant(const uint16_t* x, uint8_t* out, int64_t rows, int64
                             hipStream_t st);
 pipo_status launch_kv_dequant(const uint8_t* in, uint16_t* y, int64_t rows, int64_t d,
                               hipStream_t st);
+// greedy argmax (largest, ties to the lowest index, NaNs skipped); with a
+// workspace of argmax_workspace_bytes a row is split over several
+// workgroups and a second kernel merges their candidates (same result)
+int64_t argmax_workspace_bytes(int64_t rows, int64_t V);
 pipo_status launch_argmax(const float* logits, int32_t* next, int64_t rows, int64_t V,
-                          hipStream_t st);
+                          void* workspace, int64_t workspace_bytes, hipStream_t st);
 pipo_status launch_fill_u16(uint16_t* p, uint16_t value, int64_t n, hipStream_t st);
 pipo_status launch_copy16(void* dst, const void* src, int64_t bytes, hipStream_t st);
 

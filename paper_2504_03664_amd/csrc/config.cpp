@@ -215,6 +215,7 @@ HbmPlan hbm_plan(const pipo_shape& sh, const pipo_policy& pol) {
   p.next = (int64_t)pol.max_batch * 4;
   p.ids = rows * 4;
   p.emb = pol.embed_on_host ? rows * d * 2 : 0;
+  p.argmax_ws = argmax_workspace_bytes(pol.max_batch, V);
   p.attn_ws = attn_decode_workspace_bytes(pol.max_batch, sh.n_heads, (int)(d / sh.n_heads),
                                           kAttnDecodeMaxSplits);
   const int64_t shapes[5][3] = {

@@ -177,30 +177,23 @@ __global__ __launch_bounds__(256) void swiglu_k(const uint16_t* __restrict__ gu,
   *reinterpret_cast<u32x4*>(h + m * F + i) = out;
 }
 
-// greedy token: largest logit, ties to the lowest index (NaNs are skipped)
-__global__ __launch_bounds__(256) void argmax_k(const float* __restrict__ logits,
-                                                int32_t* __restrict__ next, int64_t V) {
-  __shared__ float bv[4];
-  __shared__ int bi[4];
-  const int64_t row = blockIdx.x;
-  const float* lr = logits + row * V;
-  float best = -INFINITY;
-  int idx = INT_MAX;
-  for (int64_t i = threadIdx.x; i < V; i += 256) {
-    const float v = lr[i];
-    if (v > best || (idx == INT_MAX && v == best)) {
-      best = v;
-      idx = (int)i;
-    }
+// greedy token: largest logit, ties to the lowest index (NaNs are skipped).
+// A candidate (v, i) replaces (best, idx) if v > best, or v == best and
+// i < idx; the result does not depend on the order candidates are seen.
+__device__ __forceinline__ void argmax_take(float& best, int& idx, float v, int i) {
+  if (v > best || (v == best && i < idx)) {
+    best = v;
+    idx = i;
   }
+}
+
+// best of a 256-thread block, written by thread 0
+__device__ __forceinline__ void argmax_block(float& best, int& idx, float* bv, int* bi) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     const float ov = __shfl_xor(best, off, 64);
     const int oi = __shfl_xor(idx, off, 64);
-    if (ov > best || (ov == best && oi < idx)) {
-      best = ov;
-      idx = oi;
-    }
+    argmax_take(best, idx, ov, oi);
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (lane == 0) {
@@ -208,16 +201,58 @@ __global__ __launch_bounds__(256) void argmax_k(const float* __restrict__ logits
     bi[wave] = idx;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    float b = bv[0];
-    int k = bi[0];
-    for (int w = 1; w < 4; ++w)
-      if (bv[w] > b || (bv[w] == b && bi[w] < k)) {
-        b = bv[w];
-        k = bi[w];
-      }
-    next[row] = k == INT_MAX ? 0 : k;
+  if (threadIdx.x == 0)
+    for (int w = 1; w < 4; ++w) argmax_take(best, idx, bv[w], bi[w]);
+}
+
+// partition p of row `row` (grid (P, rows)): columns [p chunk, (p+1) chunk),
+// four independent loads in flight per thread; the candidate goes to
+// cand[row][p] (P == 1: straight to next[row])
+__global__ __launch_bounds__(256) void argmax_k(const float* __restrict__ logits,
+                                                int32_t* __restrict__ next,
+                                                float2* __restrict__ cand, int64_t V,
+                                                int64_t chunk) {
+  __shared__ float bv[4];
+  __shared__ int bi[4];
+  const int64_t row = blockIdx.y, p = blockIdx.x, P = gridDim.x;
+  const float* lr = logits + row * V;
+  const int64_t lo = p * chunk, hi = min(V, lo + chunk);
+  float best = -INFINITY;
+  int idx = INT_MAX;
+  for (int64_t i = lo + threadIdx.x; i < hi; i += 1024) {
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = i + 256 * u < hi ? lr[i + 256 * u] : NAN;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) argmax_take(best, idx, v[u], (int)(i + 256 * u));
   }
+  argmax_block(best, idx, bv, bi);
+  if (threadIdx.x == 0) {
+    if (P == 1)
+      next[row] = idx == INT_MAX ? 0 : idx;
+    else
+      cand[row * P + p] = make_float2(best, __int_as_float(idx));
+  }
+}
+
+// merge the P <= 64 candidates of each row (one wave per row)
+__global__ __launch_bounds__(64) void argmax_merge_k(const float2* __restrict__ cand,
+                                                     int32_t* __restrict__ next, int P) {
+  const int64_t row = blockIdx.x;
+  float best = -INFINITY;
+  int idx = INT_MAX;
+  if ((int)threadIdx.x < P) {
+    const float2 c = cand[row * P + threadIdx.x];
+    best = c.x;
+    idx = __float_as_int(c.y);
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float ov = __shfl_xor(best, off, 64);
+    const int oi = __shfl_xor(idx, off, 64);
+    argmax_take(best, idx, ov, oi);
+  }
+  if (threadIdx.x == 0) next[row] = idx == INT_MAX ? 0 : idx;
 }
 
 // plain streaming copy, 16 bytes per thread per iteration
@@ -298,13 +333,31 @@ pipo_status launch_embed(const uint16_t* tok_rows, const int32_t* ids, const uin
   return PIPO_OK;
 }
 
+// partitions of a row: about 4096 columns each, at most 64
+static int argmax_parts(int64_t V) {
+  const int64_t p = (V + 4095) / 4096;
+  return (int)(p < 1 ? 1 : (p > 64 ? 64 : p));
+}
+
+int64_t argmax_workspace_bytes(int64_t rows, int64_t V) {
+  const int P = argmax_parts(V);
+  return P > 1 ? rows * P * (int64_t)sizeof(float2) : 0;
+}
+
 pipo_status launch_argmax(const float* logits, int32_t* next, int64_t rows, int64_t V,
-                          hipStream_t st) {
-  if (rows < 1 || V < 1 || V > INT_MAX) {
+                          void* workspace, int64_t workspace_bytes, hipStream_t st) {
+  if (rows < 1 || V < 1 || V > INT_MAX || rows > 65535) {
     set_error("argmax: bad shape rows=%lld V=%lld", (long long)rows, (long long)V);
     return PIPO_ERR_ARG;
   }
-  launch(argmax_k, dim3((unsigned)rows), dim3(256), 0, st, logits, next, V);
+  int P = argmax_parts(V);
+  if (!workspace || workspace_bytes < argmax_workspace_bytes(rows, V)) P = 1;
+  const int64_t chunk = (V + P - 1) / P;
+  launch(argmax_k, dim3((unsigned)P, (unsigned)rows), dim3(256), 0, st, logits, next,
+         static_cast<float2*>(workspace), V, chunk);
+  if (P > 1)
+    launch(argmax_merge_k, dim3((unsigned)rows), dim3(64), 0, st,
+           static_cast<const float2*>(workspace), next, P);
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
 }

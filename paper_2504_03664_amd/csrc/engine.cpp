@@ -319,6 +319,8 @@ struct pipo_ctx {
   int64_t attn_ws_bytes = 0;
   float* gemm_ws = nullptr;    // GEMM K-split partials
   int64_t gemm_ws_bytes = 0;
+  void* argmax_ws = nullptr;   // argmax candidates of the row partitions
+  int64_t argmax_ws_bytes = 0;
   char* kv = nullptr;          // resident cache or KV slots
   bool kv4 = false;            // INT4 cache rows (PIPO_KV_INT4_G64)
   int64_t kv_row = 0;          // bytes of one cached key (value) row: 2 dkv, or 9 dkv / 16
@@ -553,7 +555,8 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
       return launch_gemm(ga, false, EPI_F32, c->gemm_ws, c->gemm_ws_bytes, s);
     }
     case kArgmax:
-      return launch_argmax(c->logits, c->next_dev, c->b, c->V, s);
+      return launch_argmax(c->logits, c->next_dev, c->b, c->V, c->argmax_ws, c->argmax_ws_bytes,
+                           s);
     default:
       set_error("unknown kernel %d", op.kernel);
       return PIPO_ERR_ARG;
@@ -1220,6 +1223,8 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
     PIPO_TRY(dev_alloc(c, &p, c->gemm_ws_bytes));
     c->gemm_ws = (float*)p;
   }
+  c->argmax_ws_bytes = hp.argmax_ws;
+  if (c->argmax_ws_bytes > 0) PIPO_TRY(dev_alloc(c, &c->argmax_ws, c->argmax_ws_bytes));
   c->kv_row = hp.kv_row;
   c->kv_part_bytes = hp.kv_part;
   if (hp.kstage > 0) {

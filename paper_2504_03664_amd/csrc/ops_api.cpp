@@ -296,7 +296,23 @@ pipo_status pipo_op_argmax(const float* logits, int32_t* next, int64_t rows, int
     set_error("argmax: NULL pointer");
     return PIPO_ERR_ARG;
   }
-  return launch_argmax(logits, next, rows, V, static_cast<hipStream_t>(stream));
+  return launch_argmax(logits, next, rows, V, nullptr, 0, static_cast<hipStream_t>(stream));
+}
+
+pipo_status pipo_op_argmax_ws(const float* logits, int32_t* next, int64_t rows, int64_t V,
+                              void* workspace, int64_t workspace_bytes, void* stream) {
+  clear_error();
+  if (!logits || !next || workspace_bytes < 0) {
+    set_error("argmax: NULL pointer or negative workspace size");
+    return PIPO_ERR_ARG;
+  }
+  return launch_argmax(logits, next, rows, V, workspace, workspace ? workspace_bytes : 0,
+                       static_cast<hipStream_t>(stream));
+}
+
+int64_t pipo_op_argmax_workspace_bytes(int64_t rows, int64_t V) {
+  if (rows < 1 || V < 1) return 0;
+  return argmax_workspace_bytes(rows, V);
 }
 
 pipo_status pipo_op_copy(void* dst, const void* src, int64_t bytes, void* stream) {

@@ -47,11 +47,12 @@ struct HbmPlan {
   int64_t slot_bytes = 0, slots = 0, resident = 0, tok = 0, head = 0, pos = 0, lnf = 0;
   int64_t x = 0, a = 0, q = 0, o = 0, h = 0, gu = 0, logits = 0, next = 0, ids = 0, emb = 0;
   int64_t rope = 0;                              // rotary (cos, sin) table
-  int64_t attn_ws = 0, gemm_ws = 0, kstage = 0;  // kstage: each of the K and V staging buffers
+  int64_t attn_ws = 0, gemm_ws = 0, argmax_ws = 0;
+  int64_t kstage = 0;                            // each of the K and V staging buffers
   int64_t kv_row = 0, kv_part = 0, kv = 0;
   int64_t total() const {
     return slots + resident + tok + head + pos + lnf + x + a + q + o + h + gu + logits + next +
-           ids + emb + rope + attn_ws + gemm_ws + 2 * kstage + kv;
+           ids + emb + rope + attn_ws + gemm_ws + argmax_ws + 2 * kstage + kv;
   }
 };
 HbmPlan hbm_plan(const pipo_shape& sh, const pipo_policy& pol);  // pol normalized

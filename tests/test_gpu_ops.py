@@ -326,19 +326,34 @@ def test_attn_prefill_vs_oracle(b, P, H, D):
         assert np.abs(got[i] - want).max() <= 8e-3 * max(1.0, np.abs(want).max())
 
 
-def test_argmax_ties_and_ragged():
-    log("argmax")
-    rng = np.random.default_rng(0)
-    V = 50272
-    L = rng.standard_normal((6, V)).astype(np.float32)
-    L[1, 17] = L[1, 40000] = L[1].max() + 1          # tie: lowest index wins
+@pytest.mark.parametrize("V", [50272, 128256, 4096, 4099, 7])
+def test_argmax_ties_and_ragged(V):
+    """Single-pass and split (partitions merged by a second kernel) argmax:
+    the largest logit, ties to the lowest index, NaNs skipped, a row of
+    -inf gives its first index, a row of NaNs gives 0."""
+    log(f"argmax V={V}")
+    rng = np.random.default_rng(V)
+    R = 8
+    L = rng.standard_normal((R, V)).astype(np.float32)
+    L[1, min(17, V - 1)] = L[1, V - 1] = L[1].max() + 1   # tie: lowest index wins
     L[2, :] = -np.inf
-    L[2, 5:] = 0.0                                    # first finite maximum
-    L[3, V - 1] = 100.0                               # ragged tail
-    L[4, :] = 7.0                                     # all equal -> 0
-    dl, dn = DB.from_array(L), DB(6 * 4)
-    B.pipo_op_argmax(dl.ptr, dn.ptr, 6, V)
-    B.pipo_dev_synchronize()
-    got = dn.to_array(np.int32, (6,))
-    assert got.tolist() == np.argmax(L, axis=1).tolist()
-    assert got[1] == 17 and got[2] == 5 and got[3] == V - 1 and got[4] == 0
+    L[2, min(5, V - 1):] = 0.0                             # first finite maximum
+    L[3, V - 1] = 100.0                                    # ragged tail
+    L[4, :] = 7.0                                          # all equal -> 0
+    L[5, ::3] = np.nan                                     # NaNs are skipped
+    L[6, :] = -np.inf                                      # all -inf -> 0
+    L[7, :] = np.nan                                       # all NaN -> 0
+    want = [int(np.nanargmax(r)) if not np.isnan(r).all() else 0 for r in L]
+    dl = DB.from_array(L)
+    ws_bytes = B.pipo_op_argmax_workspace_bytes(R, V)
+    assert (ws_bytes > 0) == (V > 4096)
+    ws = DB(ws_bytes) if ws_bytes else None
+    for split in (False, True):
+        dn = DB(R * 4)
+        if split:
+            B.pipo_op_argmax_ws(dl.ptr, dn.ptr, R, V, ws.ptr if ws else None, ws_bytes)
+        else:
+            B.pipo_op_argmax(dl.ptr, dn.ptr, R, V)
+        B.pipo_dev_synchronize()
+        got = dn.to_array(np.int32, (R,))
+        assert got.tolist() == want, (split, got.tolist(), want)
