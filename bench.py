@@ -234,10 +234,11 @@ def main():
                   chunk_bytes=args.chunk_mb << 20, max_batch=wl.batch, max_seq=max_seq)
     if disk:
         log(f"disk tier file written in {time.time() - t0:.1f} s")
-        # the disk's read rate for the tier's pattern, probed after the weight
-        # file is written (8 GiB, best of 3 passes)
-        dpeak, direct = B.pipo_measure_disk_read(disk["dir"], 8 << 30, args.chunk_mb << 20, 8, 3)
-        log(f"disk read peak in {disk['dir']}: {dpeak:.2f} GB/s (direct I/O: {direct})")
+        # the disk's read rate: the tier's own file read the way decode reads
+        # it (16 GiB, best of 3 passes); and whether direct I/O is possible there
+        dpeak = B.pipo_measure_disk_tier(dec.ctx, 16 << 30, 3)
+        _, direct = B.pipo_measure_disk_read(disk["dir"], 64 << 20, args.chunk_mb << 20, 8, 1)
+        log(f"disk-tier read rate in {disk['dir']}: {dpeak:.2f} GB/s (direct I/O: {direct})")
         disk.update(peak_gbps=dpeak, direct_io=direct)
     prompt = synth.prompt_tokens(wl.batch, wl.prompt, shape.vocab, seed=1, stream=args.workload)
     t0 = time.perf_counter()

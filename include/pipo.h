@@ -405,6 +405,14 @@ pipo_status pipo_pack_f16(const uint16_t* W, uint16_t* out, int64_t N, int64_t K
 pipo_status pipo_pack_w4(const uint8_t* q, const uint16_t* scale_min, uint8_t* q_out,
                          uint16_t* scale_min_out, int64_t N, int64_t K);
 
+/* The read rate of a context's own disk-tier file: its first `bytes`
+ * (whole layer units in slot layout) read `iters` times exactly as the
+ * decode passes read them (chunk_bytes pieces, copy_threads threads, direct
+ * I/O through the pageable buffer into pinned staging, no DMA); best rate
+ * in *gbps.  Waits for the context's streams first.  Errors: ARG, STATE
+ * (no disk tier), IO, HIP. */
+pipo_status pipo_measure_disk_tier(pipo_ctx* ctx, int64_t bytes, int32_t iters, double* gbps);
+
 /* Pinned (page-locked) host memory, 4 KiB aligned; NULL on failure.
  * Matrices placed here are streamed by the copy engines without staging. */
 void* pipo_host_alloc(size_t bytes);

@@ -130,6 +130,7 @@ _SIGNATURES = {
     "pipo_measure_h2d_chunked": ([i64, i64, i32, i32, ctypes.POINTER(f64)], i32),
     "pipo_measure_disk_read": ([ctypes.c_char_p, i64, i64, i32, i32, ctypes.POINTER(f64),
                                 ctypes.POINTER(i32)], i32),
+    "pipo_measure_disk_tier": ([vp, i64, i32, ctypes.POINTER(f64)], i32),
     "pipo_host_alloc": ([sz], vp),
     "pipo_host_free": ([vp], None),
     "pipo_last_error": ([], ctypes.c_char_p),
@@ -314,6 +315,14 @@ def pipo_measure_disk_read(directory: str, nbytes: int, chunk_bytes: int = 64 <<
                                         iters, ctypes.byref(g), ctypes.byref(direct)),
            "pipo_measure_disk_read")
     return g.value, bool(direct.value)
+
+
+def pipo_measure_disk_tier(ctx: int, nbytes: int, iters: int = 3) -> float:
+    """GB/s of reading the context's own disk-tier file the way decode does."""
+    g = f64()
+    _check(lib().pipo_measure_disk_tier(ctx, nbytes, iters, ctypes.byref(g)),
+           "pipo_measure_disk_tier")
+    return g.value
 
 
 def pipo_host_alloc(nbytes: int) -> int:

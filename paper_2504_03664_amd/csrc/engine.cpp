@@ -1611,6 +1611,39 @@ pipo_status pipo_measure_h2d_chunked(int64_t bytes, int64_t chunk_bytes, int32_t
   return measure_h2d(bytes, chunk_bytes, iters, n_streams, gbps);
 }
 
+pipo_status pipo_measure_disk_tier(pipo_ctx* c, int64_t bytes, int32_t iters, double* gbps) {
+  clear_error();
+  if (!c || !gbps || bytes <= 0 || iters < 1) {
+    set_error("measure_disk_tier: bad arguments");
+    return PIPO_ERR_ARG;
+  }
+  if (c->disk_fd < 0) {
+    set_error("measure_disk_tier: the context has no disk tier");
+    return PIPO_ERR_STATE;
+  }
+  PIPO_HIP_TRY(hipSetDevice(c->device));
+  for (int i = 0; i < kNumStreams; ++i) PIPO_HIP_TRY(hipStreamSynchronize(c->st[i]));
+  StagingRing& r = c->stage_h2d;
+  const int64_t total = std::min(align_up(bytes, 4096), c->L * c->layer_bytes);
+  double best = 0;
+  for (int it = 0; it < iters; ++it) {
+    const auto t0 = std::chrono::steady_clock::now();
+    for (int64_t off = 0; off < total; off += r.buf_bytes) {
+      const int64_t n = std::min(r.buf_bytes, total - off);
+      if (!c->pool->pread_all(c->disk_fd, r.buf[0], (size_t)n, off,
+                              c->disk_direct ? c->disk_bounce : nullptr)) {
+        set_error("measure_disk_tier: reading failed: %s", std::strerror(errno));
+        return PIPO_ERR_IO;
+      }
+    }
+    const double sec =
+        std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+    best = std::max(best, (double)total / sec / 1e9);
+  }
+  *gbps = best;
+  return PIPO_OK;
+}
+
 pipo_status pipo_measure_disk_read(const char* dir, int64_t bytes, int64_t chunk_bytes,
                                    int32_t n_threads, int32_t iters, double* gbps,
                                    int32_t* direct) {

@@ -160,6 +160,12 @@ def test_disk_tier_bit_identical(opt125m, tmp_path):
         st = dec.stats()
     assert st["disk_read_bytes"] == want["disk_bytes_per_step"]
     assert st["hbm_bytes"] == want["hbm_bytes"]
+    with Decoder(hw, **pol) as dec:
+        assert B.pipo_measure_disk_tier(dec.ctx, 8 << 20, 2) > 0
+    with Decoder(hw, max_batch=1, max_seq=8) as dec:
+        with pytest.raises(B.PipoError) as e:
+            B.pipo_measure_disk_tier(dec.ctx, 1 << 20)
+        assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_STATE"
 
 
 def test_disk_tier_errors(opt125m, tmp_path):
