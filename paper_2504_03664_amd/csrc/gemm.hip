@@ -3,7 +3,7 @@
 // with W in fp16 or group-wise INT4 (codes expanded to fp16 in registers,
 // the paper's "compute directly on 4-bit weights", Section 3.4).
 //
-// Three kernels, chosen by M:
+// Four kernels, chosen by M (and the weight format):
 //   * gemm_skinny (M <= 16, decode): every workgroup owns 16 or 64 rows of
 //     W and all M rows of X; its waves split K; W streams from HBM straight
 //     into MFMA operand registers (no LDS), X comes from L2.  Partial sums
@@ -16,6 +16,8 @@
 //   * gemm_tiled (M > 128, prefill): 128 x 128 output tiles, K staged
 //     through double-buffered LDS in steps of 64, 4 waves of 64 x 64; tiles
 //     ordered per XCD so that each XCD's L2 serves a compact block.
+//   * gemm_big_w4 (INT4 prefill, M >= 512): 256 x 256 tiles, 4 waves of
+//     128 x 128, each W row's codes expanded once per tile.
 // All accumulate in fp32 with v_mfma_f32_16x16x32_f16, and INT4 codes
 // become the same fp16 values (code * scale + min, rounded once) in every
 // kernel.  The kernel, its configuration and the K split depend only on
@@ -26,30 +28,60 @@
 
 namespace pipo {
 
+// Epilogue, split into what depends on the output row only (its offsets,
+// computed once per row by kernels that own many columns of it) and the
+// per-element part.  EPI_QKV: row m is sequence m / rows_per_seq at
+// position pos0 + m % rows_per_seq, whose k and v go to cache row
+// position * batch + sequence.
+struct EpiRow {
+  int64_t m;      // output row (>= M: none)
+  int64_t off;    // m * ldo, or m * d for q (EPI_QKV)
+  int64_t kvoff;  // EPI_QKV: cache row * dkv
+};
+
 template <int EPI>
-__device__ __forceinline__ void epilogue(const GemmArgs& a, int64_t m, int64_t n, float acc) {
-  if (m >= a.M || n >= a.N) return;
+__device__ __forceinline__ EpiRow epilogue_row(const GemmArgs& a, int64_t m) {
+  EpiRow r{m, 0, 0};
+  if (m >= a.M) return r;
+  if constexpr (EPI == EPI_QKV) {
+    // launch_gemm keeps M below 2^31, so 32-bit division is exact
+    const uint32_t mm = (uint32_t)m, rps = (uint32_t)a.rows_per_seq;
+    const uint32_t seq = mm / rps;
+    const int64_t pos = a.pos0 + (int64_t)(mm - seq * rps);
+    r.off = m * a.d;
+    r.kvoff = (pos * a.batch + seq) * a.dkv;
+  } else {
+    r.off = m * a.ldo;
+  }
+  return r;
+}
+
+template <int EPI>
+__device__ __forceinline__ void epilogue_at(const GemmArgs& a, const EpiRow& r, int64_t n,
+                                            float acc) {
+  if (r.m >= a.M || n >= a.N) return;
   const float v = acc + (a.bias ? h2f(a.bias[n]) : 0.f);
   if constexpr (EPI == EPI_F16) {
-    a.out16[m * a.ldo + n] = f2h(v);
+    a.out16[r.off + n] = f2h(v);
   } else if constexpr (EPI == EPI_RELU_F16) {
-    a.out16[m * a.ldo + n] = f2h(v > 0.f ? v : 0.f);
+    a.out16[r.off + n] = f2h(v > 0.f ? v : 0.f);
   } else if constexpr (EPI == EPI_ADD_F32) {
-    a.out32[m * a.ldo + n] += v;
+    a.out32[r.off + n] += v;
   } else if constexpr (EPI == EPI_F32) {
-    a.out32[m * a.ldo + n] = v;
+    a.out32[r.off + n] = v;
   } else {  // EPI_QKV
-    const int64_t seq = m / a.rows_per_seq;
-    const int64_t pos = a.pos0 + m % a.rows_per_seq;
-    const int64_t crow = pos * a.batch + seq;
-    if (n < a.d) {
-      a.q_out[m * a.d + n] = f2h(v * a.q_scale);
-    } else if (n < a.d + a.dkv) {
-      a.k_out[crow * a.dkv + (n - a.d)] = f2h(v);
-    } else {
-      a.v_out[crow * a.dkv + (n - a.d - a.dkv)] = f2h(v);
-    }
+    if (n < a.d)
+      a.q_out[r.off + n] = f2h(v * a.q_scale);
+    else if (n < a.d + a.dkv)
+      a.k_out[r.kvoff + (n - a.d)] = f2h(v);
+    else
+      a.v_out[r.kvoff + (n - a.d - a.dkv)] = f2h(v);
   }
+}
+
+template <int EPI>
+__device__ __forceinline__ void epilogue(const GemmArgs& a, int64_t m, int64_t n, float acc) {
+  epilogue_at<EPI>(a, epilogue_row<EPI>(a, m), n, acc);
 }
 
 // ---------------------------------------------------------------------------
@@ -472,7 +504,131 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// big-tile GEMM (INT4 prefill, M >= 512): 256 x 256 output tiles, 4 waves
+// of 128 x 128 (8 x 8 accumulator fragments per wave), K in steps of 64
+// through double-buffered LDS (144 KiB).  Each thread expands one W row's
+// 64 codes per step.  Against gemm_tiled a code is expanded once per 256
+// rows of X instead of once per 128, and each LDS operand read feeds twice
+// as many MFMAs; the expansion is what limits gemm_tiled with INT4 (with
+// fp16 W the smaller tiles are as fast: more waves per CU hide latency).
+// Same tile order as gemm_tiled.
+// ---------------------------------------------------------------------------
+constexpr int kBM = 256, kBN = 256, kBK = 64, kBPad = 8, kBThreads = 256;
+constexpr int64_t kBigMinM = 512;  // INT4 prefill at M >= 512 uses the big tiles
+
+template <int EPI, bool PK>
+__global__ __launch_bounds__(kBThreads) void gemm_big_w4(GemmArgs a) {
+  constexpr int LDS_ROW = kBK + kBPad;  // halves
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][kBM * LDS_ROW];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kBN * LDS_ROW];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int64_t tiles_m = (a.M + kBM - 1) / kBM, tiles_n = (a.N + kBN - 1) / kBN;
+  const int64_t total = tiles_m * tiles_n;
+  const int64_t per_xcd = (total + kXcds - 1) / kXcds;
+  const int64_t tile = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (tile >= total) return;
+  const int64_t group = tile / (kTGroupM * tiles_n);
+  const int64_t first_m = group * kTGroupM;
+  const int64_t gm = tiles_m - first_m < kTGroupM ? tiles_m - first_m : kTGroupM;
+  const int64_t in_group = tile - group * kTGroupM * tiles_n;
+  const int64_t m0 = (first_m + in_group % gm) * kBM;
+  const int64_t n0 = (in_group / gm) * kBN;
+  const int64_t K = a.K;
+  const int64_t KT = K / kBK;
+
+  h8 ra[8];
+  u32x4 qb[2];
+  uint32_t smb = 0;
+  const auto load_tile = [&](int64_t kt) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int c = tid + i * kBThreads;
+      const int row = c >> 3, col = (c & 7) * 8;
+      const int64_t m = m0 + row;
+      ra[i] = m < a.M ? load_h8(a.X + m * K + kt * kBK + col) : zero_h8();
+    }
+    // W row n0 + tid: 64 codes (two 32-code runs) and their group's pair
+    const int64_t n = n0 + tid;
+    if (n < a.N) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        qb[h] = *reinterpret_cast<const u32x4*>(a.Wq + w4_byte<PK>(n, kt * kBK + 32 * h, K));
+      smb = *reinterpret_cast<const uint32_t*>(a.Wsm + w4_sm<PK>(n, kt * kBK, K) * 2);
+    } else {
+      qb[0] = qb[1] = u32x4{0, 0, 0, 0};
+      smb = 0;
+    }
+  };
+  const auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int c = tid + i * kBThreads;
+      const int row = c >> 3, col = (c & 7) * 8;
+      *reinterpret_cast<h8*>(&As[buf][row * LDS_ROW + col]) = ra[i];
+    }
+    h2 s2, m2;
+    scale_min_pairs(smb, s2, m2);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<h8*>(&Bs[buf][tid * LDS_ROW + 32 * h + 8 * i]) =
+            dequant8(qb[h][i], s2, m2);
+  };
+
+  f4 acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  for (int64_t kt = 0; kt < KT; ++kt) {
+    const int buf = (int)(kt & 1);
+    if (kt + 1 < KT) load_tile(kt + 1);
+#pragma unroll
+    for (int ks = 0; ks < kBK / 32; ++ks) {
+      h8 af[8], bf[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        af[i] = *reinterpret_cast<const h8*>(
+            &As[buf][(wm * 128 + i * 16 + r) * LDS_ROW + ks * 32 + g * 8]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        bf[j] = *reinterpret_cast<const h8*>(
+            &Bs[buf][(wn * 128 + j * 16 + r) * LDS_ROW + ks * 32 + g * 8]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[i][j] = mfma16(af[i], bf[j], acc[i][j]);
+    }
+    if (kt + 1 < KT) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  // acc[i][j] element e: row m0 + 128 wm + 16 i + 4 g + e, col n0 + 128 wn + 16 j + r;
+  // row offsets once per row (32 rows, 8 columns per thread)
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const EpiRow row = epilogue_row<EPI>(a, m0 + wm * 128 + i * 16 + 4 * g + e);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        epilogue_at<EPI>(a, row, n0 + wn * 128 + j * 16 + r, acc[i][j][e]);
+    }
+}
+
+
+// ---------------------------------------------------------------------------
 // skinny configurations by M: (waves, steps in flight per wave)
+// ---------------------------------------------------------------------------
 template <int MF> struct SkinnyCfg;
 template <> struct SkinnyCfg<1> { static constexpr int KW = 8, UNR = 2; };
 
@@ -602,6 +758,13 @@ static pipo_status launch_epi(const GemmArgs& a, float* ws, int64_t ws_bytes, hi
       case 4: launch_stream_mf<W4, 4, EPI, PK>(a, pl, S, ws, st); break;
       default: launch_stream_mf<W4, 8, EPI, PK>(a, pl, S, ws, st); break;
     }
+  } else if (W4 && a.M >= kBigMinM) {
+    if constexpr (W4) {
+      const int64_t total = ((a.N + kBN - 1) / kBN) * ((a.M + kBM - 1) / kBM);
+      const int64_t per_xcd = (total + kXcds - 1) / kXcds;
+      launch((gemm_big_w4<EPI, PK>), dim3((unsigned)(per_xcd * kXcds)), dim3(kBThreads), 0, st,
+             a);
+    }
   } else {
     const int64_t total = ((a.N + kTBN - 1) / kTBN) * ((a.M + kTBM - 1) / kTBM);
     const int64_t per_xcd = (total + kXcds - 1) / kXcds;
@@ -638,6 +801,14 @@ pipo_status launch_gemm(const GemmArgs& a, bool w4, int epi, float* workspace,
   }
   if (a.X == nullptr || (w4 ? (a.Wq == nullptr || a.Wsm == nullptr) : a.W == nullptr)) {
     set_error("gemm: null operand");
+    return PIPO_ERR_ARG;
+  }
+  if (a.M >= (int64_t(1) << 31)) {
+    set_error("gemm: M=%lld rows exceeds 2^31 - 1", (long long)a.M);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  if (epi == EPI_QKV && a.rows_per_seq < 1) {
+    set_error("gemm: QKV output with rows_per_seq=%lld", (long long)a.rows_per_seq);
     return PIPO_ERR_ARG;
   }
   if (epi == EPI_QKV && (a.dkv <= 0 || a.N != a.d + 2 * a.dkv)) {

@@ -287,6 +287,28 @@ def test_weight_layouts_bit_identical(wfmt):
         assert np.array_equal(l.view(np.uint32), runs[0][1].view(np.uint32))
 
 
+def test_int4_prefill_big_tiles():
+    """INT4 prefill over 5 x 120 = 600 rows (256 x 256 tiles, ragged in M):
+    against the oracle, and bit-identical with the matrices in either
+    layout."""
+    shape = synth.OPTShape(2, 512, 4, 2048, vocab=1000, max_pos=160)
+    model = synth.SyntheticOPT(shape, seed=19, wfmt="int4")
+    prompt = synth.prompt_tokens(5, 120, shape.vocab, seed=12)
+    runs = []
+    for layout in ("fragment", "row_major"):
+        log(f"int4 prefill 600 rows, {layout}")
+        hw = HostWeights(shape, "int4", model, layout=layout)
+        try:
+            runs.append(_run(hw, prompt, 4))
+        finally:
+            hw.free()
+    err, agree, ties = teacher_forced_check(model, "int4", prompt, runs[0][0], list(runs[0][1]))
+    log(f"  err {err:.2e} agree {agree:.3f}")
+    assert err <= REL_TOL and (agree >= ARGMAX_MIN or ties <= 1)
+    assert np.array_equal(runs[1][0], runs[0][0])
+    assert np.array_equal(runs[1][1].view(np.uint32), runs[0][1].view(np.uint32))
+
+
 def test_head_dim_64_kv_on_host():
     shape = synth.OPTShape(3, 256, 4, 1024, vocab=512, max_pos=64)
     log("head_dim 64, kv on host")

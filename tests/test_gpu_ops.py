@@ -12,6 +12,8 @@ pytestmark = pytest.mark.gpu
 
 GEMM_SHAPES = [(1, 50, 128), (4, 100, 256), (16, 64, 128), (33, 130, 384), (64, 96, 128),
                (65, 200, 256), (128, 128, 128), (300, 257, 512),
+               # INT4 big tiles at M >= 512, ragged M and N
+               (520, 300, 256), (1024, 512, 512),
                # 64-row workgroups (N >= 12288), ragged N
                (16, 12300, 256), (40, 12288, 128), (64, 12350, 128), (7, 1000, 1024),
                # streaming kernel: K split over workgroups (up to 8 ways), INT4
@@ -99,7 +101,7 @@ def test_gemm_w4_exact_on_integers(M, N, K):
         assert np.array_equal(got.astype(np.float64), expected(X @ Wd.T, None, epi, None))
 
 
-@pytest.mark.parametrize("M", [3, 64, 200])
+@pytest.mark.parametrize("M", [3, 64, 200, 600])
 def test_gemm_random_vs_oracle_definition(M):
     log(f"gemm random M={M}")
     rng = np.random.default_rng(M)
@@ -119,11 +121,13 @@ def test_gemm_random_vs_oracle_definition(M):
 
 @pytest.mark.parametrize("M,N,K", [(1, 64, 128), (16, 12288, 256), (7, 1008, 1024),
                                    (33, 144, 384), (64, 1024, 4096), (128, 1040, 1024),
-                                   (129, 64, 256), (300, 272, 512)])
+                                   (129, 64, 256), (300, 272, 512),
+                                   # big tiles (INT4, M >= 512), ragged M and N
+                                   (512, 256, 256), (777, 528, 384), (1030, 272, 1024)])
 @pytest.mark.parametrize("w4", [False, True])
 def test_gemm_fragment_order_equals_row_major(M, N, K, w4):
-    """W in fragment order (skinny, streaming with K splits, and tiled
-    kernels): the same products in the same order, bit for bit."""
+    """W in fragment order (skinny, streaming with K splits, tiled and
+    big-tile kernels): the same products in the same order, bit for bit."""
     log(f"gemm fragment order M={M} N={N} K={K} w4={w4}")
     rng = np.random.default_rng(M + N + K + w4)
     X = rng.standard_normal((M, K)).astype(np.float16)
@@ -137,7 +141,7 @@ def test_gemm_fragment_order_equals_row_major(M, N, K, w4):
                               b.view(np.uint16 if b.dtype == np.float16 else np.uint32))
 
 
-@pytest.mark.parametrize("M", [4, 40, 100, 200])
+@pytest.mark.parametrize("M", [4, 40, 100, 200, 520])
 @pytest.mark.parametrize("w4", [False, True])
 def test_gemm_deterministic_and_split_consistent(M, w4):
     """Repeated calls give the same bits; the K-split result equals the
