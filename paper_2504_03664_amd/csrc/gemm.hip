@@ -3,7 +3,7 @@
 // with W in fp16 or group-wise INT4 (codes expanded to fp16 in registers,
 // the paper's "compute directly on 4-bit weights", Section 3.4).
 //
-// Four kernels, chosen by M (and the weight format):
+// The kernel is chosen by M (and N and the weight format):
 //   * gemm_skinny (M <= 16, decode): every workgroup owns 16 or 64 rows of
 //     W and all M rows of X; its waves split K; W streams from HBM straight
 //     into MFMA operand registers (no LDS), X comes from L2.  Partial sums
@@ -16,8 +16,11 @@
 //   * gemm_tiled (M > 128, prefill): 128 x 128 output tiles, K staged
 //     through double-buffered LDS in steps of 64, 4 waves of 64 x 64; tiles
 //     ordered per XCD so that each XCD's L2 serves a compact block.
-//   * gemm_big_w4 (INT4 prefill, M >= 512): 256 x 256 tiles, 4 waves of
-//     128 x 128, each W row's codes expanded once per tile.
+//   * gemm_big_w4 / gemm_big_f16 (prefill with at least 512 tiles of
+//     256 x 256): INT4 with 4 waves of 128 x 128, each W row's codes
+//     expanded once per tile; fp16 W in fragment order with 8 waves of
+//     128 x 64 fed by global -> LDS loads (no register staging) over four
+//     LDS stages.
 // All accumulate in fp32 with v_mfma_f32_16x16x32_f16, and INT4 codes
 // become the same fp16 values (code * scale + min, rounded once) in every
 // kernel.  The kernel, its configuration and the K split depend only on
@@ -56,11 +59,16 @@ __device__ __forceinline__ EpiRow epilogue_row(const GemmArgs& a, int64_t m) {
   return r;
 }
 
+// bias of column n (0 past N or without bias)
+__device__ __forceinline__ float epilogue_bias(const GemmArgs& a, int64_t n) {
+  return (a.bias && n < a.N) ? h2f(a.bias[n]) : 0.f;
+}
+
+// v: the sum with the column's bias added
 template <int EPI>
-__device__ __forceinline__ void epilogue_at(const GemmArgs& a, const EpiRow& r, int64_t n,
-                                            float acc) {
+__device__ __forceinline__ void epilogue_store(const GemmArgs& a, const EpiRow& r, int64_t n,
+                                               float v) {
   if (r.m >= a.M || n >= a.N) return;
-  const float v = acc + (a.bias ? h2f(a.bias[n]) : 0.f);
   if constexpr (EPI == EPI_F16) {
     a.out16[r.off + n] = f2h(v);
   } else if constexpr (EPI == EPI_RELU_F16) {
@@ -81,7 +89,7 @@ __device__ __forceinline__ void epilogue_at(const GemmArgs& a, const EpiRow& r, 
 
 template <int EPI>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, int64_t m, int64_t n, float acc) {
-  epilogue_at<EPI>(a, epilogue_row<EPI>(a, m), n, acc);
+  epilogue_store<EPI>(a, epilogue_row<EPI>(a, m), n, acc + epilogue_bias(a, n));
 }
 
 // ---------------------------------------------------------------------------
@@ -492,29 +500,41 @@ __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
     __syncthreads();
   }
 
-  // acc[i][j] element e: row m0 + 64 wm + 16 i + 4 g + e, col n0 + 64 wn + 16 j + r
+  // acc[i][j] element e: row m0 + 64 wm + 16 i + 4 g + e, col n0 + 64 wn + 16 j + r;
+  // biases once per column, row offsets once per row
+  float bias[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) bias[j] = epilogue_bias(a, n0 + wn * 64 + j * 16 + r);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int e = 0; e < 4; ++e) {
+      const EpiRow row = epilogue_row<EPI>(a, m0 + wm * 64 + i * 16 + 4 * g + e);
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        epilogue<EPI>(a, m0 + wm * 64 + i * 16 + 4 * g + e, n0 + wn * 64 + j * 16 + r,
-                      acc[i][j][e]);
+      for (int j = 0; j < 4; ++j)
+        epilogue_store<EPI>(a, row, n0 + wn * 64 + j * 16 + r, acc[i][j][e] + bias[j]);
+    }
 }
 
 // ---------------------------------------------------------------------------
-// big-tile GEMM (INT4 prefill, M >= 512): 256 x 256 output tiles, 4 waves
-// of 128 x 128 (8 x 8 accumulator fragments per wave), K in steps of 64
-// through double-buffered LDS (144 KiB).  Each thread expands one W row's
-// 64 codes per step.  Against gemm_tiled a code is expanded once per 256
-// rows of X instead of once per 128, and each LDS operand read feeds twice
-// as many MFMAs; the expansion is what limits gemm_tiled with INT4 (with
-// fp16 W the smaller tiles are as fast: more waves per CU hide latency).
-// Same tile order as gemm_tiled.
+// big-tile GEMMs (prefill with at least kBigMinTiles 256 x 256 tiles, enough
+// to fill the chip twice over): each W element read into LDS feeds 256 rows
+// of X instead of 128, and each LDS operand read feeds more MFMAs.  Same
+// tile order as gemm_tiled; the same MFMA per 32-wide k block in the same k
+// order, so for a given K every kernel gives the same bits.
 // ---------------------------------------------------------------------------
+constexpr int64_t kBigMinTiles = 512;
+
+__host__ __device__ constexpr int64_t big_tiles(int64_t M, int64_t N) {
+  return ((M + 255) / 256) * ((N + 255) / 256);
+}
+
+// INT4: 4 waves of 128 x 128 (8 x 8 accumulator fragments per wave), K in
+// steps of 64 through double-buffered LDS (144 KiB).  Each thread expands
+// one W row's 64 codes per step, so a code is expanded once per 256 rows of
+// X instead of once per 128 (the expansion is what limits gemm_tiled with
+// INT4).
 constexpr int kBM = 256, kBN = 256, kBK = 64, kBPad = 8, kBThreads = 256;
-constexpr int64_t kBigMinM = 512;  // INT4 prefill at M >= 512 uses the big tiles
 
 template <int EPI, bool PK>
 __global__ __launch_bounds__(kBThreads) void gemm_big_w4(GemmArgs a) {
@@ -613,7 +633,10 @@ __global__ __launch_bounds__(kBThreads) void gemm_big_w4(GemmArgs a) {
   }
 
   // acc[i][j] element e: row m0 + 128 wm + 16 i + 4 g + e, col n0 + 128 wn + 16 j + r;
-  // row offsets once per row (32 rows, 8 columns per thread)
+  // biases once per column, row offsets once per row (8 columns, 32 rows per thread)
+  float bias[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) bias[j] = epilogue_bias(a, n0 + wn * 128 + j * 16 + r);
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
@@ -621,10 +644,155 @@ __global__ __launch_bounds__(kBThreads) void gemm_big_w4(GemmArgs a) {
       const EpiRow row = epilogue_row<EPI>(a, m0 + wm * 128 + i * 16 + 4 * g + e);
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        epilogue_at<EPI>(a, row, n0 + wn * 128 + j * 16 + r, acc[i][j][e]);
+        epilogue_store<EPI>(a, row, n0 + wn * 128 + j * 16 + r, acc[i][j][e] + bias[j]);
     }
 }
 
+
+// fp16 W in fragment order: 8 waves (two per SIMD) of 128 x 64 (8 x 4
+// accumulator fragments), K in stages of 32.  A stage is 16 row blocks of X
+// and 16 of W, each 16 rows x 32 k = 1 KiB in MFMA operand order (lane slot
+// r + 16 g holds row r, k = 8 g .. 8 g + 7), moved from global memory
+// straight into LDS by the load unit (global_load_lds_dwordx4: lane l of a
+// wave writes bytes 16 l .. 16 l + 15 of the block), so fragment reads are
+// one contiguous KiB per wave and free of bank conflicts.  Four LDS stages
+// (128 KiB): stage t is read while t + 1 and t + 2 are in flight and t + 3
+// is issued into the buffer that stage t - 1 left.  Fragment registers are
+// double-buffered: the reads of stage t are spread over the MFMAs of stage
+// t - 1.  Rows past M (and row blocks past N) are loaded from the last
+// valid row and their results dropped.
+constexpr int kFThreads = 512;
+constexpr int kFStage = 32 * 1024;       // bytes per LDS stage: 16 KiB of X, 16 KiB of W
+constexpr int kFStages = 4;
+
+__device__ __forceinline__ void lds_dma16(const void* g, uint8_t* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+// s_waitcnt immediate: at most `vm` vector memory operations outstanding
+// and, with lgkm0, no LDS operation (vmcnt bits 3:0 and 15:14, expcnt 6:4
+// left at 7, lgkmcnt 11:8)
+__device__ constexpr int waitcnt_imm(int vm, bool lgkm0) {
+  return (vm & 15) | ((vm >> 4) << 14) | (7 << 4) | ((lgkm0 ? 0 : 15) << 8);
+}
+
+template <int EPI>
+__global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
+  constexpr int FM = 8, FN = 4;  // fragments per wave
+  constexpr int BPW = 2;         // X and W row blocks each wave moves per stage
+  constexpr int PER_STAGE = 2 * BPW;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kFStages * kFStage];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int64_t tiles_m = (a.M + kBM - 1) / kBM, tiles_n = (a.N + kBN - 1) / kBN;
+  const int64_t total = tiles_m * tiles_n;
+  const int64_t per_xcd = (total + kXcds - 1) / kXcds;
+  const int64_t tile = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (tile >= total) return;
+  const int64_t group = tile / (kTGroupM * tiles_n);
+  const int64_t first_m = group * kTGroupM;
+  const int64_t gm = tiles_m - first_m < kTGroupM ? tiles_m - first_m : kTGroupM;
+  const int64_t in_group = tile - group * kTGroupM * tiles_n;
+  const int64_t m0 = (first_m + in_group % gm) * kBM;
+  const int64_t n0 = (in_group / gm) * kBN;
+  const int64_t K = a.K;
+  const int KT = (int)(K / 32);  // K % 128 == 0: KT is even and >= 4
+
+  const int r = lane & 15, g = lane >> 4;
+  const uint16_t* asrc[BPW];
+  const uint16_t* bsrc[BPW];
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) {
+    int64_t m = m0 + 16 * (BPW * wave + i) + r;
+    m = m < a.M ? m : a.M - 1;
+    asrc[i] = a.X + m * K + 8 * g;
+    int64_t nb = (n0 >> 4) + BPW * wave + i;
+    nb = nb < (a.N >> 4) ? nb : (a.N >> 4) - 1;
+    bsrc[i] = a.W + nb * (K >> 5) * 512 + lane * 8;
+  }
+  // stage `src` of K into LDS buffer `buf` % kFStages
+  const auto issue = [&](int src, int buf) {
+    uint8_t* st = lds + (buf % kFStages) * kFStage;
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) {
+      const int b = BPW * wave + i;
+      lds_dma16(asrc[i] + src * 32, st + b * 1024);
+      lds_dma16(bsrc[i] + src * 512, st + 16 * 1024 + b * 1024);
+    }
+  };
+  const auto read = [&](int t, h8 (&fa)[FM], h8 (&fb)[FN]) {
+    const uint8_t* st = lds + (t % kFStages) * kFStage;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+      fb[j] = *reinterpret_cast<const h8*>(st + 16 * 1024 + (FN * wn + j) * 1024 + lane * 16);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+      fa[i] = *reinterpret_cast<const h8*>(st + (FM * wm + i) * 1024 + lane * 16);
+  };
+  f4 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+  const auto mma = [&](const h8 (&fa)[FM], const h8 (&fb)[FN]) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = mfma16(fa[i], fb[j], acc[i][j]);
+  };
+  // Every step issues one stage (past the last, a repeat of it into the
+  // buffer just freed), so the wait count is the same in every step.
+  // Step t: stage t landed in every wave's view (two stages after it may be
+  // in flight) and every wave's reads of stage t - 1 are done; stage t + 3
+  // goes into t - 1's buffer; stage t is read while stage t - 1's MFMAs run.
+  h8 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
+  const auto step = [&](int t, h8 (&ra)[FM], h8 (&rb)[FN], h8 (&ca)[FM], h8 (&cb)[FN]) {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(2 * PER_STAGE, true));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    issue(t + 3 < KT ? t + 3 : KT - 1, t + 3);
+    read(t, ra, rb);
+    mma(ca, cb);
+    // one fragment read, then two MFMAs, in turn
+#pragma unroll
+    for (int k = 0; k < FM + FN; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - 2 * (FM + FN), 0);
+  };
+  issue(0, 0);
+  issue(1, 1);
+  issue(2, 2);
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(2 * PER_STAGE, true));
+  __builtin_amdgcn_s_barrier();
+  issue(3, 3);
+  read(0, fa0, fb0);
+  int t = 1;
+  for (; t < KT - 1; t += 2) {
+    step(t, fa1, fb1, fa0, fb0);
+    step(t + 1, fa0, fb0, fa1, fb1);
+  }
+  step(t, fa1, fb1, fa0, fb0);
+  // every load landed (none may write LDS after the workgroup ends)
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, true));
+  mma(fa1, fb1);
+
+  // acc[i][j] element e: row m0 + 128 wm + 16 i + 4 g + e, col n0 + 64 wn + 16 j + r
+  float bias[FN];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) bias[j] = epilogue_bias(a, n0 + wn * 64 + j * 16 + r);
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const EpiRow row = epilogue_row<EPI>(a, m0 + wm * 128 + i * 16 + 4 * g + e);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        epilogue_store<EPI>(a, row, n0 + wn * 64 + j * 16 + r, acc[i][j][e] + bias[j]);
+    }
+}
 
 // ---------------------------------------------------------------------------
 // skinny configurations by M: (waves, steps in flight per wave)
@@ -758,13 +926,13 @@ static pipo_status launch_epi(const GemmArgs& a, float* ws, int64_t ws_bytes, hi
       case 4: launch_stream_mf<W4, 4, EPI, PK>(a, pl, S, ws, st); break;
       default: launch_stream_mf<W4, 8, EPI, PK>(a, pl, S, ws, st); break;
     }
-  } else if (W4 && a.M >= kBigMinM) {
-    if constexpr (W4) {
-      const int64_t total = ((a.N + kBN - 1) / kBN) * ((a.M + kBM - 1) / kBM);
-      const int64_t per_xcd = (total + kXcds - 1) / kXcds;
-      launch((gemm_big_w4<EPI, PK>), dim3((unsigned)(per_xcd * kXcds)), dim3(kBThreads), 0, st,
-             a);
-    }
+  } else if ((W4 || PK) && big_tiles(a.M, a.N) >= kBigMinTiles) {
+    const int64_t per_xcd = (big_tiles(a.M, a.N) + kXcds - 1) / kXcds;
+    const dim3 grid((unsigned)(per_xcd * kXcds));
+    if constexpr (W4)
+      launch((gemm_big_w4<EPI, PK>), grid, dim3(kBThreads), 0, st, a);
+    else
+      launch((gemm_big_f16<EPI>), grid, dim3(kFThreads), 0, st, a);
   } else {
     const int64_t total = ((a.N + kTBN - 1) / kTBN) * ((a.M + kTBM - 1) / kTBM);
     const int64_t per_xcd = (total + kXcds - 1) / kXcds;

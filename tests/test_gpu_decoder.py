@@ -287,10 +287,9 @@ def test_weight_layouts_bit_identical(wfmt):
         assert np.array_equal(l.view(np.uint32), runs[0][1].view(np.uint32))
 
 
-def test_int4_prefill_big_tiles():
-    """INT4 prefill over 5 x 120 = 600 rows (256 x 256 tiles, ragged in M):
-    against the oracle, and bit-identical with the matrices in either
-    layout."""
+def test_int4_prefill_600_rows_layouts():
+    """INT4 prefill over 5 x 120 = 600 rows (ragged prefill tiles): against
+    the oracle, and bit-identical with the matrices in either layout."""
     shape = synth.OPTShape(2, 512, 4, 2048, vocab=1000, max_pos=160)
     model = synth.SyntheticOPT(shape, seed=19, wfmt="int4")
     prompt = synth.prompt_tokens(5, 120, shape.vocab, seed=12)
