@@ -16,11 +16,11 @@
 //   * gemm_tiled (M > 128, prefill): 128 x 128 output tiles, K staged
 //     through double-buffered LDS in steps of 64, 4 waves of 64 x 64; tiles
 //     ordered per XCD so that each XCD's L2 serves a compact block.
-//   * gemm_big_w4 / gemm_big_f16 (prefill with at least 512 tiles of
-//     256 x 256): INT4 with 4 waves of 128 x 128, each W row's codes
-//     expanded once per tile; fp16 W in fragment order with 8 waves of
-//     128 x 64 fed by global -> LDS loads (no register staging) over four
-//     LDS stages.
+//   * gemm_big_f16 / gemm_big_w4 (prefill with at least 512 tiles of
+//     256 x 256; fp16 W in fragment order, or INT4): 8 waves of 128 x 64
+//     fed by global -> LDS loads (no register staging) over four LDS
+//     stages; INT4 codes reach LDS the same way and are expanded there,
+//     once per tile.
 // All accumulate in fp32 with v_mfma_f32_16x16x32_f16, and INT4 codes
 // become the same fp16 values (code * scale + min, rounded once) in every
 // kernel.  The kernel, its configuration and the K split depend only on
@@ -529,125 +529,7 @@ __host__ __device__ constexpr int64_t big_tiles(int64_t M, int64_t N) {
   return ((M + 255) / 256) * ((N + 255) / 256);
 }
 
-// INT4: 4 waves of 128 x 128 (8 x 8 accumulator fragments per wave), K in
-// steps of 64 through double-buffered LDS (144 KiB).  Each thread expands
-// one W row's 64 codes per step, so a code is expanded once per 256 rows of
-// X instead of once per 128 (the expansion is what limits gemm_tiled with
-// INT4).
-constexpr int kBM = 256, kBN = 256, kBK = 64, kBPad = 8, kBThreads = 256;
-
-template <int EPI, bool PK>
-__global__ __launch_bounds__(kBThreads) void gemm_big_w4(GemmArgs a) {
-  constexpr int LDS_ROW = kBK + kBPad;  // halves
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][kBM * LDS_ROW];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kBN * LDS_ROW];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int r = lane & 15, g = lane >> 4;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int64_t tiles_m = (a.M + kBM - 1) / kBM, tiles_n = (a.N + kBN - 1) / kBN;
-  const int64_t total = tiles_m * tiles_n;
-  const int64_t per_xcd = (total + kXcds - 1) / kXcds;
-  const int64_t tile = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-  if (tile >= total) return;
-  const int64_t group = tile / (kTGroupM * tiles_n);
-  const int64_t first_m = group * kTGroupM;
-  const int64_t gm = tiles_m - first_m < kTGroupM ? tiles_m - first_m : kTGroupM;
-  const int64_t in_group = tile - group * kTGroupM * tiles_n;
-  const int64_t m0 = (first_m + in_group % gm) * kBM;
-  const int64_t n0 = (in_group / gm) * kBN;
-  const int64_t K = a.K;
-  const int64_t KT = K / kBK;
-
-  h8 ra[8];
-  u32x4 qb[2];
-  uint32_t smb = 0;
-  const auto load_tile = [&](int64_t kt) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int c = tid + i * kBThreads;
-      const int row = c >> 3, col = (c & 7) * 8;
-      const int64_t m = m0 + row;
-      ra[i] = m < a.M ? load_h8(a.X + m * K + kt * kBK + col) : zero_h8();
-    }
-    // W row n0 + tid: 64 codes (two 32-code runs) and their group's pair
-    const int64_t n = n0 + tid;
-    if (n < a.N) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-        qb[h] = *reinterpret_cast<const u32x4*>(a.Wq + w4_byte<PK>(n, kt * kBK + 32 * h, K));
-      smb = *reinterpret_cast<const uint32_t*>(a.Wsm + w4_sm<PK>(n, kt * kBK, K) * 2);
-    } else {
-      qb[0] = qb[1] = u32x4{0, 0, 0, 0};
-      smb = 0;
-    }
-  };
-  const auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int c = tid + i * kBThreads;
-      const int row = c >> 3, col = (c & 7) * 8;
-      *reinterpret_cast<h8*>(&As[buf][row * LDS_ROW + col]) = ra[i];
-    }
-    h2 s2, m2;
-    scale_min_pairs(smb, s2, m2);
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        *reinterpret_cast<h8*>(&Bs[buf][tid * LDS_ROW + 32 * h + 8 * i]) =
-            dequant8(qb[h][i], s2, m2);
-  };
-
-  f4 acc[8][8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
-
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-  for (int64_t kt = 0; kt < KT; ++kt) {
-    const int buf = (int)(kt & 1);
-    if (kt + 1 < KT) load_tile(kt + 1);
-#pragma unroll
-    for (int ks = 0; ks < kBK / 32; ++ks) {
-      h8 af[8], bf[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        af[i] = *reinterpret_cast<const h8*>(
-            &As[buf][(wm * 128 + i * 16 + r) * LDS_ROW + ks * 32 + g * 8]);
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        bf[j] = *reinterpret_cast<const h8*>(
-            &Bs[buf][(wn * 128 + j * 16 + r) * LDS_ROW + ks * 32 + g * 8]);
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = mfma16(af[i], bf[j], acc[i][j]);
-    }
-    if (kt + 1 < KT) store_tile(buf ^ 1);
-    __syncthreads();
-  }
-
-  // acc[i][j] element e: row m0 + 128 wm + 16 i + 4 g + e, col n0 + 128 wn + 16 j + r;
-  // biases once per column, row offsets once per row (8 columns, 32 rows per thread)
-  float bias[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) bias[j] = epilogue_bias(a, n0 + wn * 128 + j * 16 + r);
-#pragma unroll
-  for (int i = 0; i < 8; ++i)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const EpiRow row = epilogue_row<EPI>(a, m0 + wm * 128 + i * 16 + 4 * g + e);
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        epilogue_store<EPI>(a, row, n0 + wn * 128 + j * 16 + r, acc[i][j][e] + bias[j]);
-    }
-}
-
+constexpr int kBM = 256, kBN = 256;
 
 // fp16 W in fragment order: 8 waves (two per SIMD) of 128 x 64 (8 x 4
 // accumulator fragments), K in stages of 32.  A stage is 16 row blocks of X
@@ -780,6 +662,151 @@ __global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
   mma(fa1, fb1);
 
   // acc[i][j] element e: row m0 + 128 wm + 16 i + 4 g + e, col n0 + 64 wn + 16 j + r
+  float bias[FN];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) bias[j] = epilogue_bias(a, n0 + wn * 64 + j * 16 + r);
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const EpiRow row = epilogue_row<EPI>(a, m0 + wm * 128 + i * 16 + 4 * g + e);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        epilogue_store<EPI>(a, row, n0 + wn * 64 + j * 16 + r, acc[i][j][e] + bias[j]);
+    }
+}
+
+// INT4 W (fragment order or row-major): as gemm_big_f16, with the W area of
+// a stage filled by the threads.  The codes (16 bytes per W row and stage)
+// and (scale, min) pairs of a stage reach LDS through the load unit one
+// stage ahead of X; at step t every thread expands 16 codes of stage t + 1
+// (W row tid / 2, k 16 (tid & 1) .. + 15) into two 16-byte fragment slots,
+// so each code is expanded once per 256 rows of X.  A stage is X 16 KiB,
+// expanded W 16 KiB, codes 4 KiB, pairs 1 KiB; four stages, 148 KiB.
+template <int EPI, bool PK>
+__global__ __launch_bounds__(kFThreads) void gemm_big_w4(GemmArgs a) {
+  constexpr int FM = 8, FN = 4;
+  constexpr int BPW = 2;
+  constexpr int PER_STEP = BPW + 1;               // X blocks + one code or pair load
+  constexpr int STAGE = 32 * 1024 + 4096 + 1024;  // bytes per LDS stage
+  constexpr int WOFF = 16 * 1024, COFF = 32 * 1024, SOFF = 36 * 1024;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kFStages * STAGE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int64_t tiles_m = (a.M + kBM - 1) / kBM, tiles_n = (a.N + kBN - 1) / kBN;
+  const int64_t total = tiles_m * tiles_n;
+  const int64_t per_xcd = (total + kXcds - 1) / kXcds;
+  const int64_t tile = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (tile >= total) return;
+  const int64_t group = tile / (kTGroupM * tiles_n);
+  const int64_t first_m = group * kTGroupM;
+  const int64_t gm = tiles_m - first_m < kTGroupM ? tiles_m - first_m : kTGroupM;
+  const int64_t in_group = tile - group * kTGroupM * tiles_n;
+  const int64_t m0 = (first_m + in_group % gm) * kBM;
+  const int64_t n0 = (in_group / gm) * kBN;
+  const int64_t K = a.K;
+  const int KT = (int)(K / 32);
+
+  const int r = lane & 15, g = lane >> 4;
+  const uint16_t* asrc[BPW];
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) {
+    int64_t m = m0 + 16 * (BPW * wave + i) + r;
+    m = m < a.M ? m : a.M - 1;
+    asrc[i] = a.X + m * K + 8 * g;
+  }
+  // waves 0-3: the codes of W rows 64 w + lane; waves 4-7: their pairs
+  int64_t wn_row = n0 + 64 * (wave & 3) + lane;
+  wn_row = wn_row < a.N ? wn_row : a.N - 1;
+  const auto issue_x = [&](int src, int buf) {
+    uint8_t* st = lds + (buf % kFStages) * STAGE;
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) lds_dma16(asrc[i] + src * 32, st + (BPW * wave + i) * 1024);
+  };
+  const auto issue_w = [&](int src, int buf) {
+    uint8_t* st = lds + (buf % kFStages) * STAGE;
+    if (wave < 4)
+      lds_dma16(a.Wq + w4_byte<PK>(wn_row, 32 * src, K), st + COFF + 64 * wave * 16);
+    else
+      __builtin_amdgcn_global_load_lds(a.Wsm + w4_sm<PK>(wn_row, 32 * src, K) * 2,
+                                       (__attribute__((address_space(3))) void*)(st + SOFF + 64 * (wave - 4) * 4),
+                                       4, 0, 0);
+  };
+  // thread: W row tid / 2 of the tile, k 16 (tid & 1) .. + 15 of the stage
+  const auto expand = [&](int buf) {
+    uint8_t* st = lds + (buf % kFStages) * STAGE;
+    const int row = tid >> 1, half = tid & 1;
+    const u32x2 c = *reinterpret_cast<const u32x2*>(st + COFF + row * 16 + half * 8);
+    const uint32_t sm = *reinterpret_cast<const uint32_t*>(st + SOFF + row * 4);
+    h2 s2, m2;
+    scale_min_pairs(sm, s2, m2);
+    uint8_t* wb = st + WOFF + (row >> 4) * 1024 + ((row & 15) + 32 * half) * 16;
+    *reinterpret_cast<h8*>(wb) = dequant8(c[0], s2, m2);
+    *reinterpret_cast<h8*>(wb + 256) = dequant8(c[1], s2, m2);
+  };
+  const auto read = [&](int t, h8 (&fa)[FM], h8 (&fb)[FN]) {
+    const uint8_t* st = lds + (t % kFStages) * STAGE;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+      fb[j] = *reinterpret_cast<const h8*>(st + WOFF + (FN * wn + j) * 1024 + lane * 16);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+      fa[i] = *reinterpret_cast<const h8*>(st + (FM * wm + i) * 1024 + lane * 16);
+  };
+  f4 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+  const auto mma = [&](const h8 (&fa)[FM], const h8 (&fb)[FN]) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = mfma16(fa[i], fb[j], acc[i][j]);
+  };
+  const auto clampk = [&](int s) { return s < KT ? s : KT - 1; };
+  // step t: codes of stage t + 1 and X of stage t landed; codes of t + 4
+  // and X of t + 3 issued; codes of t + 1 expanded; stage t read while the
+  // MFMAs of t - 1 run
+  h8 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
+  const auto step = [&](int t, h8 (&ra)[FM], h8 (&rb)[FN], h8 (&ca)[FM], h8 (&cb)[FN], bool mm) {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(2 * PER_STEP, true));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    issue_w(clampk(t + 4), t + 4);
+    issue_x(clampk(t + 3), t + 3);
+    expand(t + 1);
+    read(t, ra, rb);
+    if (mm) mma(ca, cb);
+#pragma unroll
+    for (int k = 0; k < FM + FN; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - 2 * (FM + FN), 0);
+  };
+  issue_w(0, 0);
+  issue_w(1, 1);
+  issue_x(0, 0);
+  issue_w(2, 2);
+  issue_x(1, 1);
+  issue_w(3, 3);
+  issue_x(2, 2);
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(2 * PER_STEP + 2, true));  // codes of stage 0
+  __builtin_amdgcn_s_barrier();
+  expand(0);
+  step(0, fa0, fb0, fa1, fb1, false);
+  int t = 1;
+  for (; t < KT - 1; t += 2) {
+    step(t, fa1, fb1, fa0, fb0, true);
+    step(t + 1, fa0, fb0, fa1, fb1, true);
+  }
+  step(t, fa1, fb1, fa0, fb0, true);
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, true));
+  mma(fa1, fb1);
+
   float bias[FN];
 #pragma unroll
   for (int j = 0; j < FN; ++j) bias[j] = epilogue_bias(a, n0 + wn * 64 + j * 16 + r);
@@ -930,7 +957,7 @@ static pipo_status launch_epi(const GemmArgs& a, float* ws, int64_t ws_bytes, hi
     const int64_t per_xcd = (big_tiles(a.M, a.N) + kXcds - 1) / kXcds;
     const dim3 grid((unsigned)(per_xcd * kXcds));
     if constexpr (W4)
-      launch((gemm_big_w4<EPI, PK>), grid, dim3(kBThreads), 0, st, a);
+      launch((gemm_big_w4<EPI, PK>), grid, dim3(kFThreads), 0, st, a);
     else
       launch((gemm_big_f16<EPI>), grid, dim3(kFThreads), 0, st, a);
   } else {
