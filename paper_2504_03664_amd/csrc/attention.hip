@@ -345,134 +345,191 @@ __global__ __launch_bounds__(D) void attn_decode_combine(const float* __restrict
 }
 
 // ---------------------------------------------------------------------------
-// prefill: grid (ceil(P / 64), heads, b), 4 waves x 16 queries.  Keys come
-// in blocks of 64 (K row-major and V transposed in LDS); each wave keeps an
-// online softmax per query row and its O tile in MFMA accumulators.
-template <int D>
-__global__ __launch_bounds__(256) void attn_prefill_k(const uint16_t* __restrict__ q,
-                                                      const uint16_t* __restrict__ kc,
-                                                      const uint16_t* __restrict__ vc,
-                                                      uint16_t* __restrict__ o, int b, int P,
-                                                      int H, int Hkv) {
-  constexpr int KB = 64;
-  constexpr int KROW = D + 8;
-  constexpr int VROW = KB + 8;
-  constexpr int PROW = KB + 8;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[KB * KROW];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VROW];
-  __shared__ __attribute__((aligned(16))) uint16_t Ps[4][16 * PROW];
+// prefill (flash-style): a workgroup owns 128 queries of one head and
+// sequence, 4 waves x 32 queries (two sub-blocks of 16).  Keys come in
+// blocks of 64, K and V moved from the cache straight into LDS by the load
+// unit (double-buffered), rows stored with their 16-byte chunks permuted by
+// an XOR of the row so that fragment reads hit distinct banks.  The wave
+// computes S^T = K Q^T (keys on the MFMA rows, its queries on the columns,
+// so each lane holds scores of one query), an online softmax per query in
+// fp32, and O^T += V^T P^T: the probabilities stay in the registers they
+// were computed in (a lane's 8 keys per MFMA are the ones its S^T fragment
+// gave it; V^T is read with the same key order through transposed LDS
+// reads).  Workgroups with the most key blocks start first.
+constexpr int kPQ = 128;  // queries per workgroup
+constexpr int kPK = 64;   // keys per block
 
-  const int qb = blockIdx.x, h = blockIdx.y, bi = blockIdx.z;
+template <int D>
+__device__ __forceinline__ int kv_swz(int key, int chunk) {
+  // rows of D halves; 256 / (2 D) rows share a 256-byte line of LDS
+  return chunk ^ ((key / (128 / D)) & (D / 8 - 1));
+}
+
+// two waves per SIMD (the register budget the compiler is held to)
+template <int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_prefill_k(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
+    const uint16_t* __restrict__ vc, uint16_t* __restrict__ o, int b, int P, int H, int Hkv) {
+  constexpr int ROWB = 2 * D;               // bytes per key row in LDS
+  constexpr int BLK = kPK * ROWB;           // bytes of K (or V) per block
+  constexpr int DMA = BLK / 1024 / 4;       // DMA instructions per wave for K (and for V)
+  constexpr int KK = D / 32;                // MFMA k steps over the head dimension
+  constexpr int NF = D / 16;                // head-dimension fragments of O^T
+  constexpr float kLog2e = 1.4426950408889634f;
+  __shared__ __attribute__((aligned(1024))) uint8_t kv[2][2][BLK];  // [buffer][K, V]
+
+  const int nqb = (P + kPQ - 1) / kPQ;
+  const int qb = nqb - 1 - (int)blockIdx.x;  // most key blocks first
+  const int h = blockIdx.y, bi = blockIdx.z;
   const int64_t d = (int64_t)H * D, dkv = (int64_t)Hkv * D;
-  const int kh = h / (H / Hkv);  // key/value head of query head h
+  const int kh = h / (H / Hkv);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, g = lane >> 4;
-  const int q0 = qb * 64 + wave * 16;
+  const int qw = qb * kPQ + wave * 32;       // this wave's first query
+  const int nkb = (min(qb * kPQ + kPQ, P) + kPK - 1) / kPK;
 
-  h8 qf[D / 32];
-  {
-    const int qp = q0 + r;
+  // Q^T fragments (B operand): lane (r, g) holds query qw + 16 u + r, dims 32 kk + 8 g ..
+  h8 qf[2][KK];
 #pragma unroll
-    for (int kk = 0; kk < D / 32; ++kk)
-      qf[kk] = qp < P ? load_h8(q + ((int64_t)bi * P + qp) * d + (int64_t)h * D + 32 * kk + 8 * g)
-                      : zero_h8();
-  }
-  f4 oacc[D / 16];
+  for (int u = 0; u < 2; ++u) {
+    const int qp = qw + 16 * u + r;
 #pragma unroll
-  for (int n = 0; n < D / 16; ++n) oacc[n] = f4{0.f, 0.f, 0.f, 0.f};
-  float mrow[4], lrow[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    mrow[e] = -INFINITY;
-    lrow[e] = 0.f;
+    for (int kk = 0; kk < KK; ++kk)
+      qf[u][kk] = qp < P ? load_h8(q + ((int64_t)bi * P + qp) * d + (int64_t)h * D + 32 * kk + 8 * g)
+                         : zero_h8();
   }
 
-  for (int kb = 0; kb <= qb; ++kb) {
-    __syncthreads();
-    for (int c = tid; c < KB * (D / 8); c += 256) {
-      const int key = c / (D / 8), col = (c % (D / 8)) * 8;
-      const int kp = kb * KB + key;
-      const int64_t off = ((int64_t)kp * b + bi) * dkv + (int64_t)kh * D + col;
-      const h8 kv = kp < P ? load_h8(kc + off) : zero_h8();
-      const h8 vv = kp < P ? load_h8(vc + off) : zero_h8();
-      *reinterpret_cast<h8*>(&Ks[key * KROW + col]) = kv;
-      const u32x4 vw = __builtin_bit_cast(u32x4, vv);
+  // DMA of key block kb into buffer buf: LDS byte p of a block holds row
+  // p / ROWB, chunk slot (p % ROWB) / 16, i.e. cache chunk kv_swz(row, slot)
+  const auto issue = [&](int kb, int buf) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-        Vt[(col + i) * VROW + key] = (uint16_t)(vw[i >> 1] >> (16 * (i & 1)));
+    for (int i = 0; i < DMA; ++i) {
+      const int p = (wave * DMA + i) * 1024 + lane * 16;
+      const int row = p / ROWB, slot = (p % ROWB) / 16;
+      int kp = kb * kPK + row;
+      kp = kp < P ? kp : P - 1;
+      const int64_t off = ((int64_t)kp * b + bi) * dkv + (int64_t)kh * D + 8 * kv_swz<D>(row, slot);
+      lds_dma16(kc + off, &kv[buf][0][(wave * DMA + i) * 1024]);
+      lds_dma16(vc + off, &kv[buf][1][(wave * DMA + i) * 1024]);
     }
-    __syncthreads();
+  };
 
-    f4 s[4];
+  f4 oacc[2][NF];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      s[j] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int kk = 0; kk < D / 32; ++kk) {
-        const h8 kf = *reinterpret_cast<const h8*>(&Ks[(j * 16 + r) * KROW + 32 * kk + 8 * g]);
-        s[j] = mfma16(qf[kk], kf, s[j]);
-      }
-    }
-    // s[j][e]: query q0 + 4 g + e, key kb * 64 + 16 j + r
-    float bm[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int qpos = q0 + 4 * g + e;
-      bm[e] = -INFINITY;
+    for (int n = 0; n < NF; ++n) oacc[u][n] = f4{0.f, 0.f, 0.f, 0.f};
+  float mrow[2] = {-INFINITY, -INFINITY}, lrow[2] = {0.f, 0.f};
+
+  issue(0, 0);
+  if (nkb > 1) issue(1, 1);
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int buf = kb & 1;
+    // block kb landed (block kb + 1 may still be in flight)
+    if (kb + 1 < nkb) __builtin_amdgcn_s_waitcnt(waitcnt_imm(2 * DMA, false));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, false));
+    wg_barrier();
+    const int k0 = kb * kPK;
+    if (k0 <= qw + 31) {  // some key of the block is visible to this wave
+      const uint8_t* Kl = kv[buf][0];
+      const uint8_t* Vl = kv[buf][1];
+      // S^T: s[u][j][e] = score of key k0 + 16 j + 4 g + e for query qw + 16 u + r
+      f4 s[2][4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int key = kb * KB + 16 * j + r;
-        if (key > qpos || key >= P) s[j][e] = -INFINITY;
-        bm[e] = fmaxf(bm[e], s[j][e]);
+        s[0][j] = f4{0.f, 0.f, 0.f, 0.f};
+        s[1][j] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          const int row = 16 * j + r;
+          const h8 kf = *reinterpret_cast<const h8*>(Kl + row * ROWB + 16 * kv_swz<D>(row, 4 * kk + g));
+          s[0][j] = mfma16(kf, qf[0][kk], s[0][j]);
+          s[1][j] = mfma16(kf, qf[1][kk], s[1][j]);
+        }
       }
+      const bool edge = k0 + kPK - 1 > qw || k0 + kPK > P;  // the block needs masking
+      h8 pf[2][2];  // P^T fragments (B operand) per sub-block and 32-key half
 #pragma unroll
-      for (int off = 1; off < 16; off <<= 1) bm[e] = fmaxf(bm[e], __shfl_xor(bm[e], off, 64));
-    }
-    float alpha[4], rs[4];
+      for (int u = 0; u < 2; ++u) {
+        const int qp = qw + 16 * u + r;
+        float bm = -INFINITY;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float mnew = fmaxf(mrow[e], bm[e]);
-      alpha[e] = mrow[e] == -INFINITY ? 0.f : expf(mrow[e] - mnew);
-      mrow[e] = mnew;
-      rs[e] = 0.f;
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float p = expf(s[j][e] - mnew);
-        s[j][e] = p;
-        rs[e] += p;
+          for (int e = 0; e < 4; ++e) {
+            const int key = k0 + 16 * j + 4 * g + e;
+            if (edge && (key > qp || key >= P)) s[u][j][e] = -INFINITY;
+            bm = fmaxf(bm, s[u][j][e]);
+          }
+        bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
+        bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+        const float mnew = fmaxf(mrow[u], bm);
+        // every query row has a visible key in its first block, so mnew is finite
+        const float alpha = exp2f((mrow[u] - mnew) * kLog2e);
+        const float mb = mnew * kLog2e;
+        mrow[u] = mnew;
+        float rs = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float p = exp2f(s[u][j][e] * kLog2e - mb);
+            s[u][j][e] = p;
+            rs += p;
+          }
+        rs += __shfl_xor(rs, 16, 64);
+        rs += __shfl_xor(rs, 32, 64);
+        lrow[u] = lrow[u] * alpha + rs;
+#pragma unroll
+        for (int n = 0; n < NF; ++n) oacc[u][n] *= alpha;
+#pragma unroll
+        for (int hk = 0; hk < 2; ++hk)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            pf[u][hk][e] = (_Float16)s[u][2 * hk][e];
+            pf[u][hk][4 + e] = (_Float16)s[u][2 * hk + 1][e];
+          }
       }
+      // O^T += V^T P^T over the two 32-key halves: lane (r, g) needs V rows
+      // 32 hk + 4 g + (0..3) and 32 hk + 16 + 4 g + (0..3), dim 16 n + r;
+      // lane i' of its group addresses row base + i' / 4, dims 16 n + 4 (i' % 4)
 #pragma unroll
-      for (int off = 1; off < 16; off <<= 1) rs[e] += __shfl_xor(rs[e], off, 64);
-      lrow[e] = lrow[e] * alpha[e] + rs[e];
+      for (int hk = 0; hk < 2; ++hk)
+#pragma unroll
+        for (int n = 0; n < NF; ++n) {
+          h8 vf;
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            const int row = 32 * hk + 16 * half + 4 * g + (r >> 2);
+            const int dim = 16 * n + 4 * (r & 3);
+            const h4 t = lds_read_tr16(Vl + row * ROWB + 16 * kv_swz<D>(row, dim / 8) + 2 * (dim % 8));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) vf[4 * half + e] = t[e];
+          }
+          oacc[0][n] = mfma16(vf, pf[0][hk], oacc[0][n]);
+          oacc[1][n] = mfma16(vf, pf[1][hk], oacc[1][n]);
+        }
     }
-#pragma unroll
-    for (int n = 0; n < D / 16; ++n)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) oacc[n][e] *= alpha[e];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) Ps[wave][(4 * g + e) * PROW + 16 * j + r] = f2h(s[j][e]);
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < KB / 32; ++kk) {
-      const h8 pf = *reinterpret_cast<const h8*>(&Ps[wave][r * PROW + 32 * kk + 8 * g]);
-#pragma unroll
-      for (int n = 0; n < D / 16; ++n) {
-        const h8 vf = *reinterpret_cast<const h8*>(&Vt[(16 * n + r) * VROW + 32 * kk + 8 * g]);
-        oacc[n] = mfma16(pf, vf, oacc[n]);
-      }
-    }
+    // every wave is done with this buffer
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, true));
+    wg_barrier();
+    if (kb + 2 < nkb) issue(kb + 2, buf);
   }
 
+  // oacc[u][n][e]: dim 16 n + 4 g + e of query qw + 16 u + r
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int qpos = q0 + 4 * g + e;
-    if (qpos >= P) continue;
-    const float inv = 1.f / lrow[e];
-    uint16_t* orow = o + ((int64_t)bi * P + qpos) * d + (int64_t)h * D;
+  for (int u = 0; u < 2; ++u) {
+    const int qp = qw + 16 * u + r;
+    if (qp >= P) continue;
+    const float inv = 1.f / lrow[u];
+    uint16_t* orow = o + ((int64_t)bi * P + qp) * d + (int64_t)h * D;
 #pragma unroll
-    for (int n = 0; n < D / 16; ++n) orow[16 * n + r] = f2h(oacc[n][e] * inv);
+    for (int n = 0; n < NF; ++n) {
+      u32x2 w;
+      w[0] = (uint32_t)f2h(oacc[u][n][0] * inv) | ((uint32_t)f2h(oacc[u][n][1] * inv) << 16);
+      w[1] = (uint32_t)f2h(oacc[u][n][2] * inv) | ((uint32_t)f2h(oacc[u][n][3] * inv) << 16);
+      *reinterpret_cast<u32x2*>(orow + 16 * n + 4 * g) = w;
+    }
   }
 }
 
@@ -601,7 +658,7 @@ pipo_status launch_attn_prefill(const uint16_t* q, const uint16_t* kc, const uin
     return PIPO_ERR_ARG;
   }
   PIPO_TRY(check_heads("attn_prefill", n_heads, n_kv_heads, head_dim));
-  const dim3 grid((unsigned)((P + 63) / 64), (unsigned)n_heads, (unsigned)b);
+  const dim3 grid((unsigned)((P + kPQ - 1) / kPQ), (unsigned)n_heads, (unsigned)b);
   if (head_dim == 128)
     launch(attn_prefill_k<128>, grid, dim3(256), 0, st, q, kc, vc, o, b, P, n_heads, n_kv_heads);
   else

@@ -126,6 +126,42 @@ __device__ __forceinline__ int64_t w4_sm(int64_t n, int64_t k, int64_t K) {
     return n * (K / 64) + k / 64;
 }
 
+// 16 bytes from global memory straight into LDS (global_load_lds_dwordx4):
+// lane l of the wave writes bytes 16 l .. 16 l + 15 from `lds`, which must
+// be the same for every lane.  Counted by vmcnt like any vector load.
+__device__ __forceinline__ void lds_dma16(const void* g, uint8_t* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+// s_waitcnt immediate: at most `vm` vector memory operations outstanding
+// and, with lgkm0, no LDS operation (vmcnt bits 3:0 and 15:14, expcnt 6:4
+// left at 7, lgkmcnt 11:8)
+__device__ constexpr int waitcnt_imm(int vm, bool lgkm0) {
+  return (vm & 15) | ((vm >> 4) << 14) | (7 << 4) | ((lgkm0 ? 0 : 15) << 8);
+}
+
+// Workgroup barrier without the fence of __syncthreads (whose release half
+// waits for every outstanding vector load, prefetches into LDS included);
+// the empty asm statements keep the compiler from moving memory operations
+// across it.  LDS writes must have been waited for (s_waitcnt) before it.
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Transposed LDS read (ds_read_b64_tr_b16).  Within each group of 16
+// lanes, lane i receives element j (j = 0..3) from the 8-byte row that lane
+// 4 j + i / 4 of the group addresses, at 16-bit position i % 4: the group's
+// 16 addresses form a 4 x 16 matrix of halves and each lane gets a column.
+typedef short s4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ h4 lds_read_tr16(const uint8_t* lds) {
+  // the whole vector is reinterpreted: clang's bit_cast of a single vector
+  // element reads element 0
+  return __builtin_bit_cast(
+      h4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)lds));
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_shfl_xor(T v, int mask) {
   return __shfl_xor(v, mask, 64);

@@ -547,16 +547,6 @@ constexpr int kFThreads = 512;
 constexpr int kFStage = 32 * 1024;       // bytes per LDS stage: 16 KiB of X, 16 KiB of W
 constexpr int kFStages = 4;
 
-__device__ __forceinline__ void lds_dma16(const void* g, uint8_t* lds) {
-  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
-}
-// s_waitcnt immediate: at most `vm` vector memory operations outstanding
-// and, with lgkm0, no LDS operation (vmcnt bits 3:0 and 15:14, expcnt 6:4
-// left at 7, lgkmcnt 11:8)
-__device__ constexpr int waitcnt_imm(int vm, bool lgkm0) {
-  return (vm & 15) | ((vm >> 4) << 14) | (7 << 4) | ((lgkm0 ? 0 : 15) << 8);
-}
-
 template <int EPI>
 __global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
   constexpr int FM = 8, FN = 4;  // fragments per wave

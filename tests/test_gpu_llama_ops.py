@@ -162,7 +162,8 @@ def test_attn_decode_gqa_with_one_group_is_the_mha_kernel():
 
 
 @pytest.mark.parametrize("b,P,H,Hkv,D", [(1, 1, 4, 2, 64), (2, 37, 8, 2, 128),
-                                         (1, 130, 8, 1, 64), (2, 64, 32, 8, 128)])
+                                         (1, 130, 8, 1, 64), (2, 64, 32, 8, 128),
+                                         (1, 300, 8, 2, 128)])
 def test_attn_prefill_gqa_vs_oracle(b, P, H, Hkv, D):
     log(f"attn_prefill_gqa b={b} P={P} H={H}/{Hkv} D={D}")
     rng = np.random.default_rng(P * 5 + b + H)
