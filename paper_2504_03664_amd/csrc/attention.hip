@@ -473,7 +473,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
         for (int j = 0; j < 4; ++j)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float p = exp2f(s[u][j][e] * kLog2e - mb);
+            // v_exp_f32 without denormal scaling: p below 2^-126 becomes 0
+            const float p = __builtin_amdgcn_exp2f(s[u][j][e] * kLog2e - mb);
             s[u][j][e] = p;
             rs += p;
           }
