@@ -147,25 +147,32 @@ class CopyPool {
   // n bytes of file `fd` at `off` into dst, one 4 KiB-aligned piece per
   // thread (direct I/O needs aligned offsets and lengths; off and n are
   // multiples of 4 KiB).  With `bounce` (pageable, 4 KiB aligned, n bytes)
-  // each thread reads its piece there and copies it to dst: direct I/O
-  // cannot target pinned device-mapped pages.  False on an error or a
-  // short file.
+  // each thread reads its piece there and copies it to dst (direct I/O
+  // cannot target pinned device-mapped pages), 2 MiB at a time, so that
+  // the other threads keep the disk busy while one copies and only the last
+  // 2 MiB copy of each piece is left when the reads end.  False on an error
+  // or a short file.
   bool pread_all(int fd, void* dst, size_t n, int64_t off, char* bounce) {
+    constexpr size_t kSub = 2u << 20;
     std::atomic<bool> ok{true};
     run([&, dst, n, off, bounce](int i) {
       const size_t per = (n / n_ + 4095) / 4096 * 4096;
       const size_t a = std::min(n, i * per), b = (i == n_ - 1) ? n : std::min(n, a + per);
       char* to = bounce ? bounce : (char*)dst;
-      for (size_t p = a; p < b && ok.load();) {
-        const ssize_t r = ::pread(fd, to + p, b - p, off + (int64_t)p);
-        if (r < 0 && errno == EINTR) continue;
-        if (r <= 0) {
-          ok = false;
-          break;
+      for (size_t s = a; s < b && ok.load();) {
+        const size_t e = std::min(b, s + kSub);
+        for (size_t p = s; p < e && ok.load();) {
+          const ssize_t r = ::pread(fd, to + p, e - p, off + (int64_t)p);
+          if (r < 0 && errno == EINTR) continue;
+          if (r <= 0) {
+            ok = false;
+            break;
+          }
+          p += (size_t)r;
         }
-        p += (size_t)r;
+        if (bounce && ok.load()) std::memcpy((char*)dst + s, bounce + s, e - s);
+        s = e;
       }
-      if (bounce && ok.load() && b > a) std::memcpy((char*)dst + a, bounce + a, b - a);
     });
     return ok.load();
   }
