@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--no-timestamps", action="store_true",
                     help="skip device timestamps (no busy %% or kernel roofline)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--segment-copies", action="store_true",
+                    help="copy each tensor of a layer separately instead of one merged range "
+                         "(ablation of the paper's data merging)")
     ap.add_argument("--layers", type=int, default=0, help="override layer count (testing only)")
     ap.add_argument("--disk-dir", default=None,
                     help="directory of the disk tier's file (disk workloads; default: the "
@@ -238,7 +241,8 @@ def main():
                   kv_fmt=wl.kv_fmt, weights_on_disk=wl.weights_on_disk,
                   disk_dir=disk["dir"] if disk else None,
                   n_weight_slots=args.slots, n_h2d_streams=args.h2d_streams,
-                  chunk_bytes=args.chunk_mb << 20, max_batch=wl.batch, max_seq=max_seq)
+                  chunk_bytes=args.chunk_mb << 20, max_batch=wl.batch, max_seq=max_seq,
+                  debug_flags=B.PIPO_DBG_SEGMENT_COPIES if args.segment_copies else 0)
     if disk:
         log(f"disk tier file written in {time.time() - t0:.1f} s")
         # the disk's read rate: the tier's whole file (what a step reads) read
@@ -305,7 +309,8 @@ def main():
                    "kv_cache": ("host (pinned, or pageable through pinned staging), streamed"
                                 if wl.kv_on_host else "HBM") + f", {wl.kv_fmt}",
                    "chunk_bytes": args.chunk_mb << 20, "slots": args.slots,
-                   "h2d_streams": args.h2d_streams},
+                   "h2d_streams": args.h2d_streams,
+                   "copies": "per tensor" if args.segment_copies else "merged per layer"},
         "h2d_link": {"peak_gbps": round(peak, 2), "peak_1stream_gbps": round(peak1, 2),
                      "sustained_gbps": round(sustained, 2),
                      "frac_of_peak": round(sustained / peak, 4),
