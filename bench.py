@@ -78,14 +78,14 @@ def gemm_symbols(M, N, K, epi, w4, frag):
     workgroup when N >= 12288), streaming (16 < M <= 128; K split into the
     largest power of two <= 8 keeping the grid within 256 workgroups, plus
     its combine kernel), tiled, or big tiles (at least 512 tiles of
-    256 x 256, INT4 or fragment-ordered fp16); `frag`: W in fragment order."""
+    256 x 256); `frag`: W in fragment order."""
     b = "true" if w4 else "false"
     pk = "true" if frag else "false"
     if M <= 16:
         nf = 4 if N >= 64 * 192 else 1
         return [f"gemm_skinny<{nf}, 1, 8, 2, {b}, {epi}, {pk}>(GemmArgs)"]
-    if (w4 or frag) and -(-M // 256) * -(-N // 256) >= 512:
-        return [f"gemm_big_w4<{epi}, {pk}>(GemmArgs)" if w4 else f"gemm_big_f16<{epi}>(GemmArgs)"]
+    if -(-M // 256) * -(-N // 256) >= 512:
+        return [f"gemm_big_w4<{epi}, {pk}>(GemmArgs)" if w4 else f"gemm_big_f16<{epi}, {pk}>(GemmArgs)"]
     if M > 128:
         return [f"gemm_tiled<{b}, {epi}, {pk}>(GemmArgs)"]
     mf = 2 if M <= 32 else (4 if M <= 64 else 8)

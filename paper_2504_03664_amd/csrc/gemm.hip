@@ -13,14 +13,13 @@
 //     and each wave keeps several chunks of its W rows in flight in
 //     registers.  K may be split over workgroups; their fp32 partial sums
 //     go to a workspace that gemm_combine adds up in a fixed order.
-//   * gemm_tiled (M > 128, prefill): 128 x 128 output tiles, K staged
+//   * gemm_tiled (M > 128, prefill with fewer big tiles): 128 x 128 output tiles, K staged
 //     through double-buffered LDS in steps of 64, 4 waves of 64 x 64; tiles
 //     ordered per XCD so that each XCD's L2 serves a compact block.
 //   * gemm_big_f16 / gemm_big_w4 (prefill with at least 512 tiles of
-//     256 x 256; fp16 W in fragment order, or INT4): 8 waves of 128 x 64
-//     fed by global -> LDS loads (no register staging) over four LDS
-//     stages; INT4 codes reach LDS the same way and are expanded there,
-//     once per tile.
+//     256 x 256): 8 waves of 128 x 64 fed by global -> LDS loads (no
+//     register staging) over four LDS stages; INT4 codes reach LDS the
+//     same way and are expanded there, once per tile.
 // All accumulate in fp32 with v_mfma_f32_16x16x32_f16, and INT4 codes
 // become the same fp16 values (code * scale + min, rounded once) in every
 // kernel.  The kernel, its configuration and the K split depend only on
@@ -531,7 +530,7 @@ __host__ __device__ constexpr int64_t big_tiles(int64_t M, int64_t N) {
 
 constexpr int kBM = 256, kBN = 256;
 
-// fp16 W in fragment order: 8 waves (two per SIMD) of 128 x 64 (8 x 4
+// fp16 W (fragment order, or row-major: PK): 8 waves (two per SIMD) of 128 x 64 (8 x 4
 // accumulator fragments), K in stages of 32.  A stage is 16 row blocks of X
 // and 16 of W, each 16 rows x 32 k = 1 KiB in MFMA operand order (lane slot
 // r + 16 g holds row r, k = 8 g .. 8 g + 7), moved from global memory
@@ -547,7 +546,7 @@ constexpr int kFThreads = 512;
 constexpr int kFStage = 32 * 1024;       // bytes per LDS stage: 16 KiB of X, 16 KiB of W
 constexpr int kFStages = 4;
 
-template <int EPI>
+template <int EPI, bool PK>
 __global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
   constexpr int FM = 8, FN = 4;  // fragments per wave
   constexpr int BPW = 2;         // X and W row blocks each wave moves per stage
@@ -578,10 +577,17 @@ __global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
     int64_t m = m0 + 16 * (BPW * wave + i) + r;
     m = m < a.M ? m : a.M - 1;
     asrc[i] = a.X + m * K + 8 * g;
-    int64_t nb = (n0 >> 4) + BPW * wave + i;
-    nb = nb < (a.N >> 4) ? nb : (a.N >> 4) - 1;
-    bsrc[i] = a.W + nb * (K >> 5) * 512 + lane * 8;
+    if constexpr (PK) {  // the block is 1 KiB contiguous in W
+      int64_t nb = (n0 >> 4) + BPW * wave + i;
+      nb = nb < (a.N >> 4) ? nb : (a.N >> 4) - 1;
+      bsrc[i] = a.W + nb * (K >> 5) * 512 + lane * 8;
+    } else {             // gathered from 16 rows, like X
+      int64_t n = n0 + 16 * (BPW * wave + i) + r;
+      n = n < a.N ? n : a.N - 1;
+      bsrc[i] = a.W + n * K + 8 * g;
+    }
   }
+  constexpr int kBStep = PK ? 512 : 32;  // halves between the stages of a W block
   // stage `src` of K into LDS buffer `buf` % kFStages
   const auto issue = [&](int src, int buf) {
     uint8_t* st = lds + (buf % kFStages) * kFStage;
@@ -589,7 +595,7 @@ __global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
     for (int i = 0; i < BPW; ++i) {
       const int b = BPW * wave + i;
       lds_dma16(asrc[i] + src * 32, st + b * 1024);
-      lds_dma16(bsrc[i] + src * 512, st + 16 * 1024 + b * 1024);
+      lds_dma16(bsrc[i] + src * kBStep, st + 16 * 1024 + b * 1024);
     }
   };
   const auto read = [&](int t, h8 (&fa)[FM], h8 (&fb)[FN]) {
@@ -943,13 +949,13 @@ static pipo_status launch_epi(const GemmArgs& a, float* ws, int64_t ws_bytes, hi
       case 4: launch_stream_mf<W4, 4, EPI, PK>(a, pl, S, ws, st); break;
       default: launch_stream_mf<W4, 8, EPI, PK>(a, pl, S, ws, st); break;
     }
-  } else if ((W4 || PK) && big_tiles(a.M, a.N) >= kBigMinTiles) {
+  } else if (big_tiles(a.M, a.N) >= kBigMinTiles) {
     const int64_t per_xcd = (big_tiles(a.M, a.N) + kXcds - 1) / kXcds;
     const dim3 grid((unsigned)(per_xcd * kXcds));
     if constexpr (W4)
       launch((gemm_big_w4<EPI, PK>), grid, dim3(kFThreads), 0, st, a);
     else
-      launch((gemm_big_f16<EPI>), grid, dim3(kFThreads), 0, st, a);
+      launch((gemm_big_f16<EPI, PK>), grid, dim3(kFThreads), 0, st, a);
   } else {
     const int64_t total = ((a.N + kTBN - 1) / kTBN) * ((a.M + kTBM - 1) / kTBM);
     const int64_t per_xcd = (total + kXcds - 1) / kXcds;

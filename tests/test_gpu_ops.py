@@ -146,6 +146,27 @@ def test_gemm_fragment_order_equals_row_major(M, N, K, w4):
                               b.view(np.uint16 if b.dtype == np.float16 else np.uint32))
 
 
+@pytest.mark.parametrize("w4", [False, True])
+@pytest.mark.parametrize("frag", [False, True])
+def test_gemm_big_tiles_equal_tiled(w4, frag):
+    """At M = 2050, N = 16400 (585 tiles of 256 x 256) the big-tile kernels
+    run; the first 300 rows alone (130 tiles) run on the 128 x 128 kernel.
+    Both sum every output over the same k blocks in the same order: the
+    same bits."""
+    log(f"gemm big vs tiled w4={w4} frag={frag}")
+    rng = np.random.default_rng(11 + w4 + 2 * frag)
+    M, N, K = 2050, 16400, 256
+    X = rng.standard_normal((M, K)).astype(np.float16)
+    W = (rng.standard_normal((N, K)) * 0.05).astype(np.float16)
+    bias = (rng.standard_normal(N) * 0.05).astype(np.float16)
+    q = synth.quant_int4_g64(W) if w4 else None
+    for epi in (B.PIPO_EPI_F32, B.PIPO_EPI_F16):
+        big = run_gemm(X, W, bias, epi, w4=q, frag=frag)
+        small = run_gemm(X[:300], W, bias, epi, w4=q, frag=frag)
+        view = np.uint32 if epi == B.PIPO_EPI_F32 else np.uint16
+        assert np.array_equal(big[:300].view(view), small.view(view))
+
+
 @pytest.mark.parametrize("M", [4, 40, 100, 200])
 @pytest.mark.parametrize("w4", [False, True])
 def test_gemm_deterministic_and_split_consistent(M, w4):
