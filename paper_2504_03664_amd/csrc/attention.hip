@@ -63,6 +63,7 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
                                                      float* __restrict__ part, int b, int Hkv,
                                                      int t, int chunk) {
   static_assert(G == 1 || HP == 1, "several heads per workgroup only without grouping");
+  constexpr float kLog2e = 1.4426950408889634f;
   constexpr int LPP = D / 8;      // lanes per head of a key
   constexpr int LPK = HP * LPP;   // lanes per key
   constexpr int PPW = 64 / LPK;   // keys per wave per pass
@@ -117,20 +118,49 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
       kf[i] = (float)kv[i];
       vf[i] = (float)vv[i];
     }
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
+    if constexpr (G == 1) {  // bound by HBM: the plain update
       float s = 0.f;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) s += qf[g][i] * kf[i];
+      for (int i = 0; i < 8; ++i) s += qf[0][i] * kf[i];
 #pragma unroll
       for (int off = LPP / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
-      const float mn = fmaxf(m[g], s);
-      const float alpha = expf(m[g] - mn);
+      const float mn = fmaxf(m[0], s);
+      const float alpha = expf(m[0] - mn);
       const float e = expf(s - mn);
-      l[g] = l[g] * alpha + e;
+      l[0] = l[0] * alpha + e;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[g][i] = acc[g][i] * alpha + e * vf[i];
-      m[g] = mn;
+      for (int i = 0; i < 8; ++i) acc[0][i] = acc[0][i] * alpha + e * vf[i];
+      m[0] = mn;
+    } else {  // G query heads per key: bound by arithmetic
+      float alpha[G], e[G];
+      bool grew = false;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s += qf[g][i] * kf[i];
+#pragma unroll
+        for (int off = LPP / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+        const float mn = fmaxf(m[g], s);
+        // hardware exp2; m = -inf on the first key gives alpha = 0
+        alpha[g] = __builtin_amdgcn_exp2f((m[g] - mn) * kLog2e);
+        e[g] = __builtin_amdgcn_exp2f((s - mn) * kLog2e);
+        l[g] = l[g] * alpha[g] + e[g];
+        grew |= alpha[g] != 1.f;
+        m[g] = mn;
+      }
+      // the running maxima rarely grow after the first keys: rescale only
+      // when some lane's did (alpha = 1 exactly otherwise)
+      if (__any(grew)) {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[g][i] *= alpha[g];
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[g][i] += e[g] * vf[i];
     }
   };
   for (int p = p0 + wave * PPW + sub; p < p1; p += 8 * PPW) {
@@ -198,7 +228,12 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
 // as attn_decode_k, but a lane holds 32 elements of a key's head (one
 // 16-byte load of codes and one (scale, min) pair instead of four 4-byte
 // loads for 8 elements each), so a wave issues a quarter of the load
-// instructions per byte; D/32 lanes per head of a key.
+// instructions per byte; D/32 lanes per head of a key.  The kernel is
+// bound by its arithmetic, so codes are expanded in pairs (k, k + 4) of
+// each group of 8 (one shift and mask per pair), q is held as fp16 pairs
+// in that order for two-element dot products (v_dot2_f32_f16), the
+// accumulators follow the same order until they are stored, and the
+// softmax uses the hardware exp2.
 template <int D, int HP>
 __global__ __launch_bounds__(256) void attn_decode_kv4_k(const uint16_t* __restrict__ q,
                                                          const void* __restrict__ kc,
@@ -220,12 +255,15 @@ __global__ __launch_bounds__(256) void attn_decode_kv4_k(const uint16_t* __restr
   const int p0 = sp * chunk, p1 = min(T, p0 + chunk);
   const int64_t col = (int64_t)(kb * HP + hl) * D + cd;
 
-  float qf[EPL];
+  constexpr float kLog2e = 1.4426950408889634f;
+  // qh[4 j + u] = (q[8 j + u], q[8 j + u + 4]); acc[8 j + 2 u + h] is element
+  // 8 j + u + 4 h
+  h2 qh[EPL / 2];
 #pragma unroll
   for (int j = 0; j < EPL / 8; ++j) {
-    const h8 qv = load_h8(q + (int64_t)bi * d + col + 8 * j);
+    const h8 qi = interleave_h8(load_h8(q + (int64_t)bi * d + col + 8 * j));
 #pragma unroll
-    for (int i = 0; i < 8; ++i) qf[8 * j + i] = (float)qv[i];
+    for (int u = 0; u < 4; ++u) qh[4 * j + u] = h2{qi[2 * u], qi[2 * u + 1]};
   }
   float m = -INFINITY, l = 0.f, acc[EPL];
 #pragma unroll
@@ -249,23 +287,32 @@ __global__ __launch_bounds__(256) void attn_decode_kv4_k(const uint16_t* __restr
     scale_min_pairs(vr.sm, vs, vm);
     float s = 0.f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const h8 kv = dequant8(kr.codes[j], ks, km);
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) s += qf[8 * j + i] * (float)kv[i];
-    }
+      for (int u = 0; u < 4; ++u)
+        s = __builtin_amdgcn_fdot2(
+            qh[4 * j + u], dequant_pair((kr.codes[j] >> (4 * u)) & 0x000F000Fu, ks, km), s, false);
 #pragma unroll
     for (int off = LPP / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
     const float mn = fmaxf(m, s);
-    const float alpha = expf(m - mn);
-    const float e = expf(s - mn);
+    // m = -inf on the first key: exp2(-inf) = 0
+    const float alpha = __builtin_amdgcn_exp2f((m - mn) * kLog2e);
+    const float e = __builtin_amdgcn_exp2f((s - mn) * kLog2e);
     l = l * alpha + e;
+    // the running maxima rarely grow after the first keys: rescale only
+    // when some lane's did (alpha = 1 exactly otherwise)
+    if (__any(alpha != 1.f)) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const h8 vv = dequant8(vr.codes[j], vs, vm);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) acc[8 * j + i] = acc[8 * j + i] * alpha + e * (float)vv[i];
+      for (int i = 0; i < EPL; ++i) acc[i] *= alpha;
     }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const h2 vp = dequant_pair((vr.codes[j] >> (4 * u)) & 0x000F000Fu, vs, vm);
+        acc[8 * j + 2 * u] += e * (float)vp[0];
+        acc[8 * j + 2 * u + 1] += e * (float)vp[1];
+      }
     m = mn;
   };
   for (int p = p0 + wave * PPW + sub; p < p1; p += 8 * PPW) {
@@ -294,7 +341,8 @@ __global__ __launch_bounds__(256) void attn_decode_kv4_k(const uint16_t* __restr
       wl[wave][hl] = l;
     }
 #pragma unroll
-    for (int i = 0; i < EPL; ++i) wacc[wave][hl * D + cd + i] = acc[i];
+    for (int i = 0; i < EPL; ++i)
+      wacc[wave][hl * D + cd + 8 * (i / 8) + (i % 8) / 2 + 4 * (i % 2)] = acc[i];
   }
   __syncthreads();
   for (int c = tid; c < HP * D; c += 256) {
