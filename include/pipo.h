@@ -49,12 +49,17 @@ typedef enum {
   PIPO_OK = 0,
   PIPO_ERR_ARG = -1,          /* invalid argument or shape */
   PIPO_ERR_OOM_DEVICE = -2,   /* HBM allocation failed or exceeds hbm_budget_bytes */
-  PIPO_ERR_OOM_HOST = -3,     /* pinned host allocation failed */
+  PIPO_ERR_OOM_HOST = -3,     /* host allocation failed (pinned memory or heap) */
   PIPO_ERR_HIP = -4,          /* a HIP runtime call failed */
   PIPO_ERR_STATE = -5,        /* call not valid in the context's state */
   PIPO_ERR_UNSUPPORTED = -6,  /* shape or policy outside what the kernels support */
   PIPO_ERR_IO = -7            /* a file operation of the disk tier failed */
 } pipo_status;
+/* No entry point lets a C++ exception escape: an exhausted host heap inside
+ * any call that returns pipo_status is reported as PIPO_ERR_OOM_HOST, in
+ * addition to the errors each call lists; a helper thread that the system
+ * refuses makes the call do that share of its host work on the calling
+ * thread instead. */
 
 /* Weight storage format of the four per-layer matrices. */
 enum { PIPO_W_FP16 = 0, PIPO_W_INT4_G64 = 1 };

@@ -6,6 +6,9 @@
 
 #include <cstdint>
 #include <cstdio>
+#include <exception>
+#include <functional>
+#include <new>
 
 #include "pipo.h"
 #include "pipo_ops.h"
@@ -30,6 +33,29 @@ void clear_error();
     pipo_status s_ = (expr);       \
     if (s_ != PIPO_OK) return s_;  \
   } while (0)
+
+// Runs the body of a C entry point so that no C++ exception leaves it: an
+// exhausted host heap (std::bad_alloc from a container or `new`) or any
+// other exception of the host code becomes PIPO_ERR_OOM_HOST with its text.
+template <typename F>
+inline pipo_status guarded(F&& body) noexcept {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    set_error("host memory allocation failed");
+  } catch (const std::exception& e) {
+    set_error("host resources exhausted: %s", e.what());
+  } catch (...) {
+    set_error("unexpected host exception");
+  }
+  return PIPO_ERR_OOM_HOST;
+}
+
+// fn(a, b) over the contiguous pieces of [0, n) cut into `nt` parts, each
+// on a thread of its own; when the system refuses a thread, the caller runs
+// the rest of the range itself, and every started thread is joined before
+// the call returns.
+void parallel_ranges(int64_t n, int64_t nt, const std::function<void(int64_t, int64_t)>& fn);
 
 // Events that bracket the kernel launches of one operation made on this
 // thread.  They are attached to the dispatches themselves

@@ -302,8 +302,10 @@ pipo_status pipo_rope_table(const pipo_shape* shape, int32_t n_pos, float* out) 
     set_error("rope_table: NULL output, negative n_pos or not a LLaMA shape");
     return PIPO_ERR_ARG;
   }
-  rope_table(*shape, n_pos, out);
-  return PIPO_OK;
+  return guarded([&] {
+    rope_table(*shape, n_pos, out);
+    return PIPO_OK;
+  });
 }
 
 pipo_status pipo_plan_policy(const pipo_shape* shape, const pipo_policy* policy,

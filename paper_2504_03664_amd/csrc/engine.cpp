@@ -31,8 +31,10 @@
 #include <cstring>
 #include <functional>
 #include <map>
+#include <memory>
 #include <mutex>
 #include <string>
+#include <system_error>
 #include <thread>
 #include <vector>
 
@@ -83,8 +85,13 @@ static void* host_alloc_pinned(size_t bytes) {
     (void)hipGetLastError();
     return nullptr;
   }
-  std::lock_guard<std::mutex> lk(g_pin_mu);
-  g_pinned[(uintptr_t)p] = bytes;
+  try {
+    std::lock_guard<std::mutex> lk(g_pin_mu);
+    g_pinned[(uintptr_t)p] = bytes;
+  } catch (...) {
+    (void)hipHostFree(p);
+    return nullptr;
+  }
   return p;
 }
 
@@ -100,19 +107,14 @@ static void host_free_pinned(void* p) {
 // host memcpy on several threads (large weight copies at create)
 static void par_memcpy(void* dst, const void* src, size_t n) {
   const size_t kMin = 64u << 20;
-  unsigned nt = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+  const unsigned nt = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
   if (n < kMin || nt == 1) {
     std::memcpy(dst, src, n);
     return;
   }
-  std::vector<std::thread> th;
-  const size_t per = (n + nt - 1) / nt;
-  for (unsigned i = 0; i < nt; ++i) {
-    const size_t a = i * per, b = std::min(n, a + per);
-    if (a >= b) break;
-    th.emplace_back([=] { std::memcpy((char*)dst + a, (const char*)src + a, b - a); });
-  }
-  for (auto& t : th) t.join();
+  parallel_ranges((int64_t)n, nt, [=](int64_t a, int64_t b) {
+    std::memcpy((char*)dst + a, (const char*)src + a, (size_t)(b - a));
+  });
 }
 
 // dst row r = table row ids[r] (row_bytes each) for r < n; large gathers on
@@ -129,14 +131,7 @@ static void par_gather(void* dst, const void* table, const int32_t* ids, int64_t
     rows(0, n);
     return;
   }
-  std::vector<std::thread> th;
-  const int64_t per = (n + nt - 1) / nt;
-  for (unsigned i = 0; i < nt; ++i) {
-    const int64_t a = i * per, b = std::min<int64_t>(n, a + per);
-    if (a >= b) break;
-    th.emplace_back(rows, a, b);
-  }
-  for (auto& t : th) t.join();
+  parallel_ranges(n, nt, rows);
 }
 
 
@@ -145,8 +140,17 @@ static void par_gather(void* dst, const void* table, const int32_t* ids, int64_t
 // one contiguous piece per thread; the caller runs piece 0 and waits.
 class CopyPool {
  public:
+  // with fewer threads than asked for when the system refuses one
   explicit CopyPool(int n) : n_(std::max(1, n)) {
-    for (int i = 1; i < n_; ++i) th_.emplace_back([this, i] { worker(i); });
+    th_.reserve((size_t)n_);
+    for (int i = 1; i < n_; ++i) {
+      try {
+        th_.emplace_back([this, i] { worker(i); });
+      } catch (const std::system_error&) {
+        n_ = i;
+        break;
+      }
+    }
   }
   ~CopyPool() {
     {
@@ -1437,8 +1441,11 @@ pipo_status pipo_create(const pipo_shape* shape, const pipo_host_weights* weight
     return PIPO_ERR_ARG;
   }
   *out = nullptr;
-  pipo_ctx* c = new pipo_ctx();
-  const pipo_status s = create_ctx(shape, weights, policy, c);
+  pipo_ctx* c = nullptr;
+  const pipo_status s = guarded([&] {
+    c = new pipo_ctx();
+    return create_ctx(shape, weights, policy, c);
+  });
   if (s != PIPO_OK) {
     destroy_ctx(c);
     return s;
@@ -1461,19 +1468,21 @@ pipo_status pipo_prefill(pipo_ctx* c, const int32_t* tokens, int32_t b, int32_t 
               c->pol.max_seq);
     return PIPO_ERR_ARG;
   }
-  PIPO_HIP_TRY(hipSetDevice(c->device));
-  const auto t0 = std::chrono::steady_clock::now();
-  c->have_seq = false;
-  c->b = b;
-  // tokens[b][P] -> row i * P + p, the order the kernels use
-  PIPO_TRY(stage_tokens(c, tokens, (int64_t)b * P));
-  c->pass = PassInfo{true, 0, P, (int64_t)b * c->kv_row};
-  PIPO_TRY(run_pass(c, logits_out, next_out, false));
-  c->pos = P;
-  c->have_seq = true;
-  c->stats.prefill_wall_ms =
-      std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
-  return PIPO_OK;
+  return guarded([&]() -> pipo_status {
+    PIPO_HIP_TRY(hipSetDevice(c->device));
+    const auto t0 = std::chrono::steady_clock::now();
+    c->have_seq = false;
+    c->b = b;
+    // tokens[b][P] -> row i * P + p, the order the kernels use
+    PIPO_TRY(stage_tokens(c, tokens, (int64_t)b * P));
+    c->pass = PassInfo{true, 0, P, (int64_t)b * c->kv_row};
+    PIPO_TRY(run_pass(c, logits_out, next_out, false));
+    c->pos = P;
+    c->have_seq = true;
+    c->stats.prefill_wall_ms =
+        std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    return PIPO_OK;
+  });
 }
 
 pipo_status pipo_decode_step(pipo_ctx* c, const int32_t* tokens, float* logits_out,
@@ -1491,16 +1500,18 @@ pipo_status pipo_decode_step(pipo_ctx* c, const int32_t* tokens, float* logits_o
     set_error("sequences already hold max_seq=%d positions", c->pol.max_seq);
     return PIPO_ERR_STATE;
   }
-  PIPO_HIP_TRY(hipSetDevice(c->device));
-  const auto t0 = std::chrono::steady_clock::now();
-  PIPO_TRY(stage_tokens(c, tokens, c->b));
-  c->pass = PassInfo{false, c->pos, 1, (int64_t)c->b * c->kv_row};
-  PIPO_TRY(run_pass(c, logits_out, next_out, true));
-  c->pos += 1;
-  c->stats.decode_steps++;
-  c->stats.decode_wall_ms +=
-      std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
-  return PIPO_OK;
+  return guarded([&]() -> pipo_status {
+    PIPO_HIP_TRY(hipSetDevice(c->device));
+    const auto t0 = std::chrono::steady_clock::now();
+    PIPO_TRY(stage_tokens(c, tokens, c->b));
+    c->pass = PassInfo{false, c->pos, 1, (int64_t)c->b * c->kv_row};
+    PIPO_TRY(run_pass(c, logits_out, next_out, true));
+    c->pos += 1;
+    c->stats.decode_steps++;
+    c->stats.decode_wall_ms +=
+        std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    return PIPO_OK;
+  });
 }
 
 pipo_status pipo_get_stats(pipo_ctx* c, pipo_stats* out) {
@@ -1509,22 +1520,24 @@ pipo_status pipo_get_stats(pipo_ctx* c, pipo_stats* out) {
     set_error("NULL argument");
     return PIPO_ERR_ARG;
   }
-  PIPO_HIP_TRY(hipSetDevice(c->device));
-  PIPO_TRY(resolve_timeline(c));
-  *out = c->stats;
-  int n = 0;
-  for (int k = 0; k < kNumKernels * 2 && n < PIPO_MAX_KERNEL_STATS; ++k) {
-    if (c->kstat_n[k] == 0) continue;
-    pipo_kernel_stat& ks = out->kernels[n++];
-    std::snprintf(ks.name, sizeof ks.name, "%s_%s", kKernelNames[k / 2],
-                  (k & 1) ? "prefill" : "decode");
-    ks.launches = c->kstat_n[k];
-    ks.total_ms = c->kstat_ms[k];
-    ks.alg_bytes = c->kstat_bytes[k];
-    ks.alg_flops = c->kstat_flops[k];
-  }
-  out->n_kernel_stats = n;
-  return PIPO_OK;
+  return guarded([&]() -> pipo_status {
+    PIPO_HIP_TRY(hipSetDevice(c->device));
+    PIPO_TRY(resolve_timeline(c));
+    *out = c->stats;
+    int n = 0;
+    for (int k = 0; k < kNumKernels * 2 && n < PIPO_MAX_KERNEL_STATS; ++k) {
+      if (c->kstat_n[k] == 0) continue;
+      pipo_kernel_stat& ks = out->kernels[n++];
+      std::snprintf(ks.name, sizeof ks.name, "%s_%s", kKernelNames[k / 2],
+                    (k & 1) ? "prefill" : "decode");
+      ks.launches = c->kstat_n[k];
+      ks.total_ms = c->kstat_ms[k];
+      ks.alg_bytes = c->kstat_bytes[k];
+      ks.alg_flops = c->kstat_flops[k];
+    }
+    out->n_kernel_stats = n;
+    return PIPO_OK;
+  });
 }
 
 pipo_status pipo_set_timestamps(pipo_ctx* c, int32_t on) {
@@ -1533,10 +1546,12 @@ pipo_status pipo_set_timestamps(pipo_ctx* c, int32_t on) {
     set_error("NULL argument");
     return PIPO_ERR_ARG;
   }
-  PIPO_HIP_TRY(hipSetDevice(c->device));
-  PIPO_TRY(resolve_timeline(c));
-  c->timestamps = on != 0;
-  return PIPO_OK;
+  return guarded([&]() -> pipo_status {
+    PIPO_HIP_TRY(hipSetDevice(c->device));
+    PIPO_TRY(resolve_timeline(c));
+    c->timestamps = on != 0;
+    return PIPO_OK;
+  });
 }
 
 pipo_status pipo_reset_stats(pipo_ctx* c) {
@@ -1652,27 +1667,29 @@ pipo_status pipo_measure_disk_tier(pipo_ctx* c, int64_t bytes, int32_t iters, do
     set_error("measure_disk_tier: the context has no disk tier");
     return PIPO_ERR_STATE;
   }
-  PIPO_HIP_TRY(hipSetDevice(c->device));
-  for (int i = 0; i < kNumStreams; ++i) PIPO_HIP_TRY(hipStreamSynchronize(c->st[i]));
-  StagingRing& r = c->stage_h2d;
-  const int64_t total = std::min(align_up(bytes, 4096), c->L * c->layer_bytes);
-  double best = 0;
-  for (int it = 0; it < iters; ++it) {
-    const auto t0 = std::chrono::steady_clock::now();
-    for (int64_t off = 0; off < total; off += r.buf_bytes) {
-      const int64_t n = std::min(r.buf_bytes, total - off);
-      if (!c->pool->pread_all(c->disk_fd, r.buf[0], (size_t)n, off,
-                              c->disk_direct ? c->disk_bounce : nullptr)) {
-        set_error("measure_disk_tier: reading failed: %s", std::strerror(errno));
-        return PIPO_ERR_IO;
+  return guarded([&]() -> pipo_status {
+    PIPO_HIP_TRY(hipSetDevice(c->device));
+    for (int i = 0; i < kNumStreams; ++i) PIPO_HIP_TRY(hipStreamSynchronize(c->st[i]));
+    StagingRing& r = c->stage_h2d;
+    const int64_t total = std::min(align_up(bytes, 4096), c->L * c->layer_bytes);
+    double best = 0;
+    for (int it = 0; it < iters; ++it) {
+      const auto t0 = std::chrono::steady_clock::now();
+      for (int64_t off = 0; off < total; off += r.buf_bytes) {
+        const int64_t n = std::min(r.buf_bytes, total - off);
+        if (!c->pool->pread_all(c->disk_fd, r.buf[0], (size_t)n, off,
+                                c->disk_direct ? c->disk_bounce : nullptr)) {
+          set_error("measure_disk_tier: reading failed: %s", std::strerror(errno));
+          return PIPO_ERR_IO;
+        }
       }
+      const double sec =
+          std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+      best = std::max(best, (double)total / sec / 1e9);
     }
-    const double sec =
-        std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
-    best = std::max(best, (double)total / sec / 1e9);
-  }
-  *gbps = best;
-  return PIPO_OK;
+    *gbps = best;
+    return PIPO_OK;
+  });
 }
 
 pipo_status pipo_measure_disk_read(const char* dir, int64_t bytes, int64_t chunk_bytes,
@@ -1685,6 +1702,11 @@ pipo_status pipo_measure_disk_read(const char* dir, int64_t bytes, int64_t chunk
   }
   chunk_bytes = align_up(chunk_bytes, 4096);
   bytes = align_up(bytes, chunk_bytes);
+  std::unique_ptr<CopyPool> pool;
+  PIPO_TRY(guarded([&] {
+    pool.reset(new CopyPool(n_threads));
+    return PIPO_OK;
+  }));
   const std::string d = dir && dir[0] ? dir : ".";
   std::string path = d + "/pipo_probe_XXXXXX";
   int fd = ::mkstemp(&path[0]);
@@ -1707,11 +1729,10 @@ pipo_status pipo_measure_disk_read(const char* dir, int64_t bytes, int64_t chunk
     set_error("measure_disk_read: host allocation failed");
     st = PIPO_ERR_OOM_HOST;
   }
-  CopyPool pool(n_threads);
   if (st == PIPO_OK) {
     std::memset(buf, 0x5a, (size_t)chunk_bytes);
     for (int64_t off = 0; off < bytes && st == PIPO_OK; off += chunk_bytes)
-      if (!pool.pwrite_all(fd, buf, (size_t)chunk_bytes, off)) {
+      if (!pool->pwrite_all(fd, buf, (size_t)chunk_bytes, off)) {
         set_error("measure_disk_read: writing %s failed: %s", d.c_str(), std::strerror(errno));
         st = PIPO_ERR_IO;
       }
@@ -1720,7 +1741,7 @@ pipo_status pipo_measure_disk_read(const char* dir, int64_t bytes, int64_t chunk
   for (int it = 0; it < iters && st == PIPO_OK; ++it) {
     const auto t0 = std::chrono::steady_clock::now();
     for (int64_t off = 0; off < bytes && st == PIPO_OK; off += chunk_bytes)
-      if (!pool.pread_all(fd, buf, (size_t)chunk_bytes, off, is_direct ? bounce : nullptr)) {
+      if (!pool->pread_all(fd, buf, (size_t)chunk_bytes, off, is_direct ? bounce : nullptr)) {
         set_error("measure_disk_read: reading %s failed: %s", d.c_str(), std::strerror(errno));
         st = PIPO_ERR_IO;
       }

@@ -4,6 +4,7 @@
 // fragment is one contiguous 1 KiB read.  Row groups are split over threads.
 #include <algorithm>
 #include <cstring>
+#include <system_error>
 #include <thread>
 #include <vector>
 
@@ -11,20 +12,32 @@
 
 namespace pipo {
 
-static void over_row_groups(int64_t groups, const std::function<void(int64_t, int64_t)>& fn) {
-  const int64_t nt = std::max<int64_t>(
-      1, std::min<int64_t>({16, (int64_t)std::thread::hardware_concurrency(), groups / 64 + 1}));
-  if (nt == 1) {
-    fn(0, groups);
+void parallel_ranges(int64_t n, int64_t nt, const std::function<void(int64_t, int64_t)>& fn) {
+  nt = std::max<int64_t>(1, std::min(nt, n));
+  if (nt <= 1) {
+    if (n > 0) fn(0, n);
     return;
   }
   std::vector<std::thread> th;
-  const int64_t per = (groups + nt - 1) / nt;
-  for (int64_t t = 0; t < nt; ++t) {
-    const int64_t a = t * per, b = std::min(groups, a + per);
-    if (a < b) th.emplace_back(fn, a, b);
+  th.reserve((size_t)nt);
+  const int64_t per = (n + nt - 1) / nt;
+  int64_t a = 0;
+  for (; a < n; a += per) {
+    try {
+      th.emplace_back(fn, a, std::min(n, a + per));
+    } catch (const std::system_error&) {
+      break;
+    }
   }
+  if (a < n) fn(a, n);
   for (auto& t : th) t.join();
+}
+
+static void over_row_groups(int64_t groups, const std::function<void(int64_t, int64_t)>& fn) {
+  parallel_ranges(groups,
+                  std::min<int64_t>({16, (int64_t)std::thread::hardware_concurrency(),
+                                     groups / 64 + 1}),
+                  fn);
 }
 
 void pack_f16(const uint16_t* W, uint16_t* out, int64_t N, int64_t K) {
@@ -79,8 +92,10 @@ pipo_status pipo_pack_f16(const uint16_t* W, uint16_t* out, int64_t N, int64_t K
     set_error("pack_f16: NULL or aliased buffers, or N %% 16 / K %% 32 != 0");
     return PIPO_ERR_ARG;
   }
-  pack_f16(W, out, N, K);
-  return PIPO_OK;
+  return guarded([&] {
+    pack_f16(W, out, N, K);
+    return PIPO_OK;
+  });
 }
 
 pipo_status pipo_pack_w4(const uint8_t* q, const uint16_t* scale_min, uint8_t* q_out,
@@ -91,9 +106,11 @@ pipo_status pipo_pack_w4(const uint8_t* q, const uint16_t* scale_min, uint8_t* q
     set_error("pack_w4: NULL or aliased buffers, or N %% 16 / K %% 128 != 0");
     return PIPO_ERR_ARG;
   }
-  pack_w4_codes(q, q_out, N, K);
-  pack_w4_scale_min(scale_min, scale_min_out, N, K);
-  return PIPO_OK;
+  return guarded([&] {
+    pack_w4_codes(q, q_out, N, K);
+    pack_w4_scale_min(scale_min, scale_min_out, N, K);
+    return PIPO_OK;
+  });
 }
 
 }  // extern "C"

@@ -36,23 +36,28 @@ extern "C" int64_t pipo_sched_trace(const pipo_sched_config* c, int32_t n_passes
   }
   sc.poison = c->poison != 0;
   sc.delay = c->delay != 0;
-  pipo::Scheduler sched(sc);
-  std::string text;
-  std::vector<pipo::Op> ops;
-  for (int i = 0; i < n_passes; ++i) {
-    pipo::PassInfo p;
-    p.prefill = prefill[i] != 0;
-    p.pos0 = pos0[i];
-    p.T = T[i];
-    p.kv_row_bytes = kv_row_bytes;
-    ops.clear();
-    sched.pass(p, ops);
-    for (const auto& o : ops) {
-      text += pipo::op_to_string(o);
-      text += '\n';
+  // no C++ exception (an exhausted heap) may leave the C entry point
+  try {
+    pipo::Scheduler sched(sc);
+    std::string text;
+    std::vector<pipo::Op> ops;
+    for (int i = 0; i < n_passes; ++i) {
+      pipo::PassInfo p;
+      p.prefill = prefill[i] != 0;
+      p.pos0 = pos0[i];
+      p.T = T[i];
+      p.kv_row_bytes = kv_row_bytes;
+      ops.clear();
+      sched.pass(p, ops);
+      for (const auto& o : ops) {
+        text += pipo::op_to_string(o);
+        text += '\n';
+      }
     }
+    if ((int64_t)text.size() + 1 > buflen) return -1;
+    std::memcpy(buf, text.c_str(), text.size() + 1);
+    return (int64_t)text.size();
+  } catch (...) {
+    return -1;
   }
-  if ((int64_t)text.size() + 1 > buflen) return -1;
-  std::memcpy(buf, text.c_str(), text.size() + 1);
-  return (int64_t)text.size();
 }
