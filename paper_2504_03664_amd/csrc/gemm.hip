@@ -553,7 +553,9 @@ __global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
   constexpr int PER_STAGE = 2 * BPW;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[kFStages * kFStage];
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  // the wave index in a scalar register: LDS destinations of the loads are
+  // then scalar and go to M0 without a vector-to-scalar move per load
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 2, wn = wave & 3;
   const int64_t tiles_m = (a.M + kBM - 1) / kBM, tiles_n = (a.N + kBN - 1) / kBN;
   const int64_t total = tiles_m * tiles_n;
@@ -632,13 +634,20 @@ __global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
     issue(t + 3 < KT ? t + 3 : KT - 1, t + 3);
     read(t, ra, rb);
     mma(ca, cb);
-    // one fragment read, then two MFMAs, in turn
+    // two MFMAs, then one of the loads, four times, so that the MFMA pipe
+    // restarts right after the barrier and the loads' address arithmetic
+    // hides behind MFMAs; then one fragment read and two MFMAs, in turn
+#pragma unroll
+    for (int k = 0; k < PER_STAGE; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // global -> LDS load
+    }
 #pragma unroll
     for (int k = 0; k < FM + FN; ++k) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - 2 * (FM + FN), 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - 2 * PER_STAGE - 2 * (FM + FN), 0);
   };
   issue(0, 0);
   issue(1, 1);
@@ -688,7 +697,7 @@ __global__ __launch_bounds__(kFThreads) void gemm_big_w4(GemmArgs a) {
   constexpr int WOFF = 16 * 1024, COFF = 32 * 1024, SOFF = 36 * 1024;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[kFStages * STAGE];
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 2, wn = wave & 3;
   const int64_t tiles_m = (a.M + kBM - 1) / kBM, tiles_n = (a.N + kBN - 1) / kBN;
   const int64_t total = tiles_m * tiles_n;
@@ -776,12 +785,16 @@ __global__ __launch_bounds__(kFThreads) void gemm_big_w4(GemmArgs a) {
     expand(t + 1);
     read(t, ra, rb);
     if (mm) mma(ca, cb);
+    // two MFMAs before the loads, so that the MFMA pipe restarts right
+    // after the barrier; then one fragment read and two MFMAs, in turn
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, PER_STEP, 0);
 #pragma unroll
     for (int k = 0; k < FM + FN; ++k) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - 2 * (FM + FN), 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - 2 - 2 * (FM + FN), 0);
   };
   issue_w(0, 0);
   issue_w(1, 1);
