@@ -102,11 +102,12 @@ def gemm_symbols(M, N, K, epi, w4, frag):
     return syms
 
 
-def measured_traffic(workload_name, symbols):
-    """HBM bytes per dispatch of the kernels `symbols` (summed) from the
-    committed rocprofv3 PMC summary of this workload, or None if there is
-    none, a kernel is missing from it, or the kernel sources changed since
-    it was taken."""
+def measured_traffic(workload_name, symbols, optional=()):
+    """HBM bytes per dispatch of the kernels `symbols` (summed, plus those of
+    `optional` that the profile holds) from the committed rocprofv3 PMC
+    summary of this workload, or None if there is none, a kernel of
+    `symbols` is missing from it, or the kernel sources changed since it was
+    taken."""
     import hashlib
     tag = workload_name.split()[0] + "_" + workload_name.split()[1]
     path = os.path.join(ROOT, "profiles", f"hbm_traffic_{tag}.json")
@@ -122,8 +123,9 @@ def measured_traffic(workload_name, symbols):
         return None, None
     if any(sym not in rec["per_dispatch"] for sym in symbols):
         return None, None
+    present = list(symbols) + [sym for sym in optional if sym in rec["per_dispatch"]]
     total = sum(rec["per_dispatch"][sym]["fetch_bytes"] + rec["per_dispatch"][sym]["write_bytes"]
-                for sym in symbols)
+                for sym in present)
     return total, os.path.relpath(path, ROOT).replace(".json", ".md")
 
 
@@ -380,7 +382,7 @@ def main():
             peak, unit = HBM_PEAK_GBPS, "GB/s"
         epi = {"oproj": 2, "fc1": 0 if llama else 1, "qkv": 4, "head": 3}
         fam_key = name.split("(")[1].split("+")[0].rstrip(")")
-        symbols = None
+        symbols, symbols_opt = None, []
         d, F, dh = shape.d_model, shape.d_ffn, shape.d_model // shape.n_heads
         hkv = shape.n_kv_heads if llama else shape.n_heads
         if fam_key in epi:
@@ -394,9 +396,14 @@ def main():
             kv4 = "true" if wl.kv_fmt == "int4" else "false"
             G = shape.n_heads // hkv
             hp = 1 if G > 1 else (4 if hkv % 4 == 0 else (2 if hkv % 2 == 0 else 1))
-            symbols = [f"attn_decode_k<{dh}, {G}, {hp}, {kv4}>"]
+            symbols = ([f"attn_decode_kv4_k<{dh}, {hp}>"] if kv4 == "true" and G == 1
+                       else [f"attn_decode_k<{dh}, {G}, {hp}, {kv4}>"])
+            # with key splits the launch also runs the merge kernel (one
+            # dispatch per attention launch), whose bytes count too
+            symbols_opt = [f"attn_decode_combine<{dh}>"]
         symbol = " + ".join(symbols) if symbols else None
-        traffic, tsrc = measured_traffic(wl.name, symbols) if symbols else (None, None)
+        traffic, tsrc = (measured_traffic(wl.name, symbols, symbols_opt) if symbols
+                         else (None, None))
         out["roofline"] = {"kernel": name, "symbol": symbol,
                            "bound": "mfma" if mfma_bound else "hbm",
                            "achieved": round(ach, 1), "peak": peak, "unit": unit,
