@@ -107,12 +107,12 @@ def measured_traffic(workload_name, symbols, optional=()):
     `optional` that the profile holds) from the committed rocprofv3 PMC
     summary of this workload, or None if there is none, a kernel of
     `symbols` is missing from it, or the kernel sources changed since it was
-    taken."""
+    taken.  Returns (bytes, summary path, the kernels counted)."""
     import hashlib
     tag = workload_name.split()[0] + "_" + workload_name.split()[1]
     path = os.path.join(ROOT, "profiles", f"hbm_traffic_{tag}.json")
     if not os.path.exists(path):
-        return None, None
+        return None, None, list(symbols)
     with open(path) as f:
         rec = json.load(f)
     h = hashlib.sha256()
@@ -120,13 +120,13 @@ def measured_traffic(workload_name, symbols, optional=()):
         with open(os.path.join(ROOT, "paper_2504_03664_amd", "csrc", src), "rb") as f:
             h.update(f.read())
     if rec.get("kernel_source_sha256") != h.hexdigest():
-        return None, None
+        return None, None, list(symbols)
     if any(sym not in rec["per_dispatch"] for sym in symbols):
-        return None, None
+        return None, None, list(symbols)
     present = list(symbols) + [sym for sym in optional if sym in rec["per_dispatch"]]
     total = sum(rec["per_dispatch"][sym]["fetch_bytes"] + rec["per_dispatch"][sym]["write_bytes"]
                 for sym in present)
-    return total, os.path.relpath(path, ROOT).replace(".json", ".md")
+    return total, os.path.relpath(path, ROOT).replace(".json", ".md"), present
 
 
 def cpu_baseline(wl, seed, sample_layers=2, steps=3):
@@ -401,9 +401,9 @@ def main():
             # with key splits the launch also runs the merge kernel (one
             # dispatch per attention launch), whose bytes count too
             symbols_opt = [f"attn_decode_combine<{dh}>"]
-        symbol = " + ".join(symbols) if symbols else None
-        traffic, tsrc = (measured_traffic(wl.name, symbols, symbols_opt) if symbols
-                         else (None, None))
+        traffic, tsrc, counted = (measured_traffic(wl.name, symbols, symbols_opt) if symbols
+                                  else (None, None, None))
+        symbol = " + ".join(counted) if counted else None
         out["roofline"] = {"kernel": name, "symbol": symbol,
                            "bound": "mfma" if mfma_bound else "hbm",
                            "achieved": round(ach, 1), "peak": peak, "unit": unit,
