@@ -311,7 +311,7 @@ pipo_status pipo_create(const pipo_shape* shape, const pipo_host_weights* weight
  * logits_out is not NULL it receives the fp32 logits [b][vocab] of the last
  * prompt position.  Returns once next_out is written.
  * Errors: ARG (b < 1 or > max_batch, P < 1 or > max_seq, id out of range),
- * HIP.
+ * STATE (an earlier pass of this context failed part way), HIP.
  */
 pipo_status pipo_prefill(pipo_ctx* ctx, const int32_t* tokens, int32_t b, int32_t P,
                          float* logits_out, int32_t* next_out);
@@ -321,8 +321,8 @@ pipo_status pipo_prefill(pipo_ctx* ctx, const int32_t* tokens, int32_t b, int32_
  * next_out, any id for teacher forcing) at the next position and return the
  * greedy next tokens (next_out[b]) and optionally the fp32 logits [b][vocab].
  * b must equal the prefill's b.
- * Errors: STATE (no prefill yet, or the sequences already hold max_seq
- * positions), ARG, HIP.
+ * Errors: STATE (no prefill yet, the sequences already hold max_seq
+ * positions, or an earlier pass of this context failed part way), ARG, HIP.
  */
 pipo_status pipo_decode_step(pipo_ctx* ctx, const int32_t* tokens, float* logits_out,
                              int32_t* next_out);
@@ -363,6 +363,16 @@ pipo_status pipo_configure(const pipo_shape* shape, int32_t wfmt, int32_t kv_fmt
  * ends by synchronising all of the context's streams (which stops the next
  * call's loads from running ahead); figures recorded so far are kept. */
 pipo_status pipo_set_timestamps(pipo_ctx* ctx, int32_t on);
+
+/* Test hook for failure handling: the context's next pass (prefill or
+ * decode step) stops after issuing n_ops of its planned copy and kernel
+ * operations and returns PIPO_ERR_HIP, as a failed copy or launch in the
+ * middle of a pass would.  Everything already issued still runs to its end
+ * (the failing call waits for it).  After any pass that fails part way the
+ * context refuses pipo_prefill and pipo_decode_step with PIPO_ERR_STATE
+ * until it is destroyed: its schedule had already counted the rest of the
+ * pass as issued.  n_ops < 0 clears the hook.  Errors: ARG. */
+pipo_status pipo_debug_fail_pass(pipo_ctx* ctx, int64_t n_ops);
 
 /* Zero the counters and timelines of pipo_stats (allocation figures stay). */
 pipo_status pipo_reset_stats(pipo_ctx* ctx);

@@ -213,17 +213,20 @@ class LlamaDecoder:
     def head(self, x: np.ndarray) -> np.ndarray:
         return self.act(rms_norm(x, self.lnf(), self.s.ln_eps)) @ self.lm_head().T
 
-    def forward(self, tokens: np.ndarray, layers: Optional[int] = None) -> np.ndarray:
-        """Full recomputation: logits [b][s][V]."""
+    def forward(self, tokens: np.ndarray, layers: Optional[int] = None,
+                last: Optional[int] = None) -> np.ndarray:
+        """Full recomputation: logits [b][s][V] (or of the last ``last``
+        positions only, [b][last][V])."""
         tokens = np.asarray(tokens)
         B, S = tokens.shape
         nl = self.s.n_layers if layers is None else layers
+        first = 0 if last is None else S - last
         pos = np.arange(S)
         xs = [self.embed(tokens[i]) for i in range(B)]
         for j in range(nl):
             L = self.layer(j)
             xs = [self.layer_forward(L, x, pos, None, None)[0] for x in xs]
-        return np.stack([self.head(x) for x in xs])
+        return np.stack([self.head(x[first:]) for x in xs])
 
     def prefill(self, tokens: np.ndarray) -> Tuple[np.ndarray, List]:
         tokens = np.asarray(tokens)

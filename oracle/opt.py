@@ -269,18 +269,22 @@ class OracleDecoder:
         return self.act(layer_norm(x, g, b, self.s.ln_eps)) @ self.tok_emb().T
 
     # -- whole passes -------------------------------------------------------
-    def forward(self, tokens: np.ndarray, layers: Optional[int] = None) -> np.ndarray:
+    def forward(self, tokens: np.ndarray, layers: Optional[int] = None,
+                last: Optional[int] = None) -> np.ndarray:
         """Full recomputation: logits [b][s][V] of every position of every
-        sequence, no cache.  ``layers`` truncates the stack (a layer slice)."""
+        sequence, no cache.  ``layers`` truncates the stack (a layer slice);
+        ``last`` returns only the logits of the last ``last`` positions
+        ([b][last][V]; the head is applied to those positions alone)."""
         tokens = np.asarray(tokens)
         B, S = tokens.shape
         nl = self.s.n_layers if layers is None else layers
+        first = 0 if last is None else S - last
         pos = np.arange(S)
         xs = [self.embed(tokens[i], pos) for i in range(B)]
         for j in range(nl):
             L = self.layer(j)
             xs = [self.layer_forward(L, x, None, None)[0] for x in xs]
-        return np.stack([self.head(x) for x in xs])
+        return np.stack([self.head(x[first:]) for x in xs])
 
     def prefill(self, tokens: np.ndarray) -> Tuple[np.ndarray, List]:
         """Logits [b][V] at the last prompt position, plus the KV cache

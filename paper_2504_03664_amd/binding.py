@@ -121,6 +121,7 @@ _SIGNATURES = {
     "pipo_reset_stats": ([vp], i32),
     "pipo_destroy": ([vp], None),
     "pipo_set_timestamps": ([vp, i32], i32),
+    "pipo_debug_fail_pass": ([vp, i64], i32),
     "pipo_plan_policy": ([ctypes.POINTER(PipoShape), ctypes.POINTER(PipoPolicy),
                           ctypes.POINTER(PipoPlan)], i32),
     "pipo_configure": ([ctypes.POINTER(PipoShape), i32, i32, i32, i32,
@@ -286,6 +287,10 @@ def pipo_configure(shape: PipoShape, wfmt: int, kv_fmt: int, max_batch: int, max
 
 def pipo_set_timestamps(ctx: int, on: bool) -> None:
     _check(lib().pipo_set_timestamps(ctx, int(on)), "pipo_set_timestamps")
+
+
+def pipo_debug_fail_pass(ctx: int, n_ops: int) -> None:
+    _check(lib().pipo_debug_fail_pass(ctx, n_ops), "pipo_debug_fail_pass")
 
 
 def pipo_destroy(ctx: int) -> None:

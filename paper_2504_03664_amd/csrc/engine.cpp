@@ -367,6 +367,11 @@ struct pipo_ctx {
   int b = 0;
   int64_t pos = 0;   // positions held per sequence
   bool have_seq = false;
+  // A pass that stopped part way leaves the schedule's view of the slots,
+  // events and streams ahead of what was enqueued; the context then refuses
+  // further passes (PIPO_ERR_STATE) until it is destroyed.
+  bool failed = false;
+  int64_t fail_after_ops = -1;   // test hook (pipo_debug_fail_pass): stop after this many ops
 
   // pass being executed
   PassInfo pass;
@@ -848,7 +853,7 @@ static pipo_status exec_op(pipo_ctx* c, const Op& op) {
   return PIPO_ERR_ARG;
 }
 
-static pipo_status run_pass(pipo_ctx* c, float* logits_out, int32_t* next_out, bool decode) {
+static pipo_status run_pass_ops(pipo_ctx* c, float* logits_out, int32_t* next_out, bool decode) {
   c->ops.clear();
   c->sched->pass(c->pass, c->ops);
   hipEvent_t w0 = nullptr, w1 = nullptr;
@@ -856,7 +861,15 @@ static pipo_status run_pass(pipo_ctx* c, float* logits_out, int32_t* next_out, b
     w0 = tevent(c);
     PIPO_HIP_TRY(hipEventRecord(w0, c->st[kCompute]));
   }
-  for (const Op& op : c->ops) PIPO_TRY(exec_op(c, op));
+  for (size_t i = 0; i < c->ops.size(); ++i) {
+    if (c->fail_after_ops >= 0 && (int64_t)i == c->fail_after_ops) {
+      c->fail_after_ops = -1;
+      set_error("pass stopped after %lld of %lld ops (pipo_debug_fail_pass)", (long long)i,
+                (long long)c->ops.size());
+      return PIPO_ERR_HIP;
+    }
+    PIPO_TRY(exec_op(c, c->ops[i]));
+  }
   if (c->timestamps && decode) {
     w1 = tevent(c);
     PIPO_HIP_TRY(hipEventRecord(w1, c->st[kCompute]));
@@ -870,6 +883,29 @@ static pipo_status run_pass(pipo_ctx* c, float* logits_out, int32_t* next_out, b
     c->stats.d2h_bytes += (int64_t)c->b * c->V * 4;
   }
   return PIPO_OK;
+}
+
+// A pass that fails (or throws) after the schedule planned it: wait for
+// everything already enqueued on the context's streams (and the host copy
+// threads), so no copy or kernel is left running against memory the caller
+// may free, then refuse further passes.
+static pipo_status run_pass(pipo_ctx* c, float* logits_out, int32_t* next_out, bool decode) {
+  pipo_status s = PIPO_ERR_OOM_HOST;
+  std::string msg;
+  try {
+    s = run_pass_ops(c, logits_out, next_out, decode);
+  } catch (...) {
+    s = guarded([]() -> pipo_status { throw; });
+  }
+  if (s == PIPO_OK) return s;
+  msg = pipo_last_error();
+  for (int i = 0; i < kNumStreams; ++i)
+    if (c->st[i]) (void)hipStreamSynchronize(c->st[i]);
+  (void)hipGetLastError();
+  c->failed = true;
+  c->have_seq = false;
+  set_error("%s (the context can no longer run passes; destroy it)", msg.c_str());
+  return s;
 }
 
 // ---------------------------------------------------------------------------
@@ -1468,6 +1504,10 @@ pipo_status pipo_prefill(pipo_ctx* c, const int32_t* tokens, int32_t b, int32_t 
               c->pol.max_seq);
     return PIPO_ERR_ARG;
   }
+  if (c->failed) {
+    set_error("an earlier pass failed part way; the context must be destroyed");
+    return PIPO_ERR_STATE;
+  }
   return guarded([&]() -> pipo_status {
     PIPO_HIP_TRY(hipSetDevice(c->device));
     const auto t0 = std::chrono::steady_clock::now();
@@ -1491,6 +1531,10 @@ pipo_status pipo_decode_step(pipo_ctx* c, const int32_t* tokens, float* logits_o
   if (!c || !tokens || !next_out) {
     set_error("NULL argument");
     return PIPO_ERR_ARG;
+  }
+  if (c->failed) {
+    set_error("an earlier pass failed part way; the context must be destroyed");
+    return PIPO_ERR_STATE;
   }
   if (!c->have_seq) {
     set_error("decode before prefill");
@@ -1538,6 +1582,16 @@ pipo_status pipo_get_stats(pipo_ctx* c, pipo_stats* out) {
     out->n_kernel_stats = n;
     return PIPO_OK;
   });
+}
+
+pipo_status pipo_debug_fail_pass(pipo_ctx* c, int64_t n_ops) {
+  clear_error();
+  if (!c) {
+    set_error("NULL argument");
+    return PIPO_ERR_ARG;
+  }
+  c->fail_after_ops = n_ops < 0 ? -1 : n_ops;
+  return PIPO_OK;
 }
 
 pipo_status pipo_set_timestamps(pipo_ctx* c, int32_t on) {

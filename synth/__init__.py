@@ -350,3 +350,69 @@ def synthetic_model(shape, seed: int = DEFAULT_SEED, wfmt: str = "fp16", **kw):
     if getattr(shape, "family", "opt") == "llama":
         return SyntheticLlama(shape, seed=seed, wfmt=wfmt, **kw)
     return SyntheticOPT(shape, seed=seed, wfmt=wfmt, **kw)
+
+
+def teacher_tokens(wl: Workload, stream: int, batch: Optional[int] = None):
+    """The inputs of a teacher-forced run of workload ``wl``: the prompt
+    ids [b][prompt] and the ids fed at the gen - 1 decode steps [b][gen - 1]
+    (both uniform in [0, vocab), seeded, independent streams), so a run's
+    inputs never depend on what either implementation generated."""
+    b = wl.batch if batch is None else batch
+    prompt = prompt_tokens(b, wl.prompt, wl.shape.vocab, seed=1, stream=stream)
+    forced = prompt_tokens(b, wl.gen - 1, wl.shape.vocab, seed=2, stream=stream)
+    return prompt, forced
+
+
+class ZeroKV:
+    """A weight provider whose key and value projections are zero: every key
+    and value row is its bias (an fp16 value).  Wraps another provider; the
+    query rows, every other tensor and the encodings are the base's."""
+
+    def __init__(self, base):
+        self.base, self.shape, self.wfmt = base, base.shape, base.wfmt
+
+    def _kv_rows(self) -> slice:
+        return slice(self.shape.d_model, None)
+
+    def fill(self, layer, name, out):
+        self.base.fill(layer, name, out)
+        if name == "wqkv":
+            out[self._kv_rows()] = 0
+        return out
+
+    def fill_int4(self, layer, name, q, sm):
+        # an INT4 row of zeros: codes 0, scale 0, min 0
+        self.base.fill_int4(layer, name, q, sm)
+        if name == "wqkv":
+            q[self._kv_rows()] = 0
+            sm[self._kv_rows()] = 0
+        return q, sm
+
+    def layer(self, j):
+        L = dict(self.base.layer(j))
+        w = L["wqkv"]
+        if isinstance(w, tuple):
+            q, sm = np.array(w[0]), np.array(w[1])
+            q[self._kv_rows()] = 0
+            sm[self._kv_rows()] = 0
+            L["wqkv"] = (q, sm)
+        else:
+            w = np.array(w)
+            w[self._kv_rows()] = 0
+            L["wqkv"] = w
+        return L
+
+    def layer_shapes(self):
+        return self.base.layer_shapes()
+
+    def tensor(self, layer, name):
+        return self.base.tensor(layer, name)
+
+    def tok_emb(self):
+        return self.base.tok_emb()
+
+    def pos_emb(self):
+        return self.base.pos_emb()
+
+    def lnf(self):
+        return self.base.lnf()

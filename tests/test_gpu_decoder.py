@@ -22,27 +22,43 @@ def normwise(g, o):
     return np.abs(g - o).max(axis=-1) / np.abs(o).max(axis=-1)
 
 
+def forced_tokens(prompt, gen, vocab):
+    """The ids fed at the gen - 1 decode steps of a teacher-forced run:
+    seeded uniform ids, a function of the prompt's shape only, so that the
+    oracle's inputs never come from the GPU."""
+    b, P = prompt.shape
+    return synth.prompt_tokens(b, gen - 1, vocab, seed=3, stream=P * 1000 + b)
+
+
 def teacher_forced_check(model, wfmt, prompt, gen_tokens, gpu_logits, dtype=np.float32,
                          kv_int4=False):
-    """Oracle logits at every generated position, fed the GPU's tokens.  With
-    an INT4 cache the oracle keeps fp16 activations, so that its codes are
-    decided on the same fp16 keys and values as the kernels'."""
-    full = np.concatenate([prompt, gen_tokens[:, :-1]], axis=1)
-    ref = OracleDecoder(model, dtype, kv_int4=kv_int4, fp16_operands=kv_int4).forward(full)
-    P = prompt.shape[1]
+    """Oracle logits at every generated position of a teacher-forced run
+    (prompt, then forced_tokens).  The normwise error is taken against the
+    plain fp32 oracle; the greedy tokens are compared with the oracle
+    reading that keeps the paper's fp16 activations (Section 4.1), the
+    precision in which the kernels decide them: at least 99 % must agree and
+    every disagreement must be a near tie.  With an INT4 cache both checks
+    use that reading, so that its codes are decided on the same fp16 keys
+    and values as the kernels'."""
+    gen = gen_tokens.shape[1]
+    full = np.concatenate([prompt, forced_tokens(prompt, gen, model.shape.vocab)], axis=1)
+    ref = OracleDecoder(model, dtype, kv_int4=kv_int4, fp16_operands=kv_int4).forward(
+        full, last=gen)
+    ref16 = ref if kv_int4 else OracleDecoder(model, dtype, fp16_operands=True).forward(
+        full, last=gen)
     errs, agree, total, ties = [], 0, 0, 0
     for s, lg in enumerate(gpu_logits):
-        o = ref[:, P - 1 + s]
+        o, o16 = ref[:, s], ref16[:, s]
         e = normwise(lg.astype(np.float64), o.astype(np.float64))
         errs.append(e.max())
-        ga, oa = lg.argmax(-1), o.argmax(-1)
+        ga, oa = lg.argmax(-1), o16.argmax(-1)
+        assert (ga == gen_tokens[:, s]).all()
         agree += int((ga == oa).sum())
         total += len(ga)
         for r in np.nonzero(ga != oa)[0]:
-            gap = o[r, oa[r]] - o[r, ga[r]]
-            assert gap <= REL_TOL * np.abs(o[r]).max(), "argmax differs without a near tie"
+            gap = o16[r, oa[r]] - o16[r, ga[r]]
+            assert gap <= REL_TOL * np.abs(o16[r]).max(), "argmax differs without a near tie"
             ties += 1
-        assert (ga == gen_tokens[:, s]).all()
     return max(errs), agree / total, ties
 
 
@@ -61,12 +77,39 @@ def test_opt125m_streamed_parity(opt125m):
     wl, model, hw = opt125m
     log(f"parity {wl.name}")
     prompt = synth.prompt_tokens(wl.batch, wl.prompt, wl.shape.vocab, seed=1, stream=0)
+    forced = forced_tokens(prompt, wl.gen, wl.shape.vocab)
     with Decoder(hw, max_batch=wl.batch, max_seq=wl.prompt + wl.gen, chunk_bytes=1 << 20) as dec:
-        toks, logits = dec.generate(prompt, wl.gen, want_logits=True)
+        toks, logits = dec.generate(prompt, wl.gen, want_logits=True, forced=forced)
     err, agree, ties = teacher_forced_check(model, "fp16", prompt, toks, logits)
     log(f"  max normwise err {err:.2e}, argmax agreement {agree:.4f} ({ties} near ties)")
     assert err <= REL_TOL
-    assert agree >= ARGMAX_MIN or ties <= 1
+    assert agree >= ARGMAX_MIN
+
+
+def test_opt125m_free_running_greedy(opt125m):
+    """Greedy generation feeding each step its own output (no forcing),
+    against the oracle's own greedy decode (prefill, then incremental steps
+    fed the oracle's tokens): the sequences are equal up to the first
+    position where the oracle's top two logits are a near tie."""
+    wl, model, hw = opt125m
+    prompt = synth.prompt_tokens(wl.batch, wl.prompt, wl.shape.vocab, seed=1, stream=0)
+    with Decoder(hw, max_batch=wl.batch, max_seq=wl.prompt + wl.gen) as dec:
+        toks, _ = dec.generate(prompt, wl.gen)
+    orc = OracleDecoder(model, np.float32, fp16_operands=True)
+    lg, cache = orc.prefill(prompt)
+    want, gaps = [orc.argmax(lg)], [lg]
+    for _ in range(wl.gen - 1):
+        lg = orc.decode(cache, want[-1])
+        want.append(orc.argmax(lg))
+        gaps.append(lg)
+    want = np.stack(want, axis=1)
+    for r in range(wl.batch):
+        diff = np.nonzero(toks[r] != want[r])[0]
+        if diff.size:
+            s = diff[0]
+            o = np.sort(gaps[s][r])[::-1]
+            log(f"  row {r} diverges at step {s}: oracle top-2 gap {o[0] - o[1]:.2e}")
+            assert o[0] - o[1] <= REL_TOL * np.abs(gaps[s][r]).max()
 
 
 def test_opt125m_longer_generation_parity(opt125m):
@@ -74,15 +117,18 @@ def test_opt125m_longer_generation_parity(opt125m):
     log("parity opt-125m b4 p48 g40")
     prompt = synth.prompt_tokens(4, 48, wl.shape.vocab, seed=2)
     with Decoder(hw, max_batch=4, max_seq=88) as dec:
-        toks, logits = dec.generate(prompt, 40, want_logits=True)
+        toks, logits = dec.generate(prompt, 40, want_logits=True,
+                                    forced=forced_tokens(prompt, 40, wl.shape.vocab))
     err, agree, ties = teacher_forced_check(model, "fp16", prompt, toks, logits)
     log(f"  max normwise err {err:.2e}, argmax agreement {agree:.4f}")
     assert err <= REL_TOL and agree >= ARGMAX_MIN
 
 
 def _run(hw, prompt, gen, **pol):
+    """A teacher-forced run (forced_tokens): tokens [b][gen], logits [gen][b][V]."""
+    forced = forced_tokens(prompt, gen, hw.shape.vocab)
     with Decoder(hw, max_batch=prompt.shape[0], max_seq=prompt.shape[1] + gen, **pol) as dec:
-        toks, logits = dec.generate(prompt, gen, want_logits=True)
+        toks, logits = dec.generate(prompt, gen, want_logits=True, forced=forced)
     return toks, np.stack(logits)
 
 
@@ -209,15 +255,44 @@ def test_edge_shapes_and_states(opt125m):
         # one sequence, one prompt token
         prompt = np.array([[7]], np.int32)
         n0, l0 = dec.prefill(prompt, want_logits=True)
-        n1, l1 = dec.decode(n0, want_logits=True)
-        n2, l2 = dec.decode(n1, want_logits=True)
+        n1, l1 = dec.decode(np.array([123], np.int32), want_logits=True)
+        n2, l2 = dec.decode(np.array([wl.shape.vocab - 1], np.int32), want_logits=True)
         with pytest.raises(B.PipoError) as e:
             dec.decode(n2)                                     # max_seq reached
         assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_STATE"
-    full = np.array([[7, n0[0], n1[0]]])
+    full = np.array([[7, 123, wl.shape.vocab - 1]])
     ref = OracleDecoder(model).forward(full)[0]
     for s, lg in enumerate((l0, l1, l2)):
         assert normwise(lg[0].astype(np.float64), ref[s].astype(np.float64)) <= REL_TOL
+
+
+def test_failed_pass_refuses_later_passes(opt125m):
+    """A pass that stops part way (a failed copy or launch, forced here from
+    the host: the pass issues only its first n operations) returns the
+    error, waits for what it had issued, and leaves the context refusing
+    further passes with PIPO_ERR_STATE; a new context runs as before."""
+    wl, model, hw = opt125m
+    prompt = synth.prompt_tokens(4, 32, wl.shape.vocab, seed=3)
+    t0, l0 = _run(hw, prompt, 4)
+    for where, n_ops in (("decode", 7), ("decode", 40), ("prefill", 3), ("prefill", 30)):
+        log(f"  {where} pass stopped after {n_ops} operations")
+        with Decoder(hw, max_batch=4, max_seq=40) as dec:
+            if where == "decode":
+                dec.prefill(prompt)
+            B.pipo_debug_fail_pass(dec.ctx, n_ops)
+            with pytest.raises(B.PipoError) as e:
+                if where == "decode":
+                    dec.decode(np.zeros(4, np.int32))
+                else:
+                    dec.prefill(prompt)
+            assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_HIP"
+            for call in (lambda: dec.decode(np.zeros(4, np.int32)), lambda: dec.prefill(prompt)):
+                with pytest.raises(B.PipoError) as e:
+                    call()
+                assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_STATE"
+    t1, l1 = _run(hw, prompt, 4)
+    assert np.array_equal(t1, t0)
+    assert np.array_equal(l1.view(np.uint32), l0.view(np.uint32))
 
 
 def test_hbm_budget_is_enforced(opt125m):
@@ -243,7 +318,7 @@ def test_small_model_parity_and_kv_on_host(wfmt):
         t0, l0 = _run(hw, prompt, 6)
         err, agree, ties = teacher_forced_check(model, wfmt, prompt, t0, list(l0))
         log(f"  err {err:.2e} agree {agree:.3f}")
-        assert err <= REL_TOL
+        assert err <= REL_TOL and agree >= ARGMAX_MIN
         tr, lr = _run(hw, prompt, 6, weights_on_host=False, embed_on_host=False)
         assert np.array_equal(lr.view(np.uint32), l0.view(np.uint32))
         for v in (dict(kv_on_host=True),
@@ -303,7 +378,7 @@ def test_int4_prefill_600_rows_layouts():
             hw.free()
     err, agree, ties = teacher_forced_check(model, "int4", prompt, runs[0][0], list(runs[0][1]))
     log(f"  err {err:.2e} agree {agree:.3f}")
-    assert err <= REL_TOL and (agree >= ARGMAX_MIN or ties <= 1)
+    assert err <= REL_TOL and agree >= ARGMAX_MIN
     assert np.array_equal(runs[1][0], runs[0][0])
     assert np.array_equal(runs[1][1].view(np.uint32), runs[0][1].view(np.uint32))
 
@@ -317,7 +392,7 @@ def test_head_dim_64_kv_on_host():
         prompt = synth.prompt_tokens(5, 17, shape.vocab, seed=7)
         t0, l0 = _run(hw, prompt, 9, kv_on_host=True, n_weight_slots=2)
         err, agree, ties = teacher_forced_check(model, "fp16", prompt, t0, list(l0))
-        assert err <= REL_TOL
+        assert err <= REL_TOL and agree >= ARGMAX_MIN
         tr, lr = _run(hw, prompt, 9, weights_on_host=False, embed_on_host=False)
         assert np.array_equal(lr.view(np.uint32), l0.view(np.uint32))
     finally:
@@ -339,7 +414,7 @@ def test_int4_kv_cache_parity_and_placements(wfmt):
         err, agree, ties = teacher_forced_check(model, wfmt, prompt, t0, list(l0), kv_int4=True)
         log(f"  err {err:.2e} agree {agree:.3f} ({ties} near ties)")
         assert err <= REL_TOL
-        assert agree >= ARGMAX_MIN or ties <= 1
+        assert agree >= ARGMAX_MIN
         for v in (dict(weights_on_host=False, embed_on_host=False),
                   dict(kv_on_host=True),
                   dict(kv_on_host=True, debug_flags=B.PIPO_DBG_KV_PAGEABLE, chunk_bytes=1 << 16),
@@ -353,54 +428,21 @@ def test_int4_kv_cache_parity_and_placements(wfmt):
         hw.free()
 
 
-class _BiasKV:
-    """A synthetic model whose key and value projections are zero: every
-    key and value row is its bias, an fp16 value, so the GPU and the oracle
-    quantize identical rows and the codes cannot differ."""
-
-    def __init__(self, base):
-        self.base, self.shape, self.wfmt = base, base.shape, base.wfmt
-
-    def fill(self, layer, name, out):
-        self.base.fill(layer, name, out)
-        if name == "wqkv":
-            out[self.shape.d_model:] = 0
-        return out
-
-    def layer(self, j):
-        L = dict(self.base.layer(j))
-        w = np.array(L["wqkv"])
-        w[self.shape.d_model:] = 0
-        L["wqkv"] = w
-        return L
-
-    def layer_shapes(self):
-        return self.base.layer_shapes()
-
-    def tok_emb(self):
-        return self.base.tok_emb()
-
-    def pos_emb(self):
-        return self.base.pos_emb()
-
-    def lnf(self):
-        return self.base.lnf()
-
-
 def test_int4_kv_cache_exact_decisions():
     """With the same rows quantized on both sides the INT4-cache decoder meets
     the fp16 bar against the plain fp32 oracle with the same cache format."""
     log("int4 kv cache, identical codes")
-    model = _BiasKV(synth.SyntheticOPT(SMALL, seed=16))
+    model = synth.ZeroKV(synth.SyntheticOPT(SMALL, seed=16))
     hw = HostWeights(SMALL, "fp16", model)
     try:
         prompt = synth.prompt_tokens(2, 40, SMALL.vocab, seed=10)
         t0, l0 = _run(hw, prompt, 6, kv_fmt="int4", kv_on_host=True)
-        full = np.concatenate([prompt, t0[:, :-1]], axis=1)
-        ref = OracleDecoder(model, np.float32, kv_int4=True).forward(full)
+        full = np.concatenate([prompt, forced_tokens(prompt, 6, SMALL.vocab)], axis=1)
+        ref = OracleDecoder(model, np.float32, kv_int4=True).forward(full, last=6)
         for s, lg in enumerate(l0):
-            o = ref[:, 40 - 1 + s]
+            o = ref[:, s]
             assert normwise(lg.astype(np.float64), o.astype(np.float64)).max() <= REL_TOL
+            assert np.array_equal(lg.argmax(-1), o.argmax(-1))
     finally:
         hw.free()
 
@@ -414,7 +456,7 @@ def test_int4_kv_cache_head_dim_64_and_bad_width():
         prompt = synth.prompt_tokens(5, 17, shape.vocab, seed=9)
         t0, l0 = _run(hw, prompt, 9, kv_fmt="int4", kv_on_host=True, n_weight_slots=2)
         err, agree, ties = teacher_forced_check(model, "fp16", prompt, t0, list(l0), kv_int4=True)
-        assert err <= REL_TOL
+        assert err <= REL_TOL and agree >= ARGMAX_MIN
     finally:
         hw.free()
     odd = synth.OPTShape(2, 384, 3, 768, vocab=100, max_pos=16)
@@ -453,7 +495,8 @@ def test_planned_memory_is_allocated_memory_and_configured_runs():
         pol, plan = B.pipo_configure(shape, B.PIPO_W_FP16, B.PIPO_KV_FP16, 3, 76, me, 1 << 34)
         assert plan["pipeline"] == B.PIPO_PIPE_MEMORY_EFFICIENT and pol.n_weight_slots == 1
         with Decoder(hw, policy=pol) as dec:
-            t1, l1 = dec.generate(prompt, 6, want_logits=True)
+            t1, l1 = dec.generate(prompt, 6, want_logits=True,
+                                  forced=forced_tokens(prompt, 6, SMALL.vocab))
             assert dec.stats()["hbm_bytes"] == plan["hbm_bytes"] <= me
         assert np.array_equal(t1, t0)
         assert np.array_equal(np.stack(l1).view(np.uint32), l0.view(np.uint32))

@@ -1,0 +1,223 @@
+"""Parity at the full workload batches, in the configuration bench.py times
+(every layer and the output head streamed from pinned host memory in 64 MiB
+chunks over 3 slots and 2 copy streams; the KV cache where the workload puts
+it).
+
+Every run is teacher-forced with seeded inputs (the prompt, then gen - 1
+uniform ids; ``synth.teacher_tokens``), so the oracle's side never depends
+on what the GPU generated.  The oracle's results at every batch row and
+every generated position were written by ``tests/golden/make_fullbatch.py``
+(which calls only ``oracle/`` and ``synth/``): the 8 largest logits with
+their ids, the largest |logit|, and the logits of 64 fixed ids.  At each
+position the GPU must
+
+* pick the oracle's greedy token, on at least 99 % of the positions of a
+  case, and where it does not, pick one whose oracle logit is within
+  tol * max|logit| of the largest (a near tie);
+* match the stored logits within tol * max|logit| (normwise, sampled).
+
+Rows 0 and b - 1 of the two-layer slices are also recomputed in full by the
+oracle here and compared over the whole vocabulary.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import decoder_for
+from paper_2504_03664_amd.model import Decoder, HostWeights
+
+pytestmark = pytest.mark.gpu
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+FIX = os.path.join(HERE, "golden", "fullbatch")
+
+REL_TOL = 2e-2          # normwise per logits row: max|g - o| / max|o|
+ARGMAX_MIN = 0.99       # share of positions whose greedy token is the oracle's
+# INT4 KV cache with real key/value projections (secondary check): a cached
+# code moves by a whole quantization step when a key or value lies within
+# rounding of a decision boundary, so two implementations that differ only in
+# summation order (or the oracle's own fp32 and fp16-activation readings)
+# differ by far more than with an fp16 cache.  The 2e-2 bar and the 99 %
+# agreement are shown on the same shape with identical codes on both sides
+# (test_kv4_identical_codes_full_batch).
+KV4_TOL = 5e-2
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def load_fixture(name):
+    path = os.path.join(FIX, name + ".npz")
+    with np.load(path, allow_pickle=False) as z:
+        fx = {k: z[k] for k in z.files}
+    fx["meta"] = json.loads(str(fx["meta"]))
+    return fx
+
+
+def case_setup(fx):
+    """Workload, shape and weight provider of a stored case."""
+    m = fx["meta"]
+    widx = m["stream"]
+    wl = synth.WORKLOADS[widx]
+    assert wl.name == m["workload"]
+    shape = wl.shape.with_layers(m["layers"])
+    model = synth.synthetic_model(shape, seed=m["weight_seed"], wfmt=wl.wfmt)
+    if m["zero_kv"]:
+        model = synth.ZeroKV(model)
+    prompt, forced = synth.teacher_tokens(wl, stream=widx)
+    return wl, shape, model, prompt, forced
+
+
+def gpu_run(wl, shape, model, prompt, forced):
+    """Teacher-forced GPU generation of the whole batch: tokens [b][gen] and
+    logits [b][gen][V] (fp32)."""
+    hw = HostWeights(shape, wl.wfmt, model)
+    try:
+        with Decoder(hw, max_batch=prompt.shape[0], max_seq=wl.prompt + wl.gen,
+                     kv_on_host=wl.kv_on_host, kv_fmt=wl.kv_fmt, chunk_bytes=64 << 20) as dec:
+            toks, logits = dec.generate(prompt, wl.gen, want_logits=True, forced=forced)
+    finally:
+        hw.free()
+    logits = np.stack(logits, axis=1)
+    # the returned token is the greedy pick of the returned logits (ties to the lowest id)
+    assert np.array_equal(toks, logits.argmax(-1))
+    return toks, logits
+
+
+def compare_fixture(fx, toks, logits, tol):
+    """Argmax agreement and sampled normwise error of the GPU rows against
+    the stored oracle results; asserts that every disagreement is a near
+    tie.  Returns (agreement, worst sampled normwise error, disagreements)."""
+    top_idx, top_val, absmax = fx["top_idx"], fx["top_val"], fx["absmax"]
+    cols, samp_val = fx["samp_idx"], fx["samp_val"]
+    rows = fx["rows"]
+    agree, total, worst, flips = 0, 0, 0.0, []
+    for i, r in enumerate(rows):
+        g = logits[r]
+        for s in range(g.shape[0]):
+            scale = float(absmax[i, s])
+            ids = np.concatenate([cols, top_idx[i, s]])
+            want = np.concatenate([samp_val[i, s], top_val[i, s]]).astype(np.float64)
+            err = np.abs(g[s, ids].astype(np.float64) - want).max()
+            err = max(err, abs(float(np.abs(g[s]).max()) - scale))
+            worst = max(worst, err / scale)
+            total += 1
+            if toks[r, s] == top_idx[i, s, 0]:
+                agree += 1
+                continue
+            hit = np.nonzero(top_idx[i, s] == toks[r, s])[0]
+            assert hit.size, f"row {r} step {s}: GPU token {toks[r, s]} not in the oracle's top 8"
+            gap = float(top_val[i, s, 0] - top_val[i, s, hit[0]])
+            assert gap <= tol * scale, f"row {r} step {s}: argmax differs, gap {gap / scale:.2e}"
+            flips.append((int(r), s, gap / scale))
+    return agree / total, worst, flips
+
+
+def live_rows(model, wl, shape, prompt, forced, logits, rows, kv_int4=False, fp16ops=False):
+    """Oracle recomputation of `rows` over the whole vocabulary; returns the
+    worst normwise error and the argmax agreement of those rows."""
+    tokens = np.concatenate([prompt[rows], forced[rows]], axis=1)
+    ref = decoder_for(model, np.float32, kv_int4=kv_int4,
+                      fp16_operands=fp16ops).forward(tokens, last=wl.gen)
+    worst, agree, total = 0.0, 0, 0
+    for i, r in enumerate(rows):
+        o = ref[i].astype(np.float64)
+        g = logits[r].astype(np.float64)
+        worst = max(worst, float((np.abs(g - o).max(-1) / np.abs(o).max(-1)).max()))
+        agree += int((g.argmax(-1) == o.argmax(-1)).sum())
+        total += o.shape[0]
+    return worst, agree / total
+
+
+def report(name, agree, worst, flips, n):
+    log(f"  {name}: argmax agreement {agree:.4f} of {n} positions, "
+        f"sampled normwise {worst:.2e}, {len(flips)} near ties {flips[:6]}")
+
+
+SLICES = ["opt-6.7b-l2", "opt-13b-int4-l2", "opt-30b-l2", "opt-30b-int4-kvhost-l2",
+          "llama3.1-8b-l2", "llama3.1-8b-int4-l2"]
+
+
+@pytest.mark.parametrize("name", SLICES)
+def test_two_layer_slice_full_batch(name):
+    """The first 2 layers (same d, heads, FFN, vocab) at the workload's full
+    batch, prompt 512 and 32 tokens: every row against the oracle."""
+    fx = load_fixture(name)
+    wl, shape, model, prompt, forced = case_setup(fx)
+    log(f"{name}: {wl.name}, {shape.n_layers} layers, batch {wl.batch}")
+    toks, logits = gpu_run(wl, shape, model, prompt, forced)
+    n = toks.shape[0] * toks.shape[1]
+    agree, worst, flips = compare_fixture(fx, toks, logits, REL_TOL)
+    report(name, agree, worst, flips, n)
+    assert n >= 500
+    assert worst <= REL_TOL and agree >= ARGMAX_MIN
+    rows = [0, wl.batch - 1]
+    lw, la = live_rows(model, wl, shape, prompt, forced, logits, rows)
+    log(f"  rows {rows} in full: normwise {lw:.2e}, argmax {la:.4f}")
+    assert lw <= REL_TOL
+
+
+def test_kv4_identical_codes_full_batch():
+    """OPT-30B shape, INT4 weights, INT4 KV cache in host memory, batch 128:
+    with zero key/value projections both sides quantize identical rows, and
+    the decoder meets the fp16 bars against the plain fp32 oracle at every
+    row and position."""
+    name = "opt-30b-int4-kv4-zerokv-l2"
+    fx = load_fixture(name)
+    assert fx["meta"]["reading"] == "fp32" and fx["meta"]["kv_int4"]
+    wl, shape, model, prompt, forced = case_setup(fx)
+    log(f"{name}: {wl.name}, {shape.n_layers} layers, batch {wl.batch}")
+    toks, logits = gpu_run(wl, shape, model, prompt, forced)
+    agree, worst, flips = compare_fixture(fx, toks, logits, REL_TOL)
+    report(name, agree, worst, flips, toks.size)
+    assert worst <= REL_TOL and agree >= ARGMAX_MIN
+    lw, la = live_rows(model, wl, shape, prompt, forced, logits, [0, wl.batch - 1], kv_int4=True)
+    log(f"  rows 0, {wl.batch - 1} in full: normwise {lw:.2e}, argmax {la:.4f}")
+    assert lw <= REL_TOL
+
+
+def test_kv4_full_batch_secondary():
+    """OPT-30B shape, INT4 weights and INT4 KV cache in host memory, batch
+    128, real key/value projections: against the oracle with fp16
+    activations (the precision in which both sides decide the codes).  The
+    GPU may not disagree with it on more positions than the oracle's own
+    fp32 reading does, nor on more than 5 %; each disagreement must be a near
+    tie at the INT4-cache tolerance."""
+    fx = load_fixture("opt-30b-int4-kv4-l2-fp16ops")
+    fx32 = load_fixture("opt-30b-int4-kv4-l2-fp32")
+    wl, shape, model, prompt, forced = case_setup(fx)
+    log(f"kv4 secondary: {wl.name}, {shape.n_layers} layers, batch {wl.batch}")
+    toks, logits = gpu_run(wl, shape, model, prompt, forced)
+    agree, worst, flips = compare_fixture(fx, toks, logits, KV4_TOL)
+    report("vs fp16-activation oracle", agree, worst, flips, toks.size)
+    own = float((fx32["top_idx"][..., 0] == fx["top_idx"][..., 0]).mean())
+    log(f"  oracle fp32 vs fp16-activation readings agree on {own:.4f}")
+    assert worst <= KV4_TOL
+    assert agree >= min(ARGMAX_MIN, own) and agree >= 0.95
+
+
+FULL = ["opt-6.7b-full", "opt-13b-int4-full", "llama3.1-8b-full", "llama3.1-8b-int4-full",
+        "opt-30b-full-r16", "opt-30b-int4-kvhost-full-r16"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_depth(name):
+    """Every layer of the workload, the full batch on the GPU; the stored
+    oracle rows (the whole batch, or the first 16 of 64 / 128) at every
+    position."""
+    path = os.path.join(FIX, name + ".npz")
+    if not os.path.exists(path):
+        pytest.skip(f"no stored oracle results for {name} (tests/golden/make_fullbatch.py)")
+    fx = load_fixture(name)
+    wl, shape, model, prompt, forced = case_setup(fx)
+    log(f"{name}: {wl.name}, {shape.n_layers} layers, batch {wl.batch}, "
+        f"{len(fx['rows'])} oracle rows")
+    toks, logits = gpu_run(wl, shape, model, prompt, forced)
+    agree, worst, flips = compare_fixture(fx, toks, logits, REL_TOL)
+    report(name, agree, worst, flips, len(fx["rows"]) * wl.gen)
+    assert len(fx["rows"]) * wl.gen >= 500
+    assert worst <= REL_TOL and agree >= ARGMAX_MIN

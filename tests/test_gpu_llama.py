@@ -12,7 +12,8 @@ from paper_2504_03664_amd.model import Decoder, HostWeights, c_policy, c_shape
 pytestmark = pytest.mark.gpu
 
 REL_TOL = 2e-2          # normwise per logits row: max|g - o| / max|o|
-KV4_TOL = 5e-2          # INT4 cache: code flips between implementations (as for OPT)
+KV4_TOL = 5e-2          # INT4 cache with real key/value projections: code flips between
+                        # implementations that differ only in summation order
 ARGMAX_MIN = 0.99
 
 # head_dim 64, 4 query heads per key/value head (dkv 128); prompts with a
@@ -38,33 +39,53 @@ def _model(shape, seed, wfmt="fp16"):
     return synth.SyntheticLlama(shape, seed=seed, wfmt=wfmt, gain_std=0.2)
 
 
+def forced_tokens(prompt, gen, vocab):
+    """The ids fed at the gen - 1 decode steps of a teacher-forced run
+    (seeded, a function of the prompt's shape), so that the oracle's inputs
+    never come from the GPU."""
+    b, P = prompt.shape
+    return synth.prompt_tokens(b, gen - 1, vocab, seed=3, stream=P * 1000 + b)
+
+
 def _run(hw, prompt, gen, **pol):
+    """A teacher-forced run: tokens [b][gen], logits [gen][b][V]."""
+    forced = forced_tokens(prompt, gen, hw.shape.vocab)
     with Decoder(hw, max_batch=prompt.shape[0], max_seq=prompt.shape[1] + gen, **pol) as dec:
-        toks, logits = dec.generate(prompt, gen, want_logits=True)
+        toks, logits = dec.generate(prompt, gen, want_logits=True, forced=forced)
     return toks, np.stack(logits)
 
 
 def teacher_forced_check(model, prompt, toks, logits, kv_int4=False, tol=REL_TOL):
-    """Oracle logits at every generated position, fed the GPU's tokens; an
-    argmax disagreement must be a near tie.  With an INT4 cache the oracle
-    keeps fp16 activations, so that its codes are decided on the same fp16
-    keys and values as the kernels'."""
-    full = np.concatenate([prompt, toks[:, :-1]], axis=1)
-    ref = LlamaDecoder(model, np.float32, kv_int4=kv_int4, fp16_operands=kv_int4).forward(full)
-    P = prompt.shape[1]
+    """Oracle logits at every generated position of a teacher-forced run.
+    The normwise error is taken against the plain fp32 oracle; the greedy
+    tokens against the reading that keeps the paper's fp16 activations
+    (Section 4.1), the precision in which the kernels decide them; every
+    disagreement must be a near tie.  With an INT4 cache both use that
+    reading (its codes are decided on the same fp16 keys and values as the
+    kernels').  Returns (worst normwise error, agreement, near ties, the
+    agreement of the oracle's fp32 and fp16-activation readings)."""
+    gen = toks.shape[1]
+    full = np.concatenate([prompt, forced_tokens(prompt, gen, model.shape.vocab)], axis=1)
+    ref32 = LlamaDecoder(model, np.float32, kv_int4=kv_int4).forward(full, last=gen)
+    ref16 = LlamaDecoder(model, np.float32, kv_int4=kv_int4,
+                         fp16_operands=True).forward(full, last=gen)
+    ref = ref16 if kv_int4 else ref32
     worst, agree, total, ties = 0.0, 0, 0, 0
-    for s in range(toks.shape[1]):
-        o = ref[:, P - 1 + s].astype(np.float64)
+    for s in range(gen):
+        o = ref[:, s].astype(np.float64)
+        o16 = ref16[:, s].astype(np.float64)
         g = logits[s].astype(np.float64)
         worst = max(worst, float(normwise(g, o).max()))
-        ga, oa = g.argmax(-1), o.argmax(-1)
+        ga, oa = g.argmax(-1), o16.argmax(-1)
+        assert (ga == toks[:, s]).all()
         agree += int((ga == oa).sum())
         total += len(ga)
         for r in np.nonzero(ga != oa)[0]:
-            assert o[r, oa[r]] - o[r, ga[r]] <= tol * np.abs(o[r]).max(), "argmax, no near tie"
+            assert o16[r, oa[r]] - o16[r, ga[r]] <= tol * np.abs(o16[r]).max(), \
+                "argmax, no near tie"
             ties += 1
-        assert (ga == toks[:, s]).all()
-    return worst, agree / total, ties
+    own = float((ref32.argmax(-1) == ref16.argmax(-1)).mean())
+    return worst, agree / total, ties, own
 
 
 @pytest.mark.parametrize("shape,wfmt", [(SMALL64, "fp16"), (SMALL128, "fp16"),
@@ -79,9 +100,9 @@ def test_llama_streamed_parity_and_resident_identity(shape, wfmt):
     try:
         prompt = synth.prompt_tokens(3, 37, shape.vocab, seed=4)
         t0, l0 = _run(hw, prompt, 8, chunk_bytes=1 << 20)
-        err, agree, ties = teacher_forced_check(model, prompt, t0, l0)
+        err, agree, ties, _ = teacher_forced_check(model, prompt, t0, l0)
         log(f"  err {err:.2e} agree {agree:.3f} ({ties} near ties)")
-        assert err <= REL_TOL and (agree >= ARGMAX_MIN or ties <= 1)
+        assert err <= REL_TOL and agree >= ARGMAX_MIN
         for v in (dict(weights_on_host=False, embed_on_host=False),
                   dict(embed_on_host=False),
                   dict(n_weight_slots=1),
@@ -124,15 +145,16 @@ def test_llama_int4_kv_cache(wfmt):
     try:
         prompt = synth.prompt_tokens(4, 70, SMALL128.vocab, seed=5)
         t0, l0 = _run(hw, prompt, 8, kv_fmt="int4")
-        err, agree, ties = teacher_forced_check(model, prompt, t0, l0, kv_int4=True,
-                                                tol=KV4_TOL)
-        log(f"  err {err:.2e} agree {agree:.3f} ({ties} near ties)")
-        # every disagreement was checked to be a near tie.  With an INT4
-        # cache a key or value one rounding away from a code boundary takes
-        # a different code on each side, and the fp32 summation order of a
-        # kernel decides which; each such flip moves the fraction by 3% of
-        # these 32 samples (the row-wise errors stay at 0.7-1.8e-2)
-        assert err <= KV4_TOL and agree >= 0.85
+        err, agree, ties, own = teacher_forced_check(model, prompt, t0, l0, kv_int4=True,
+                                                     tol=KV4_TOL)
+        log(f"  err {err:.2e} agree {agree:.3f} ({ties} near ties); the oracle's fp32 and "
+            f"fp16-activation readings agree on {own:.3f}")
+        # With an INT4 cache a key or value within rounding of a code
+        # boundary takes a different code on each side (the fp32 summation
+        # order decides which), so the GPU is held to the 99 % bar or, where
+        # the oracle's own two readings agree less, to theirs; every
+        # disagreement was checked to be a near tie at KV4_TOL.
+        assert err <= KV4_TOL and agree >= min(ARGMAX_MIN, own)
         for v in (dict(weights_on_host=False, embed_on_host=False),
                   dict(kv_on_host=True),
                   dict(kv_on_host=True, debug_flags=B.PIPO_DBG_KV_PAGEABLE, chunk_bytes=1 << 16)):
@@ -152,7 +174,7 @@ def test_llama_longer_generation_crosses_prefill_tiles():
     try:
         prompt = synth.prompt_tokens(2, 130, SMALL64.vocab, seed=6)
         t0, l0 = _run(hw, prompt, 40)
-        err, agree, ties = teacher_forced_check(model, prompt, t0, l0)
+        err, agree, ties, _ = teacher_forced_check(model, prompt, t0, l0)
         log(f"  err {err:.2e} agree {agree:.3f}")
         assert err <= REL_TOL and agree >= ARGMAX_MIN
     finally:

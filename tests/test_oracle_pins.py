@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 import synth
-from oracle import (OracleDecoder, causal_attention, dequant_int4_g64, layer_norm,
+from oracle import (OracleDecoder, causal_attention, decoder_for, dequant_int4_g64, layer_norm,
                     param_count, quant_kv_int4_g64, streamed_bytes_per_step)
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -290,6 +290,24 @@ def test_incremental_decode_equals_full_recompute():
     for t in range(P, toks.shape[1]):
         step = dec.decode(cache, toks[:, t])
         assert np.allclose(step, full[:, t], rtol=1e-12, atol=1e-12)
+
+
+def test_forward_last_positions_are_the_full_pass_tail():
+    """forward(last=n) applies the head to the last n positions only: the
+    same values as the tail of the full pass (OPT and LLaMA oracles)."""
+    w = random_hand(seed=5)
+    toks = np.array([[1, 2, 3, 4, 5, 6, 7], [7, 6, 5, 4, 3, 2, 1]])
+    dec = OracleDecoder(w, np.float64)
+    full = dec.forward(toks)
+    # equal up to the summation order of the head's matrix product (fp64)
+    for n in (1, 3, 7):
+        assert np.allclose(dec.forward(toks, last=n), full[:, -n:], rtol=1e-12, atol=1e-12)
+    shape = synth.LlamaShape(2, 64, 4, 2, 96, vocab=50, max_pos=16)
+    ld = decoder_for(synth.SyntheticLlama(shape, seed=3, gain_std=0.2), np.float64)
+    lt = np.array([[3, 1, 4, 1, 5, 9]])
+    assert np.allclose(ld.forward(lt, last=2), ld.forward(lt)[:, -2:], rtol=1e-12, atol=1e-12)
+    assert np.allclose(ld.forward(lt, layers=1, last=4), ld.forward(lt, layers=1)[:, -4:],
+                       rtol=1e-12, atol=1e-12)
 
 
 def test_causality_and_batch_independence():

@@ -98,3 +98,45 @@ def test_synthetic_model_layout():
     q, sm = m4.layer(1)["w1"]
     q2, sm2 = synth.quant_int4_g64(L["w1"])
     assert (q == q2).all() and (sm.view(np.uint16) == sm2.view(np.uint16)).all()
+
+
+def test_teacher_tokens_are_seeded_and_independent():
+    wl = synth.WORKLOADS[1]
+    p, f = synth.teacher_tokens(wl, stream=1)
+    assert p.shape == (wl.batch, wl.prompt) and f.shape == (wl.batch, wl.gen - 1)
+    assert p.min() >= 0 and f.max() < wl.shape.vocab
+    p2, f2 = synth.teacher_tokens(wl, stream=1)
+    assert (p == p2).all() and (f == f2).all()
+    assert (f != p[:, :wl.gen - 1]).any()
+    assert (synth.teacher_tokens(wl, stream=2)[1] != f).any()
+
+
+@pytest.mark.parametrize("wfmt", ["fp16", "int4"])
+def test_zero_kv_provider(wfmt):
+    """ZeroKV zeroes exactly the key and value rows of wqkv (an INT4 zero
+    row: codes 0, scale 0, min 0) in every access path; the query rows and
+    every other tensor are the base provider's."""
+    base = synth.SyntheticOPT(synth.OPTShape(2, 128, 2, 256, vocab=100, max_pos=16), wfmt=wfmt)
+    z = synth.ZeroKV(base)
+    d = 128
+    Lb, Lz = base.layer(1), z.layer(1)
+    for nm in ("wo", "w1", "w2", "bqkv", "ln1_g"):
+        a, b = Lb[nm], Lz[nm]
+        if isinstance(a, tuple):
+            assert all(np.array_equal(x.view(np.uint8), y.view(np.uint8)) for x, y in zip(a, b))
+        else:
+            assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
+    if wfmt == "fp16":
+        w = Lz["wqkv"]
+        assert np.array_equal(w[:d].view(np.uint16), Lb["wqkv"][:d].view(np.uint16))
+        assert (w[d:] == 0).all()
+        out = z.fill(1, "wqkv", np.empty((3 * d, d), np.float16))
+        assert np.array_equal(out.view(np.uint16), w.view(np.uint16))
+    else:
+        q, sm = Lz["wqkv"]
+        assert np.array_equal(q[:d], Lb["wqkv"][0][:d]) and (q[d:] == 0).all()
+        assert (sm[d:].view(np.uint16) == 0).all()
+        q2 = np.empty_like(q)
+        sm2 = np.empty_like(sm)
+        z.fill_int4(1, "wqkv", q2, sm2)
+        assert np.array_equal(q2, q) and np.array_equal(sm2.view(np.uint16), sm.view(np.uint16))
