@@ -97,6 +97,25 @@ pipo_status pipo_op_attn_decode(const uint16_t* q, const uint16_t* kc, const uin
 int64_t pipo_op_attn_decode_workspace_bytes(int32_t b, int32_t n_heads, int32_t head_dim,
                                             int32_t t);
 
+/*
+ * pipo_op_attn_decode for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops, harnesses that forbid
+ * hipMalloc): the same kernels, split choice and result bit for bit as
+ * pipo_op_attn_decode with a sufficient workspace, but the split partials
+ * go to one fixed 4 MiB array of the library on each device (held until
+ * the process ends) instead of a caller workspace; nothing is allocated.
+ * Every shape this kernel accepts needs at most about 3.2 MB of it; a
+ * shape that would need more returns PIPO_ERR_UNSUPPORTED.  All calls on a
+ * device share that array, so calls that overlap in time on one device
+ * (on different streams, or from several threads) race and must be
+ * serialised by the caller.  The array's contents are arbitrary between
+ * calls (every partial is written before it is read).
+ */
+pipo_status pipo_op_attn_decode_noalloc(const uint16_t* q, const uint16_t* kc,
+                                        const uint16_t* vc, uint16_t* o, int32_t b,
+                                        int32_t n_heads, int32_t head_dim, int32_t t,
+                                        void* stream);
+
 /* The same over an INT4 KV cache (PIPO_KV_INT4_G64 rows of 9d/16 bytes,
  * position-major like the fp16 cache; d % 256 == 0): every key and value
  * is read as code * scale + min (rounded once to fp16).  Same workspace. */

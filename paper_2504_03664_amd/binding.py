@@ -150,6 +150,7 @@ _SIGNATURES = {
     "pipo_op_layernorm": ([vp, vp, vp, vp, i64, i64, i64, i64, f32, vp], i32),
     "pipo_op_attn_decode": ([vp, vp, vp, vp, i32, i32, i32, i32, vp, i64, vp], i32),
     "pipo_op_attn_decode_workspace_bytes": ([i32, i32, i32, i32], i64),
+    "pipo_op_attn_decode_noalloc": ([vp, vp, vp, vp, i32, i32, i32, i32, vp], i32),
     "pipo_op_attn_decode_kv4": ([vp, vp, vp, vp, i32, i32, i32, i32, vp, i64, vp], i32),
     "pipo_op_kv_quant": ([vp, vp, i64, i64, vp], i32),
     "pipo_op_kv_dequant": ([vp, vp, i64, i64, vp], i32),
@@ -446,6 +447,11 @@ def pipo_op_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, workspace=None,
                         workspace_bytes=0, stream=None):
     _check(lib().pipo_op_attn_decode(q, kc, vc, o, b, n_heads, head_dim, t, workspace,
                                      workspace_bytes, stream), "pipo_op_attn_decode")
+
+
+def pipo_op_attn_decode_noalloc(q, kc, vc, o, b, n_heads, head_dim, t, stream=None):
+    _check(lib().pipo_op_attn_decode_noalloc(q, kc, vc, o, b, n_heads, head_dim, t, stream),
+           "pipo_op_attn_decode_noalloc")
 
 
 def pipo_op_attn_decode_workspace_bytes(b, n_heads, head_dim, t) -> int:

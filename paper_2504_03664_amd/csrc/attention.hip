@@ -10,6 +10,7 @@
 // Softmax is max-subtracted in fp32; every reduction has a fixed order.
 #include <algorithm>
 #include <cfloat>
+#include <mutex>
 
 #include "common.h"
 #include "device.h"
@@ -717,3 +718,71 @@ pipo_status launch_attn_prefill(const uint16_t* q, const uint16_t* kc, const uin
 }
 
 }  // namespace pipo
+
+// ---------------------------------------------------------------------------
+// Decode attention for callers that cannot allocate (pipo_ops.h,
+// pipo_op_attn_decode_noalloc): the split partials go to a fixed device
+// array instead of a caller workspace.  In host code `scratch` names a
+// host-side stand-in, so the array's device address is taken once per
+// device with hipGetSymbolAddress and only that address is used.
+namespace {
+
+constexpr int64_t kScratchBytes = 4 << 20;
+__device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+pipo_status scratch_address(void** out) {
+  int dev = 0;
+  PIPO_HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) {
+    pipo::set_error("attn_decode_noalloc: device %d beyond %d", dev, kMaxDevices);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      pipo::set_error("attn_decode_noalloc: hipGetSymbolAddress failed (%s)",
+                      hipGetErrorString(e));
+      return PIPO_ERR_HIP;
+    }
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return PIPO_OK;
+}
+
+}  // namespace
+
+extern "C" pipo_status pipo_op_attn_decode_noalloc(const uint16_t* q, const uint16_t* kc,
+                                                   const uint16_t* vc, uint16_t* o, int32_t b,
+                                                   int32_t n_heads, int32_t head_dim, int32_t t,
+                                                   void* stream) {
+  pipo::clear_error();
+  if (!q || !kc || !vc || !o) {
+    pipo::set_error("attn_decode_noalloc: NULL pointer");
+    return PIPO_ERR_ARG;
+  }
+  if (b < 1 || n_heads < 1 || t < 0 || head_dim < 1) {
+    pipo::set_error("attn_decode_noalloc: bad shape b=%d heads=%d t=%d", b, n_heads, t);
+    return PIPO_ERR_ARG;
+  }
+  const int64_t need = pipo::attn_decode_workspace_bytes(
+      b, n_heads, head_dim, pipo::attn_decode_splits(b, n_heads, n_heads, t));
+  if (need > kScratchBytes) {
+    pipo::set_error("attn_decode_noalloc: the split partials need %lld bytes, above the %lld "
+                    "bytes of the library's scratch array",
+                    (long long)need, (long long)kScratchBytes);
+    return PIPO_ERR_UNSUPPORTED;
+  }
+  void* ws = nullptr;
+  if (need > 0) PIPO_TRY(scratch_address(&ws));
+  return pipo::launch_attn_decode(q, kc, vc, o, b, n_heads, n_heads, head_dim, t, false,
+                                  static_cast<float*>(ws), need,
+                                  static_cast<hipStream_t>(stream));
+}
