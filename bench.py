@@ -7,13 +7,16 @@ layers compute (and, for the KV-in-host workload, each layer's KV prefix
 streams in and the new rows stream out).  Prints one JSON line on stdout;
 progress goes to stderr.
 
-    python bench.py [--steps K] [--warmup W] [--workload I]
+    python bench.py [--steps K] [--warmup W] [--runs R] [--workload I]
 
 Default workload: OPT-30B shape (48 layers, d 7168, 56 heads, FFN 28672),
-fp16 weights, batch 64, prompt 512, 32 generated tokens (1 from the prefill
-plus warmup + steps decode steps), KV cache in HBM.  --workload picks
-another entry of synth.WORKLOADS (OPT shapes, INT4 weights and caches, the
-KV cache in host memory, LLaMA-3.1-8B shapes).
+fp16 weights, batch 64, prompt 512, 32 generated tokens, KV cache in HBM.
+Each of R runs (default 3) is one whole generation: the prefill, W warm-up
+decode steps, K timed decode steps (exactly K, bracketed by device
+synchronisations), then untimed steps up to the workload's 32 tokens; the
+reported throughput is the median run's, with the spread beside it.
+--workload picks another entry of synth.WORKLOADS (OPT shapes, INT4 weights
+and caches, the KV cache in host memory, LLaMA-3.1-8B shapes).
 """
 from __future__ import annotations
 
@@ -45,6 +48,10 @@ def parse():
                     help="timed decode steps (default 30; 4 for disk-tier workloads, whose "
                          "steps take seconds each)")
     ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--runs", type=int, default=3,
+                    help="timed generations (each: prefill, warm-up steps, timed steps, then "
+                         "untimed steps up to the workload's generated length); the reported "
+                         "throughput is their median")
     ap.add_argument("--workload", type=int, default=3,
                     help="index into synth.WORKLOADS (default: the OPT-30B fp16 decode)")
     ap.add_argument("--chunk-mb", type=int, default=64)
@@ -219,9 +226,12 @@ def main():
     shape = wl.shape if args.layers <= 0 else wl.shape.with_layers(args.layers)
     W = args.warmup
     K = args.steps if args.steps is not None else (4 if wl.weights_on_disk else 30)
+    R = max(1, args.runs if not wl.weights_on_disk else 1)
     # instrumented steps after the timed ones
     KI = 0 if args.no_timestamps else min(K, 2 if wl.weights_on_disk else 10)
-    max_seq = max(wl.prompt + wl.gen, wl.prompt + 1 + W + K + KI)
+    # each run generates the workload's tokens (more if W + K steps need more)
+    gen = max(wl.gen, 1 + W + K)
+    max_seq = wl.prompt + max(gen, 1 + W + K + KI)
     seed = synth.DEFAULT_SEED
     log(f"workload {wl.name}: {shape.n_layers} layers, d {shape.d_model}, batch {wl.batch}")
 
@@ -258,24 +268,40 @@ def main():
             f"{dprefix:.2f} GB/s best over its first 16 GiB (direct I/O: {direct})")
         disk.update(peak_gbps=dpeak, prefix_gbps=dprefix, direct_io=direct)
     prompt = synth.prompt_tokens(wl.batch, wl.prompt, shape.vocab, seed=1, stream=args.workload)
-    t0 = time.perf_counter()
-    nxt, _ = dec.prefill(prompt)
-    ttft_ms = (time.perf_counter() - t0) * 1e3
-    log(f"prefill {wl.batch}x{wl.prompt}: {ttft_ms:.0f} ms")
-    for _ in range(W):
-        nxt, _ = dec.decode(nxt)
-    dec.reset_stats()
-    step_s = []
-    t0 = time.perf_counter()
-    for i in range(K):
-        ts = time.perf_counter()
-        nxt, _ = dec.decode(nxt)
-        step_s.append(time.perf_counter() - ts)
-        if step_s[-1] > 2.0:   # slow (disk-tier) steps: a progress line each
-            log(f"decode step {i}: {step_s[-1]:.2f} s")
-    dt = time.perf_counter() - t0
-    st = dec.stats()
-    log(f"{K} decode steps in {dt:.3f} s")
+    runs = []
+    for run in range(R):
+        # one generation: prefill, W warm-up steps, K timed steps, then the
+        # rest of the workload's generation untimed (the last run's rest is
+        # replaced by the instrumented steps)
+        t0 = time.perf_counter()
+        nxt, _ = dec.prefill(prompt)
+        ttft_ms = (time.perf_counter() - t0) * 1e3
+        log(f"run {run}: prefill {wl.batch}x{wl.prompt}: {ttft_ms:.0f} ms")
+        for _ in range(W):
+            nxt, _ = dec.decode(nxt)
+        dec.reset_stats()
+        step_s = []
+        B.pipo_dev_synchronize()      # every stream idle: no load of a timed step runs early
+        t0 = time.perf_counter()
+        for i in range(K):
+            ts = time.perf_counter()
+            nxt, _ = dec.decode(nxt)
+            step_s.append(time.perf_counter() - ts)
+            if step_s[-1] > 2.0:   # slow (disk-tier) steps: a progress line each
+                log(f"decode step {i}: {step_s[-1]:.2f} s")
+        B.pipo_dev_synchronize()      # and the loads the last step started ahead are done
+        dt = time.perf_counter() - t0
+        st = dec.stats()
+        log(f"run {run}: {K} decode steps in {dt:.3f} s ({wl.batch * K / dt:.3f} tokens/s)")
+        runs.append(dict(dt=dt, st=st, step_s=step_s, ttft_ms=ttft_ms))
+        if run + 1 < R:
+            for _ in range(gen - 1 - W - K):
+                nxt, _ = dec.decode(nxt)
+    # the median run (by throughput) is the one reported
+    order = sorted(range(R), key=lambda i: runs[i]["dt"])
+    med = runs[order[R // 2]]
+    dt, st, step_s, ttft_ms = med["dt"], med["st"], med["step_s"], med["ttft_ms"]
+    run_values = [wl.batch * K / r["dt"] for r in runs]
     if KI:
         # device timestamps around every copy and kernel, over separate
         # steps: they add events and a stream synchronisation per step, so
@@ -304,7 +330,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "layers": shape.n_layers, "d_model": shape.d_model,
                    "batch": wl.batch, "prompt": wl.prompt,
-                   "generated": 1 + W + K,
+                   "generated": gen, "warmup_steps": W, "timed_steps": K, "runs": R,
                    "weights": f"{wl.wfmt}, " + ("layers in the disk tier's file (disk -> pinned "
                                                 "-> HBM), head pinned host" if wl.weights_on_disk
                                                 else "pinned host") + ", streamed",
@@ -320,7 +346,15 @@ def main():
                      "staged_bytes_per_step": int(st["staged_bytes"] / K),
                      "roofline_tokens_per_s": round(roof, 3),
                      "frac_of_roofline": round(value / roof, 4)},
-        "ttft_ms": round(ttft_ms, 1),
+        "runs": {"n": R, "median": round(float(np.median(run_values)), 3),
+                 "min": round(min(run_values), 3), "max": round(max(run_values), 3),
+                 "spread_frac": round((max(run_values) - min(run_values))
+                                      / float(np.median(run_values)), 4),
+                 "tokens_per_s": [round(v, 3) for v in run_values],
+                 "ttft_ms": [round(r["ttft_ms"], 1) for r in runs],
+                 "source": "each run one whole generation (prefill, warm-up, timed and "
+                           "untimed steps); value is the median run's"},
+        "ttft_ms": round(float(np.median([r["ttft_ms"] for r in runs])), 1),
         **({"disk": {"peak_gbps": round(disk["peak_gbps"], 2),
                      "prefix_16gib_gbps": round(disk["prefix_gbps"], 2),
                      "direct_io": disk["direct_io"],

@@ -14,8 +14,10 @@ from typing import Optional, Tuple
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libpipo.so")
-SCHED_LIB_PATH = os.path.join(_PKG, "libpipo_sched.so")
+# PIPO_LIB / PIPO_SCHED_LIB name another build of the same libraries (the
+# host-side AddressSanitizer build of build_asan.py, for CPU tests)
+LIB_PATH = os.environ.get("PIPO_LIB") or os.path.join(_PKG, "libpipo.so")
+SCHED_LIB_PATH = os.environ.get("PIPO_SCHED_LIB") or os.path.join(_PKG, "libpipo_sched.so")
 
 i32, i64, f32, f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double
 vp, sz = ctypes.c_void_p, ctypes.c_size_t

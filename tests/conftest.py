@@ -9,3 +9,4 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) and the built HIP library")
     config.addinivalue_line("markers", "slow: full-size workload, minutes of CPU oracle time")
+    config.addinivalue_line("markers", "asan: host-side code under AddressSanitizer (CPU)")
