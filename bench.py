@@ -73,7 +73,7 @@ def parse():
 # the decode GEMM kernel plan of gemm.hip, restated to name the kernels in
 # rocprofv3 output: (NF, KW, PD, KC) of the streaming kernel by (INT4, MF)
 _STREAM_SEL = {(False, 2): (1, 8, 2, 128), (False, 4): (1, 8, 2, 128), (False, 8): (1, 8, 2, 128),
-               (True, 2): (1, 8, 4, 256), (True, 4): (2, 8, 4, 256), (True, 8): (2, 8, 4, 128)}
+               (True, 2): (1, 8, 2, 256), (True, 4): (2, 8, 4, 256), (True, 8): (2, 8, 4, 128)}
 
 
 def gemm_family(M):

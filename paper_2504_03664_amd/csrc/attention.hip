@@ -398,7 +398,8 @@ __global__ __launch_bounds__(D) void attn_decode_combine(const float* __restrict
 // sequence, 4 waves x 32 queries (two sub-blocks of 16).  Keys come in
 // blocks of 64, K and V moved from the cache straight into LDS by the load
 // unit (double-buffered), rows stored with their 16-byte chunks permuted by
-// an XOR of the row so that fragment reads hit distinct banks.  The wave
+// row (kv_swz) so that the K fragment reads and the transposed V reads hit
+// distinct banks.  The wave
 // computes S^T = K Q^T (keys on the MFMA rows, its queries on the columns,
 // so each lane holds scores of one query), an online softmax per query in
 // fp32, and O^T += V^T P^T: the probabilities stay in the registers they
@@ -407,15 +408,49 @@ __global__ __launch_bounds__(D) void attn_decode_combine(const float* __restrict
 // reads).  Workgroups with the most key blocks start first.
 constexpr int kPQ = 128;  // queries per workgroup
 constexpr int kPK = 64;   // keys per block
+constexpr int kPrefillStages = 2;
 
+// LDS slot of 16-byte chunk `chunk` of key row `key`.  A row holds R = D / 8
+// chunks and 128 / D rows share a 256-byte line (64 banks); the chunk is
+// XORed with x rotated left by one bit, x = the row's line index mod R.
+// K fragment reads (16 lanes: rows r = 0..15, one chunk) then hit 16
+// distinct slots of a line's banks, as with any bijection of x; the
+// transposed V reads (16 lanes: rows 4 g + 0..3, the chunk pair 2 n, 2 n + 1)
+// need the four rows' keys to differ in more than their lowest bit, which a
+// plain XOR with x does not give (rows 4 g and 4 g + 1 then share both
+// chunks, a 2-way conflict on every V read); the rotation does.
 template <int D>
 __device__ __forceinline__ int kv_swz(int key, int chunk) {
-  // rows of D halves; 256 / (2 D) rows share a 256-byte line of LDS
-  return chunk ^ ((key / (128 / D)) & (D / 8 - 1));
+  constexpr int R = D / 8, LOG_R = D == 128 ? 4 : 3;
+  const int x = (key / (128 / D)) & (R - 1);
+  return chunk ^ (((x << 1) | (x >> (LOG_R - 1))) & (R - 1));
 }
 
-// two waves per SIMD (the register budget the compiler is held to)
-template <int D>
+// NS LDS stages of K and V blocks: NS - 1 blocks are in flight while one is
+// computed.  Two waves per SIMD (the register budget the compiler is held to).
+template <int NS, int DMA>
+__device__ __forceinline__ void wait_blocks_landed(int pending) {
+  // at most `pending` later blocks (2 DMA loads per wave each) outstanding
+  if constexpr (NS >= 4) {
+    if (pending >= 3) {
+      __builtin_amdgcn_s_waitcnt(waitcnt_imm(3 * 2 * DMA, false));
+      return;
+    }
+  }
+  if constexpr (NS >= 3) {
+    if (pending >= 2) {
+      __builtin_amdgcn_s_waitcnt(waitcnt_imm(2 * 2 * DMA, false));
+      return;
+    }
+  }
+  if (pending >= 1) {
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(2 * DMA, false));
+    return;
+  }
+  __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, false));
+}
+
+template <int D, int NS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_prefill_k(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, uint16_t* __restrict__ o, int b, int P, int H, int Hkv) {
@@ -425,7 +460,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   constexpr int KK = D / 32;                // MFMA k steps over the head dimension
   constexpr int NF = D / 16;                // head-dimension fragments of O^T
   constexpr float kLog2e = 1.4426950408889634f;
-  __shared__ __attribute__((aligned(1024))) uint8_t kv[2][2][BLK];  // [buffer][K, V]
+  __shared__ __attribute__((aligned(1024))) uint8_t kv[NS][2][BLK];  // [stage][K, V]
 
   const int nqb = (P + kPQ - 1) / kPQ;
   const int qb = nqb - 1 - (int)blockIdx.x;  // most key blocks first
@@ -470,13 +505,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     for (int n = 0; n < NF; ++n) oacc[u][n] = f4{0.f, 0.f, 0.f, 0.f};
   float mrow[2] = {-INFINITY, -INFINITY}, lrow[2] = {0.f, 0.f};
 
-  issue(0, 0);
-  if (nkb > 1) issue(1, 1);
+#pragma unroll
+  for (int i = 0; i < NS; ++i)
+    if (i < nkb) issue(i, i);
   for (int kb = 0; kb < nkb; ++kb) {
-    const int buf = kb & 1;
-    // block kb landed (block kb + 1 may still be in flight)
-    if (kb + 1 < nkb) __builtin_amdgcn_s_waitcnt(waitcnt_imm(2 * DMA, false));
-    else __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, false));
+    const int buf = kb % NS;
+    // block kb landed (blocks kb + 1 .. kb + NS - 1 may still be in flight)
+    wait_blocks_landed<NS, DMA>(min(NS - 1, nkb - 1 - kb));
     wg_barrier();
     const int k0 = kb * kPK;
     if (k0 <= qw + 31) {  // some key of the block is visible to this wave
@@ -563,7 +598,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     // every wave is done with this buffer
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, true));
     wg_barrier();
-    if (kb + 2 < nkb) issue(kb + 2, buf);
+    if (kb + NS < nkb) issue(kb + NS, buf);
   }
 
   // oacc[u][n][e]: dim 16 n + 4 g + e of query qw + 16 u + r
@@ -710,9 +745,11 @@ pipo_status launch_attn_prefill(const uint16_t* q, const uint16_t* kc, const uin
   PIPO_TRY(check_heads("attn_prefill", n_heads, n_kv_heads, head_dim));
   const dim3 grid((unsigned)((P + kPQ - 1) / kPQ), (unsigned)n_heads, (unsigned)b);
   if (head_dim == 128)
-    launch(attn_prefill_k<128>, grid, dim3(256), 0, st, q, kc, vc, o, b, P, n_heads, n_kv_heads);
+    launch(attn_prefill_k<128, kPrefillStages>, grid, dim3(256), 0, st, q, kc, vc, o, b, P,
+           n_heads, n_kv_heads);
   else
-    launch(attn_prefill_k<64>, grid, dim3(256), 0, st, q, kc, vc, o, b, P, n_heads, n_kv_heads);
+    launch(attn_prefill_k<64, kPrefillStages>, grid, dim3(256), 0, st, q, kc, vc, o, b, P,
+           n_heads, n_kv_heads);
   PIPO_HIP_TRY(hipGetLastError());
   return PIPO_OK;
 }

@@ -172,7 +172,12 @@ UnitLayout unit_layout(const pipo_shape& sh, bool w4) {
       u.seg_bytes[seg] = N * K * 2;
     }
   };
-  u.seg_bytes[kSegMisc] = u.misc_bytes;
+  // The small tensors are copied on their own; a host-to-device copy
+  // shorter than 32 KiB is served by a blit kernel on the compute units
+  // instead of a DMA engine (measured: 16 KiB copies run
+  // __amd_rocclr_copyBuffer, 32 KiB ones do not), so that copy is padded to
+  // kMinDmaCopyBytes (zeros beyond the last layer's tensors).
+  u.seg_bytes[kSegMisc] = std::max(u.misc_bytes, kMinDmaCopyBytes);
   mat(kSegWqkv, qkv_rows(sh), d);
   mat(kSegWo, d, d);
   mat(kSegW1, fc1_rows(sh), d);
@@ -184,6 +189,7 @@ UnitLayout unit_layout(const pipo_shape& sh, bool w4) {
     off = align_up(off + u.seg_bytes[sg], 4096);
     u.copy_bytes += u.seg_bytes[sg];
   }
+  u.tensor_bytes = u.copy_bytes - (u.seg_bytes[kSegMisc] - u.misc_bytes);
   u.layer_bytes = off;
   u.head_bytes = V * d * 2;
   return u;
@@ -248,7 +254,7 @@ int64_t staging_bytes(const pipo_policy& pol) {
 int64_t host_weight_bytes(const pipo_shape& sh, const pipo_policy& pol) {
   const UnitLayout u = unit_layout(sh, pol.wfmt == PIPO_W_INT4_G64);
   int64_t bytes = staging_bytes(pol);
-  if (pol.weights_on_host && !pol.weights_on_disk) bytes += (int64_t)sh.n_layers * u.copy_bytes;
+  if (pol.weights_on_host && !pol.weights_on_disk) bytes += (int64_t)sh.n_layers * u.tensor_bytes;
   if (pol.embed_on_host) bytes += u.head_bytes;
   return bytes;
 }
@@ -275,7 +281,7 @@ static void fill_plan(const pipo_shape& sh, const pipo_policy& pol, pipo_plan* o
   const HbmPlan p = hbm_plan(sh, pol);
   std::memset(out, 0, sizeof *out);
   out->weight_bytes =
-      (int64_t)sh.n_layers * u.copy_bytes + u.head_bytes +
+      (int64_t)sh.n_layers * u.tensor_bytes + u.head_bytes +
       (is_llama(sh) ? u.head_bytes + 2 * sh.d_model
                     : ((int64_t)sh.max_pos + sh.pos_offset) * sh.d_model * 2 + 4 * sh.d_model);
   out->kv_bytes = (int64_t)sh.n_layers * 2 * p.kv_part;

@@ -54,15 +54,50 @@ __device__ __forceinline__ h2 dequant_pair(uint32_t t, h2 s2, h2 m2) {
   return __builtin_elementwise_fma(c, s2, m2);
 }
 
-// eight codes in the order (0, 4, 1, 5, 2, 6, 3, 7): two operations per pair
+// eight codes in the order (0, 4, 1, 5, 2, 6, 3, 7).  Codes 0 and 4 (bits
+// 0-3 and 16-19) go under the exponent of 1024 as above; codes 1 and 5
+// (bits 4-7 and 20-23) are left where they are, under the exponent of 64
+// (fp16 0x5400, spacing 1/16), where a code c at bits 4-7 reads as 64 + c:
+// one AND-OR per pair and one shift per word, no per-pair shifts.  The
+// biases 1024 and 64 are subtracted exactly before the fused multiply-add,
+// so the values are those of dequant_pair.
+__device__ __forceinline__ h2 dequant_biased(uint32_t t, _Float16 bias, h2 s2, h2 m2) {
+  const h2 c = __builtin_bit_cast(h2, t) - h2{bias, bias};
+  return __builtin_elementwise_fma(c, s2, m2);
+}
+
+// 32-bit constants the compiler sees as register values.  A three-operand
+// instruction here encodes no literal and reads at most one scalar
+// register, so (x & mask) | magic becomes a single v_and_or_b32 only with
+// the mask in a scalar and the magic in a vector register.
+__device__ __forceinline__ uint32_t sgpr_const(uint32_t v) {
+  uint32_t r;
+  asm("s_mov_b32 %0, %1" : "=s"(r) : "i"(v));
+  return r;
+}
+__device__ __forceinline__ uint32_t vgpr_const(uint32_t v) {
+  uint32_t r;
+  asm("v_mov_b32 %0, %1" : "=v"(r) : "i"(v));
+  return r;
+}
+
 __device__ __forceinline__ h8 dequant8_interleaved(uint32_t v, h2 s2, h2 m2) {
+  const uint32_t v8 = v >> 8;
+  const uint32_t e1024 = vgpr_const(0x64006400u), e64 = vgpr_const(0x54005400u);
+  const uint32_t lo = sgpr_const(0x000F000Fu), hi = sgpr_const(0x00F000F0u);
+  const h2 w0 = dequant_biased((v & lo) | e1024, (_Float16)1024.f, s2, m2);
+  const h2 w1 = dequant_biased((v & hi) | e64, (_Float16)64.f, s2, m2);
+  const h2 w2 = dequant_biased((v8 & lo) | e1024, (_Float16)1024.f, s2, m2);
+  const h2 w3 = dequant_biased((v8 & hi) | e64, (_Float16)64.f, s2, m2);
   h8 out;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const h2 w = dequant_pair((v >> (4 * j)) & 0x000F000Fu, s2, m2);
-    out[2 * j] = w[0];
-    out[2 * j + 1] = w[1];
-  }
+  out[0] = w0[0];
+  out[1] = w0[1];
+  out[2] = w1[0];
+  out[3] = w1[1];
+  out[4] = w2[0];
+  out[5] = w2[1];
+  out[6] = w3[0];
+  out[7] = w3[1];
   return out;
 }
 

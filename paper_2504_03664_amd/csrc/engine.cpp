@@ -1114,8 +1114,13 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
     }
   c->packed = w->layout == PIPO_LAYOUT_FRAGMENT || !in_place_row_major;
   c->pack_on_copy = c->packed && w->layout == PIPO_LAYOUT_ROW_MAJOR;
+  // every layer's small tensors, back to back; a layer's copy takes
+  // seg_bytes[kSegMisc] >= misc_bytes bytes (the minimum DMA copy), so the
+  // region ends with that much zero padding after the last layer
   void* misc_all = nullptr;
-  PIPO_TRY(pin_alloc(c, &misc_all, L * c->misc_bytes));
+  const int64_t misc_region = L * c->misc_bytes + (c->seg_bytes[kSegMisc] - c->misc_bytes);
+  PIPO_TRY(pin_alloc(c, &misc_all, misc_region));
+  std::memset(misc_all, 0, (size_t)misc_region);
   for (int64_t j = 0; j < L; ++j) {
     const pipo_layer_host& lw = w->layers[j];
     const uint16_t* small[kNumMisc] = {lw.ln1_g, lw.ln1_b, lw.bqkv, lw.bo,

@@ -207,9 +207,11 @@ __global__ __launch_bounds__(KW * 64) void gemm_skinny(GemmArgs a) {
 // Workgroup = KW waves; wave w owns W rows n0 + 16 NF w .. + 16 NF and the
 // workgroup covers k in [z kper, (z + 1) kper), z = blockIdx.y.  K is walked
 // in chunks of KC: the X chunk (16 MF rows x KC) is loaded once per
-// workgroup into one of two LDS buffers, one barrier per chunk; each wave
-// holds PD chunks of its W rows in registers, refilling a chunk's registers
-// as soon as its MFMAs are issued.  Every load is unconditional (row and
+// workgroup, PD chunks ahead into registers and then into one of two LDS
+// buffers, one barrier per chunk; each wave holds PD chunks of its W rows
+// in registers, refilling a chunk's registers as soon as its MFMAs are
+// issued.  (With X loaded only one chunk ahead, every chunk waited for an
+// L2 round trip before its barrier.)  Every load is unconditional (row and
 // chunk indexes are clamped: rows past M or N are computed and never
 // stored, a clamped chunk is loaded again and not used), which keeps the
 // compiler's wait counts exact so that the prefetch really stays in flight.
@@ -248,8 +250,46 @@ __global__ __launch_bounds__(KW * 64) void gemm_stream(GemmArgs a, float* part, 
     u32x4 w[NF][C::kWRegs];
     uint32_t sm[NF][W4 ? KC / 128 : 1];
   };
+  // Fragment order: a lane's 16 bytes of a 16-row block sit at the same
+  // offset in every block of its row group, and the blocks of a row group
+  // follow each other along k, so a lane's address is its own base plus a
+  // workgroup-uniform block offset (fp16: 32-k blocks of 1 KiB; INT4:
+  // 128-k blocks of 1 KiB of codes and 32 (scale, min) words).
+  const uint8_t* wlane[NF];
+  const uint32_t* smlane[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int64_t grp = wrow[f] >> 4;
+    if constexpr (W4) {
+      wlane[f] = a.Wq + grp * (K >> 7) * 1024 + (((wrow[f] & 15) + 16 * g) << 4);
+      smlane[f] = reinterpret_cast<const uint32_t*>(a.Wsm) + grp * (K >> 7) * 32 +
+                  (wrow[f] & 15) * 2 + (g >> 1);
+    } else {
+      wlane[f] = reinterpret_cast<const uint8_t*>(a.W) + grp * (K >> 5) * 1024 +
+                 (((wrow[f] & 15) + 16 * g) << 4);
+      smlane[f] = nullptr;
+    }
+  }
   const auto load_w = [&](WChunk& F, int64_t c) {
     const int64_t k0 = kbeg + clamp_hi(c, nch - 1) * KC;
+    if constexpr (PK) {
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        if constexpr (W4) {
+#pragma unroll
+          for (int t = 0; t < KC / 128; ++t) {
+            const int64_t blk = (k0 >> 7) + t;
+            F.w[f][t] = *reinterpret_cast<const u32x4*>(wlane[f] + blk * 1024);
+            F.sm[f][t] = smlane[f][blk * 32];
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < C::kWRegs; ++i)
+            F.w[f][i] = *reinterpret_cast<const u32x4*>(wlane[f] + ((k0 >> 5) + i) * 1024);
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
       if constexpr (W4) {
@@ -266,25 +306,29 @@ __global__ __launch_bounds__(KW * 64) void gemm_stream(GemmArgs a, float* part, 
       }
     }
   };
-  h8 xr[C::kXPerThread];
-  const auto load_x = [&](int64_t c) {
+  // X chunks travel through registers PD chunks ahead of their use, like W:
+  // chunk c sits in ring slot c % PD from its load (iteration c - 1 - PD)
+  // until it is stored to LDS (end of iteration c - 1)
+  h8 xr[PD][C::kXPerThread];
+  const auto load_x = [&](int slot, int64_t c) {
     const int64_t k0 = kbeg + clamp_hi(c, nch - 1) * KC;
 #pragma unroll
     for (int j = 0; j < C::kXPerThread; ++j) {
       const int e = tid + j * C::kThreads < C::kXH8 ? tid + j * C::kThreads : C::kXH8 - 1;
       const int row = e / (KC / 8), col = (e % (KC / 8)) * 8;
-      xr[j] = load_h8(a.X + clamp_hi(row, a.M - 1) * K + k0 + col);
+      xr[slot][j] = load_h8(a.X + clamp_hi(row, a.M - 1) * K + k0 + col);
     }
   };
   // INT4: X is stored already permuted to the codes' interleaved order
   // (once per workgroup rather than once per wave and use)
-  const auto store_x = [&](int b) {
+  const auto store_x = [&](int b, int slot) {
 #pragma unroll
     for (int j = 0; j < C::kXPerThread; ++j) {
       const int e = tid + j * C::kThreads;
       if (e < C::kXH8) {
         const int row = e / (KC / 8), col = (e % (KC / 8)) * 8;
-        *reinterpret_cast<h8*>(&Xs[b][row * C::kXLd + col]) = W4 ? interleave_h8(xr[j]) : xr[j];
+        *reinterpret_cast<h8*>(&Xs[b][row * C::kXLd + col]) =
+            W4 ? interleave_h8(xr[slot][j]) : xr[slot][j];
       }
     }
   };
@@ -320,24 +364,27 @@ __global__ __launch_bounds__(KW * 64) void gemm_stream(GemmArgs a, float* part, 
   };
 
   WChunk F[PD];
+  load_x(0, 0);
+  store_x(0, 0);
+#pragma unroll
+  for (int p = 1; p <= PD; ++p) load_x(p % PD, p);
 #pragma unroll
   for (int p = 0; p < PD; ++p) {
     load_w(F[p], p);
     __builtin_amdgcn_sched_barrier(0);  // keep the chunks' loads in chunk order
   }
-  load_x(0);
-  store_x(0);
   __syncthreads();
   for (int64_t c0 = 0; c0 < nch; c0 += PD) {
 #pragma unroll
     for (int p = 0; p < PD; ++p) {
       const int64_t c = c0 + p;
-      load_x(c + 1);
       if (c < nch) compute(F[p], (int)(c & 1));
       load_w(F[p], c + PD);
       __builtin_amdgcn_sched_barrier(0);
       // buffer (c + 1) & 1 was last read in chunk c - 1, before the barrier
-      store_x((int)((c + 1) & 1));
+      store_x((int)((c + 1) & 1), (p + 1) % PD);
+      load_x((p + 1) % PD, c + 1 + PD);
+      __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
     }
   }
@@ -850,7 +897,7 @@ template <bool W4, int MF> struct StreamSel;
 template <> struct StreamSel<false, 2> { static constexpr int NF = 1, KW = 8, PD = 2, KC = 128; };
 template <> struct StreamSel<false, 4> { static constexpr int NF = 1, KW = 8, PD = 2, KC = 128; };
 template <> struct StreamSel<false, 8> { static constexpr int NF = 1, KW = 8, PD = 2, KC = 128; };
-template <> struct StreamSel<true, 2> { static constexpr int NF = 1, KW = 8, PD = 4, KC = 256; };
+template <> struct StreamSel<true, 2> { static constexpr int NF = 1, KW = 8, PD = 2, KC = 256; };
 template <> struct StreamSel<true, 4> { static constexpr int NF = 2, KW = 8, PD = 4, KC = 256; };
 template <> struct StreamSel<true, 8> { static constexpr int NF = 2, KW = 8, PD = 4, KC = 128; };
 template <bool W4, int MF> struct StreamFallback {

@@ -28,6 +28,8 @@ pipo_status normalize_policy(const pipo_shape* shape, pipo_policy* pol);
 
 // small tensors of a layer, packed in this order (absent ones take no room)
 enum MiscTensor { kLn1G, kLn1B, kBqkv, kBo, kLn2G, kLn2B, kB1, kB2, kNumMisc };
+// shortest host-to-device copy that the runtime gives to a DMA engine
+constexpr int64_t kMinDmaCopyBytes = 32768;
 
 // one layer unit as it sits in a weight slot: segments at 4 KiB offsets
 struct UnitLayout {
@@ -38,6 +40,8 @@ struct UnitLayout {
   int64_t misc_bytes = 0;    // small tensors of a layer, packed
   int64_t layer_bytes = 0;   // slot bytes of a layer unit
   int64_t copy_bytes = 0;    // bytes a layer unit's copies move (sum of segments)
+  int64_t tensor_bytes = 0;  // bytes of a layer's tensors (copy_bytes without the padding
+                             // of the small-tensor copy to kMinDmaCopyBytes)
   int64_t head_bytes = 0;    // the output head (the token table when tied)
 };
 UnitLayout unit_layout(const pipo_shape& sh, bool w4);

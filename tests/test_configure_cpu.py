@@ -7,7 +7,7 @@ import itertools
 import pytest
 
 import synth
-from oracle import streamed_bytes_per_step
+from oracle import layer_param_count, streamed_bytes_per_step
 from paper_2504_03664_amd import binding as B
 from paper_2504_03664_amd.model import c_policy, c_shape
 
@@ -27,9 +27,12 @@ def plan(shape, **pol):
 ])
 def test_step_bytes_match_oracle_accounting(shape, wfmt, kv_fmt, b, s):
     """Streamed bytes per step = the oracle's closed form (weights, head and
-    the KV prefix) + token ids and embedding rows."""
+    the KV prefix) + token ids and embedding rows + the padding of each
+    layer's small-tensor copy to 32 KiB (shorter copies would run on a blit
+    kernel instead of a DMA engine)."""
     d = shape.d_model
-    extra = b * 4 + b * d * 2
+    small = layer_param_count(d, shape.d_ffn) - (4 * d * d + 2 * d * shape.d_ffn)
+    extra = b * 4 + b * d * 2 + shape.n_layers * max(0, 32768 - 2 * small)
     p = plan(shape, wfmt=wfmt, kv_fmt=kv_fmt, max_batch=b, max_seq=s)
     want = streamed_bytes_per_step(shape.n_layers, d, shape.d_ffn, shape.vocab, wfmt)
     assert p["h2d_bytes_per_step"] == want + extra

@@ -102,11 +102,14 @@ def test_plan_matches_the_papers_size_formulas(shape):
 
 def test_streamed_bytes_per_step():
     """A decode step with everything streamed moves every layer and the
-    untied head once (plus the token rows gathered on the host)."""
+    untied head once (plus the token rows gathered on the host); each
+    layer's two norm gains (2 d fp16 values) travel in a copy padded to 32
+    KiB, the shortest copy the runtime gives to a DMA engine."""
     sh = synth.LLAMA31_8B
     b, s = 16, 544
     plan = B.pipo_plan_policy(c_shape(sh), c_policy(max_batch=b, max_seq=s))
     W = llama_param_count(sh.n_layers, sh.d_model, sh.n_heads, sh.n_kv_heads, sh.d_ffn, sh.vocab)
     tok_table, final_norm = sh.vocab * sh.d_model, sh.d_model
+    pad = sh.n_layers * max(0, 32768 - 2 * 2 * sh.d_model)
     assert plan["h2d_bytes_per_step"] == 2 * (W - tok_table - final_norm) + b * sh.d_model * 2 \
-        + b * 4
+        + b * 4 + pad
