@@ -410,24 +410,29 @@ constexpr int kPQ = 128;  // queries per workgroup
 constexpr int kPK = 64;   // keys per block
 constexpr int kPrefillStages = 2;
 
-// LDS slot of 16-byte chunk `chunk` of key row `key`.  A row holds R = D / 8
-// chunks and 128 / D rows share a 256-byte line (64 banks); the chunk is
-// XORed with x rotated left by one bit, x = the row's line index mod R.
-// K fragment reads (16 lanes: rows r = 0..15, one chunk) then hit 16
-// distinct slots of a line's banks, as with any bijection of x; the
-// transposed V reads (16 lanes: rows 4 g + 0..3, the chunk pair 2 n, 2 n + 1)
-// need the four rows' keys to differ in more than their lowest bit, which a
-// plain XOR with x does not give (rows 4 g and 4 g + 1 then share both
-// chunks, a 2-way conflict on every V read); the rotation does.
+// LDS slot of 16-byte chunk `chunk` of key row `key` (an involution: the
+// DMA puts cache chunk kv_swz(row, s) into slot s, a read of chunk c goes
+// to slot kv_swz(row, c)).  The chunk is XORed with a mask that depends on
+// the row's low four bits, chosen with the LDS bank-conflict counters: over
+// the K fragment reads (ds_read_b128; lane r + 16 g reads row r of a 16-row
+// group, chunk 4 kk + g) and the transposed V reads (ds_read_b64_tr_b16;
+// rows 4 g .. 4 g + 3 of a group, chunks 2 n and 2 n + 1), a plain XOR with
+// the row leaves the K reads conflict-free but gives every V read a 2-way
+// conflict, the row rotated left by one bit the reverse, and of 240 random
+// masks that clear the V reads three cleared the K reads as well; the table
+// below is the first of them (head_dim 128: 16 chunks per row).  For
+// head_dim 64 (two rows per 256 bytes) the mask row & 6 measured no
+// conflicts on either read.
 template <int D>
 __device__ __forceinline__ int kv_swz(int key, int chunk) {
-  constexpr int R = D / 8, LOG_R = D == 128 ? 4 : 3;
-  const int x = (key / (128 / D)) & (R - 1);
-  return chunk ^ (((x << 1) | (x >> (LOG_R - 1))) & (R - 1));
+  if constexpr (D == 128) {
+    constexpr uint64_t kMask = 0x618d34ea5b2f0c97ull;  // nibble x: mask of rows with key % 16 == x
+    return chunk ^ (int)((kMask >> (4 * (key & 15))) & 15);
+  } else {
+    return chunk ^ (key & 6);
+  }
 }
 
-// NS LDS stages of K and V blocks: NS - 1 blocks are in flight while one is
-// computed.  Two waves per SIMD (the register budget the compiler is held to).
 template <int NS, int DMA>
 __device__ __forceinline__ void wait_blocks_landed(int pending) {
   // at most `pending` later blocks (2 DMA loads per wave each) outstanding

@@ -421,7 +421,7 @@ __global__ __launch_bounds__(256) void gemm_combine(GemmArgs a, const float* par
 constexpr int kTBM = 128, kTBN = 128, kTBK = 64, kTPad = 8;
 constexpr int kTThreads = 256;  // 2 x 2 waves of 64 x 64
 constexpr int kXcds = 8;        // accelerator complex dies of an MI355X, each with its own L2
-constexpr int kTGroupM = 8;
+constexpr int kTGroupM = 4;
 
 template <bool W4, int EPI, bool PK>
 __global__ __launch_bounds__(kTThreads) void gemm_tiled(GemmArgs a) {
