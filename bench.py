@@ -430,6 +430,10 @@ def main():
             kv4 = "true" if wl.kv_fmt == "int4" else "false"
             G = shape.n_heads // hkv
             hp = 1 if G > 1 else (4 if hkv % 4 == 0 else (2 if hkv % 2 == 0 else 1))
+            # fp16 rows: the library narrows workgroups to fewer heads while
+            # that leaves fewer than 1536 of them
+            while kv4 == "false" and hp > 1 and wl.batch * (hkv // hp) < 1536:
+                hp //= 2
             symbols = ([f"attn_decode_kv4_k<{dh}, {hp}>"] if kv4 == "true" and G == 1
                        else [f"attn_decode_k<{dh}, {G}, {hp}, {kv4}>"])
             # with key splits the launch also runs the merge kernel (one

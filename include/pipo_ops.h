@@ -88,7 +88,8 @@ pipo_status pipo_op_layernorm(const float* x, const uint16_t* gamma, const uint1
  * (device, caller-owned, contents arbitrary) of
  * pipo_op_attn_decode_workspace_bytes(b, n_heads, head_dim, t) bytes.  With
  * less (or NULL) the kernel runs unsplit; the result is the same up to
- * rounding.  Calls sharing a workspace must not overlap in time.
+ * rounding.  Calls sharing a workspace must not overlap in time.  The
+ * workspace size covers this call and pipo_op_attn_decode_kv4 alike.
  */
 pipo_status pipo_op_attn_decode(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                                 uint16_t* o, int32_t b, int32_t n_heads, int32_t head_dim,
@@ -104,7 +105,7 @@ int64_t pipo_op_attn_decode_workspace_bytes(int32_t b, int32_t n_heads, int32_t 
  * pipo_op_attn_decode with a sufficient workspace, but the split partials
  * go to one fixed 4 MiB array of the library on each device (held until
  * the process ends) instead of a caller workspace; nothing is allocated.
- * Every shape this kernel accepts needs at most about 3.2 MB of it; a
+ * Every shape this kernel accepts needs at most about 0.8 MB of it; a
  * shape that would need more returns PIPO_ERR_UNSUPPORTED.  All calls on a
  * device share that array, so calls that overlap in time on one device
  * (on different streams, or from several threads) race and must be

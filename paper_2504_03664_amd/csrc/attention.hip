@@ -35,7 +35,8 @@ __device__ __forceinline__ float wave_max(float v) {
 // so each cached row is read from HBM once per step and a key's HP heads
 // are one contiguous HP * D * 2-byte read.  Split z of a (sequence, head
 // group) covers keys [z * chunk, min(T, (z + 1) * chunk)).  A key's head is
-// handled by D/8 lanes (8 dims each); every lane group keeps, per query
+// handled by D/8 lanes (8 dims each; fp16 rows are read with non-temporal
+// loads, as every row is read once); every lane group keeps, per query
 // head, its own online softmax state (running max m, sum l, 8 accumulators)
 // over the keys it visits, two keys at a time so that K and V of both are
 // in flight together (the second one's index is clamped, so the loads are
@@ -109,7 +110,7 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
       scale_min_pairs(*reinterpret_cast<const uint32_t*>(row + sm_off), s2, m2);
       return dequant8(*reinterpret_cast<const uint32_t*>(row + code_off), s2, m2);
     } else {
-      return load_h8(reinterpret_cast<const uint16_t*>(row + code_off));
+      return load_h8_stream(reinterpret_cast<const uint16_t*>(row + code_off));
     }
   };
   const auto visit = [&](h8 kv, h8 vv) {
@@ -624,16 +625,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
 }
 
 // ---------------------------------------------------------------------------
-int attn_decode_heads_per_wg(int n_heads, int n_kv_heads) {
+int attn_decode_heads_per_wg(int b, int n_heads, int n_kv_heads, bool kv4) {
   if (n_heads != n_kv_heads) return 1;
-  return n_heads % 4 == 0 ? 4 : (n_heads % 2 == 0 ? 2 : 1);
+  int hp = n_heads % 4 == 0 ? 4 : (n_heads % 2 == 0 ? 2 : 1);
+  // fp16 rows are bound by HBM: fewer heads per workgroup while that leaves
+  // fewer than kAttnDecodeWideWGs workgroups (six per CU keep more loads in
+  // flight than a longer key loop per wave).  INT4 rows are bound by the
+  // expansion arithmetic, which the wide rows amortise better.
+  if (!kv4)
+    while (hp > 1 && (int64_t)b * (n_heads / hp) < kAttnDecodeWideWGs) hp /= 2;
+  return hp;
 }
 
-int attn_decode_splits(int b, int n_heads, int n_kv_heads, int t) {
+int attn_decode_splits(int b, int n_heads, int n_kv_heads, int t, bool kv4) {
   // at least kAttnDecodeMinWGs workgroups (three per CU: fewer leave HBM
   // idle, more only add merge traffic), at least 64 keys per split
   const int T = t + 1;
-  const int wgs = b * (n_kv_heads / attn_decode_heads_per_wg(n_heads, n_kv_heads));
+  const int wgs = b * (n_kv_heads / attn_decode_heads_per_wg(b, n_heads, n_kv_heads, kv4));
   int S = (kAttnDecodeMinWGs + wgs - 1) / wgs;
   S = std::min(S, std::max(1, T / 64));
   S = std::min(S, kAttnDecodeMaxSplits);
@@ -724,9 +732,9 @@ pipo_status launch_attn_decode(const uint16_t* q, const void* kc, const void* vc
     return PIPO_ERR_UNSUPPORTED;
   }
   const int G = n_heads / n_kv_heads;
-  const int HP = attn_decode_heads_per_wg(n_heads, n_kv_heads);
+  const int HP = attn_decode_heads_per_wg(b, n_heads, n_kv_heads, kv4);
   const int T = t + 1;
-  int S = attn_decode_splits(b, n_heads, n_kv_heads, t);
+  int S = attn_decode_splits(b, n_heads, n_kv_heads, t, kv4);
   if (!workspace || workspace_bytes < attn_decode_workspace_bytes(b, n_heads, head_dim, S)) S = 1;
   const int chunk = (T + S - 1) / S;
   S = (T + chunk - 1) / chunk;
@@ -815,7 +823,7 @@ extern "C" pipo_status pipo_op_attn_decode_noalloc(const uint16_t* q, const uint
     return PIPO_ERR_ARG;
   }
   const int64_t need = pipo::attn_decode_workspace_bytes(
-      b, n_heads, head_dim, pipo::attn_decode_splits(b, n_heads, n_heads, t));
+      b, n_heads, head_dim, pipo::attn_decode_splits(b, n_heads, n_heads, t, false));
   if (need > kScratchBytes) {
     pipo::set_error("attn_decode_noalloc: the split partials need %lld bytes, above the %lld "
                     "bytes of the library's scratch array",

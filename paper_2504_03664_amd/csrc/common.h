@@ -148,9 +148,9 @@ pipo_status launch_swiglu(const uint16_t* gu, uint16_t* h, int64_t M, int64_t F,
 // Query head h reads key/value head h / (n_heads / n_kv_heads); cache rows
 // hold the n_kv_heads heads side by side.
 // heads of a decode-attention workgroup: 4, 2 or 1 adjacent heads without
-// grouping, one key/value head (and its query heads) with it
-int attn_decode_heads_per_wg(int n_heads, int n_kv_heads);
-int attn_decode_splits(int b, int n_heads, int n_kv_heads, int t);
+// grouping, one key/value head (and its query heads) with it; kv4: INT4 rows
+int attn_decode_heads_per_wg(int b, int n_heads, int n_kv_heads, bool kv4);
+int attn_decode_splits(int b, int n_heads, int n_kv_heads, int t, bool kv4);
 int64_t attn_decode_workspace_bytes(int b, int n_heads, int head_dim, int splits);
 // kc, vc: fp16 rows, or INT4 rows (kv4; see kvcache.hip) of the cache
 pipo_status launch_attn_decode(const uint16_t* q, const void* kc, const void* vc, uint16_t* o,
@@ -177,5 +177,6 @@ pipo_status launch_copy16(void* dst, const void* src, int64_t bytes, hipStream_t
 constexpr int kAttnDecodeMaxT = 65536;
 constexpr int kAttnDecodeMaxSplits = 16;
 constexpr int kAttnDecodeMinWGs = 768;
+constexpr int kAttnDecodeWideWGs = 1536;
 
 }  // namespace pipo

@@ -25,6 +25,11 @@ __device__ __forceinline__ uint16_t f2h(float f) {
 __device__ __forceinline__ h8 load_h8(const uint16_t* p) {
   return __builtin_bit_cast(h8, *reinterpret_cast<const u32x4*>(p));
 }
+// a 16-byte load of data read once (a streamed KV-cache row): non-temporal,
+// so it does not displace reused lines from the caches
+__device__ __forceinline__ h8 load_h8_stream(const uint16_t* p) {
+  return __builtin_bit_cast(h8, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+}
 __device__ __forceinline__ h8 zero_h8() { return h8{0, 0, 0, 0, 0, 0, 0, 0}; }
 
 // D = A . B + C for a 16x16 tile with K = 32 (v_mfma_f32_16x16x32_f16).

@@ -193,8 +193,12 @@ pipo_status pipo_op_kv_dequant(const uint8_t* in, uint16_t* y, int64_t rows, int
 int64_t pipo_op_attn_decode_workspace_bytes(int32_t b, int32_t n_heads, int32_t head_dim,
                                             int32_t t) {
   if (b < 1 || n_heads < 1 || t < 0 || head_dim < 1) return 0;
-  return attn_decode_workspace_bytes(b, n_heads, head_dim,
-                                     attn_decode_splits(b, n_heads, n_heads, t));
+  // enough for the fp16 and the INT4 cache (their workgroups differ)
+  return std::max(
+      attn_decode_workspace_bytes(b, n_heads, head_dim,
+                                  attn_decode_splits(b, n_heads, n_heads, t, false)),
+      attn_decode_workspace_bytes(b, n_heads, head_dim,
+                                  attn_decode_splits(b, n_heads, n_heads, t, true)));
 }
 
 pipo_status pipo_op_attn_prefill(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
@@ -227,8 +231,11 @@ pipo_status pipo_op_attn_decode_gqa(const uint16_t* q, const void* kc, const voi
 int64_t pipo_op_attn_decode_gqa_workspace_bytes(int32_t b, int32_t n_heads, int32_t n_kv_heads,
                                                 int32_t head_dim, int32_t t) {
   if (b < 1 || n_heads < 1 || n_kv_heads < 1 || t < 0 || head_dim < 1) return 0;
-  return attn_decode_workspace_bytes(b, n_heads, head_dim,
-                                     attn_decode_splits(b, n_heads, n_kv_heads, t));
+  return std::max(
+      attn_decode_workspace_bytes(b, n_heads, head_dim,
+                                  attn_decode_splits(b, n_heads, n_kv_heads, t, false)),
+      attn_decode_workspace_bytes(b, n_heads, head_dim,
+                                  attn_decode_splits(b, n_heads, n_kv_heads, t, true)));
 }
 
 pipo_status pipo_op_attn_prefill_gqa(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,

@@ -239,8 +239,11 @@ def _attn_inputs(rng, b, T, H, D):
 @pytest.mark.parametrize("b,T,H,D", [(1, 1, 2, 64), (3, 7, 4, 128), (2, 64, 2, 64),
                                      (2, 65, 3, 128), (1, 544, 2, 128), (4, 300, 1, 64),
                                      (2, 2000, 2, 128), (16, 543, 4, 128),
-                                     # 4, 2 and 1 heads per workgroup with key splits
-                                     (3, 600, 56, 128), (5, 129, 6, 64), (2, 700, 5, 128)])
+                                     # one head per workgroup with key splits
+                                     (3, 600, 56, 128), (5, 129, 6, 64), (2, 700, 5, 128),
+                                     # 4 and 2 heads per workgroup (b * H >= 6144, 3072),
+                                     # unsplit
+                                     (112, 40, 56, 128), (56, 41, 56, 128), (60, 33, 52, 64)])
 @pytest.mark.parametrize("split", [False, True])
 def test_attn_decode_vs_oracle(b, T, H, D, split):
     log(f"attn_decode b={b} T={T} H={H} D={D} split={split}")
