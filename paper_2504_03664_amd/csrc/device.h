@@ -25,10 +25,13 @@ __device__ __forceinline__ uint16_t f2h(float f) {
 __device__ __forceinline__ h8 load_h8(const uint16_t* p) {
   return __builtin_bit_cast(h8, *reinterpret_cast<const u32x4*>(p));
 }
-// a 16-byte load of data read once (a streamed KV-cache row): non-temporal,
-// so it does not displace reused lines from the caches
+// 16-byte loads of data read once per pass (streamed weights, KV-cache
+// rows): non-temporal, so they do not displace reused lines from the caches
+__device__ __forceinline__ u32x4 load_u32x4_stream(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
 __device__ __forceinline__ h8 load_h8_stream(const uint16_t* p) {
-  return __builtin_bit_cast(h8, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+  return __builtin_bit_cast(h8, load_u32x4_stream(p));
 }
 __device__ __forceinline__ h8 zero_h8() { return h8{0, 0, 0, 0, 0, 0, 0, 0}; }
 

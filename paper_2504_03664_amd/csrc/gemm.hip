@@ -20,6 +20,8 @@
 //     256 x 256): 8 waves of 128 x 64 fed by global -> LDS loads (no
 //     register staging) over four LDS stages; INT4 codes reach LDS the
 //     same way and are expanded there, once per tile.
+// The decode kernels read each weight once per pass and do so with
+// non-temporal loads.
 // All accumulate in fp32 with v_mfma_f32_16x16x32_f16, and INT4 codes
 // become the same fp16 values (code * scale + min, rounded once) in every
 // kernel.  The kernel, its configuration and the K split depend only on
@@ -118,13 +120,13 @@ struct SkinnyStep {
       const bool ok = n < a.N;
       if constexpr (W4) {
         const int64_t kb = s * 128 + 32 * g;
-        w[f][0] = ok ? *reinterpret_cast<const u32x4*>(a.Wq + w4_byte<PK>(n, kb, K))
+        w[f][0] = ok ? load_u32x4_stream(a.Wq + w4_byte<PK>(n, kb, K))
                      : u32x4{0, 0, 0, 0};
         sm[f] = ok ? *reinterpret_cast<const uint32_t*>(a.Wsm + w4_sm<PK>(n, kb, K) * 2) : 0u;
       } else {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          w[f][i] = ok ? *reinterpret_cast<const u32x4*>(a.W + w16_index<PK>(n, s * 128 + koff(i, g), K))
+          w[f][i] = ok ? load_u32x4_stream(a.W + w16_index<PK>(n, s * 128 + koff(i, g), K))
                        : u32x4{0, 0, 0, 0};
       }
     }
@@ -279,13 +281,13 @@ __global__ __launch_bounds__(KW * 64) void gemm_stream(GemmArgs a, float* part, 
 #pragma unroll
           for (int t = 0; t < KC / 128; ++t) {
             const int64_t blk = (k0 >> 7) + t;
-            F.w[f][t] = *reinterpret_cast<const u32x4*>(wlane[f] + blk * 1024);
+            F.w[f][t] = load_u32x4_stream(wlane[f] + blk * 1024);
             F.sm[f][t] = smlane[f][blk * 32];
           }
         } else {
 #pragma unroll
           for (int i = 0; i < C::kWRegs; ++i)
-            F.w[f][i] = *reinterpret_cast<const u32x4*>(wlane[f] + ((k0 >> 5) + i) * 1024);
+            F.w[f][i] = load_u32x4_stream(wlane[f] + ((k0 >> 5) + i) * 1024);
         }
       }
       return;
@@ -296,13 +298,13 @@ __global__ __launch_bounds__(KW * 64) void gemm_stream(GemmArgs a, float* part, 
 #pragma unroll
         for (int t = 0; t < KC / 128; ++t) {
           const int64_t kb = k0 + 128 * t + 32 * g;
-          F.w[f][t] = *reinterpret_cast<const u32x4*>(a.Wq + w4_byte<PK>(wrow[f], kb, K));
+          F.w[f][t] = load_u32x4_stream(a.Wq + w4_byte<PK>(wrow[f], kb, K));
           F.sm[f][t] = *reinterpret_cast<const uint32_t*>(a.Wsm + w4_sm<PK>(wrow[f], kb, K) * 2);
         }
       } else {
 #pragma unroll
         for (int i = 0; i < C::kWRegs; ++i)
-          F.w[f][i] = *reinterpret_cast<const u32x4*>(a.W + w16_index<PK>(wrow[f], k0 + 32 * i + 8 * g, K));
+          F.w[f][i] = load_u32x4_stream(a.W + w16_index<PK>(wrow[f], k0 + 32 * i + 8 * g, K));
       }
     }
   };

@@ -64,6 +64,7 @@ CASES = {
     "opt-13b-int4-full": dict(widx=2),
     "llama3.1-8b-full": dict(widx=6),
     "llama3.1-8b-int4-full": dict(widx=7),
+    "llama3.1-8b-int4-full-fp16ops": dict(widx=7, reading="fp16ops"),
     "opt-30b-full-r16": dict(widx=3, rows=16),
     "opt-30b-int4-kvhost-full-r16": dict(widx=4, rows=16),
 }
