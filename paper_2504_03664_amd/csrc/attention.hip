@@ -473,7 +473,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   const int h = blockIdx.y, bi = blockIdx.z;
   const int64_t d = (int64_t)H * D, dkv = (int64_t)Hkv * D;
   const int kh = h / (H / Hkv);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index in a scalar register, so that everything derived from
+  // it (the wave's queries, which blocks it masks) is wave-uniform
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 15, g = lane >> 4;
   const int qw = qb * kPQ + wave * 32;       // this wave's first query
   const int nkb = (min(qb * kPQ + kPQ, P) + kPK - 1) / kPK;
@@ -490,17 +492,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   }
 
   // DMA of key block kb into buffer buf: LDS byte p of a block holds row
-  // p / ROWB, chunk slot (p % ROWB) / 16, i.e. cache chunk kv_swz(row, slot)
+  // p / ROWB, chunk slot (p % ROWB) / 16, i.e. cache chunk kv_swz(row, slot).
+  // The block's first row is a wave-uniform address and a lane's offsets
+  // from it do not depend on the block (32-bit: the host checks that a
+  // block of rows spans less than 2^31 elements), so they are computed
+  // once; only a block that reaches past P clamps its rows.
+  const int row_elems = b * (int)dkv;  // elements between positions
+  const uint16_t* kbase = kc + (int64_t)bi * dkv + (int64_t)kh * D;
+  const uint16_t* vbase = vc + (int64_t)bi * dkv + (int64_t)kh * D;
+  int doff[DMA];
+#pragma unroll
+  for (int i = 0; i < DMA; ++i) {
+    const int p = (wave * DMA + i) * 1024 + lane * 16;
+    doff[i] = (p / ROWB) * row_elems + 8 * kv_swz<D>(p / ROWB, (p % ROWB) / 16);
+  }
   const auto issue = [&](int kb, int buf) {
+    const int k0 = kb * kPK;
+    const uint16_t* kblk = kbase + (int64_t)k0 * row_elems;
+    const uint16_t* vblk = vbase + (int64_t)k0 * row_elems;
+    const bool clamp = k0 + kPK > P;
 #pragma unroll
     for (int i = 0; i < DMA; ++i) {
-      const int p = (wave * DMA + i) * 1024 + lane * 16;
-      const int row = p / ROWB, slot = (p % ROWB) / 16;
-      int kp = kb * kPK + row;
-      kp = kp < P ? kp : P - 1;
-      const int64_t off = ((int64_t)kp * b + bi) * dkv + (int64_t)kh * D + 8 * kv_swz<D>(row, slot);
-      lds_dma16(kc + off, &kv[buf][0][(wave * DMA + i) * 1024]);
-      lds_dma16(vc + off, &kv[buf][1][(wave * DMA + i) * 1024]);
+      int off = doff[i];
+      if (clamp) {
+        const int p = (wave * DMA + i) * 1024 + lane * 16, row = p / ROWB;
+        off += (min(k0 + row, P - 1) - (k0 + row)) * row_elems;
+      }
+      lds_dma16(kblk + off, &kv[buf][0][(wave * DMA + i) * 1024]);
+      lds_dma16(vblk + off, &kv[buf][1][(wave * DMA + i) * 1024]);
     }
   };
 
@@ -537,20 +556,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
           s[1][j] = mfma16(kf, qf[1][kk], s[1][j]);
         }
       }
-      const bool edge = k0 + kPK - 1 > qw || k0 + kPK > P;  // the block needs masking
+      // the block needs masking (a wave-uniform test)
+      const bool edge = k0 + kPK - 1 > qw || k0 + kPK > P;
+      if (edge) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int qp = qw + 16 * u + r;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int key = k0 + 16 * j + 4 * g + e;
+              s[u][j][e] = key > qp || key >= P ? -INFINITY : s[u][j][e];
+            }
+        }
+      }
       h8 pf[2][2];  // P^T fragments (B operand) per sub-block and 32-key half
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const int qp = qw + 16 * u + r;
         float bm = -INFINITY;
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int key = k0 + 16 * j + 4 * g + e;
-            if (edge && (key > qp || key >= P)) s[u][j][e] = -INFINITY;
-            bm = fmaxf(bm, s[u][j][e]);
-          }
+          for (int e = 0; e < 4; ++e) bm = fmaxf(bm, s[u][j][e]);
         bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
         bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
         const float mnew = fmaxf(mrow[u], bm);
@@ -571,8 +599,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
         rs += __shfl_xor(rs, 16, 64);
         rs += __shfl_xor(rs, 32, 64);
         lrow[u] = lrow[u] * alpha + rs;
+        // after the first blocks the running maxima rarely grow: rescale
+        // only when some lane's did (alpha is exactly 1 otherwise)
+        if (__any(alpha != 1.f)) {
 #pragma unroll
-        for (int n = 0; n < NF; ++n) oacc[u][n] *= alpha;
+          for (int n = 0; n < NF; ++n) oacc[u][n] *= alpha;
+        }
 #pragma unroll
         for (int hk = 0; hk < 2; ++hk)
 #pragma unroll
@@ -756,6 +788,11 @@ pipo_status launch_attn_prefill(const uint16_t* q, const uint16_t* kc, const uin
     return PIPO_ERR_ARG;
   }
   PIPO_TRY(check_heads("attn_prefill", n_heads, n_kv_heads, head_dim));
+  if ((int64_t)b * n_kv_heads * head_dim * kPK >= ((int64_t)1 << 31)) {
+    set_error("attn_prefill: %d sequences of %d key/value heads of %d: a key block spans 2^31 "
+              "elements or more", b, n_kv_heads, head_dim);
+    return PIPO_ERR_UNSUPPORTED;
+  }
   const dim3 grid((unsigned)((P + kPQ - 1) / kPQ), (unsigned)n_heads, (unsigned)b);
   if (head_dim == 128)
     launch(attn_prefill_k<128, kPrefillStages>, grid, dim3(256), 0, st, q, kc, vc, o, b, P,
