@@ -103,6 +103,10 @@ def gemm_symbols(M, N, K, epi, w4, frag):
     S = 1
     while S < 8 and blocks * 2 * S <= 256 and K % (2 * S * kc) == 0:
         S *= 2
+    # fp16 grids left under 192 workgroups unsplit take 6 waves per workgroup
+    if not w4 and kc == _STREAM_SEL[(w4, mf)][3] and S == 1 and blocks < 192 \
+            and -(-N // (16 * nf * 6)) <= 256:
+        kw = 6
     syms = [f"gemm_stream<{nf}, {mf}, {kw}, {pd}, {b}, {kc}, {epi}, {pk}>(GemmArgs, float*, long)"]
     if S > 1:
         syms.append(f"gemm_combine<{epi}>(GemmArgs, float const*, int)")

@@ -924,8 +924,14 @@ static int stream_splits(int64_t N, int64_t K, int rows_per_wg, int kc) {
   return S;
 }
 
+// fp16 shapes whose unsplit 8-wave grid would leave many CUs idle (under
+// kStreamMinWGs workgroups) take 6 waves per workgroup instead: more
+// workgroups, each output summed by one wave in the same order as before
+constexpr int kStreamNarrowKW = 6;
+constexpr int64_t kStreamMinWGs = 192;
+
 struct StreamPlan {
-  bool fallback;
+  bool fallback, narrow;
   int rows_per_wg, kc, splits;
 };
 
@@ -935,9 +941,18 @@ static StreamPlan stream_plan_mf(int64_t N, int64_t K) {
   using B = StreamFallback<W4, MF>;
   StreamPlan pl;
   pl.fallback = K % P::KC != 0;
+  pl.narrow = false;
   pl.rows_per_wg = pl.fallback ? 16 * B::NF * B::KW : 16 * P::NF * P::KW;
   pl.kc = pl.fallback ? B::KC : P::KC;
   pl.splits = stream_splits(N, K, pl.rows_per_wg, pl.kc);
+  if (!W4 && !pl.fallback && pl.splits == 1) {
+    const int rows6 = 16 * P::NF * kStreamNarrowKW;
+    if ((N + pl.rows_per_wg - 1) / pl.rows_per_wg < kStreamMinWGs &&
+        (N + rows6 - 1) / rows6 <= kStreamMaxWGs) {
+      pl.narrow = true;
+      pl.rows_per_wg = rows6;
+    }
+  }
   return pl;
 }
 
@@ -988,6 +1003,12 @@ static void launch_stream_mf(const GemmArgs& a, const StreamPlan& pl, int S, flo
     launch_stream_cfg<B::NF, MF, B::KW, B::PD, W4, B::KC, EPI, PK>(a, S, ws, st);
   } else {
     using P = StreamSel<W4, MF>;
+    if constexpr (!W4) {
+      if (pl.narrow) {
+        launch_stream_cfg<P::NF, MF, kStreamNarrowKW, P::PD, W4, P::KC, EPI, PK>(a, S, ws, st);
+        return;
+      }
+    }
     launch_stream_cfg<P::NF, MF, P::KW, P::PD, W4, P::KC, EPI, PK>(a, S, ws, st);
   }
 }

@@ -19,7 +19,10 @@ GEMM_SHAPES = [(1, 50, 128), (4, 100, 256), (16, 64, 128), (33, 130, 384), (64, 
                # streaming kernel: K split over workgroups (up to 8 ways), INT4
                # chunk length not dividing K, ragged M and N
                (17, 130, 4096), (32, 200, 2048), (50, 1000, 1280), (100, 300, 640),
-               (128, 1030, 1024), (129, 64, 256)]
+               (128, 1030, 1024), (129, 64, 256),
+               # fp16 streaming grid of 129..191 eight-wave workgroups unsplit:
+               # six waves per workgroup, ragged N
+               (64, 18440, 128)]
 EPIS = [B.PIPO_EPI_F16, B.PIPO_EPI_RELU_F16, B.PIPO_EPI_ADD_F32, B.PIPO_EPI_F32]
 
 
