@@ -137,7 +137,9 @@ pipo_status pipo_op_kv_dequant(const uint8_t* in, uint16_t* y, int64_t rows, int
 /*
  * Causal prefill attention over P positions of b sequences.
  * q: [b][P][d] fp16 (scaled); kc, vc: [>= P][b][d] position-major as
- * above; o: [b][P][d] fp16.  head_dim 64 or 128.
+ * above; o: [b][P][d] fp16.  head_dim 64 or 128.  b * d * 64 (64 cached
+ * positions of every sequence) must stay below 2^31 elements, else
+ * PIPO_ERR_UNSUPPORTED.
  */
 pipo_status pipo_op_attn_prefill(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                                  uint16_t* o, int32_t b, int32_t P, int32_t n_heads,
