@@ -163,3 +163,24 @@ def test_pack_w4_matches_the_layout_definition():
             assert gsm[2 * pair] == sm[n, grp, 0] and gsm[2 * pair + 1] == sm[n, grp, 1]
     with pytest.raises(B.PipoError):
         B.pipo_pack_w4(q[:, :40], sm[:, :1])   # K = 80 is not a multiple of 128
+
+
+def test_attention_workspace_and_limits_without_a_gpu():
+    """Decode-attention workspace sizing and the prefill size limit are host
+    logic: splits only while a grid would have fewer than 768 workgroups, the
+    workspace covers the fp16 and the INT4 cache, and a prefill whose 64-row
+    key block would span 2^31 elements is refused before any launch."""
+    # batch 16, 56 heads: fp16 rows take one head per workgroup (896 of
+    # them, no split), INT4 rows four (224, so 4 splits): sized for the latter
+    assert B.pipo_op_attn_decode_workspace_bytes(16, 56, 128, 543) == 16 * 56 * 4 * 130 * 4
+    # batch 64: 1792 two-head (fp16) or 896 four-head (INT4) workgroups, no split
+    assert B.pipo_op_attn_decode_workspace_bytes(64, 56, 128, 543) == 0
+    assert B.pipo_op_attn_decode_gqa_workspace_bytes(64, 56, 56, 128, 543) == 0
+    # batch 1: keys split, S * (head_dim + 2) floats per head, S <= 16
+    ws = B.pipo_op_attn_decode_workspace_bytes(1, 56, 128, 16383)
+    assert 0 < ws <= 56 * 16 * 130 * 4 and ws % (56 * 130 * 4) == 0
+    # batch 128, 56 heads: 1792 four-head workgroups for either cache, no split
+    assert B.pipo_op_attn_decode_workspace_bytes(128, 56, 128, 543) == 0
+    with pytest.raises(B.PipoError) as e:                 # never dereferenced
+        B.pipo_op_attn_prefill(8, 8, 8, 8, 40000, 1, 56, 128)
+    assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_UNSUPPORTED"
