@@ -82,7 +82,8 @@ pipo_status pipo_op_layernorm(const float* x, const uint16_t* gamma, const uint1
  * Decode attention for b sequences at position t (keys 0..t visible).
  * q: [b][d] fp16 (already scaled by head_dim^-1/2); kc, vc: KV cache
  * [>= t+1][b][d] fp16 (position-major: row p*b + i holds sequence i's key at
- * position p); o: [b][d] fp16.  head_dim 64 or 128, t + 1 <= 65536.
+ * position p); o: [b][d] fp16.  head_dim 64 or 128, t + 1 <= 65536 (beyond:
+ * PIPO_ERR_UNSUPPORTED).
  * When b * n_heads is small the keys are split over several workgroups and
  * a second kernel merges the splits in order; the partials need `workspace`
  * (device, caller-owned, contents arbitrary) of

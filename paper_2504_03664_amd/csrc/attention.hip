@@ -758,6 +758,10 @@ pipo_status launch_attn_decode(const uint16_t* q, const void* kc, const void* vc
     set_error("attn_decode: bad shape b=%d heads=%d t=%d", b, n_heads, t);
     return PIPO_ERR_ARG;
   }
+  if (t >= kAttnDecodeMaxT) {
+    set_error("attn_decode: %d keys, above the %d this kernel takes", t + 1, kAttnDecodeMaxT);
+    return PIPO_ERR_UNSUPPORTED;
+  }
   PIPO_TRY(check_heads("attn_decode", n_heads, n_kv_heads, head_dim));
   if (kv4 && ((int64_t)n_kv_heads * head_dim) % 256 != 0) {
     set_error("attn_decode: INT4 KV rows need a width %% 256 == 0 (%d)", n_kv_heads * head_dim);

@@ -184,3 +184,13 @@ def test_attention_workspace_and_limits_without_a_gpu():
     with pytest.raises(B.PipoError) as e:                 # never dereferenced
         B.pipo_op_attn_prefill(8, 8, 8, 8, 40000, 1, 56, 128)
     assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_UNSUPPORTED"
+
+
+def test_decode_attention_context_limit_without_a_gpu():
+    """t + 1 keys beyond 65536 are refused before any launch (the largest
+    context is run on the GPU in test_gpu_ops.py)."""
+    for fn in (lambda t: B.pipo_op_attn_decode(8, 8, 8, 8, 1, 2, 128, t),
+               lambda t: B.pipo_op_attn_decode_gqa(8, 8, 8, 8, 1, 8, 2, 128, t, B.PIPO_KV_FP16)):
+        with pytest.raises(B.PipoError) as e:
+            fn(65536)
+        assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_UNSUPPORTED"

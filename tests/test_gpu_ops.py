@@ -246,7 +246,9 @@ def _attn_inputs(rng, b, T, H, D):
                                      (3, 600, 56, 128), (5, 129, 6, 64), (2, 700, 5, 128),
                                      # 4 and 2 heads per workgroup (b * H >= 6144, 3072),
                                      # unsplit
-                                     (112, 40, 56, 128), (56, 41, 56, 128), (60, 33, 52, 64)])
+                                     (112, 40, 56, 128), (56, 41, 56, 128), (60, 33, 52, 64),
+                                     # the longest context the kernel takes
+                                     (1, 65536, 2, 128)])
 @pytest.mark.parametrize("split", [False, True])
 def test_attn_decode_vs_oracle(b, T, H, D, split):
     log(f"attn_decode b={b} T={T} H={H} D={D} split={split}")
