@@ -346,7 +346,9 @@ def test_attn_decode_kv4(b, T, H, D, split):
 @pytest.mark.parametrize("b,P,H,D", [(1, 1, 2, 64), (2, 5, 2, 128), (1, 64, 3, 64),
                                      (2, 100, 2, 128), (1, 130, 1, 64), (3, 33, 4, 128),
                                      # several 128-query blocks and 64-key blocks, ragged
-                                     (2, 300, 2, 128), (1, 513, 3, 64), (1, 256, 2, 128)])
+                                     (2, 300, 2, 128), (1, 513, 3, 64), (1, 256, 2, 128),
+                                     # a long prompt: 16 query blocks, 32 key blocks
+                                     (1, 2048, 2, 128)])
 def test_attn_prefill_vs_oracle(b, P, H, D):
     log(f"attn_prefill b={b} P={P} H={H} D={D}")
     rng = np.random.default_rng(P * 3 + b)
