@@ -18,8 +18,8 @@
 //     ordered per XCD so that each XCD's L2 serves a compact block.
 //   * gemm_big_f16 / gemm_big_w4 (prefill with at least 512 tiles of
 //     256 x 256): 8 waves of 128 x 64 fed by global -> LDS loads (no
-//     register staging) over four LDS stages; INT4 codes reach LDS the
-//     same way and are expanded there, once per tile.
+//     register staging) through rings of LDS stages; INT4 codes reach LDS
+//     the same way and are expanded there, once per tile.
 // The decode kernels read each weight once per pass and do so with
 // non-temporal loads.
 // All accumulate in fp32 with v_mfma_f32_16x16x32_f16, and INT4 codes
@@ -580,30 +580,36 @@ __host__ __device__ constexpr int64_t big_tiles(int64_t M, int64_t N) {
 constexpr int kBM = 256, kBN = 256;
 
 // fp16 W (fragment order, or row-major: PK): 8 waves (two per SIMD) of 128 x 64 (8 x 4
-// accumulator fragments), K in stages of 32.  A stage is 16 row blocks of X
-// and 16 of W, each 16 rows x 32 k = 1 KiB in MFMA operand order (lane slot
-// r + 16 g holds row r, k = 8 g .. 8 g + 7), moved from global memory
-// straight into LDS by the load unit (global_load_lds_dwordx4: lane l of a
-// wave writes bytes 16 l .. 16 l + 15 of the block), so fragment reads are
-// one contiguous KiB per wave and free of bank conflicts.  Four LDS stages
-// (128 KiB): stage t is read while t + 1 and t + 2 are in flight and t + 3
-// is issued into the buffer that stage t - 1 left.  Fragment registers are
-// double-buffered: the reads of stage t are spread over the MFMAs of stage
-// t - 1.  Rows past M (and row blocks past N) are loaded from the last
-// valid row and their results dropped.
+// accumulator fragments), K in stages of 32.  Everything moves from global
+// memory straight into LDS by the load unit (global_load_lds_dwordx4: lane
+// l of a wave writes bytes 16 l .. 16 l + 15 of its destination).  A W
+// stage is 16 row blocks of 16 rows x 32 k = 1 KiB in MFMA operand order
+// (lane slot r + 16 g holds row r, k = 8 g .. 8 g + 7), in a ring of four
+// stages; fragment reads are one contiguous KiB per wave.  X moves 64 k at
+// a time: each load covers 8 rows x 128 bytes, whole cache lines of the
+// row-major activations (loads of 16 rows x 64 bytes fetched every line
+// twice, once per 32-k stage), into a ring of three 32 KiB slots where row
+// r of a 16-row block keeps its 16-byte chunk c at position c ^ ((r / 2) %
+// 8), which leaves the fragment reads free of bank conflicts (160 KiB of
+// LDS in all).  Stage t is read while the next two are in flight and the
+// loads of stage t + 3 (W) and of half a 64-k X stage are issued into
+// buffers already read.  Fragment registers are double-buffered: the reads
+// of stage t are spread over the MFMAs of stage t - 1.  Rows past M (and
+// row blocks past N) are loaded from the last valid row and their results
+// dropped.
 constexpr int kFThreads = 512;
-constexpr int kFStage = 32 * 1024;       // bytes per LDS stage: 16 KiB of X, 16 KiB of W
-constexpr int kFStages = 4;
+constexpr int kFStages = 4;              // LDS stages of the INT4 kernel's ring
 
 template <int EPI, bool PK>
 __global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
   constexpr int FM = 8, FN = 4;  // fragments per wave
-  constexpr int BPW = 2;         // X and W row blocks each wave moves per stage
+  constexpr int BPW = 2;         // W row blocks each wave moves per stage
   constexpr int PER_STAGE = 2 * BPW;
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kFStages * kFStage];
+  constexpr int XSLOT = 32 * 1024, XSLOTS = 3, WSLOT = 16 * 1024, WSLOTS = 4;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[XSLOTS * XSLOT + WSLOTS * WSLOT];
+  uint8_t* const xring = lds;
+  uint8_t* const wring = lds + XSLOTS * XSLOT;
   const int tid = threadIdx.x;
-  // the wave index in a scalar register: LDS destinations of the loads are
-  // then scalar and go to M0 without a vector-to-scalar move per load
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 2, wn = wave & 3;
   const int64_t tiles_m = (a.M + kBM - 1) / kBM, tiles_n = (a.N + kBN - 1) / kBN;
@@ -618,45 +624,66 @@ __global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
   const int64_t m0 = (first_m + in_group % gm) * kBM;
   const int64_t n0 = (in_group / gm) * kBN;
   const int64_t K = a.K;
-  const int KT = (int)(K / 32);  // K % 128 == 0: KT is even and >= 4
+  const int KT = (int)(K / 32);
+  const int KS = KT / 2;         // 64-wide X stages
 
   const int r = lane & 15, g = lane >> 4;
-  const uint16_t* asrc[BPW];
+  // X: wave w moves row blocks 2w and 2w + 1, half q (rows 8q .. 8q + 7)
+  // of a 64-k stage per step; lane l takes row 8q + l / 8 and chunk
+  // (l % 8) ^ ((row >> 1) & 7) of the row's 128 bytes
+  const uint16_t* xsrc[2][2];
+#pragma unroll
+  for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int row = 8 * q + (lane >> 3);
+      const int c = (lane & 7) ^ ((row >> 1) & 7);
+      int64_t m = m0 + 16 * (2 * wave + bb) + row;
+      m = m < a.M ? m : a.M - 1;
+      xsrc[bb][q] = a.X + m * K + 8 * c;
+    }
   const uint16_t* bsrc[BPW];
 #pragma unroll
   for (int i = 0; i < BPW; ++i) {
-    int64_t m = m0 + 16 * (BPW * wave + i) + r;
-    m = m < a.M ? m : a.M - 1;
-    asrc[i] = a.X + m * K + 8 * g;
-    if constexpr (PK) {  // the block is 1 KiB contiguous in W
+    if constexpr (PK) {
       int64_t nb = (n0 >> 4) + BPW * wave + i;
       nb = nb < (a.N >> 4) ? nb : (a.N >> 4) - 1;
       bsrc[i] = a.W + nb * (K >> 5) * 512 + lane * 8;
-    } else {             // gathered from 16 rows, like X
+    } else {
       int64_t n = n0 + 16 * (BPW * wave + i) + r;
       n = n < a.N ? n : a.N - 1;
       bsrc[i] = a.W + n * K + 8 * g;
     }
   }
-  constexpr int kBStep = PK ? 512 : 32;  // halves between the stages of a W block
-  // stage `src` of K into LDS buffer `buf` % kFStages
-  const auto issue = [&](int src, int buf) {
-    uint8_t* st = lds + (buf % kFStages) * kFStage;
+  constexpr int kBStep = PK ? 512 : 32;
+  // step u issues W stage u + 3 and half u & 1 of X stage (u >> 1) + 2
+  // (arithmetic shift: u = -4 .. -1 are the prologue)
+  const auto issue = [&](int u) {
+    if (u >= -3) {
+      const int ws = u + 3 < KT ? u + 3 : KT - 1;
+      uint8_t* st = wring + ((u + 3) % WSLOTS) * WSLOT;
 #pragma unroll
-    for (int i = 0; i < BPW; ++i) {
-      const int b = BPW * wave + i;
-      lds_dma16(asrc[i] + src * 32, st + b * 1024);
-      lds_dma16(bsrc[i] + src * kBStep, st + 16 * 1024 + b * 1024);
+      for (int i = 0; i < BPW; ++i)
+        lds_dma16(bsrc[i] + ws * kBStep, st + (BPW * wave + i) * 1024);
     }
+    const int s = (u >> 1) + 2, q = u & 1;
+    const int sc = s < KS ? s : KS - 1;
+    uint8_t* xs = xring + (s % XSLOTS) * XSLOT;
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+      lds_dma16(xsrc[bb][q] + sc * 64, xs + (2 * wave + bb) * 2048 + q * 1024);
   };
   const auto read = [&](int t, h8 (&fa)[FM], h8 (&fb)[FN]) {
-    const uint8_t* st = lds + (t % kFStages) * kFStage;
+    const uint8_t* ws = wring + (t % WSLOTS) * WSLOT;
 #pragma unroll
     for (int j = 0; j < FN; ++j)
-      fb[j] = *reinterpret_cast<const h8*>(st + 16 * 1024 + (FN * wn + j) * 1024 + lane * 16);
+      fb[j] = *reinterpret_cast<const h8*>(ws + (FN * wn + j) * 1024 + lane * 16);
+    const uint8_t* xs = xring + ((t >> 1) % XSLOTS) * XSLOT;
+    const int c = (g + 4 * (t & 1)) ^ ((r >> 1) & 7);
+    const int off = (r >> 3) * 1024 + (r & 7) * 128 + 16 * c;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
-      fa[i] = *reinterpret_cast<const h8*>(st + (FM * wm + i) * 1024 + lane * 16);
+      fa[i] = *reinterpret_cast<const h8*>(xs + (FM * wm + i) * 2048 + off);
   };
   f4 acc[FM][FN];
 #pragma unroll
@@ -669,23 +696,15 @@ __global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < FN; ++j) acc[i][j] = mfma16(fa[i], fb[j], acc[i][j]);
   };
-  // Every step issues one stage (past the last, a repeat of it into the
-  // buffer just freed), so the wait count is the same in every step.
-  // Step t: stage t landed in every wave's view (two stages after it may be
-  // in flight) and every wave's reads of stage t - 1 are done; stage t + 3
-  // goes into t - 1's buffer; stage t is read while stage t - 1's MFMAs run.
   h8 fa0[FM], fb0[FN], fa1[FM], fb1[FN];
   const auto step = [&](int t, h8 (&ra)[FM], h8 (&rb)[FN], h8 (&ca)[FM], h8 (&cb)[FN]) {
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(waitcnt_imm(2 * PER_STAGE, true));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    issue(t + 3 < KT ? t + 3 : KT - 1, t + 3);
+    issue(t);
     read(t, ra, rb);
     mma(ca, cb);
-    // two MFMAs, then one of the loads, four times, so that the MFMA pipe
-    // restarts right after the barrier and the loads' address arithmetic
-    // hides behind MFMAs; then one fragment read and two MFMAs, in turn
 #pragma unroll
     for (int k = 0; k < PER_STAGE; ++k) {
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
@@ -698,12 +717,14 @@ __global__ __launch_bounds__(kFThreads) void gemm_big_f16(GemmArgs a) {
     }
     __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - 2 * PER_STAGE - 2 * (FM + FN), 0);
   };
-  issue(0, 0);
-  issue(1, 1);
-  issue(2, 2);
+  issue(-4);  // X stage 0, rows 0-7 of each block (no W)
+  issue(-3);
+  issue(-2);
+  issue(-1);
+  // W stage 0 and both halves of X stage 0 landed (steps -2, -1 may be in flight)
   __builtin_amdgcn_s_waitcnt(waitcnt_imm(2 * PER_STAGE, true));
   __builtin_amdgcn_s_barrier();
-  issue(3, 3);
+  issue(0);
   read(0, fa0, fb0);
   int t = 1;
   for (; t < KT - 1; t += 2) {
