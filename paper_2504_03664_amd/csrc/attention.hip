@@ -434,6 +434,17 @@ __device__ __forceinline__ int kv_swz(int key, int chunk) {
   }
 }
 
+// the pair of values that v_permlane16/32_swap leave in a lane: its own
+// and that of the lane 16 (32) apart, in either order
+template <typename P>
+__device__ __forceinline__ float pair_max(P p) {
+  return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+}
+template <typename P>
+__device__ __forceinline__ float pair_sum(P p) {
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+
 template <int NS, int DMA>
 __device__ __forceinline__ void wait_blocks_landed(int pending) {
   // at most `pending` later blocks (2 DMA loads per wave each) outstanding
@@ -579,8 +590,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
         for (int j = 0; j < 4; ++j)
 #pragma unroll
           for (int e = 0; e < 4; ++e) bm = fmaxf(bm, s[u][j][e]);
-        bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
-        bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+        bm = pair_max(__builtin_amdgcn_permlane16_swap(__float_as_uint(bm), __float_as_uint(bm), false, false));
+        bm = pair_max(__builtin_amdgcn_permlane32_swap(__float_as_uint(bm), __float_as_uint(bm), false, false));
         const float mnew = fmaxf(mrow[u], bm);
         // every query row has a visible key in its first block, so mnew is finite
         const float alpha = exp2f((mrow[u] - mnew) * kLog2e);
@@ -596,8 +607,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
             s[u][j][e] = p;
             rs += p;
           }
-        rs += __shfl_xor(rs, 16, 64);
-        rs += __shfl_xor(rs, 32, 64);
+        rs = pair_sum(__builtin_amdgcn_permlane16_swap(__float_as_uint(rs), __float_as_uint(rs), false, false));
+        rs = pair_sum(__builtin_amdgcn_permlane32_swap(__float_as_uint(rs), __float_as_uint(rs), false, false));
         lrow[u] = lrow[u] * alpha + rs;
         // after the first blocks the running maxima rarely grow: rescale
         // only when some lane's did (alpha is exactly 1 otherwise)
