@@ -28,6 +28,24 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Sum over aligned groups of N <= 16 lanes with DPP moves inside a row of 16
+// lanes (swap neighbours, swap pairs, mirror within 8, mirror within 16):
+// ALU operations instead of the LDS round trips of lane shuffles.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __uint_as_float(
+      __builtin_amdgcn_update_dpp(0u, __float_as_uint(v), CTRL, 0xF, 0xF, false));
+}
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(N == 1 || N == 2 || N == 4 || N == 8 || N == 16, "groups of up to 16 lanes");
+  if constexpr (N >= 2) v += dpp_move<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  if constexpr (N >= 4) v += dpp_move<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  if constexpr (N >= 8) v += dpp_move<0x141>(v);  // row_half_mirror
+  if constexpr (N >= 16) v += dpp_move<0x140>(v); // row_mirror
+  return v;
+}
+
 // ---------------------------------------------------------------------------
 // decode: grid (key/value head groups, b, splits), 256 threads.  A workgroup
 // serves HP adjacent key/value heads of one sequence and the G = H / Hkv
@@ -120,7 +138,7 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
       kf[i] = (float)kv[i];
       vf[i] = (float)vv[i];
     }
-    if constexpr (G == 1) {  // bound by HBM: the plain update
+    if constexpr (G == 1) {  // bound by HBM: the plain update (DPP sums measured no faster)
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < 8; ++i) s += qf[0][i] * kf[i];
@@ -141,8 +159,7 @@ __global__ __launch_bounds__(256) void attn_decode_k(const uint16_t* __restrict_
         float s = 0.f;
 #pragma unroll
         for (int i = 0; i < 8; ++i) s += qf[g][i] * kf[i];
-#pragma unroll
-        for (int off = LPP / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+        s = group_sum<LPP>(s);
         const float mn = fmaxf(m[g], s);
         // hardware exp2; m = -inf on the first key gives alpha = 0
         alpha[g] = __builtin_amdgcn_exp2f((m[g] - mn) * kLog2e);
@@ -294,8 +311,7 @@ __global__ __launch_bounds__(256) void attn_decode_kv4_k(const uint16_t* __restr
       for (int u = 0; u < 4; ++u)
         s = __builtin_amdgcn_fdot2(
             qh[4 * j + u], dequant_pair((kr.codes[j] >> (4 * u)) & 0x000F000Fu, ks, km), s, false);
-#pragma unroll
-    for (int off = LPP / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+    s = group_sum<LPP>(s);
     const float mn = fmaxf(m, s);
     // m = -inf on the first key: exp2(-inf) = 0
     const float alpha = __builtin_amdgcn_exp2f((m - mn) * kLog2e);
