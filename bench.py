@@ -109,7 +109,8 @@ def gemm_symbols(M, N, K, epi, w4, frag):
         kw = 6
     syms = [f"gemm_stream<{nf}, {mf}, {kw}, {pd}, {b}, {kc}, {epi}, {pk}>(GemmArgs, float*, long)"]
     if S > 1:
-        syms.append(f"gemm_combine<{epi}>(GemmArgs, float const*, int)")
+        # four columns per thread when N allows (the engine's partials are aligned)
+        syms.append(f"gemm_combine<{epi}, {S}, {4 if N % 4 == 0 else 1}>(GemmArgs, float const*)")
     return syms
 
 

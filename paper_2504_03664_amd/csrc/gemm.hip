@@ -407,15 +407,55 @@ __global__ __launch_bounds__(KW * 64) void gemm_stream(GemmArgs a, float* part, 
       }
 }
 
-// out = sum over z = 0 .. S-1 (in that order) of part[z], then the epilogue
-template <int EPI>
-__global__ __launch_bounds__(256) void gemm_combine(GemmArgs a, const float* part, int S) {
+// out = sum over z = 0 .. S-1 (in that order, from 0) of part[z], then the
+// epilogue.  A thread takes V adjacent columns of one row (V = 4 when N is a
+// multiple of 4 and the partials are 16-byte aligned) and issues the loads
+// of all S partials before the first add; M * N < 2^31 (checked by the host).
+template <int EPI, int S, int V>
+__global__ __launch_bounds__(256) void gemm_combine(GemmArgs a, const float* __restrict__ part) {
+  const int NV = (int)(a.N / V);
+  const int q = (int)blockIdx.x * 256 + (int)threadIdx.x;
+  if (q >= (int)a.M * NV) return;
+  const int m = q / NV, n = (q - m * NV) * V;
   const int64_t MN = a.M * a.N;
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= MN) return;
-  float sum = 0.f;
-  for (int z = 0; z < S; ++z) sum += part[z * MN + e];
-  epilogue<EPI>(a, e / a.N, e % a.N, sum);
+  const float* p = part + (int64_t)m * a.N + n;
+  float v[S][V];
+#pragma unroll
+  for (int z = 0; z < S; ++z) {
+    if constexpr (V == 4) {
+      const f4 t = *reinterpret_cast<const f4*>(p + z * MN);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[z][j] = t[j];
+    } else {
+      v[z][0] = p[z * MN];
+    }
+  }
+  const EpiRow row = epilogue_row<EPI>(a, m);
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    float sum = 0.f;
+#pragma unroll
+    for (int z = 0; z < S; ++z) sum += v[z][j];
+    epilogue_store<EPI>(a, row, n + j, sum + epilogue_bias(a, n + j));
+  }
+}
+
+template <int EPI, int V>
+static void launch_combine_v(const GemmArgs& a, const float* ws, int S, hipStream_t st) {
+  const dim3 grid((unsigned)((a.M * (a.N / V) + 255) / 256));
+  switch (S) {
+    case 2: launch((gemm_combine<EPI, 2, V>), grid, dim3(256), 0, st, a, ws); break;
+    case 4: launch((gemm_combine<EPI, 4, V>), grid, dim3(256), 0, st, a, ws); break;
+    default: launch((gemm_combine<EPI, 8, V>), grid, dim3(256), 0, st, a, ws); break;
+  }
+}
+
+template <int EPI>
+static void launch_combine(const GemmArgs& a, const float* ws, int S, hipStream_t st) {
+  if (a.N % 4 == 0 && reinterpret_cast<uintptr_t>(ws) % 16 == 0)
+    launch_combine_v<EPI, 4>(a, ws, S, st);
+  else
+    launch_combine_v<EPI, 1>(a, ws, S, st);
 }
 
 // ---------------------------------------------------------------------------
@@ -1009,11 +1049,7 @@ static void launch_stream_cfg(const GemmArgs& a, int S, float* ws, hipStream_t s
   const dim3 grid((unsigned)((a.N + rows - 1) / rows), (unsigned)S);
   launch((gemm_stream<NF, MF, KW, PD, W4, KC, EPI, PK>), grid, dim3(KW * 64), 0, st, a, ws,
          a.K / S);
-  if (S > 1) {
-    const int64_t MN = a.M * a.N;
-    launch((gemm_combine<EPI>), dim3((unsigned)((MN + 255) / 256)), dim3(256), 0, st, a,
-           (const float*)ws, S);
-  }
+  if (S > 1) launch_combine<EPI>(a, ws, S, st);
 }
 
 template <bool W4, int MF, int EPI, bool PK>
@@ -1046,7 +1082,7 @@ static pipo_status launch_epi(const GemmArgs& a, float* ws, int64_t ws_bytes, hi
   } else if (a.M <= kStreamMaxM) {
     const StreamPlan pl = stream_plan(a.M, a.N, a.K, W4);
     // without room for the partial sums the K split is dropped
-    const int S = (pl.splits > 1 && ws != nullptr &&
+    const int S = (pl.splits > 1 && ws != nullptr && a.M * a.N < ((int64_t)1 << 31) &&
                    ws_bytes >= (int64_t)pl.splits * a.M * a.N * 4) ? pl.splits : 1;
     switch (stream_mf(a.M)) {
       case 2: launch_stream_mf<W4, 2, EPI, PK>(a, pl, S, ws, st); break;
