@@ -195,6 +195,38 @@ def test_gemm_deterministic_and_split_consistent(M, w4):
         assert np.array_equal(got.view(np.uint32), unsplit[:, n0:n1].view(np.uint32))
 
 
+@pytest.mark.parametrize("w4", [False, True])
+def test_gemm_split_merge_workspace_alignment(w4):
+    """The K-split merge reads four partial columns at a time from a 16-byte
+    aligned workspace and one at a time otherwise: a workspace 4 bytes off
+    that alignment gives the same bits."""
+    log(f"gemm split merge alignment w4={w4}")
+    rng = np.random.default_rng(11)
+    M, N, K = 40, 1024, 2048
+    X = rng.standard_normal((M, K)).astype(np.float16)
+    W = (rng.standard_normal((N, K)) * 0.05).astype(np.float16)
+    wfmt = B.PIPO_W_INT4_G64 if w4 else B.PIPO_W_FP16
+    ws_bytes = B.pipo_op_gemm_workspace_bytes(M, N, K, wfmt)
+    assert ws_bytes > 0
+    dX, dO = DB.from_array(X), DB(M * N * 4)
+    dWs = DB(ws_bytes + 256)
+    if w4:
+        q, sm = synth.quant_int4_g64(W)
+        dq, dsm = DB.from_array(q), DB.from_array(sm)
+        call = lambda ws: B.pipo_op_gemm_w4(dX.ptr, dq.ptr, dsm.ptr, None, dO.ptr, M, N, K,
+                                            B.PIPO_EPI_F32, ws, ws_bytes)
+    else:
+        dW = DB.from_array(W)
+        call = lambda ws: B.pipo_op_gemm_f16(dX.ptr, dW.ptr, None, dO.ptr, M, N, K,
+                                             B.PIPO_EPI_F32, ws, ws_bytes)
+    outs = []
+    for off in (0, 4):
+        call(dWs.ptr + off)
+        B.pipo_dev_synchronize()
+        outs.append(dO.to_array(np.float32, (M, N)))
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+
+
 def test_attention_workspace_reuse():
     """Repeated split calls on one workspace give identical results."""
     log("attention workspace reuse")
