@@ -121,7 +121,10 @@ def measured_traffic(workload_name, symbols, optional=()):
     `symbols` is missing from it, or the kernel sources changed since it was
     taken.  Returns (bytes, summary path, the kernels counted)."""
     import hashlib
-    tag = workload_name.split()[0] + "_" + workload_name.split()[1]
+    # model and batch, plus where the KV cache lives and its format (a disk
+    # tier runs the kernels of the same workload without it)
+    toks = workload_name.split()
+    tag = "_".join(toks[:2] + [t for t in toks[2:] if t in ("kv-host", "kv-int4")])
     path = os.path.join(ROOT, "profiles", f"hbm_traffic_{tag}.json")
     if not os.path.exists(path):
         return None, None, list(symbols)
