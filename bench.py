@@ -89,7 +89,8 @@ def gemm_symbols(M, N, K, epi, w4, frag):
     b = "true" if w4 else "false"
     pk = "true" if frag else "false"
     if M <= 16:
-        nf = 4 if N >= 64 * 192 else 1
+        # (the SwiGLU epilogue, 5, always pairs two gate and two up fragments)
+        nf = 4 if N >= 64 * 192 or epi == 5 else 1
         return [f"gemm_skinny<{nf}, 1, 8, 2, {b}, {epi}, {pk}>(GemmArgs)"]
     if -(-M // 256) * -(-N // 256) >= 512:
         return [f"gemm_big_w4<{epi}, {pk}>(GemmArgs)" if w4 else f"gemm_big_f16<{epi}, {pk}>(GemmArgs)"]
@@ -397,7 +398,9 @@ def main():
         llama = getattr(shape, "family", "opt") == "llama"
         # LLaMA: FC1 is the gate/up GEMM (fp16 out) followed by the SwiGLU kernel,
         # QKV is followed by the rotary kernel
-        fc1_label = f"{gemm}<f16>+swiglu (fc1)" if llama else f"{gemm}<relu_f16> (fc1)"
+        # (at batch <= 16 the SwiGLU gate runs in the GEMM's epilogue)
+        fc1_label = ((f"{gemm}<swiglu> (fc1)" if wl.batch <= 16 else f"{gemm}<f16>+swiglu (fc1)")
+                     if llama else f"{gemm}<relu_f16> (fc1)")
         qkv_label = f"{gemm}<qkv>+rope (qkv)" if llama else f"{gemm}<qkv> (qkv)"
         families = {f"{gemm}<add_f32> (oproj+fc2)": ("oproj_decode", "fc2_decode"),
                     fc1_label: ("fc1_decode",),
@@ -422,7 +425,7 @@ def main():
         else:
             ach = ks["alg_bytes"] / (ks["total_ms"] * 1e-3) / 1e9
             peak, unit = HBM_PEAK_GBPS, "GB/s"
-        epi = {"oproj": 2, "fc1": 0 if llama else 1, "qkv": 4, "head": 3}
+        epi = {"oproj": 2, "fc1": (5 if wl.batch <= 16 else 0) if llama else 1, "qkv": 4, "head": 3}
         fam_key = name.split("(")[1].split("+")[0].rstrip(")")
         symbols, symbols_opt = None, []
         d, F, dh = shape.d_model, shape.d_ffn, shape.d_model // shape.n_heads

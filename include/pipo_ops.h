@@ -28,8 +28,17 @@ pipo_status pipo_dev_synchronize(void);
  *   PIPO_EPI_RELU_F16:  out_f16[m][n] = max(acc + bias[n], 0)
  *   PIPO_EPI_ADD_F32:   out_f32[m][n] += acc + bias[n]     (residual stream)
  *   PIPO_EPI_F32:       out_f32[m][n] = acc + bias[n]      (logits)
- * bias may be NULL (treated as 0). */
-enum { PIPO_EPI_F16 = 0, PIPO_EPI_RELU_F16 = 1, PIPO_EPI_ADD_F32 = 2, PIPO_EPI_F32 = 3 };
+ * bias may be NULL (treated as 0).
+ *   PIPO_EPI_SWIGLU:    the gated MLP's SwiGLU (LLaMA): W stacks the gate rows
+ *                       [0, F) over the up rows [F, 2F) (N = 2F, even), bias
+ *                       must be NULL, out_f16 has F columns (row stride F):
+ *                       out_f16[m][i] = silu(g) * u in fp32, rounded once, with
+ *                       g = fp16(acc of row i), u = fp16(acc of row F + i),
+ *                       silu(g) = g / (1 + exp(-g)); the same values as
+ *                       PIPO_EPI_F16 followed by pipo_op_swiglu.  Only for
+ *                       M <= 16 (else PIPO_ERR_UNSUPPORTED). */
+enum { PIPO_EPI_F16 = 0, PIPO_EPI_RELU_F16 = 1, PIPO_EPI_ADD_F32 = 2, PIPO_EPI_F32 = 3,
+       PIPO_EPI_SWIGLU = 5 };
 
 /*
  * Y = X . W^T with the chosen epilogue (the projections of a layer and the

@@ -88,6 +88,7 @@ enum : int {
   EPI_ADD_F32 = PIPO_EPI_ADD_F32,
   EPI_F32 = PIPO_EPI_F32,
   EPI_QKV = 4,  // q (scaled) to q_out, k and v rows into a position-major KV cache
+  EPI_SWIGLU = PIPO_EPI_SWIGLU,  // gate and up rows stacked in W; silu(g) * u to out16
 };
 
 struct GemmArgs {

@@ -563,6 +563,11 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
     case kFc1: {
       GemmArgs ga;
       if (c->llama) {  // gate and up in one GEMM, then the SwiGLU gate
+        if (rows <= 16) {  // decode: the gate in the GEMM's epilogue, same values
+          ga.out16 = c->h;
+          ga.ldo = F;
+          return gemm(kSegW1, c->a, nullptr, rows, 2 * F, d, EPI_SWIGLU, ga);
+        }
         ga.out16 = c->gu;
         ga.ldo = 2 * F;
         PIPO_TRY(gemm(kSegW1, c->a, nullptr, rows, 2 * F, d, EPI_F16, ga));
@@ -628,7 +633,10 @@ static void kernel_cost(const pipo_ctx* c, const Op& op, double* bytes, double* 
     case kFc1:
       if (c->llama) {
         g(rows, 2 * F, d, 2, wbytes(2 * F, d));
-        *bytes += rows * F * 6;  // SwiGLU: read gate and up, write h
+        if (rows <= 16)
+          *bytes -= rows * F * 2;  // SwiGLU in the epilogue: h (F columns) written instead
+        else
+          *bytes += rows * F * 6;  // SwiGLU: read gate and up, write h
       } else {
         g(rows, F, d, 2, wbytes(F, d));
       }

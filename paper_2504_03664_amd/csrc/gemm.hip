@@ -112,11 +112,13 @@ struct SkinnyStep {
 
   __device__ __forceinline__ static int koff(int i, int g) { return W4 ? 32 * g + 8 * i : 32 * i + 8 * g; }
 
-  __device__ __forceinline__ void load(const GemmArgs& a, int64_t n0, int64_t s, int r, int g) {
+  // nb[f]: the first W row of fragment f
+  __device__ __forceinline__ void load(const GemmArgs& a, const int64_t (&nb)[NF], int64_t s,
+                                       int r, int g) {
     const int64_t K = a.K;
 #pragma unroll
     for (int f = 0; f < NF; ++f) {
-      const int64_t n = n0 + 16 * f + r;
+      const int64_t n = nb[f] + r;
       const bool ok = n < a.N;
       if constexpr (W4) {
         const int64_t kb = s * 128 + 32 * g;
@@ -166,8 +168,20 @@ __global__ __launch_bounds__(KW * 64) void gemm_skinny(GemmArgs a) {
   __shared__ f4 red[KW][NF][MF][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
+  static_assert(EPI != EPI_SWIGLU || NF % 2 == 0, "SwiGLU pairs gate and up fragments");
   const int64_t n0 = (int64_t)blockIdx.x * (16 * NF);
   const int64_t nsteps = a.K / 128;
+  // fragment f's first W row: 16 NF consecutive rows, or with EPI_SWIGLU the
+  // gate rows h0 .. h0 + 8 NF - 1 and the up rows F + h0 .. (F = N / 2)
+  const int64_t h0 = (int64_t)blockIdx.x * (8 * NF);
+  int64_t nb[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    if constexpr (EPI == EPI_SWIGLU)
+      nb[f] = f < NF / 2 ? h0 + 16 * f : a.N / 2 + h0 + 16 * (f - NF / 2);
+    else
+      nb[f] = n0 + 16 * f;
+  }
 
   f4 acc[NF][MF];
 #pragma unroll
@@ -179,7 +193,7 @@ __global__ __launch_bounds__(KW * 64) void gemm_skinny(GemmArgs a) {
     SkinnyStep<NF, MF, KW, UNR, W4, PK> st[UNR];
 #pragma unroll
     for (int u = 0; u < UNR; ++u)
-      if (s + u * KW < nsteps) st[u].load(a, n0, s + u * KW, r, g);
+      if (s + u * KW < nsteps) st[u].load(a, nb, s + u * KW, r, g);
 #pragma unroll
     for (int u = 0; u < UNR; ++u)
       if (s + u * KW < nsteps) st[u].mma(acc);
@@ -191,15 +205,38 @@ __global__ __launch_bounds__(KW * 64) void gemm_skinny(GemmArgs a) {
     for (int mf = 0; mf < MF; ++mf) red[wave][f][mf][lane] = acc[f][mf];
   __syncthreads();
 
-  // element (f, mf, lane', j): W row n0 + 16 f + 4 (lane' / 16) + j, X row 16 mf + lane' % 16
-  constexpr int kElems = NF * MF * 64 * 4;
-  for (int e = threadIdx.x; e < kElems; e += KW * 64) {
-    const int j = e & 3, ln = (e >> 2) & 63, fm = e >> 8;
-    const int f = fm / MF, mf = fm % MF;
-    float sum = 0.f;
+  if constexpr (EPI == EPI_SWIGLU) {
+    // element (f < NF / 2, mf, lane', j): output column h0 + 16 f + 4 (lane' / 16) + j
+    // from the gate sum of fragment f and the up sum of fragment f + NF / 2,
+    // each rounded to fp16 as a separate GEMM output would be
+    constexpr int kElems = NF / 2 * MF * 64 * 4;
+    const int64_t F = a.N / 2;
+    for (int e = threadIdx.x; e < kElems; e += KW * 64) {
+      const int j = e & 3, ln = (e >> 2) & 63, fm = e >> 8;
+      const int f = fm / MF, mf = fm % MF;
+      float gs = 0.f, us = 0.f;
 #pragma unroll
-    for (int w = 0; w < KW; ++w) sum += red[w][f][mf][ln][j];
-    epilogue<EPI>(a, 16 * mf + (ln & 15), n0 + 16 * f + 4 * (ln >> 4) + j, sum);
+      for (int w = 0; w < KW; ++w) {
+        gs += red[w][f][mf][ln][j];
+        us += red[w][f + NF / 2][mf][ln][j];
+      }
+      const int64_t m = 16 * mf + (ln & 15), i = h0 + 16 * f + 4 * (ln >> 4) + j;
+      if (m < a.M && i < F) {
+        const float gv = h2f(f2h(gs + 0.f)), uv = h2f(f2h(us + 0.f));
+        a.out16[m * a.ldo + i] = f2h(gv / (1.f + expf(-gv)) * uv);
+      }
+    }
+  } else {
+    // element (f, mf, lane', j): W row n0 + 16 f + 4 (lane' / 16) + j, X row 16 mf + lane' % 16
+    constexpr int kElems = NF * MF * 64 * 4;
+    for (int e = threadIdx.x; e < kElems; e += KW * 64) {
+      const int j = e & 3, ln = (e >> 2) & 63, fm = e >> 8;
+      const int f = fm / MF, mf = fm % MF;
+      float sum = 0.f;
+#pragma unroll
+      for (int w = 0; w < KW; ++w) sum += red[w][f][mf][ln][j];
+      epilogue<EPI>(a, 16 * mf + (ln & 15), n0 + 16 * f + 4 * (ln >> 4) + j, sum);
+    }
   }
 }
 
@@ -1072,38 +1109,50 @@ static void launch_stream_mf(const GemmArgs& a, const StreamPlan& pl, int S, flo
 
 template <bool W4, int EPI, bool PK>
 static pipo_status launch_epi(const GemmArgs& a, float* ws, int64_t ws_bytes, hipStream_t st) {
-  if (a.M <= 16) {
-    // 64 W rows per workgroup (less X traffic per W byte) once that still
-    // gives enough workgroups to fill the chip, else 16
-    if (a.N >= 64 * 192)
-      launch_skinny<4, W4, EPI, PK>(a, st);
-    else
-      launch_skinny<1, W4, EPI, PK>(a, st);
-  } else if (a.M <= kStreamMaxM) {
-    const StreamPlan pl = stream_plan(a.M, a.N, a.K, W4);
-    // without room for the partial sums the K split is dropped
-    const int S = (pl.splits > 1 && ws != nullptr && a.M * a.N < ((int64_t)1 << 31) &&
-                   ws_bytes >= (int64_t)pl.splits * a.M * a.N * 4) ? pl.splits : 1;
-    switch (stream_mf(a.M)) {
-      case 2: launch_stream_mf<W4, 2, EPI, PK>(a, pl, S, ws, st); break;
-      case 4: launch_stream_mf<W4, 4, EPI, PK>(a, pl, S, ws, st); break;
-      default: launch_stream_mf<W4, 8, EPI, PK>(a, pl, S, ws, st); break;
+  if constexpr (EPI == EPI_SWIGLU) {
+    (void)ws;
+    (void)ws_bytes;
+    if (a.M > 16) {
+      set_error("gemm: the SwiGLU epilogue needs M <= 16 (M=%lld)", (long long)a.M);
+      return PIPO_ERR_UNSUPPORTED;
     }
-  } else if (big_tiles(a.M, a.N) >= kBigMinTiles) {
-    const int64_t per_xcd = (big_tiles(a.M, a.N) + kXcds - 1) / kXcds;
-    const dim3 grid((unsigned)(per_xcd * kXcds));
-    if constexpr (W4)
-      launch((gemm_big_w4<EPI, PK>), grid, dim3(kFThreads), 0, st, a);
-    else
-      launch((gemm_big_f16<EPI, PK>), grid, dim3(kFThreads), 0, st, a);
+    launch_skinny<4, W4, EPI, PK>(a, st);
+    PIPO_HIP_TRY(hipGetLastError());
+    return PIPO_OK;
   } else {
-    const int64_t total = ((a.N + kTBN - 1) / kTBN) * ((a.M + kTBM - 1) / kTBM);
-    const int64_t per_xcd = (total + kXcds - 1) / kXcds;
-    launch((gemm_tiled<W4, EPI, PK>), dim3((unsigned)(per_xcd * kXcds)), dim3(kTThreads), 0, st,
-           a);
+    if (a.M <= 16) {
+      // 64 W rows per workgroup (less X traffic per W byte) once that still
+      // gives enough workgroups to fill the chip, else 16
+      if (a.N >= 64 * 192)
+        launch_skinny<4, W4, EPI, PK>(a, st);
+      else
+        launch_skinny<1, W4, EPI, PK>(a, st);
+    } else if (a.M <= kStreamMaxM) {
+      const StreamPlan pl = stream_plan(a.M, a.N, a.K, W4);
+      // without room for the partial sums the K split is dropped
+      const int S = (pl.splits > 1 && ws != nullptr && a.M * a.N < ((int64_t)1 << 31) &&
+                     ws_bytes >= (int64_t)pl.splits * a.M * a.N * 4) ? pl.splits : 1;
+      switch (stream_mf(a.M)) {
+        case 2: launch_stream_mf<W4, 2, EPI, PK>(a, pl, S, ws, st); break;
+        case 4: launch_stream_mf<W4, 4, EPI, PK>(a, pl, S, ws, st); break;
+        default: launch_stream_mf<W4, 8, EPI, PK>(a, pl, S, ws, st); break;
+      }
+    } else if (big_tiles(a.M, a.N) >= kBigMinTiles) {
+      const int64_t per_xcd = (big_tiles(a.M, a.N) + kXcds - 1) / kXcds;
+      const dim3 grid((unsigned)(per_xcd * kXcds));
+      if constexpr (W4)
+        launch((gemm_big_w4<EPI, PK>), grid, dim3(kFThreads), 0, st, a);
+      else
+        launch((gemm_big_f16<EPI, PK>), grid, dim3(kFThreads), 0, st, a);
+    } else {
+      const int64_t total = ((a.N + kTBN - 1) / kTBN) * ((a.M + kTBM - 1) / kTBM);
+      const int64_t per_xcd = (total + kXcds - 1) / kXcds;
+      launch((gemm_tiled<W4, EPI, PK>), dim3((unsigned)(per_xcd * kXcds)), dim3(kTThreads), 0, st,
+             a);
+    }
+    PIPO_HIP_TRY(hipGetLastError());
+    return PIPO_OK;
   }
-  PIPO_HIP_TRY(hipGetLastError());
-  return PIPO_OK;
 }
 
 template <bool W4, bool PK>
@@ -1115,6 +1164,7 @@ static pipo_status launch_fmt(const GemmArgs& a, int epi, float* ws, int64_t ws_
     case EPI_ADD_F32: return launch_epi<W4, EPI_ADD_F32, PK>(a, ws, ws_bytes, st);
     case EPI_F32: return launch_epi<W4, EPI_F32, PK>(a, ws, ws_bytes, st);
     case EPI_QKV: return launch_epi<W4, EPI_QKV, PK>(a, ws, ws_bytes, st);
+    case EPI_SWIGLU: return launch_epi<W4, EPI_SWIGLU, PK>(a, ws, ws_bytes, st);
     default: set_error("gemm: unknown epilogue %d", epi); return PIPO_ERR_ARG;
   }
 }
@@ -1145,6 +1195,12 @@ pipo_status launch_gemm(const GemmArgs& a, bool w4, int epi, float* workspace,
   if (epi == EPI_QKV && (a.dkv <= 0 || a.N != a.d + 2 * a.dkv)) {
     set_error("gemm: QKV output of %lld columns for d=%lld dkv=%lld", (long long)a.N,
               (long long)a.d, (long long)a.dkv);
+    return PIPO_ERR_ARG;
+  }
+  if (epi == EPI_SWIGLU && (a.N % 2 != 0 || a.bias != nullptr || a.out16 == nullptr ||
+                            a.ldo < a.N / 2)) {
+    set_error("gemm: the SwiGLU epilogue needs an even N (gate over up rows), no bias and an "
+              "fp16 output of N / 2 columns (N=%lld ldo=%lld)", (long long)a.N, (long long)a.ldo);
     return PIPO_ERR_ARG;
   }
   if (a.packed && a.N % 16 != 0) {

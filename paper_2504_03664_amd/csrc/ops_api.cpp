@@ -48,7 +48,7 @@ pipo_status pipo_dev_synchronize(void) {
 
 static pipo_status gemm_common(GemmArgs& a, bool w4, void* out, int32_t epi, void* workspace,
                                int64_t workspace_bytes, void* stream) {
-  if (epi < 0 || epi > PIPO_EPI_F32 || !out) {
+  if (((epi < 0 || epi > PIPO_EPI_F32) && epi != PIPO_EPI_SWIGLU) || !out) {
     set_error("gemm: bad epilogue %d or NULL output", epi);
     return PIPO_ERR_ARG;
   }
@@ -56,8 +56,8 @@ static pipo_status gemm_common(GemmArgs& a, bool w4, void* out, int32_t epi, voi
     set_error("gemm: negative workspace size");
     return PIPO_ERR_ARG;
   }
-  a.ldo = a.N;
-  if (epi == PIPO_EPI_F16 || epi == PIPO_EPI_RELU_F16)
+  a.ldo = epi == PIPO_EPI_SWIGLU ? a.N / 2 : a.N;
+  if (epi == PIPO_EPI_F16 || epi == PIPO_EPI_RELU_F16 || epi == PIPO_EPI_SWIGLU)
     a.out16 = static_cast<uint16_t*>(out);
   else
     a.out32 = static_cast<float*>(out);

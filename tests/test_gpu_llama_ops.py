@@ -90,6 +90,62 @@ def test_swiglu_vs_oracle(M, F):
     assert np.all(np.abs(got - want) <= 2e-3 * np.abs(want) + 1e-6)
 
 
+@pytest.mark.parametrize("M,F,K", [(1, 14336, 4096), (16, 1000, 256), (7, 64, 512),
+                                   (3, 40, 128)])
+@pytest.mark.parametrize("w4", [False, True])
+@pytest.mark.parametrize("frag", [False, True])
+def test_gemm_swiglu_epilogue(M, F, K, w4, frag):
+    """The SwiGLU epilogue of the decode GEMM (gate rows over up rows, M <=
+    16) gives the bits of the GEMM's fp16 output followed by the SwiGLU
+    kernel, and the oracle's SwiGLU of the exact products within fp16
+    rounding."""
+    if frag and (2 * F) % 16:
+        pytest.skip("fragment order needs N % 16 == 0")
+    log(f"gemm swiglu M={M} F={F} K={K} w4={w4} frag={frag}")
+    rng = np.random.default_rng(M + F + K + 2 * w4 + frag)
+    X = (rng.standard_normal((M, K)) * 0.5).astype(np.float16)
+    W = (rng.standard_normal((2 * F, K)) * 0.05).astype(np.float16)
+    dX = DB.from_array(X)
+    dgu, dh, dh2 = DB(M * 2 * F * 2), DB(M * F * 2), DB(M * F * 2)
+    if w4:
+        q, sm = synth.quant_int4_g64(W)
+        Wd = dequant_int4_g64(q, sm, np.float64)
+        if frag:
+            q, sm = B.pipo_pack_w4(q, sm)
+        dq, dsm = DB.from_array(q), DB.from_array(sm)
+        op = B.pipo_op_gemm_w4_frag if frag else B.pipo_op_gemm_w4
+        call = lambda epi, out: op(dX.ptr, dq.ptr, dsm.ptr, None, out.ptr, M, 2 * F, K, epi, None, 0)
+    else:
+        Wd = W.astype(np.float64)
+        dW = DB.from_array(B.pipo_pack_f16(W) if frag else W)
+        op = B.pipo_op_gemm_f16_frag if frag else B.pipo_op_gemm_f16
+        call = lambda epi, out: op(dX.ptr, dW.ptr, None, out.ptr, M, 2 * F, K, epi, None, 0)
+    call(B.PIPO_EPI_F16, dgu)
+    B.pipo_op_swiglu(dgu.ptr, dh2.ptr, M, F)
+    call(B.PIPO_EPI_SWIGLU, dh)
+    B.pipo_dev_synchronize()
+    fused = dh.to_array(np.uint16, (M, F))
+    assert np.array_equal(fused, dh2.to_array(np.uint16, (M, F)))
+    acc = X.astype(np.float64) @ Wd.T
+    want = swiglu(acc[:, :F], acc[:, F:])
+    got = fused.view(np.float16).astype(np.float64)
+    assert np.all(np.abs(got - want) <= 4e-3 * np.abs(want) + 2e-3 * np.abs(want).max())
+
+
+def test_gemm_swiglu_epilogue_limits():
+    """The SwiGLU epilogue runs only where the decode GEMM does (M <= 16) and
+    needs N = 2F even; other calls fail cleanly."""
+    rng = np.random.default_rng(3)
+    K, F = 128, 64
+    for M, N, status in ((17, 2 * F, -6), (4, 2 * F + 1, -1)):   # UNSUPPORTED, ARG
+        dX = DB.from_array((rng.standard_normal((M, K))).astype(np.float16))
+        dW = DB.from_array((rng.standard_normal((N, K))).astype(np.float16))
+        dh = DB(M * N * 2)
+        with pytest.raises(B.PipoError) as e:
+            B.pipo_op_gemm_f16(dX.ptr, dW.ptr, None, dh.ptr, M, N, K, B.PIPO_EPI_SWIGLU, None, 0)
+        assert e.value.status == status
+
+
 def _kv_rows(codes, sm):
     R = codes.shape[0]
     return np.ascontiguousarray(np.concatenate([codes, sm.view(np.uint8).reshape(R, -1)], axis=1))
