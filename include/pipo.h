@@ -81,8 +81,11 @@ enum {
   PIPO_DBG_COPY_DELAY = 2,    /* host-side sleep of copy_delay_us before every chunk copy */
   PIPO_DBG_TIMESTAMPS = 4,    /* record device timestamps of copies and kernels (stats) */
   PIPO_DBG_KV_PAGEABLE = 8,   /* keep the host KV cache in pageable memory (staged copies) */
-  PIPO_DBG_SEGMENT_COPIES = 16  /* copy each tensor of a layer on its own, even where the
+  PIPO_DBG_SEGMENT_COPIES = 16, /* copy each tensor of a layer on its own, even where the
                                    layer's matrices could be copied as one merged range */
+  PIPO_DBG_UNFUSED = 32         /* run the LLaMA SwiGLU as its own kernel after the gate/up
+                                   GEMM also at decode, where it is otherwise that GEMM's
+                                   epilogue (same values; for tests) */
 };
 
 /* Model families (pipo_shape.family).

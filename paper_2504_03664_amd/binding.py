@@ -32,7 +32,7 @@ PIPO_LAYOUT_ROW_MAJOR, PIPO_LAYOUT_FRAGMENT = 0, 1
 PIPO_KV_FP16, PIPO_KV_INT4_G64 = 0, 1
 PIPO_PIPE_PERFORMANCE, PIPO_PIPE_MEMORY_EFFICIENT = 0, 1
 PIPO_DBG_POISON_SLOTS, PIPO_DBG_COPY_DELAY, PIPO_DBG_TIMESTAMPS = 1, 2, 4
-PIPO_DBG_KV_PAGEABLE, PIPO_DBG_SEGMENT_COPIES = 8, 16
+PIPO_DBG_KV_PAGEABLE, PIPO_DBG_SEGMENT_COPIES, PIPO_DBG_UNFUSED = 8, 16, 32
 PIPO_EPI_F16, PIPO_EPI_RELU_F16, PIPO_EPI_ADD_F32, PIPO_EPI_F32 = 0, 1, 2, 3
 PIPO_EPI_SWIGLU = 5
 PIPO_MAX_KERNEL_STATS = 16

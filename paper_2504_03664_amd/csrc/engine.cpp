@@ -380,6 +380,7 @@ struct pipo_ctx {
   // statistics
   pipo_stats stats{};
   bool timestamps = false;
+  bool fuse_swiglu = true;      // LLaMA decode: SwiGLU as the gate/up GEMM's epilogue
   std::vector<hipEvent_t> tpool;
   size_t tpool_used = 0;
   std::vector<TimedRec> trec;
@@ -563,7 +564,7 @@ static pipo_status run_kernel(pipo_ctx* c, const Op& op) {
     case kFc1: {
       GemmArgs ga;
       if (c->llama) {  // gate and up in one GEMM, then the SwiGLU gate
-        if (rows <= 16) {  // decode: the gate in the GEMM's epilogue, same values
+        if (rows <= 16 && c->fuse_swiglu) {  // decode: the gate in the GEMM's epilogue, same values
           ga.out16 = c->h;
           ga.ldo = F;
           return gemm(kSegW1, c->a, nullptr, rows, 2 * F, d, EPI_SWIGLU, ga);
@@ -633,7 +634,7 @@ static void kernel_cost(const pipo_ctx* c, const Op& op, double* bytes, double* 
     case kFc1:
       if (c->llama) {
         g(rows, 2 * F, d, 2, wbytes(2 * F, d));
-        if (rows <= 16)
+        if (rows <= 16 && c->fuse_swiglu)
           *bytes -= rows * F * 2;  // SwiGLU in the epilogue: h (F columns) written instead
         else
           *bytes += rows * F * 6;  // SwiGLU: read gate and up, write h
@@ -1061,6 +1062,7 @@ static pipo_status create_ctx(const pipo_shape* shape, const pipo_host_weights* 
   c->dkv = kv_width(*shape);
   c->llama = llama;
   c->timestamps = (pol.debug_flags & PIPO_DBG_TIMESTAMPS) != 0;
+  c->fuse_swiglu = (pol.debug_flags & PIPO_DBG_UNFUSED) == 0;
   PIPO_HIP_TRY(hipGetDevice(&c->device));
   const int64_t d = c->d, F = c->F, V = c->V, L = c->L;
 

@@ -108,6 +108,7 @@ def test_llama_streamed_parity_and_resident_identity(shape, wfmt):
                   dict(n_weight_slots=1),
                   dict(n_weight_slots=2, chunk_bytes=4096 * 37, n_h2d_streams=1),
                   dict(debug_flags=B.PIPO_DBG_SEGMENT_COPIES),
+                  dict(debug_flags=B.PIPO_DBG_UNFUSED),   # SwiGLU as its own kernel
                   dict(kv_on_host=True, debug_flags=B.PIPO_DBG_POISON_SLOTS),
                   dict(kv_on_host=True, n_weight_slots=1, chunk_bytes=1 << 18)):
             log(f"  variant {v}")
