@@ -194,3 +194,37 @@ def test_decode_attention_context_limit_without_a_gpu():
         with pytest.raises(B.PipoError) as e:
             fn(65536)
         assert B.STATUS_NAMES[e.value.status] == "PIPO_ERR_UNSUPPORTED"
+
+
+def test_bench_kernel_symbols_follow_the_library_plan():
+    """bench.py names the kernels a projection launches (to find their
+    counters in the committed profiles) by restating the library's K-split
+    rule; the split it implies must be the one the library plans, for every
+    projection of every decode workload (the library's workspace query gives
+    S · M · N · 4 bytes for S > 1 splits)."""
+    import sys
+    sys.path.insert(0, ROOT)
+    import bench
+    import synth
+    for wl in synth.WORKLOADS:
+        sh = wl.shape
+        d, M = sh.d_model, wl.batch
+        llama = getattr(sh, "family", "opt") == "llama"
+        hkv = sh.n_kv_heads if llama else sh.n_heads
+        dh = d // sh.n_heads
+        F = sh.d_ffn
+        mats = {"qkv": (d + 2 * hkv * dh, d), "oproj": (d, d),
+                "fc1": (2 * F if llama else F, d), "fc2": (d, F)}
+        w4 = wl.wfmt == "int4"
+        for name, (N, K) in mats.items():
+            epi = {"qkv": 4, "oproj": 2, "fc2": 2,
+                   "fc1": (5 if M <= 16 else 0) if llama else 1}[name]
+            syms = bench.gemm_symbols(M, N, K, epi, w4, True)
+            ws = B.pipo_op_gemm_workspace_bytes(M, N, K, B.PIPO_W_INT4_G64 if w4 else B.PIPO_W_FP16)
+            splits = ws // (M * N * 4)
+            combine = [s for s in syms if s.startswith("gemm_combine<")]
+            if splits > 1:
+                assert combine and combine[0].startswith(f"gemm_combine<{epi}, {splits}, "), \
+                    (wl.name, name, syms, splits)
+            else:
+                assert not combine, (wl.name, name, syms)
