@@ -115,6 +115,14 @@ def gemm_symbols(M, N, K, epi, w4, frag):
     return syms
 
 
+def profile_tag(workload_name):
+    """Key of a workload's committed profile summaries: model and batch, plus
+    where the KV cache lives and its format (a disk tier runs the kernels of
+    the same workload and shares its key)."""
+    toks = workload_name.split()
+    return "_".join(toks[:2] + [t for t in toks[2:] if t in ("kv-host", "kv-int4")])
+
+
 def measured_traffic(workload_name, symbols, optional=()):
     """HBM bytes per dispatch of the kernels `symbols` (summed, plus those of
     `optional` that the profile holds) from the committed rocprofv3 PMC
@@ -122,10 +130,7 @@ def measured_traffic(workload_name, symbols, optional=()):
     `symbols` is missing from it, or the kernel sources changed since it was
     taken.  Returns (bytes, summary path, the kernels counted)."""
     import hashlib
-    # model and batch, plus where the KV cache lives and its format (a disk
-    # tier runs the kernels of the same workload without it)
-    toks = workload_name.split()
-    tag = "_".join(toks[:2] + [t for t in toks[2:] if t in ("kv-host", "kv-int4")])
+    tag = profile_tag(workload_name)
     path = os.path.join(ROOT, "profiles", f"hbm_traffic_{tag}.json")
     if not os.path.exists(path):
         return None, None, list(symbols)

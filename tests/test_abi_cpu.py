@@ -228,3 +228,23 @@ def test_bench_kernel_symbols_follow_the_library_plan():
                     (wl.name, name, syms, splits)
             else:
                 assert not combine, (wl.name, name, syms)
+
+
+def test_bench_profile_tags_are_distinct():
+    """bench.py keys the committed traffic summaries by model, batch, KV
+    placement and KV format: every workload with its own kernels has its own
+    key (the disk-tier run shares the kernels, and the key, of the workload
+    it streams), and every committed summary belongs to a workload."""
+    import sys
+    sys.path.insert(0, ROOT)
+    import bench
+    import synth
+    keys = {}
+    for wl in synth.WORKLOADS:
+        kernels = " ".join(t for t in wl.name.split() if t != "disk")
+        assert keys.setdefault(bench.profile_tag(wl.name), kernels) == kernels, wl.name
+    assert len(keys) == len({" ".join(t for t in w.name.split() if t != "disk")
+                             for w in synth.WORKLOADS})
+    for f in os.listdir(os.path.join(ROOT, "profiles")):
+        if f.startswith("hbm_traffic_") and f.endswith(".json"):
+            assert f[len("hbm_traffic_"):-len(".json")] in keys, f
