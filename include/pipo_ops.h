@@ -43,8 +43,9 @@ enum { PIPO_EPI_F16 = 0, PIPO_EPI_RELU_F16 = 1, PIPO_EPI_ADD_F32 = 2, PIPO_EPI_F
 /*
  * Y = X . W^T with the chosen epilogue (the projections of a layer and the
  * output head).  X: [M][K] fp16 (row stride K); W: [N][K] fp16; out: [M][N]
- * (row stride N), fp16 or fp32 per epilogue.  K must be a multiple of 128
- * and M below 2^31 (else PIPO_ERR_UNSUPPORTED).
+ * (row stride N), fp16 or fp32 per epilogue ([M][N/2] fp16 for
+ * PIPO_EPI_SWIGLU).  K must be a multiple of 128 and M below 2^31 (else
+ * PIPO_ERR_UNSUPPORTED).
  * For 16 < M <= 128 the K range may be split over workgroups whose fp32
  * partial sums go to `workspace` (device, caller-owned, contents
  * arbitrary) of pipo_op_gemm_workspace_bytes(M, N, K, wfmt) bytes; a second
